@@ -1,0 +1,90 @@
+"""Brute-force composer for tiny graphs: longest paths by enumerating every path.
+
+Independent of the oracle's event queue: it lists every path of the merged
+dependency graph (each collective is one node that all its member ops feed,
+weighted by its running time; every other op is a node weighted by its
+duration) and takes maxima over the lists.  Exponential; for <= ~25 nodes.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+COMPUTE, COMM = 0, 1
+
+
+class Cycle(Exception):
+    pass
+
+
+def _preds(g):
+    n = len(g["op_rank"])
+    last = {}
+    preds = []
+    for v in range(n):
+        key = (int(g["op_rank"][v]), int(g["op_stream"][v]))
+        p = set(int(u) for u in g["pred_idx"][g["pred_off"][v]:g["pred_off"][v + 1]])
+        if key in last:
+            p.add(last[key])
+        last[key] = v
+        preds.append(sorted(p))
+    return preds
+
+
+def all_paths_to(node, node_preds, stack=()):
+    """Every path (tuple of nodes) that ends at `node`."""
+    if node in stack:
+        raise Cycle(node)
+    yield (node,)
+    for p in node_preds[node]:
+        for path in all_paths_to(p, node_preds, stack + (node,)):
+            yield path + (node,)
+
+
+def compose(g, dur, cost):
+    """Per-op start/finish by path enumeration. dur: per-op durations, cost: per-collective times."""
+    n = len(g["op_rank"])
+    kind, coll = g["op_kind"], g["op_coll"]
+    preds = _preds(g)
+
+    def node(v):
+        return ("c", int(coll[v])) if kind[v] == COMM else ("o", v)
+
+    node_preds, weight = {}, {}
+    for v in range(n):
+        x = node(v)
+        node_preds.setdefault(x, set()).update(node(u) for u in preds[v])
+        weight[x] = int(cost[x[1]]) if x[0] == "c" else int(dur[v])
+    node_preds = {x: sorted(ps) for x, ps in node_preds.items()}
+    longest = {x: max(sum(weight[y] for y in path) for path in all_paths_to(x, node_preds))
+               for x in node_preds}
+    s = np.zeros(n, np.int64)
+    f = np.zeros(n, np.int64)
+    for v in range(n):
+        s[v] = max([longest[node(u)] for u in preds[v]], default=0)
+        f[v] = longest[node(v)]
+    return s, f
+
+
+def factors(g, s, f, slowdown):
+    """Slowdown factor of every op by checking every (compute, comm) pair of a rank."""
+    n = len(g["op_rank"])
+    F = np.full(n, 65536, np.int64)
+    for v in range(n):
+        if g["op_kind"][v] != COMPUTE:
+            continue
+        for c in range(n):
+            if g["op_kind"][c] == COMM and g["op_rank"][c] == g["op_rank"][v]:
+                if max(s[v], s[c]) < min(f[v], f[c]):
+                    F[v] = max(F[v], int(slowdown[g["op_class"][v]][g["coll_type"][g["op_coll"][c]]]))
+    return F
+
+
+def compose_validated(g, base, cost, slowdown, n_refine):
+    """Pass 1 with base durations, then n_refine rounds of overlap -> inflate -> recompose."""
+    s, f = compose(g, base, cost)
+    for _ in range(n_refine):
+        F = factors(g, s, f, slowdown)
+        d = np.array([(int(base[v]) * int(F[v]) + 32768) >> 16 if g["op_kind"][v] == COMPUTE
+                      else int(base[v]) for v in range(len(base))], np.int64)
+        s, f = compose(g, d, cost)
+    return s, f

@@ -1,0 +1,474 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test ties one part of the oracle to something other than itself:
+printed tables (chunk sizes), hand-worked values of Eq. 2-5, published
+SplitMix64 outputs, brute-force longest paths on tiny graphs, the 1F1B
+pipeline closed form, and structural invariants of any composed timeline.
+"""
+from __future__ import annotations
+
+import itertools
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from tests import bruteforce, tinygraph
+from tests.tinygraph import AG, AR, P2P, RS, Builder
+from workloads import configs, gpt1f1b, scenarios
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rows(name):
+    out = []
+    for line in open(os.path.join(GOLDEN, name)):
+        line = line.split("#")[0].strip()
+        if line:
+            out.append(line.split())
+    return out
+
+
+_ALIAS = {"alpha": "alpha_ns", "bw_intra": "bw_intra_MBps", "bw_inter": "bw_inter_MBps",
+          "reduce": "reduce_MBps"}
+
+
+def _scen(n=1, **kw):
+    sc = scenarios.default_scenarios(n)
+    for k, v in kw.items():
+        k = _ALIAS.get(k, k)
+        sc[k] = np.full_like(sc[k], v) if np.isscalar(v) else np.asarray(v, sc[k].dtype)
+    return sc
+
+
+# ---------------------------------------------------------------- CC estimator
+@pytest.mark.parametrize("row", _rows("table6_chunk_sizes.txt"), ids=lambda r: r[0])
+def test_chunk_size_table6(row):
+    assert oracle.chunk_bytes(int(row[0])) == int(row[1])
+
+
+@pytest.mark.parametrize("row", _rows("cc_costs.txt"), ids=lambda r: "-".join(r[:4]))
+def test_cc_cost_hand_values(row):
+    t, algo, S, N, M, K, alpha, bwa, bwe, red, want = map(int, row)
+    got = oracle.cc_time(t, S, N, M, K, alpha=alpha, bw_intra=bwa, bw_inter=bwe, reduce=red, algo=algo)
+    assert got == want
+
+
+@pytest.mark.parametrize("S,N,M,K", [(4194304, 8, 1, 8), (26214400, 4, 4, 1), (50331648, 16, 2, 8),
+                                     (123456789, 24, 3, 8), (1, 2, 2, 1)])
+def test_ring_allreduce_is_reduce_scatter_plus_all_gather(S, N, M, K):
+    """A ring all-reduce is a reduce-scatter followed by an all-gather over the same
+    ring (Sec. 5.1); with one connection set-up, T_AR = T_RS + T_AG - alpha."""
+    kw = dict(alpha=7000, bw_intra=300000, bw_inter=40000, reduce=150000)
+    ar = oracle.cc_time(AR, S, N, M, K, **kw)
+    rs = oracle.cc_time(RS, S, N, M, K, **kw)
+    ag = oracle.cc_time(AG, S, N, M, K, **kw)
+    assert ar == rs + ag - 7000
+
+
+def test_cc_cost_monotone_in_knobs():
+    base = dict(alpha=10000, bw_intra=400000, bw_inter=50000, reduce=160000)
+    for t, algo in [(AR, 0), (AR, 1), (AG, 0), (RS, 0), (P2P, 0)]:
+        for S, N, M, K in [(26214400, 8, 2, 4), (4194304, 8, 1, 8), (50331648, 2, 2, 1)]:
+            if t == P2P and N != 2:
+                continue
+            t0 = oracle.cc_time(t, S, N, M, K, algo=algo, **base)
+            assert oracle.cc_time(t, S, N, M, K, algo=algo, **dict(base, alpha=20000)) == t0 + 10000
+            for knob in ("bw_intra", "bw_inter", "reduce"):
+                assert oracle.cc_time(t, S, N, M, K, algo=algo, **dict(base, **{knob: base[knob] * 2})) <= t0
+            assert oracle.cc_time(t, 2 * S, N, M, K, algo=algo, **base) >= t0
+
+
+def test_time_limit_reported():
+    """The largest single collective allowed by the input ranges stays below 2^62 ns,
+    but two of them in a row do not: the composer reports a range error."""
+    big = (1 << 50) - 1
+    t = oracle.cc_time(AR, big, 4096, 512, 8, alpha=0, bw_intra=1, bw_inter=1, reduce=1)
+    assert (1 << 61) < t < (1 << 62)
+    b = Builder(2)
+    c1, c2 = b.collective(AR, big), b.collective(AR, big)
+    for r in range(2):
+        b.comm(r, c1)
+        b.comm(r, c2)
+    g = b.graph()
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.run(g, _scen(1, bw_intra_MBps=1, bw_inter_MBps=1, reduce_MBps=1), 0)
+    assert e.value.code == -2
+
+
+# ---------------------------------------------------------------- fixed-point and jitter
+@pytest.mark.parametrize("row", _rows("q16_worked.txt"), ids=lambda r: "-".join(r[:2]))
+def test_q16_worked_values(row):
+    d, f, want = map(int, row)
+    assert oracle.q16(d, f) == want
+
+
+@pytest.mark.parametrize("row", _rows("splitmix64_seed0.txt"), ids=lambda r: r[0])
+def test_splitmix64_published_outputs(row):
+    k, want = int(row[0]), int(row[1], 16)
+    assert oracle.splitmix64_at(0, k) == want
+    # the digest's mixing function is SplitMix64's output function
+    golden = 0x9E3779B97F4A7C15
+    assert oracle.mix64((k * golden) % (1 << 64)) == want
+
+
+def _chain_graph(durs):
+    b = Builder(1)
+    prev = []
+    for d in durs:
+        prev = [b.compute(0, int(d), preds=prev)]
+    return b.graph()
+
+
+def test_jitter_amplitude_zero_is_identity_and_bounds_hold():
+    durs = np.random.default_rng(5).integers(1, 200_000, 400)
+    g = _chain_graph(durs)
+    r = oracle.run(g, _scen(1), 0)
+    assert r["step"][0] == durs.sum()
+    A = 6554
+    sc = _scen(3, jitter_amp_q16=A, jitter_seed=3)
+    r = oracle.run(g, sc, 0)
+    d = r["finish"] - r["start"]
+    lo = np.floor(durs * (65536 - A) / 65536) - 1
+    hi = np.ceil(durs * (65536 + A) / 65536) + 1
+    assert (d >= lo).all() and (d <= hi).all()
+    rel = (d / durs - 1.0)
+    assert abs(rel.mean()) < 0.02 and rel.max() > 0.08 and rel.min() < -0.08
+    assert not np.array_equal(d[0], d[1])          # each scenario has its own stream
+
+
+# ---------------------------------------------------------------- composer vs brute force
+def _dur_cost(g, sc, si=0):
+    r = oracle.run(g, scenarios.take(sc, [si]), 0, costs=True, jitter_stream=[si])
+    base = np.where(g["op_kind"] == 1, 0, r["finish"][0] - r["start"][0])
+    return base, r["cost"][0]
+
+
+def _tiny_cases():
+    cases = {}
+    b = Builder(1)
+    a = b.compute(0, 5)
+    b.compute(0, 7, preds=[a])
+    cases["chain"] = b.graph()
+
+    b = Builder(1)
+    a = b.compute(0, 3)
+    x = b.compute(0, 10, stream=1, preds=[a])
+    y = b.compute(0, 4, stream=2, preds=[a])
+    b.compute(0, 2, preds=[x, y])
+    cases["diamond_streams"] = b.graph()
+
+    b = Builder(4)
+    c = b.collective(AR, 4 << 20)
+    for r in range(4):
+        w = b.compute(r, 1000 * (r + 1))
+        v = b.comm(r, c, preds=[w])
+        b.compute(r, 50, preds=[v])
+    cases["skewed_allreduce"] = b.graph()
+
+    b = Builder(2, gpus_per_node=1)
+    c1 = b.collective(P2P, 1 << 20)
+    c2 = b.collective(P2P, 1 << 20)
+    w = b.compute(0, 300)
+    b.comm(0, c1, stream=3, preds=[w])
+    b.compute(0, 900, preds=[w])
+    v = b.comm(0, c2, stream=4, preds=[w])
+    b.compute(0, 40, preds=[v])
+    x = b.compute(1, 700)
+    y = b.comm(1, c1, stream=4, preds=[x])
+    z = b.compute(1, 200, preds=[y])
+    b.comm(1, c2, stream=3, preds=[z])
+    cases["p2p_pair_two_servers"] = b.graph()
+
+    b = Builder(3, gpus_per_node=2)
+    c1 = b.collective(AR, 8 << 20)
+    c2 = b.collective(RS, 30 << 20)
+    c3 = b.collective(AG, 30 << 20)
+    for r in range(3):
+        w = b.compute(r, 100 * (3 - r), cls=r)
+        v1 = b.comm(r, c1, stream=1, preds=[w])
+        u = b.compute(r, 20000 + 7 * r, cls=0, preds=[w])
+        v2 = b.comm(r, c2, stream=2, preds=[u])
+        b.compute(r, 15000, cls=3, preds=[u])
+        b.comm(r, c3, stream=2, preds=[v1])
+        b.compute(r, 500, cls=4, preds=[v2])
+    cases["three_collectives_overlap"] = b.graph()
+    return cases
+
+
+TINY = _tiny_cases()
+
+
+@pytest.mark.parametrize("name", sorted(TINY))
+@pytest.mark.parametrize("algo", [0, 1])
+def test_composer_matches_path_enumeration(name, algo):
+    g = TINY[name]
+    sc = _scen(1, ar_algo=algo, bw_inter=60000, alpha=3000)
+    base, cost = _dur_cost(g, sc)
+    s, f = bruteforce.compose(g, base, cost)
+    r = oracle.run(g, sc, 0)
+    np.testing.assert_array_equal(r["start"][0], s)
+    np.testing.assert_array_equal(r["finish"][0], f)
+
+
+@pytest.mark.parametrize("name", sorted(TINY))
+@pytest.mark.parametrize("n_refine", [1, 2])
+def test_validator_matches_pairwise_overlap(name, n_refine):
+    g = TINY[name]
+    rng = np.random.default_rng(11)
+    table = rng.integers(65536, 140000, (8, 4)).astype(np.uint32)
+    sc = _scen(1, alpha=2500)
+    sc["slowdown_q16"] = table[None].copy()
+    base, cost = _dur_cost(g, sc)
+    s, f = bruteforce.compose_validated(g, base, cost, table, n_refine)
+    r = oracle.run(g, sc, n_refine)
+    np.testing.assert_array_equal(r["start"][0], s)
+    np.testing.assert_array_equal(r["finish"][0], f)
+
+
+def test_skewed_collective_finishes_at_last_launch_plus_cost():
+    g = TINY["skewed_allreduce"]
+    sc = _scen(1)
+    r = oracle.run(g, sc, 0, costs=True)
+    T = 64565                        # 4 MiB ring AR on one server, default knobs (cc_costs.txt case A, N=8)
+    T4 = oracle.cc_time(AR, 4 << 20, 4, 1, 4, alpha=10000, bw_intra=400000, bw_inter=50000, reduce=160000)
+    assert r["cost"][0][0] == T4 and T4 < T
+    comm = np.flatnonzero(g["op_kind"] == 1)
+    assert (r["finish"][0][comm] == 4000 + T4).all()
+    assert list(r["start"][0][comm]) == [1000, 2000, 3000, 4000]
+    assert r["step"][0] == 4000 + T4 + 50
+
+
+def test_random_small_dags_match_path_enumeration():
+    rng = np.random.default_rng(123)
+    for trial in range(40):
+        n_ranks = int(rng.integers(1, 4))
+        b = Builder(n_ranks, gpus_per_node=int(rng.integers(1, 3)))
+        n_coll = int(rng.integers(0, 3))
+        colls = [b.collective(int(rng.integers(0, 3)), int(rng.integers(0, 50 << 20))) for _ in range(n_coll)]
+        for r in range(n_ranks):
+            ids = []
+            order = list(rng.permutation(n_coll))
+            for k in range(int(rng.integers(2, 6))):
+                preds = [int(u) for u in ids if rng.random() < 0.3]
+                if order and rng.random() < 0.4:
+                    ids.append(b.comm(r, colls[order.pop()], stream=int(rng.integers(1, 4)), preds=preds))
+                else:
+                    ids.append(b.compute(r, int(rng.integers(0, 5000)), stream=int(rng.integers(0, 2)),
+                                         cls=int(rng.integers(0, 8)), preds=preds))
+            for c in order:           # every rank joins every collective
+                b.comm(r, colls[c], stream=int(rng.integers(1, 4)), preds=ids[-1:])
+        g = b.graph()
+        if len(g["op_rank"]) > 26:
+            continue
+        sc = _scen(1, ar_algo=trial % 2, alpha=int(rng.integers(0, 5000)))
+        sc["slowdown_q16"] = rng.integers(65536, 100000, (1, 8, 4)).astype(np.uint32)
+        try:
+            base, cost = _dur_cost(g, sc)
+        except oracle.OracleError as e:
+            assert e.code == -4                               # oracle says deadlock ...
+            with pytest.raises(bruteforce.Cycle):             # ... and the merged graph has a cycle
+                bruteforce.compose(g, g["op_dur"], np.zeros(n_coll, np.int64))
+            continue
+        for R in (0, 1):
+            s, f = bruteforce.compose_validated(g, base, cost, sc["slowdown_q16"][0], R)
+            r = oracle.run(g, sc, R)
+            np.testing.assert_array_equal(r["start"][0], s)
+            np.testing.assert_array_equal(r["finish"][0], f)
+
+
+# ---------------------------------------------------------------- closed forms
+@pytest.mark.parametrize("P,m", [(1, 1), (1, 4), (2, 1), (2, 4), (3, 5), (4, 4), (4, 8), (8, 16)])
+def test_1f1b_makespan_closed_form(P, m):
+    """Uniform stages, free communication: a 1F1B step takes (m + P - 1)(t_f + t_b)."""
+    tf, tb = 1000, 2100
+    g = tinygraph.pipeline_1f1b(P, m, tf, tb)
+    sc = _scen(1, alpha=0)
+    r = oracle.run(g, sc, 0)
+    assert r["step"][0] == (m + P - 1) * (tf + tb)
+    if P <= 4 and m <= 8 and len(g["op_rank"]) <= 60:
+        base, cost = _dur_cost(g, sc)
+        assert (cost == 0).all()
+        s, f = bruteforce.compose(g, base, cost)
+        np.testing.assert_array_equal(r["finish"][0], f)
+
+
+def test_single_collective_step_equals_its_cost():
+    for t, S in [(AR, 4 << 20), (AG, 100 << 20), (RS, 3 << 20)]:
+        b = Builder(8)
+        c = b.collective(t, S)
+        for r in range(8):
+            b.comm(r, c)
+        g = b.graph()
+        r = oracle.run(g, _scen(1), 1, costs=True)
+        assert r["step"][0] == r["cost"][0][0]
+        assert (r["start"][0] == 0).all()
+
+
+# ---------------------------------------------------------------- invariants on real-shaped graphs
+def _check_invariants(g, r, si=0):
+    s, f = r["start"][si], r["finish"][si]
+    assert (s >= 0).all() and (f >= s).all()
+    preds = bruteforce._preds(g) if len(g["op_rank"]) < 5000 else None
+    n = len(g["op_rank"])
+    # stream FIFO and explicit dependencies: s(v) >= f(u); non-comm s(v) = max pred f
+    key = g["op_rank"].astype(np.int64) * 8 + g["op_stream"]
+    order = np.lexsort((np.arange(n), key))
+    same = key[order][1:] == key[order][:-1]
+    assert (s[order][1:][same] >= f[order][:-1][same]).all()
+    src = np.repeat(np.arange(n), np.diff(g["pred_off"]))
+    assert (s[src] >= f[g["pred_idx"]]).all()
+    comm = g["op_kind"] == 1
+    cf = {}
+    for v in np.flatnonzero(comm):
+        cf.setdefault(int(g["op_coll"][v]), set()).add(int(f[v]))
+    assert all(len(x) == 1 for x in cf.values())
+    assert r["step"][si] == f.max()
+    if preds is not None:
+        for v in range(n):
+            want = max([f[u] for u in preds[v]], default=0)
+            assert s[v] == want
+
+
+def test_invariants_config1():
+    g = configs.graph(1)
+    sc = configs.scenario_batch(4)
+    sub = scenarios.take(sc, slice(0, 8))
+    for R in (0, 1, 2):
+        r = oracle.run(g, sub, R, threads=4)
+        for si in range(8):
+            _check_invariants(g, r, si)
+
+
+def test_all_unit_factors_make_refinement_a_no_op():
+    g = configs.graph(1)
+    sc = scenarios.take(configs.scenario_batch(4), slice(0, 4))
+    sc["slowdown_q16"][:] = 65536
+    r0 = oracle.run(g, sc, 0, threads=4)
+    r1 = oracle.run(g, sc, 1, threads=4)
+    for k in ("start", "finish", "step", "digest"):
+        np.testing.assert_array_equal(r0[k], r1[k])
+
+
+def test_refinement_never_shortens_the_step():
+    """q16(d, F) >= d for F >= 1.0, so the validated step is at least the
+    interference-free critical path; with gradient buckets overlapping later
+    layers' backward kernels it is strictly longer."""
+    sc = scenarios.take(configs.scenario_batch(4), slice(0, 8))
+    g = configs.graph(1)
+    r0 = oracle.run(g, sc, 0, threads=4, timelines=False)
+    r1 = oracle.run(g, sc, 1, threads=4, timelines=False)
+    assert (r1["step"] >= r0["step"]).all()
+    g = gpt1f1b.gpt_graph(n_layers=8, hidden=1024, seq=512, tp=2, pp=2, dp=2, microbatches=4, seed=0)
+    r0 = oracle.run(g, sc, 0, threads=4, timelines=False)
+    r1 = oracle.run(g, sc, 1, threads=4, timelines=False)
+    r2 = oracle.run(g, sc, 2, threads=4, timelines=False)
+    assert (r1["step"] > r0["step"]).all() and (r2["step"] >= r0["step"]).all()
+
+
+@pytest.mark.parametrize("knob,direction", [("bw_intra_MBps", -1), ("bw_inter_MBps", -1),
+                                             ("reduce_MBps", -1), ("alpha_ns", +1)])
+def test_step_monotone_in_network_knobs_without_interference(knob, direction):
+    g = configs.graph(1, 0)
+    g = dict(g, gpus_per_node=2)          # spread the 8 ranks over 4 servers
+    vals = [2_000, 9_000, 50_000, 120_000, 400_000]
+    sc = _scen(len(vals))
+    sc[knob] = np.array(vals, np.int64)
+    r = oracle.run(g, sc, 0, threads=4, timelines=False)
+    steps = r["step"]
+    assert (np.diff(steps) * direction >= 0).all()
+    assert steps[0] != steps[-1]
+
+
+def test_renumbering_servers_keeps_every_op_time():
+    g = dict(configs.graph(1), gpus_per_node=2)
+    sc = scenarios.take(configs.scenario_batch(4), slice(0, 4))
+    sc["jitter_amp_q16"][:] = 0
+    perm = [2, 0, 3, 1]                    # server i -> perm[i]
+    gpn = 2
+    new_rank = np.array([perm[r // gpn] * gpn + r % gpn for r in range(8)])
+    old_rank_of = np.argsort(new_rank)
+    old_ids = np.concatenate([np.flatnonzero(g["op_rank"] == old_rank_of[r]) for r in range(8)])
+    new_id = np.empty_like(old_ids)
+    new_id[old_ids] = np.arange(len(old_ids))
+    pc = np.diff(g["pred_off"])[old_ids]
+    pred_lists = [g["pred_idx"][g["pred_off"][v]:g["pred_off"][v + 1]] for v in old_ids]
+    h = dict(g)
+    for k in ("op_stream", "op_kind", "op_class", "op_dur", "op_coll"):
+        h[k] = g[k][old_ids]
+    h["op_rank"] = new_rank[g["op_rank"][old_ids]].astype(np.int32)
+    h["pred_off"] = np.concatenate([[0], np.cumsum(pc)]).astype(np.int64)
+    h["pred_idx"] = np.concatenate([new_id[p] for p in pred_lists]).astype(np.int32)
+    a = oracle.run(g, sc, 1, threads=4)
+    b = oracle.run(h, sc, 1, threads=4)
+    np.testing.assert_array_equal(a["start"][:, old_ids], b["start"])
+    np.testing.assert_array_equal(a["finish"][:, old_ids], b["finish"])
+    np.testing.assert_array_equal(a["step"], b["step"])
+
+
+def test_scenario_alone_equals_scenario_in_batch():
+    g = configs.graph(1)
+    sc = configs.scenario_batch(3)      # jittered scenarios
+    full = oracle.run(configs.graph(1), scenarios.take(sc, slice(0, 6)), 1, threads=3)
+    for si in (0, 5):
+        one = oracle.run(g, scenarios.take(sc, [si]), 1, jitter_stream=[si])
+        np.testing.assert_array_equal(one["finish"][0], full["finish"][si])
+        assert one["digest"][0] == full["digest"][si]
+
+
+def test_digest_is_sum_of_mixed_op_records():
+    g = TINY["three_collectives_overlap"]
+    r = oracle.run(g, _scen(1), 1)
+    s, f = r["start"][0], r["finish"][0]
+    want = 0
+    for v in range(len(s)):
+        want = (want + oracle.mix64(oracle.mix64(v ^ int(s[v])) ^ int(f[v]))) % (1 << 64)
+    assert int(r["digest"][0]) == want
+
+
+# ---------------------------------------------------------------- error behaviour
+def test_deadlock_detected():
+    b = Builder(2)
+    c1, c2 = b.collective(AR, 1024), b.collective(AR, 1024)
+    b.comm(0, c1, stream=1)
+    b.comm(0, c2, stream=1)
+    b.comm(1, c2, stream=1)
+    b.comm(1, c1, stream=1)
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.run(b.graph(), _scen(1), 0)
+    assert e.value.code == -4
+
+
+@pytest.mark.parametrize("mutate,code", [
+    (lambda g: g["pred_idx"].__setitem__(0, 5), -1),       # dependency on a later op
+    (lambda g: g["op_dur"].__setitem__(0, 1 << 43), -2),  # duration out of range
+    (lambda g: g["coll_bytes"].__setitem__(0, 1 << 50), -2),
+    (lambda g: g["op_stream"].__setitem__(0, 8), -1),
+    (lambda g: g["op_coll"].__setitem__(0, 0), -1),        # compute op naming a collective
+])
+def test_bad_graphs_rejected(mutate, code):
+    g = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in TINY["skewed_allreduce"].items()}
+    mutate(g)
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.run(g, _scen(1), 0)
+    assert e.value.code == code
+
+
+def test_bad_scenarios_rejected():
+    g = TINY["chain"]
+    for k, v in [("bw_inter_MBps", 0), ("reduce_MBps", 0), ("alpha_ns", -1), ("jitter_amp_q16", 65536)]:
+        with pytest.raises(oracle.OracleError) as e:
+            oracle.run(g, _scen(1, **{k: v}), 0)
+        assert e.value.code == -2
+    sc = _scen(1)
+    sc["slowdown_q16"][0, 3, 1] = 65535
+    with pytest.raises(oracle.OracleError):
+        oracle.run(g, sc, 0)
+
+
+def test_all_benchmark_graphs_small_enough_compose():
+    for cfg in (1, 4):
+        g = configs.graph(cfg)
+        r = oracle.run(g, scenarios.take(configs.scenario_batch(cfg), slice(0, 2)), 1, timelines=False)
+        assert (r["step"] > 0).all()
