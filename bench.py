@@ -1,0 +1,186 @@
+"""Benchmark: op-evaluations/s of the timeline composer on one MI355X.
+
+One step = one echo_compose_batch call over the whole scenario batch of the
+workload: CC costs, composer pass 1, overlap detection, composer pass 2 (one
+refinement) with step time, on inputs already resident in HBM.  The graph is
+loaded once before timing (the simulator's initialisation, excluded as in
+Table 8 of the paper).
+
+Prints one JSON line with the metric, a roofline entry for the composer
+(walk) kernel, and the CPU oracle timed on a bounded sample of the same work.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "walk_traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2412_12487_amd", "csrc", "echo_kernels.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def merged_pred_counts(g):
+    """|preds(v)|: previous op of v's stream plus explicit dependencies, without repeats."""
+    n = len(g["op_rank"])
+    key = g["op_rank"].astype(np.int64) * 8 + g["op_stream"]
+    order = np.lexsort((np.arange(n), key))
+    sp = np.full(n, -1, np.int64)
+    same = key[order][1:] == key[order][:-1]
+    sp[order[1:][same]] = order[:-1][same]
+    src = np.repeat(np.arange(n), np.diff(g["pred_off"]))
+    pairs = np.unique(np.stack([src, g["pred_idx"].astype(np.int64)], 1), axis=0) if len(src) else \
+        np.zeros((0, 2), np.int64)
+    explicit = np.bincount(pairs[:, 0], minlength=n)
+    dup = np.bincount(pairs[pairs[:, 1] == sp[pairs[:, 0]], 0], minlength=n)
+    return explicit + (sp >= 0) - dup
+
+
+def walk_bytes(g, n_scen, n_refine):
+    """Algorithmic bytes of the composer passes (edge-relaxation model):
+    per pass and scenario, 16 B written per op (start, finish), 8 B read per
+    merged predecessor, 8 B per collective cost; a refined pass also reads a
+    4 B slowdown factor per compute op."""
+    preds = merged_pred_counts(g)
+    per_pass = (16 * len(preds) + 8 * int(preds.sum()) + 8 * len(g["coll_type"])) * n_scen
+    n_compute = int((g["op_kind"] == 0).sum())
+    passes = [per_pass] + [per_pass + 4 * n_compute * n_scen] * n_refine
+    return passes
+
+
+def source_hash():
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def cpu_baseline(g, sc, n_refine, n_sample):
+    import oracle
+    from workloads import scenarios
+    sub = scenarios.take(sc, slice(0, n_sample))
+    threads = max(1, min(n_sample, os.cpu_count() or 1))
+    t = time.perf_counter()
+    oracle.run(g, sub, n_refine, threads=threads, timelines=False)
+    dt = time.perf_counter() - t
+    return {"value": len(g["op_rank"]) * n_sample / dt, "unit": "op-evals/s", "cores": threads,
+            "kind": "oracle", "wall_s": round(dt, 3),
+            "sample": f"scenarios 0..{n_sample - 1} of the same graph, {n_refine} refinement(s), "
+                      f"{threads} thread(s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", type=int, default=3, help="workload 1-4 (see workloads/configs.py)")
+    ap.add_argument("--refine", type=int, default=1)
+    ap.add_argument("--cpu-sample", type=int, default=8, help="scenarios the CPU oracle composes (0 = skip)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU: this build composes every scenario on a single MI355X "
+              f"(asked for {max(args.gpus, world)}).  Sharding scenarios across GPUs is described "
+              f"in DESIGN.md but not built.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2412_12487_amd as E
+    from workloads import configs
+
+    E.lib()
+    t = time.perf_counter()
+    g = configs.graph(args.config)
+    sc = configs.scenario_batch(args.config)
+    log(f"graph: config {args.config} {configs.NAMES[args.config]}: {len(g['op_rank'])} ops, "
+        f"{len(g['coll_type'])} collectives, {g['n_ranks']} ranks ({time.perf_counter() - t:.1f} s)")
+    t = time.perf_counter()
+    G = E.Graph(g, 0)
+    load_s = time.perf_counter() - t
+    log(f"loaded: {G.n_levels} levels in {load_s:.1f} s")
+    d_scen, n_scen = E.scenarios_to_device(sc, "cuda:0")
+    dev = torch.device("cuda:0")
+    out = {"step": torch.empty(n_scen, dtype=torch.int64, device=dev),
+           "start": torch.empty((G.n_ops, n_scen), dtype=torch.int64, device=dev),
+           "finish": torch.empty((G.n_ops, n_scen), dtype=torch.int64, device=dev)}
+    G.set_timing(True)
+    for i in range(args.warmup):
+        G.compose(d_scen, n_scen, args.refine, out=out)
+        log(f"warmup {i}: {G.kernel_times()}")
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    step_ms, walk_ms, kernels = [], [], {}
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        G.compose(d_scen, n_scen, args.refine, out=out, check=False)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        step_ms.append(e0.elapsed_time(e1))
+        kt = G.kernel_times()
+        walk_ms.append(sum(ms for k, ms in kt if k == "walk"))
+        for k, ms in kt:
+            kernels.setdefault(k, []).append(ms)
+        log(f"step {i}: {step_ms[-1]:.3f} ms  walk {walk_ms[-1]:.3f} ms")
+    wall = time.perf_counter() - t0
+    G.sync_status()
+    ms_per_step = wall * 1000.0 / args.steps
+    value = G.n_ops * n_scen / (ms_per_step / 1000.0)
+
+    passes = walk_bytes(g, n_scen, args.refine)
+    n_walk_launches = sum(1 for k, _ in G.kernel_times() if k == "walk")
+    walk_avg_ms = float(np.mean(walk_ms)) / max(n_walk_launches, 1)
+    bytes_per_launch = sum(passes) / max(n_walk_launches, 1)
+    achieved = bytes_per_launch / (walk_avg_ms / 1000.0) / 1e9
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        tr = json.load(open(TRAFFIC_FILE))
+        if tr.get("kernel_source_sha") == source_hash() and tr.get("config") == args.config:
+            traffic = tr.get("bytes_per_launch")
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": "k_walk", "avg_launch_ms": round(walk_avg_ms, 4),
+                "algorithmic_bytes_per_launch": int(bytes_per_launch)}
+    line = {
+        "metric": "op-evaluations/sec (ops x scenarios composed), 1 GPU",
+        "value": round(value, 1),
+        "unit": "op-evals/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "gpu_ms_per_step": round(float(np.median(step_ms)), 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": f"config {args.config}: {configs.NAMES[args.config]}, "
+                               f"{G.n_ops} ops x {n_scen} scenarios, {args.refine} refinement(s)",
+                   "n_ops": G.n_ops, "n_scenarios": n_scen, "n_refine": args.refine,
+                   "ranks": int(g["n_ranks"]), "levels": G.n_levels, "load_s": round(load_s, 2)},
+        "kernels_ms": {k: round(float(np.mean(v)), 4) for k, v in kernels.items()},
+        "roofline": roofline,
+    }
+    del out
+    G.close()
+    if args.cpu_sample > 0:
+        log(f"cpu baseline: oracle on {args.cpu_sample} scenario(s) ...")
+        line["cpu_baseline"] = cpu_baseline(g, sc, args.refine, args.cpu_sample)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

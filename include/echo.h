@@ -1,0 +1,202 @@
+/*
+ * echo.h -- C ABI of the MI355X timeline composer (libecho.so).
+ *
+ * The library implements the simulation hot path of Echo (arXiv 2412.12487):
+ * given the per-rank execution graphs of a distributed training job, it costs
+ * every collective with the white-box CC model (Sec. 5.3, Eq. 1-5, Table 6),
+ * composes global per-op timelines across all ranks (Sec. 4.2) with the
+ * collective synchronisation rule of Sec. 5.2, inflates computation kernels
+ * that overlap communication by a slowdown factor (Sec. 6 and the slowdown
+ * definition next to Table 2) and recomposes.  Many what-if scenarios are
+ * evaluated in one call, one GPU lane per scenario.
+ *
+ * Conventions for every entry point:
+ *   - return 0 (ECHO_OK) or a negative ECHO_ERR_* code; nothing throws;
+ *   - echo_last_error() returns a message for the calling thread's last error;
+ *   - "host" pointers are read during the call only and may be freed after it;
+ *   - "device" pointers are HIP device memory owned by the caller and must
+ *     stay valid until the enqueued work has finished;
+ *   - all device work is enqueued asynchronously on the caller's HIP stream
+ *     (hipStream_t passed as void*, NULL = the null stream);
+ *   - times are int64 nanoseconds; slowdown factors are Q16 fixed point
+ *     (65536 = 1.0).
+ */
+#ifndef ECHO_H
+#define ECHO_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Error codes. */
+enum {
+    ECHO_OK = 0,
+    ECHO_ERR_ARG = -1,    /* malformed argument or graph structure               */
+    ECHO_ERR_RANGE = -2,  /* a value outside the documented ranges, or a time >= 2^62 */
+    ECHO_ERR_MATCH = -3,  /* collective membership breaks the matching rules      */
+    ECHO_ERR_CYCLE = -4,  /* the merged graph has a cycle: the simulated job deadlocks */
+    ECHO_ERR_NOMEM = -5,  /* host or device allocation failed                     */
+    ECHO_ERR_HIP = -6,    /* a HIP runtime call failed                            */
+    ECHO_ERR_DEVICE = -7  /* a device-side check failed (see echo_sync_status)    */
+};
+
+/* Operator kinds, collective types and all-reduce algorithms. */
+enum { ECHO_COMPUTE = 0, ECHO_COMM = 1, ECHO_MEMCPY = 2 };
+enum { ECHO_AR = 0, ECHO_AG = 1, ECHO_RS = 2, ECHO_P2P = 3 };
+enum { ECHO_RING = 0, ECHO_TREE = 1 };
+
+typedef struct echo_graph_s *echo_graph;
+
+/*
+ * Per-rank execution graphs of one training step, as the paper's workload
+ * tracer produces them (Sec. 4.1): operators with dependencies and measured
+ * durations, communication operators as placeholders naming their group
+ * and message size.  All arrays are host memory owned by the caller.
+ *
+ *   n_ops          number of operators, 0 <= n_ops < 2^31
+ *   op_rank[n]     rank issuing the op, 0 <= rank < n_ranks; non-decreasing:
+ *                  ops are rank-major and, within a rank, in program order
+ *   op_stream[n]   stream on that rank, 0..7.  Ops of one stream run FIFO in
+ *                  program order (each waits for the previous one to finish)
+ *   op_kind[n]     ECHO_COMPUTE, ECHO_COMM or ECHO_MEMCPY
+ *   op_class[n]    kernel class 0..7: the row of the slowdown table
+ *   op_dur_ns[n]   base duration of compute/memcpy ops, 0 <= d < 2^43; ignored for comm
+ *   op_coll[n]     collective id of a comm op (0 <= id < n_colls), -1 otherwise
+ *   pred_off[n+1], pred_idx[pred_off[n]]
+ *                  explicit dependencies of op v: pred_idx[pred_off[v] ..
+ *                  pred_off[v+1]-1], each an earlier op of the same rank.
+ *                  Cross-rank coupling exists only through collectives.
+ *   n_colls        number of collectives
+ *   coll_type[c]   ECHO_AR, ECHO_AG, ECHO_RS or ECHO_P2P
+ *   coll_bytes[c]  message size S, 0 <= S < 2^50 (AG/RS: the full buffer)
+ *   gpus_per_node  ranks per server: node(rank) = rank / gpus_per_node
+ *
+ * Collective membership is explicit (op_coll): every rank in a group joins
+ * with exactly one comm op.  P2P collectives have exactly two members.
+ */
+typedef struct {
+    int64_t n_ops;
+    int32_t n_ranks, gpus_per_node;
+    const int32_t *op_rank;
+    const uint8_t *op_stream, *op_kind, *op_class;
+    const int64_t *op_dur_ns;
+    const int64_t *op_coll;
+    const int64_t *pred_off;
+    const int32_t *pred_idx;
+    int64_t n_colls;
+    const uint8_t *coll_type;
+    const int64_t *coll_bytes;
+} echo_graph_desc;
+
+/*
+ * One what-if scenario (192 bytes; callers pass a device array of these).
+ *   alpha_ns          connection set-up time alpha, 0 <= alpha < 2^40
+ *   bw_intra_MBps     intra-server bandwidth; beta = ceil(chunk*1000 / bw_intra)
+ *   bw_inter_MBps     inter-server bandwidth; gamma = ceil(chunk*1000 / bw_inter)
+ *   reduce_MBps       reduction throughput; reduce time = ceil(S*1000 / reduce)
+ *                     (each of the three in [1, 2^40))
+ *   jitter_seed, jitter_stream, jitter_amp_q16
+ *                     optional per-op duration jitter of amplitude A (Q16,
+ *                     0 <= A <= 65535, 0 = off): D(v) = q16(d(v), 65536 + J) with
+ *                     J = floor((u >> 32) * (2A+1) / 2^32) - A, u the k-th output of
+ *                     SplitMix64 seeded with jitter_seed, k = jitter_stream*2^36 + v + 1
+ *   ar_algo           ECHO_RING or ECHO_TREE for all-reduce collectives
+ *   slowdown_q16[k][t] factor for a class-k compute op overlapping a type-t
+ *                     collective, 65536 <= f < 2^20
+ * q16(d, f) = (d*f + 32768) >> 16 in unsigned 64-bit arithmetic.
+ */
+typedef struct {
+    int64_t alpha_ns, bw_intra_MBps, bw_inter_MBps, reduce_MBps;
+    uint64_t jitter_seed;
+    uint32_t jitter_stream;
+    int32_t jitter_amp_q16;
+    uint8_t ar_algo;
+    uint8_t pad[15];
+    uint32_t slowdown_q16[8][4];
+} echo_scenario;
+
+/*
+ * Validate a graph, match its collectives, merge each collective into one
+ * barrier node, order the merged graph by topological level and upload it
+ * to device `hip_device` (the analogue of the simulator's initialisation,
+ * Sec. 7.5 and Table 8).  Matching rule (Sec. 4.2: predefined matching rules
+ * plus a user API): within one communicator -- the set of (rank, stream) of a
+ * collective's members -- every member rank issues that communicator's
+ * collectives in the same order.  Errors: ARG (malformed arrays), RANGE,
+ * MATCH (a rank with two members of one collective, a P2P collective without
+ * exactly two members, a collective with no member, or an issue-order
+ * mismatch), CYCLE (deadlocked job), NOMEM, HIP.  The caller's arrays are
+ * copied; on success *out owns host and device memory until echo_free_graph.
+ */
+int echo_load_graph(const echo_graph_desc *desc, int hip_device, echo_graph *out);
+
+/* Sizes of a loaded graph: ops, collectives and topological levels of the merged graph. */
+int echo_graph_info(echo_graph g, int64_t *n_ops, int64_t *n_colls, int64_t *n_levels);
+
+/* Release a graph (waits for the device to be idle first).  NULL is allowed. */
+void echo_free_graph(echo_graph g);
+
+/*
+ * CC estimator (Sec. 5.3): d_cost[c * n_scen + s] = running time of collective
+ * c under scenario s -- ring AG (Eq. 2), ring RS (Eq. 3), ring or tree AR
+ * (Eq. 4, Eq. 5) and P2P as one chunked hop -- with chunk sizes of Table 6.
+ * N = members, M = distinct servers among them, K = most members on one
+ * server.  d_scen: device, n_scen records.  d_cost: device, n_colls * n_scen
+ * int64.  Scenario ranges are checked on the device (echo_sync_status).
+ */
+int echo_cc_cost(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int64_t *d_cost,
+                 void *hip_stream);
+
+/*
+ * Compose the timelines of every scenario.  Pass 1 composes with the base
+ * (jittered) durations: op v waits for all its predecessors (stream FIFO and
+ * explicit dependencies); a comm op starts at its own launch and finishes when
+ * the last member of its collective has launched plus the collective's cost
+ * (Sec. 5.2).  Each of the n_refine >= 0 refinements then inflates every
+ * compute op that overlapped a comm op of the same rank in the previous pass
+ * -- duration q16(D, F) with F the largest slowdown_q16[class][type] over the
+ * overlapping comm ops -- and composes again from the base durations.
+ * Outputs (device, caller-owned, any of start/finish/digest may be NULL):
+ *   d_start[v * n_scen + s], d_finish[v * n_scen + s]  final-pass timeline
+ *   d_step[s]    step time: the latest finish of any op
+ *   d_digest[s]  sum over ops (mod 2^64) of mix(mix(v ^ start) ^ finish),
+ *                mix = the SplitMix64 output function
+ * Works on the device only; range violations found there are reported by
+ * echo_sync_status.  Calls on one graph must not overlap (they share its
+ * workspace); the workspace grows on demand (hipMalloc) and is freed with
+ * the graph.
+ */
+int echo_compose_batch(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n_refine,
+                       int64_t *d_start, int64_t *d_finish, int64_t *d_step, uint64_t *d_digest,
+                       void *hip_stream);
+
+/*
+ * Wait for `hip_stream` and report the device-side status of the graph's
+ * launches since the previous call: ECHO_OK, ECHO_ERR_RANGE (a scenario knob
+ * out of range or a time >= 2^62) or ECHO_ERR_DEVICE (a wait for a collective
+ * exceeded the spin limit).  Clears the status.
+ */
+int echo_sync_status(echo_graph g, void *hip_stream);
+
+/*
+ * Optional per-kernel timing of echo_compose_batch: when enabled, HIP events
+ * are recorded on the caller's stream around every kernel the call launches.
+ * echo_kernel_times (after the stream has finished, e.g. after
+ * echo_sync_status) reports the last compose call's kernels in launch order:
+ * kinds[i] is ECHO_K_* and ms[i] the event-measured duration.  *n receives the
+ * number of kernels (at most max are written).
+ */
+enum { ECHO_K_INIT = 0, ECHO_K_CC_COST = 1, ECHO_K_WALK = 2, ECHO_K_OVERLAP = 3, ECHO_K_CLEAR = 4 };
+int echo_set_timing(echo_graph g, int enable);
+int echo_kernel_times(echo_graph g, int32_t max, int32_t *kinds, float *ms, int32_t *n);
+
+/* Message of the calling thread's last error ("" if none). */
+const char *echo_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ECHO_H */

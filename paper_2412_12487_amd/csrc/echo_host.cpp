@@ -1,0 +1,644 @@
+// echo_host.cpp -- graph loader and C ABI of libecho.so.
+//
+// echo_load_graph is the simulator's initialisation step (Table 8 "Init."):
+// it validates the per-rank graphs, matches collectives (Sec. 4.2 matching
+// rules), merges every collective into one barrier node, levels the merged
+// graph with Kahn's algorithm (a cycle is a deadlocked job), and lays out one
+// level-ordered walk list per rank for the device.  echo_compose_batch is the
+// execution step: it only enqueues kernels.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <new>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "echo.h"
+#include "echo_internal.h"
+
+using namespace echo;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(ECHO_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int64_t kDurLimit = int64_t(1) << 43;
+constexpr int64_t kBytesLimit = int64_t(1) << 50;
+constexpr int64_t kI32Max = INT32_MAX;
+constexpr int64_t kDefaultSpinNs = 20LL * 1000 * 1000 * 1000;   // 20 s
+
+// Table 6 (all-reduce breakdown): NCCL chunk size by tensor size.  The size
+// row is read as MiB upper bounds, the chunk row in units of 1000 bytes.
+int64_t table6_chunk(int64_t S) {
+    static const int64_t kBound[] = {4, 8, 16, 32, 64, 128};
+    static const int64_t kChunk[] = {18000, 36000, 72000, 72000, 72000, 144000};
+    for (int i = 0; i < 6; ++i)
+        if (S <= kBound[i] << 20) return kChunk[i];
+    return 288000;
+}
+
+template <class T>
+hipError_t upload(T **dst, const std::vector<T> &src) {
+    *dst = nullptr;
+    const size_t bytes = std::max<size_t>(src.size(), 1) * sizeof(T);
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(dst), bytes);
+    if (e != hipSuccess) return e;
+    if (!src.empty()) e = hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
+    return e;
+}
+
+}  // namespace
+
+struct echo_graph_s {
+    int device = 0;
+    int64_t n_ops = 0, n_colls = 0, n_levels = 0;
+    int32_t n_ranks = 0;
+    int64_t capacity = 0;              // co-resident walk wavefronts
+    int64_t spin_limit = kDefaultSpinNs / 10;   // 100 MHz ticks
+    DeviceGraph dg;
+    std::vector<void *> owned;         // device allocations of the graph
+    // workspace, grown on demand
+    int64_t *cost = nullptr;
+    size_t cost_n = 0;
+    unsigned long long *arrive = nullptr;
+    size_t arrive_n = 0;
+    unsigned *count = nullptr;
+    size_t count_n = 0;
+    uint32_t *factor = nullptr;
+    size_t factor_n = 0;
+    int64_t *tmp_start = nullptr, *tmp_finish = nullptr;
+    size_t tmp_start_n = 0, tmp_finish_n = 0;
+    int64_t *tmp_step = nullptr;
+    size_t tmp_step_n = 0;
+    // optional kernel timing: (kind, start event, end event) per launch of the last compose
+    bool timing = false;
+    std::vector<hipEvent_t> events;
+    std::vector<int32_t> timed_kinds;
+};
+
+namespace {
+
+void free_graph(echo_graph g) {
+    if (!g) return;
+    (void)hipSetDevice(g->device);
+    (void)hipDeviceSynchronize();
+    for (void *p : g->owned) (void)hipFree(p);
+    (void)hipFree(g->cost);
+    (void)hipFree(g->arrive);
+    (void)hipFree(g->count);
+    (void)hipFree(g->factor);
+    (void)hipFree(g->tmp_start);
+    (void)hipFree(g->tmp_finish);
+    (void)hipFree(g->tmp_step);
+    for (hipEvent_t ev : g->events) (void)hipEventDestroy(ev);
+    delete g;
+}
+
+template <class T>
+int ensure(T **p, size_t *have, size_t need, const char *what) {
+    if (*have >= need && *p) return ECHO_OK;
+    (void)hipFree(*p);
+    *p = nullptr;
+    *have = 0;
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(p), std::max<size_t>(need, 1) * sizeof(T));
+    if (e != hipSuccess) {
+        *p = nullptr;
+        return fail(ECHO_ERR_NOMEM, "workspace (%s, %zu bytes): %s", what, need * sizeof(T),
+                    hipGetErrorString(e));
+    }
+    *have = need;
+    return ECHO_OK;
+}
+
+// Bracket one kernel launch with events when timing is on.
+struct Timed {
+    echo_graph g;
+    hipStream_t s;
+    size_t slot = 0;
+    hipError_t begin(int32_t kind) {
+        if (!g->timing) return hipSuccess;
+        slot = g->timed_kinds.size();
+        while (g->events.size() < 2 * (slot + 1)) {
+            hipEvent_t ev;
+            hipError_t e = hipEventCreate(&ev);
+            if (e != hipSuccess) return e;
+            g->events.push_back(ev);
+        }
+        g->timed_kinds.push_back(kind);
+        return hipEventRecord(g->events[2 * slot], s);
+    }
+    hipError_t end() { return g->timing ? hipEventRecord(g->events[2 * slot + 1], s) : hipSuccess; }
+};
+
+// ------------------------------------------------------------------ loader
+int load(const echo_graph_desc *d, int device, echo_graph *out) {
+    if (!d || !out) return fail(ECHO_ERR_ARG, "null descriptor or output handle");
+    *out = nullptr;
+    const int64_t n = d->n_ops, nc = d->n_colls;
+    const int64_t R = d->n_ranks;
+    if (n < 0 || nc < 0 || R < 1 || d->gpus_per_node < 1)
+        return fail(ECHO_ERR_ARG, "bad sizes: n_ops %lld, n_colls %lld, n_ranks %lld, gpus_per_node %d",
+                    (long long)n, (long long)nc, (long long)R, d->gpus_per_node);
+    if (n > kI32Max || nc > kI32Max) return fail(ECHO_ERR_RANGE, "more than 2^31 ops or collectives");
+    if (!d->pred_off || (n > 0 && (!d->op_rank || !d->op_stream || !d->op_kind || !d->op_class ||
+                                   !d->op_dur_ns || !d->op_coll)) ||
+        (nc > 0 && (!d->coll_type || !d->coll_bytes)))
+        return fail(ECHO_ERR_ARG, "null array in the graph descriptor");
+    if (d->pred_off[0] != 0) return fail(ECHO_ERR_ARG, "pred_off[0] must be 0");
+    if (d->pred_off[n] > kI32Max) return fail(ECHO_ERR_RANGE, "more than 2^31 explicit dependencies");
+    if (d->pred_off[n] > 0 && !d->pred_idx) return fail(ECHO_ERR_ARG, "null pred_idx");
+
+    // per-op checks
+    for (int64_t v = 0; v < n; ++v) {
+        const int32_t r = d->op_rank[v];
+        if (r < 0 || r >= R || (v > 0 && r < d->op_rank[v - 1]))
+            return fail(ECHO_ERR_ARG, "op %lld: rank %d out of range or not rank-major", (long long)v, r);
+        if (d->op_stream[v] >= kStreams || d->op_kind[v] > ECHO_MEMCPY || d->op_class[v] >= kClasses)
+            return fail(ECHO_ERR_ARG, "op %lld: bad stream/kind/class", (long long)v);
+        if (d->op_kind[v] == ECHO_COMM) {
+            if (d->op_coll[v] < 0 || d->op_coll[v] >= nc)
+                return fail(ECHO_ERR_ARG, "comm op %lld names collective %lld", (long long)v,
+                            (long long)d->op_coll[v]);
+        } else {
+            if (d->op_coll[v] != -1)
+                return fail(ECHO_ERR_ARG, "non-comm op %lld names collective %lld", (long long)v,
+                            (long long)d->op_coll[v]);
+            if (d->op_dur_ns[v] < 0 || d->op_dur_ns[v] >= kDurLimit)
+                return fail(ECHO_ERR_RANGE, "op %lld: duration %lld outside [0, 2^43)", (long long)v,
+                            (long long)d->op_dur_ns[v]);
+        }
+        if (d->pred_off[v + 1] < d->pred_off[v])
+            return fail(ECHO_ERR_ARG, "pred_off decreases at op %lld", (long long)v);
+        for (int64_t j = d->pred_off[v]; j < d->pred_off[v + 1]; ++j) {
+            const int64_t u = d->pred_idx[j];
+            if (u < 0 || u >= v || d->op_rank[u] != r)
+                return fail(ECHO_ERR_ARG, "op %lld depends on op %lld: must be an earlier op of its rank",
+                            (long long)v, (long long)u);
+        }
+    }
+    for (int64_t c = 0; c < nc; ++c) {
+        if (d->coll_type[c] > ECHO_P2P) return fail(ECHO_ERR_ARG, "collective %lld: bad type", (long long)c);
+        if (d->coll_bytes[c] < 0 || d->coll_bytes[c] >= kBytesLimit)
+            return fail(ECHO_ERR_RANGE, "collective %lld: size outside [0, 2^50)", (long long)c);
+    }
+
+    // predecessors: previous op of the stream + explicit dependencies, deduplicated
+    std::vector<int32_t> last(R * kStreams, -1);
+    std::vector<int32_t> poff(n + 1, 0), preds;
+    preds.reserve(n + d->pred_off[n]);
+    {
+        std::vector<int32_t> tmp;
+        for (int64_t v = 0; v < n; ++v) {
+            tmp.clear();
+            const int64_t key = (int64_t)d->op_rank[v] * kStreams + d->op_stream[v];
+            if (last[key] >= 0) tmp.push_back(last[key]);
+            last[key] = (int32_t)v;
+            for (int64_t j = d->pred_off[v]; j < d->pred_off[v + 1]; ++j) tmp.push_back(d->pred_idx[j]);
+            std::sort(tmp.begin(), tmp.end());
+            tmp.erase(std::unique(tmp.begin(), tmp.end()), tmp.end());
+            preds.insert(preds.end(), tmp.begin(), tmp.end());
+            poff[v + 1] = (int32_t)preds.size();
+        }
+    }
+
+    // collective membership: N, M (servers), K (most members on one server)
+    std::vector<int64_t> moff(nc + 1, 0);
+    for (int64_t v = 0; v < n; ++v)
+        if (d->op_kind[v] == ECHO_COMM) ++moff[d->op_coll[v] + 1];
+    for (int64_t c = 0; c < nc; ++c) moff[c + 1] += moff[c];
+    std::vector<int32_t> mem(moff[nc]);
+    {
+        std::vector<int64_t> fill(moff.begin(), moff.end() - 1);
+        for (int64_t v = 0; v < n; ++v)
+            if (d->op_kind[v] == ECHO_COMM) mem[fill[d->op_coll[v]]++] = (int32_t)v;
+    }
+    std::vector<int32_t> cN(nc), cM(nc), cK(nc);
+    for (int64_t c = 0; c < nc; ++c) {
+        const int64_t N = moff[c + 1] - moff[c];
+        if (N == 0) return fail(ECHO_ERR_MATCH, "collective %lld has no member op", (long long)c);
+        if (d->coll_type[c] == ECHO_P2P && N != 2)
+            return fail(ECHO_ERR_MATCH, "P2P collective %lld has %lld members", (long long)c, (long long)N);
+        int32_t servers = 0, best = 0, run = 0, prev_node = -1, prev_rank = -1;
+        for (int64_t j = moff[c]; j < moff[c + 1]; ++j) {   // ascending op id => ascending rank
+            const int32_t rk = d->op_rank[mem[j]];
+            if (rk == prev_rank)
+                return fail(ECHO_ERR_MATCH, "rank %d joins collective %lld twice", rk, (long long)c);
+            prev_rank = rk;
+            const int32_t node = rk / d->gpus_per_node;
+            if (node != prev_node) {
+                ++servers;
+                run = 0;
+                prev_node = node;
+            }
+            best = std::max(best, ++run);
+        }
+        cN[c] = (int32_t)N;
+        cM[c] = servers;
+        cK[c] = best;
+    }
+
+    // matching rule: within one communicator (the (rank, stream) set of the
+    // members) every member rank issues the communicator's collectives in the
+    // same order -- so each collective sits at the same position everywhere.
+    {
+        std::map<std::vector<int64_t>, int32_t> comm_id;
+        std::vector<int32_t> cid(nc);
+        std::vector<int64_t> key;
+        for (int64_t c = 0; c < nc; ++c) {
+            key.clear();
+            for (int64_t j = moff[c]; j < moff[c + 1]; ++j)
+                key.push_back((int64_t)d->op_rank[mem[j]] * kStreams + d->op_stream[mem[j]]);
+            auto it = comm_id.emplace(key, (int32_t)comm_id.size()).first;
+            cid[c] = it->second;
+        }
+        std::unordered_map<uint64_t, int32_t> issued;   // (communicator, rank) -> collectives so far
+        std::vector<int32_t> pos(nc, -1);
+        for (int64_t v = 0; v < n; ++v) {
+            if (d->op_kind[v] != ECHO_COMM) continue;
+            const int64_t c = d->op_coll[v];
+            const uint64_t k = ((uint64_t)cid[c] << 32) | (uint32_t)d->op_rank[v];
+            const int32_t p = issued[k]++;
+            if (pos[c] < 0) pos[c] = p;
+            else if (pos[c] != p)
+                return fail(ECHO_ERR_MATCH,
+                            "collective %lld: rank %d issues it as call %d of its communicator, "
+                            "another member as call %d",
+                            (long long)c, d->op_rank[v], p, pos[c]);
+        }
+    }
+
+    // Kahn levels of the merged graph: node v for a compute/memcpy op,
+    // node n + c for collective c (all its member ops).
+    const int64_t nn = n + nc;
+    auto node = [&](int64_t v) -> int64_t { return d->op_kind[v] == ECHO_COMM ? n + d->op_coll[v] : v; };
+    std::vector<int64_t> soff(nn + 1, 0);
+    std::vector<int32_t> indeg(nn, 0);
+    for (int64_t v = 0; v < n; ++v)
+        for (int32_t j = poff[v]; j < poff[v + 1]; ++j) {
+            ++soff[node(preds[j]) + 1];
+            ++indeg[node(v)];
+        }
+    for (int64_t x = 0; x < nn; ++x) soff[x + 1] += soff[x];
+    std::vector<int64_t> succ(soff[nn]);
+    {
+        std::vector<int64_t> fill(soff.begin(), soff.end() - 1);
+        for (int64_t v = 0; v < n; ++v)
+            for (int32_t j = poff[v]; j < poff[v + 1]; ++j) succ[fill[node(preds[j])]++] = node(v);
+    }
+    std::vector<int32_t> level(nn, 0);
+    std::vector<int64_t> queue;
+    queue.reserve(nn);
+    for (int64_t x = 0; x < nn; ++x)
+        if (indeg[x] == 0) queue.push_back(x);
+    for (size_t h = 0; h < queue.size(); ++h) {
+        const int64_t x = queue[h];
+        for (int64_t j = soff[x]; j < soff[x + 1]; ++j) {
+            const int64_t y = succ[j];
+            level[y] = std::max(level[y], level[x] + 1);
+            if (--indeg[y] == 0) queue.push_back(y);
+        }
+    }
+    if ((int64_t)queue.size() != nn) {
+        for (int64_t c = 0; c < nc; ++c)
+            if (indeg[n + c] > 0)
+                return fail(ECHO_ERR_CYCLE, "dependency cycle through collective %lld: the simulated job deadlocks",
+                            (long long)c);
+        return fail(ECHO_ERR_CYCLE, "dependency cycle: the simulated job deadlocks");
+    }
+    int64_t n_levels = 0;
+    for (int64_t x = 0; x < nn; ++x) n_levels = std::max<int64_t>(n_levels, level[x] + 1);
+    std::vector<int32_t>().swap(indeg);
+    std::vector<int64_t>().swap(succ);
+    std::vector<int64_t>().swap(soff);
+
+    // walk lists: each rank's ops by (key, program order), key = level for
+    // compute/memcpy, the launch level for a comm op
+    std::vector<int32_t> key(n);
+    for (int64_t v = 0; v < n; ++v) {
+        if (d->op_kind[v] == ECHO_COMM) {
+            int32_t k = 0;
+            for (int32_t j = poff[v]; j < poff[v + 1]; ++j) k = std::max(k, level[node(preds[j])] + 1);
+            key[v] = k;
+        } else {
+            key[v] = level[v];
+        }
+    }
+    std::vector<int64_t> rank_off(R + 1, 0);
+    for (int64_t v = 0; v < n; ++v) ++rank_off[d->op_rank[v] + 1];
+    for (int64_t r = 0; r < R; ++r) rank_off[r + 1] += rank_off[r];
+    std::vector<int32_t> order(n);
+    for (int64_t v = 0; v < n; ++v) order[v] = (int32_t)v;   // rank-major already
+    for (int64_t r = 0; r < R; ++r)
+        std::stable_sort(order.begin() + rank_off[r], order.begin() + rank_off[r + 1],
+                         [&](int32_t x, int32_t y) { return key[x] < key[y]; });
+    std::vector<WalkItem> items(n);
+    std::vector<int32_t> far;
+    {
+        std::vector<int32_t> latest(kStreams);
+        for (int64_t r = 0; r < R; ++r) {
+            std::fill(latest.begin(), latest.end(), -1);
+            for (int64_t i = rank_off[r]; i < rank_off[r + 1]; ++i) {
+                const int32_t v = order[i];
+                unsigned mask = 0;
+                const int64_t f0 = (int64_t)far.size();
+                for (int32_t j = poff[v]; j < poff[v + 1]; ++j) {
+                    const int32_t u = preds[j];
+                    if (latest[d->op_stream[u]] == u) mask |= 1u << d->op_stream[u];
+                    else far.push_back(u);
+                }
+                latest[d->op_stream[v]] = v;
+                WalkItem &it = items[i];
+                it.op = v;
+                it.meta = (uint32_t)d->op_kind[v] | ((uint32_t)d->op_stream[v] << 2) |
+                          ((uint32_t)d->op_class[v] << 5) | (mask << 8);
+                it.nfar = (int32_t)((int64_t)far.size() - f0);
+                it.far_off = (int32_t)f0;
+                it.coll = d->op_kind[v] == ECHO_COMM ? (int32_t)d->op_coll[v] : -1;
+                it.pad = 0;
+                it.dur = d->op_kind[v] == ECHO_COMM ? 0 : d->op_dur_ns[v];
+            }
+        }
+    }
+
+    // per (rank, stream) comm and compute op lists in program order
+    std::vector<int64_t> cl_off(R * kStreams + 1, 0), cp_off(R * kStreams + 1, 0);
+    for (int64_t v = 0; v < n; ++v) {
+        const int64_t k = (int64_t)d->op_rank[v] * kStreams + d->op_stream[v];
+        if (d->op_kind[v] == ECHO_COMM) ++cl_off[k + 1];
+        else if (d->op_kind[v] == ECHO_COMPUTE) ++cp_off[k + 1];
+    }
+    for (int64_t k = 0; k < R * kStreams; ++k) {
+        cl_off[k + 1] += cl_off[k];
+        cp_off[k + 1] += cp_off[k];
+    }
+    std::vector<int32_t> cl(cl_off.back()), cp(cp_off.back());
+    std::vector<uint8_t> cl_type(cl_off.back()), cp_class(cp_off.back());
+    {
+        std::vector<int64_t> fl(cl_off.begin(), cl_off.end() - 1), fp(cp_off.begin(), cp_off.end() - 1);
+        for (int64_t v = 0; v < n; ++v) {
+            const int64_t k = (int64_t)d->op_rank[v] * kStreams + d->op_stream[v];
+            if (d->op_kind[v] == ECHO_COMM) {
+                cl_type[fl[k]] = d->coll_type[d->op_coll[v]];
+                cl[fl[k]++] = (int32_t)v;
+            } else if (d->op_kind[v] == ECHO_COMPUTE) {
+                cp_class[fp[k]] = d->op_class[v];
+                cp[fp[k]++] = (int32_t)v;
+            }
+        }
+    }
+    std::vector<int64_t> c_bytes(nc), c_chunk(nc), c_eta_ring(nc), c_eta_chunks(nc);
+    std::vector<uint8_t> c_type(nc);
+    for (int64_t c = 0; c < nc; ++c) {
+        const int64_t S = d->coll_bytes[c], ch = table6_chunk(S);
+        c_bytes[c] = S;
+        c_chunk[c] = ch;
+        c_eta_ring[c] = (S + (int64_t)cN[c] * ch - 1) / ((int64_t)cN[c] * ch);   // ring rounds
+        c_eta_chunks[c] = (S + ch - 1) / ch;                                   // pipelined chunks
+        c_type[c] = d->coll_type[c];
+    }
+
+    // upload
+    echo_graph g = new (std::nothrow) echo_graph_s();
+    if (!g) return fail(ECHO_ERR_NOMEM, "host allocation");
+    g->device = device;
+    g->n_ops = n;
+    g->n_colls = nc;
+    g->n_levels = n_levels;
+    g->n_ranks = (int32_t)R;
+    hipError_t e = hipSetDevice(device);
+    if (e != hipSuccess) {
+        delete g;
+        return hip_fail(e, "hipSetDevice");
+    }
+    DeviceGraph &dg = g->dg;
+    dg.n_ops = n;
+    dg.n_colls = nc;
+    dg.n_ranks = (int32_t)R;
+#define UP(dst, src)                                                        \
+    do {                                                                    \
+        e = upload(&dst, src);                                              \
+        if (dst) g->owned.push_back(dst);                                   \
+        if (e != hipSuccess) {                                              \
+            free_graph(g);                                                  \
+            return fail(e == hipErrorOutOfMemory ? ECHO_ERR_NOMEM : ECHO_ERR_HIP, \
+                        "uploading " #src ": %s", hipGetErrorString(e));    \
+        }                                                                   \
+    } while (0)
+    UP(dg.items, items);
+    UP(dg.rank_off, rank_off);
+    UP(dg.far, far);
+    UP(dg.c_bytes, c_bytes);
+    UP(dg.c_chunk, c_chunk);
+    UP(dg.c_eta_ring, c_eta_ring);
+    UP(dg.c_eta_chunks, c_eta_chunks);
+    UP(dg.c_N, cN);
+    UP(dg.c_M, cM);
+    UP(dg.c_K, cK);
+    UP(dg.c_type, c_type);
+    UP(dg.cl_off, cl_off);
+    UP(dg.cl, cl);
+    UP(dg.cl_type, cl_type);
+    UP(dg.cp_off, cp_off);
+    UP(dg.cp, cp);
+    UP(dg.cp_class, cp_class);
+    UP(dg.status, std::vector<unsigned>(1, 0u));
+#undef UP
+    e = walk_capacity(device, &g->capacity);
+    if (e != hipSuccess) {
+        free_graph(g);
+        return hip_fail(e, "occupancy query");
+    }
+    if (g->capacity < R) {
+        const int64_t cap = g->capacity;
+        free_graph(g);
+        return fail(ECHO_ERR_RANGE, "%lld ranks exceed the %lld co-resident walk wavefronts of the device",
+                    (long long)R, (long long)cap);
+    }
+    *out = g;
+    return ECHO_OK;
+}
+
+int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n_refine, int64_t *d_start,
+            int64_t *d_finish, int64_t *d_step, uint64_t *d_digest, hipStream_t stream) {
+    if (!g || !d_scen) return fail(ECHO_ERR_ARG, "null graph or scenario array");
+    if (n_scen < 1 || n_refine < 0 || n_refine > 64)
+        return fail(ECHO_ERR_ARG, "n_scen must be >= 1 and 0 <= n_refine <= 64 (got %d, %d)", n_scen, n_refine);
+    hipError_t e = hipSetDevice(g->device);
+    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+    const int64_t ns = n_scen;
+    const int32_t n_tiles = (int32_t)((ns + kLanes - 1) / kLanes);
+    int rc;
+    if ((rc = ensure(&g->cost, &g->cost_n, (size_t)(g->n_colls * ns), "cost"))) return rc;
+    if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->n_colls * ns), "arrivals"))) return rc;
+    if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * n_tiles), "arrival counts"))) return rc;
+    if (n_refine > 0 && (rc = ensure(&g->factor, &g->factor_n, (size_t)(g->n_ops * ns), "factors"))) return rc;
+    if (!d_start && (rc = ensure(&g->tmp_start, &g->tmp_start_n, (size_t)(g->n_ops * ns), "start"))) return rc;
+    if (!d_finish && (rc = ensure(&g->tmp_finish, &g->tmp_finish_n, (size_t)(g->n_ops * ns), "finish")))
+        return rc;
+    if (!d_step && (rc = ensure(&g->tmp_step, &g->tmp_step_n, (size_t)ns, "step"))) return rc;
+    int64_t *start = d_start ? d_start : g->tmp_start;
+    int64_t *finish = d_finish ? d_finish : g->tmp_finish;
+    int64_t *step = d_step ? d_step : g->tmp_step;
+
+    const int64_t n_arrive = g->n_colls * ns, n_count = g->n_colls * n_tiles;
+    g->timed_kinds.clear();
+    Timed tm{g, stream};
+#define TIMED(kind, call, what)                                   \
+    do {                                                          \
+        if ((e = tm.begin(kind))) return hip_fail(e, "event");    \
+        if ((e = (call))) return hip_fail(e, what);               \
+        if ((e = tm.end())) return hip_fail(e, "event");          \
+    } while (0)
+    TIMED(ECHO_K_INIT, launch_init(g->dg, d_scen, n_scen, g->arrive, n_arrive, g->count, n_count, step, d_digest,
+                                   stream), "init kernel");
+    TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg, d_scen, n_scen, g->cost, stream), "cc_cost kernel");
+
+    // tiles per walk launch: every rank of a tile must be co-resident
+    const int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, g->capacity / g->n_ranks));
+    for (int32_t p = 0; p <= n_refine; ++p) {
+        if (p > 0) {
+            OverlapArgs o{g->dg.cl_off, g->dg.cp_off, g->dg.cl, g->dg.cp, g->dg.cl_type, g->dg.cp_class,
+                          d_scen, start, finish, g->factor, n_scen, n_tiles};
+            TIMED(ECHO_K_OVERLAP, launch_overlap(o, g->n_ranks, stream), "overlap kernel");
+            TIMED(ECHO_K_CLEAR, launch_clear(g->arrive, n_arrive, g->count, n_count, stream), "clear kernel");
+        }
+        for (int64_t t0 = 0; t0 < n_tiles; t0 += per_launch) {
+            WalkArgs a;
+            a.items = g->dg.items;
+            a.rank_off = g->dg.rank_off;
+            a.far = g->dg.far;
+            a.c_N = g->dg.c_N;
+            a.scen = d_scen;
+            a.cost = g->cost;
+            a.factor = p > 0 ? g->factor : nullptr;
+            a.start = start;
+            a.finish = finish;
+            a.arrive = g->arrive;
+            a.count = g->count;
+            a.step = step;
+            a.digest = d_digest;
+            a.status = g->dg.status;
+            a.spin_limit = g->spin_limit;
+            a.n_scen = n_scen;
+            a.n_tiles = n_tiles;
+            a.tile0 = (int32_t)t0;
+            a.tiles = (int32_t)std::min<int64_t>(per_launch, n_tiles - t0);
+            a.final_pass = p == n_refine;
+            if (g->n_ranks == 0 || g->n_ops == 0) continue;
+            TIMED(ECHO_K_WALK, launch_walk(a, g->n_ranks, stream), "walk kernel");
+        }
+    }
+#undef TIMED
+    return ECHO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int echo_load_graph(const echo_graph_desc *desc, int hip_device, echo_graph *out) {
+    g_last_error.clear();
+    try {
+        return load(desc, hip_device, out);
+    } catch (const std::bad_alloc &) {
+        return fail(ECHO_ERR_NOMEM, "host allocation failed while loading the graph");
+    } catch (...) {
+        return fail(ECHO_ERR_ARG, "unexpected exception while loading the graph");
+    }
+}
+
+int echo_graph_info(echo_graph g, int64_t *n_ops, int64_t *n_colls, int64_t *n_levels) {
+    if (!g) return fail(ECHO_ERR_ARG, "null graph");
+    if (n_ops) *n_ops = g->n_ops;
+    if (n_colls) *n_colls = g->n_colls;
+    if (n_levels) *n_levels = g->n_levels;
+    return ECHO_OK;
+}
+
+void echo_free_graph(echo_graph g) { free_graph(g); }
+
+int echo_cc_cost(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int64_t *d_cost, void *hip_stream) {
+    g_last_error.clear();
+    if (!g || !d_scen || !d_cost || n_scen < 1) return fail(ECHO_ERR_ARG, "null argument or n_scen < 1");
+    hipError_t e = hipSetDevice(g->device);
+    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    if ((e = launch_init(g->dg, d_scen, n_scen, nullptr, 0, nullptr, 0, nullptr, nullptr, s)))
+        return hip_fail(e, "init kernel");
+    if ((e = launch_cc_cost(g->dg, d_scen, n_scen, d_cost, s))) return hip_fail(e, "cc_cost kernel");
+    return ECHO_OK;
+}
+
+int echo_compose_batch(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n_refine,
+                       int64_t *d_start, int64_t *d_finish, int64_t *d_step, uint64_t *d_digest,
+                       void *hip_stream) {
+    g_last_error.clear();
+    try {
+        return compose(g, d_scen, n_scen, n_refine, d_start, d_finish, d_step, d_digest,
+                       static_cast<hipStream_t>(hip_stream));
+    } catch (...) {
+        return fail(ECHO_ERR_NOMEM, "unexpected exception in compose");
+    }
+}
+
+int echo_sync_status(echo_graph g, void *hip_stream) {
+    g_last_error.clear();
+    if (!g) return fail(ECHO_ERR_ARG, "null graph");
+    hipError_t e = hipSetDevice(g->device);
+    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+    if ((e = hipStreamSynchronize(static_cast<hipStream_t>(hip_stream)))) return hip_fail(e, "stream sync");
+    unsigned st = 0;
+    if ((e = hipMemcpy(&st, g->dg.status, sizeof st, hipMemcpyDeviceToHost))) return hip_fail(e, "status read");
+    const unsigned zero = 0;
+    if ((e = hipMemcpy(g->dg.status, &zero, sizeof zero, hipMemcpyHostToDevice))) return hip_fail(e, "status clear");
+    if (st & kStatusTimeout)
+        return fail(ECHO_ERR_DEVICE, "a collective barrier wait exceeded the spin limit");
+    if (st & kStatusRange) return fail(ECHO_ERR_RANGE, "a scenario knob is out of range");
+    if (st & kStatusOverflow) return fail(ECHO_ERR_RANGE, "a time reached 2^62 ns");
+    return ECHO_OK;
+}
+
+int echo_set_timing(echo_graph g, int enable) {
+    if (!g) return fail(ECHO_ERR_ARG, "null graph");
+    g->timing = enable != 0;
+    g->timed_kinds.clear();
+    return ECHO_OK;
+}
+
+int echo_kernel_times(echo_graph g, int32_t max, int32_t *kinds, float *ms, int32_t *n) {
+    g_last_error.clear();
+    if (!g || !n || max < 0 || (max > 0 && (!kinds || !ms))) return fail(ECHO_ERR_ARG, "null argument");
+    const int32_t k = (int32_t)g->timed_kinds.size();
+    *n = k;
+    hipError_t e = hipSetDevice(g->device);
+    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+    for (int32_t i = 0; i < k && i < max; ++i) {
+        kinds[i] = g->timed_kinds[i];
+        if ((e = hipEventElapsedTime(&ms[i], g->events[2 * i], g->events[2 * i + 1])))
+            return hip_fail(e, "hipEventElapsedTime");
+    }
+    return ECHO_OK;
+}
+
+const char *echo_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

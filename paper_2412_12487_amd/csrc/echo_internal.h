@@ -1,0 +1,116 @@
+// echo_internal.h -- device data layout and kernel launchers of libecho.so.
+//
+// The loader turns the caller's per-rank graphs into one "walk list" per rank:
+// that rank's ops ordered by (key, program order) where key is the op's
+// topological level in the merged graph (a collective merged into one barrier
+// node) -- for a comm op, the level at which it can launch.  A wavefront walks
+// one rank for 64 scenarios (one lane each); predecessors that are the latest
+// op of their stream stay in registers, the rest are read back from the
+// finish array.  Collective barriers are met through per-(collective,
+// scenario) arrival maxima and per-(collective, scenario tile) arrival counts.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "echo.h"
+
+namespace echo {
+
+constexpr int kStreams = 8;
+constexpr int kClasses = 8;
+constexpr int kTypes = 4;
+constexpr int kLanes = 64;                       // scenarios per wavefront
+constexpr int64_t kTimeLimit = int64_t(1) << 62;
+
+// Device status bits (per graph).
+constexpr unsigned kStatusRange = 1u;            // scenario knob out of range
+constexpr unsigned kStatusOverflow = 2u;         // a time reached 2^62
+constexpr unsigned kStatusTimeout = 4u;          // a barrier wait exceeded the spin limit
+constexpr unsigned kStatusAbort = 8u;            // stop all waits (set with timeout)
+
+// One entry of a rank's walk list (32 bytes, read wave-uniformly).
+struct WalkItem {
+    int32_t op;         // op id: row of the [op][scenario] outputs
+    uint32_t meta;      // kind | stream << 2 | class << 5 | regmask << 8
+    int32_t nfar;       // predecessors read back from memory ...
+    int32_t far_off;    // ... listed at far[far_off .. far_off + nfar)
+    int32_t coll;       // collective of a comm op, -1 otherwise
+    int32_t pad;
+    int64_t dur;        // base duration of compute / memcpy ops
+};
+static_assert(sizeof(WalkItem) == 32, "walk item must stay 32 bytes");
+
+__host__ __device__ inline int item_kind(uint32_t m) { return int(m & 3u); }
+__host__ __device__ inline int item_stream(uint32_t m) { return int((m >> 2) & 7u); }
+__host__ __device__ inline int item_class(uint32_t m) { return int((m >> 5) & 7u); }
+__host__ __device__ inline unsigned item_regmask(uint32_t m) { return (m >> 8) & 0xffu; }
+
+// Device copy of a loaded graph (all pointers are device memory).
+struct DeviceGraph {
+    int64_t n_ops = 0, n_colls = 0;
+    int32_t n_ranks = 0;
+    WalkItem *items = nullptr;       // walk lists, rank-major
+    int64_t *rank_off = nullptr;     // [n_ranks + 1] offsets into items
+    int32_t *far = nullptr;          // far predecessor op ids
+    // collectives
+    int64_t *c_bytes = nullptr;      // S
+    int64_t *c_chunk = nullptr;      // chunk size (Table 6)
+    int64_t *c_eta_ring = nullptr;   // ceil(S / (N * chunk))
+    int64_t *c_eta_chunks = nullptr; // ceil(S / chunk)
+    int32_t *c_N = nullptr, *c_M = nullptr, *c_K = nullptr;
+    uint8_t *c_type = nullptr;
+    // overlap detection: comm / compute ops of each (rank, stream), program order
+    int64_t *cl_off = nullptr;       // [n_ranks * 8 + 1]
+    int32_t *cl = nullptr;
+    uint8_t *cl_type = nullptr;      // collective type of each listed comm op
+    int64_t *cp_off = nullptr;       // [n_ranks * 8 + 1]
+    int32_t *cp = nullptr;
+    uint8_t *cp_class = nullptr;
+    unsigned *status = nullptr;      // device status word
+};
+
+struct WalkArgs {
+    const WalkItem *items;
+    const int64_t *rank_off;
+    const int32_t *far;
+    const int32_t *c_N;
+    const echo_scenario *scen;
+    const int64_t *cost;             // [coll][scen]
+    const uint32_t *factor;          // [op][scen] slowdown factors, or null (pass 1)
+    int64_t *start, *finish;         // [op][scen]
+    unsigned long long *arrive;      // [coll][scen] latest member launch
+    unsigned *count;                 // [coll][tile] members arrived
+    int64_t *step;                   // [scen]
+    uint64_t *digest;                // [scen] or null
+    unsigned *status;
+    int64_t spin_limit;              // wall-clock ticks (100 MHz) before a wait gives up
+    int32_t n_scen, n_tiles;
+    int32_t tile0, tiles;            // tiles handled by this launch
+    int32_t final_pass;              // accumulate step time (and digest)
+};
+
+struct OverlapArgs {
+    const int64_t *cl_off, *cp_off;
+    const int32_t *cl, *cp;
+    const uint8_t *cl_type, *cp_class;
+    const echo_scenario *scen;
+    const int64_t *start, *finish;
+    uint32_t *factor;
+    int32_t n_scen, n_tiles;
+};
+
+// Kernel launchers (echo_kernels.hip).  All enqueue on `stream`.
+hipError_t launch_init(const DeviceGraph &g, const echo_scenario *scen, int32_t n_scen,
+                       unsigned long long *arrive, int64_t n_arrive, unsigned *count,
+                       int64_t n_count, int64_t *step, uint64_t *digest, hipStream_t stream);
+hipError_t launch_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *count,
+                        int64_t n_count, hipStream_t stream);
+hipError_t launch_cc_cost(const DeviceGraph &g, const echo_scenario *scen, int32_t n_scen,
+                          int64_t *cost, hipStream_t stream);
+hipError_t launch_walk(const WalkArgs &a, int32_t n_ranks, hipStream_t stream);
+hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream);
+// Co-resident walk wavefronts the device can hold (one wavefront per block).
+hipError_t walk_capacity(int device, int64_t *waves);
+
+}  // namespace echo

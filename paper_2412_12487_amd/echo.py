@@ -1,0 +1,222 @@
+"""ctypes binding of libecho.so (argument marshalling only).
+
+Every step of the composer runs inside the library's HIP kernels; this module
+converts numpy graph arrays into an ``echo_graph_desc``, packs scenarios into
+``echo_scenario`` records, allocates output tensors with torch and passes
+their device pointers and the current HIP stream through the C ABI.
+There is no fallback: if libecho.so is missing, importing the library fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libecho.so")
+
+ECHO_OK, ECHO_ERR_ARG, ECHO_ERR_RANGE, ECHO_ERR_MATCH = 0, -1, -2, -3
+ECHO_ERR_CYCLE, ECHO_ERR_NOMEM, ECHO_ERR_HIP, ECHO_ERR_DEVICE = -4, -5, -6, -7
+ERROR_NAMES = {0: "OK", -1: "ARG", -2: "RANGE", -3: "MATCH", -4: "CYCLE", -5: "NOMEM", -6: "HIP",
+               -7: "DEVICE"}
+EXPORTS = ("echo_load_graph", "echo_graph_info", "echo_free_graph", "echo_cc_cost",
+           "echo_compose_batch", "echo_sync_status", "echo_set_timing", "echo_kernel_times",
+           "echo_last_error")
+KERNEL_KINDS = {0: "init", 1: "cc_cost", 2: "walk", 3: "overlap", 4: "clear"}
+
+# echo_scenario (include/echo.h): 192 bytes.
+SCENARIO_DTYPE = np.dtype({
+    "names": ["alpha_ns", "bw_intra_MBps", "bw_inter_MBps", "reduce_MBps", "jitter_seed",
+              "jitter_stream", "jitter_amp_q16", "ar_algo", "slowdown_q16"],
+    "formats": ["<i8", "<i8", "<i8", "<i8", "<u8", "<u4", "<i4", "u1", ("<u4", (8, 4))],
+    "offsets": [0, 8, 16, 24, 32, 40, 44, 48, 64],
+    "itemsize": 192,
+})
+
+
+class EchoError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"libecho error {code} ({ERROR_NAMES.get(code, '?')}): {msg}")
+        self.code = code
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [
+        ("n_ops", ctypes.c_int64), ("n_ranks", ctypes.c_int32), ("gpus_per_node", ctypes.c_int32),
+        ("op_rank", ctypes.c_void_p), ("op_stream", ctypes.c_void_p), ("op_kind", ctypes.c_void_p),
+        ("op_class", ctypes.c_void_p), ("op_dur_ns", ctypes.c_void_p), ("op_coll", ctypes.c_void_p),
+        ("pred_off", ctypes.c_void_p), ("pred_idx", ctypes.c_void_p), ("n_colls", ctypes.c_int64),
+        ("coll_type", ctypes.c_void_p), ("coll_bytes", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libecho.so.  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    L.echo_load_graph.argtypes = [ctypes.POINTER(_Desc), ctypes.c_int, ctypes.POINTER(P)]
+    L.echo_load_graph.restype = ctypes.c_int
+    L.echo_graph_info.argtypes = [P, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    L.echo_graph_info.restype = ctypes.c_int
+    L.echo_free_graph.argtypes = [P]
+    L.echo_free_graph.restype = None
+    L.echo_cc_cost.argtypes = [P, P, i32, P, P]
+    L.echo_cc_cost.restype = ctypes.c_int
+    L.echo_compose_batch.argtypes = [P, P, i32, i32, P, P, P, P, P]
+    L.echo_compose_batch.restype = ctypes.c_int
+    L.echo_sync_status.argtypes = [P, P]
+    L.echo_sync_status.restype = ctypes.c_int
+    L.echo_set_timing.argtypes = [P, ctypes.c_int]
+    L.echo_set_timing.restype = ctypes.c_int
+    L.echo_kernel_times.argtypes = [P, i32, P, P, ctypes.POINTER(i32)]
+    L.echo_kernel_times.restype = ctypes.c_int
+    L.echo_last_error.argtypes = []
+    L.echo_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _check(rc):
+    if rc != ECHO_OK:
+        raise EchoError(rc, lib().echo_last_error().decode(errors="replace"))
+
+
+def pack_scenarios(sc: dict) -> np.ndarray:
+    """Scenario dict (workloads.scenarios layout) -> array of echo_scenario records."""
+    n = int(np.asarray(sc["alpha_ns"]).shape[0])
+    rec = np.zeros(n, SCENARIO_DTYPE)
+    for k in ("alpha_ns", "bw_intra_MBps", "bw_inter_MBps", "reduce_MBps", "jitter_seed",
+              "jitter_amp_q16", "ar_algo"):
+        rec[k] = sc[k]
+    rec["jitter_stream"] = sc["jitter_stream"] if "jitter_stream" in sc else np.arange(n)
+    rec["slowdown_q16"] = np.asarray(sc["slowdown_q16"]).reshape(n, 8, 4)
+    return rec
+
+
+def scenarios_to_device(sc, device="cuda"):
+    """Upload scenarios (dict or packed records) as a uint8 tensor; returns (tensor, n)."""
+    import torch
+    rec = sc if isinstance(sc, np.ndarray) else pack_scenarios(sc)
+    t = torch.from_numpy(rec.view(np.uint8).copy()).to(device)
+    return t, int(rec.shape[0])
+
+
+def _stream_ptr(device):
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+class Graph:
+    """A loaded graph: validated, matched, levelled and resident on one GPU."""
+
+    def __init__(self, arrays: dict, device: int = 0):
+        L = lib()
+        self._keep = {
+            "op_rank": np.ascontiguousarray(arrays["op_rank"], np.int32),
+            "op_stream": np.ascontiguousarray(arrays["op_stream"], np.uint8),
+            "op_kind": np.ascontiguousarray(arrays["op_kind"], np.uint8),
+            "op_class": np.ascontiguousarray(arrays["op_class"], np.uint8),
+            "op_dur": np.ascontiguousarray(arrays["op_dur"], np.int64),
+            "op_coll": np.ascontiguousarray(arrays["op_coll"], np.int64),
+            "pred_off": np.ascontiguousarray(arrays["pred_off"], np.int64),
+            "pred_idx": np.ascontiguousarray(arrays["pred_idx"], np.int32),
+            "coll_type": np.ascontiguousarray(arrays["coll_type"], np.uint8),
+            "coll_bytes": np.ascontiguousarray(arrays["coll_bytes"], np.int64),
+        }
+        k = self._keep
+        n = k["op_rank"].shape[0]
+        if k["pred_off"].shape[0] != n + 1:
+            raise EchoError(ECHO_ERR_ARG, "pred_off must have n_ops + 1 entries")
+        ptr = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+        d = _Desc(n, int(arrays["n_ranks"]), int(arrays["gpus_per_node"]),
+                  ptr(k["op_rank"]), ptr(k["op_stream"]), ptr(k["op_kind"]), ptr(k["op_class"]),
+                  ptr(k["op_dur"]), ptr(k["op_coll"]), ptr(k["pred_off"]), ptr(k["pred_idx"]),
+                  k["coll_type"].shape[0], ptr(k["coll_type"]), ptr(k["coll_bytes"]))
+        h = ctypes.c_void_p()
+        _check(L.echo_load_graph(ctypes.byref(d), int(device), ctypes.byref(h)))
+        self._keep = None
+        self.handle = h
+        self.device = int(device)
+        a, b, c = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _check(L.echo_graph_info(h, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
+        self.n_ops, self.n_colls, self.n_levels = a.value, b.value, c.value
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().echo_free_graph(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    # ---------------------------------------------------------------- calls
+    def cc_cost(self, d_scen, n_scen, *, check=True):
+        """Collective costs [n_colls, n_scen] int64 (torch, on the graph's device)."""
+        import torch
+        dev = torch.device("cuda", self.device)
+        out = torch.empty((self.n_colls, n_scen), dtype=torch.int64, device=dev)
+        L = lib()
+        _check(L.echo_cc_cost(self.handle, ctypes.c_void_p(d_scen.data_ptr()), int(n_scen),
+                              ctypes.c_void_p(out.data_ptr()), _stream_ptr(dev)))
+        if check:
+            self.sync_status()
+        return out
+
+    def compose(self, d_scen, n_scen, n_refine=1, *, timelines=True, digest=False, out=None, check=True):
+        """Compose all scenarios.  Returns dict of torch tensors: 'step' [n_scen],
+        optional 'start'/'finish' [n_ops, n_scen] and 'digest' [n_scen] (uint64 bits
+        in an int64 tensor).  `out` may supply preallocated tensors of those names."""
+        import torch
+        dev = torch.device("cuda", self.device)
+        res = dict(out or {})
+        if "step" not in res:
+            res["step"] = torch.empty(n_scen, dtype=torch.int64, device=dev)
+        if timelines:
+            for k in ("start", "finish"):
+                if k not in res:
+                    res[k] = torch.empty((self.n_ops, n_scen), dtype=torch.int64, device=dev)
+        if digest and "digest" not in res:
+            res["digest"] = torch.empty(n_scen, dtype=torch.int64, device=dev)
+        p = lambda k: ctypes.c_void_p(res[k].data_ptr()) if k in res else ctypes.c_void_p(None)
+        _check(lib().echo_compose_batch(self.handle, ctypes.c_void_p(d_scen.data_ptr()), int(n_scen),
+                                        int(n_refine), p("start") if timelines else ctypes.c_void_p(None),
+                                        p("finish") if timelines else ctypes.c_void_p(None), p("step"),
+                                        p("digest") if digest else ctypes.c_void_p(None), _stream_ptr(dev)))
+        if check:
+            self.sync_status()
+        return res
+
+    def set_timing(self, enable=True):
+        _check(lib().echo_set_timing(self.handle, int(bool(enable))))
+
+    def kernel_times(self):
+        """[(kernel name, ms)] of the last compose call (timing must be on, stream finished)."""
+        n = ctypes.c_int32()
+        _check(lib().echo_kernel_times(self.handle, 0, None, None, ctypes.byref(n)))
+        kinds = np.zeros(max(n.value, 1), np.int32)
+        ms = np.zeros(max(n.value, 1), np.float32)
+        _check(lib().echo_kernel_times(self.handle, n.value, kinds.ctypes.data_as(ctypes.c_void_p),
+                                       ms.ctypes.data_as(ctypes.c_void_p), ctypes.byref(n)))
+        return [(KERNEL_KINDS[int(k)], float(t)) for k, t in zip(kinds[:n.value], ms[:n.value])]
+
+    def sync_status(self):
+        import torch
+        _check(lib().echo_sync_status(self.handle, _stream_ptr(torch.device("cuda", self.device))))

@@ -1,0 +1,279 @@
+"""Parity of the HIP composer with the CPU oracle, bit for bit (int64 ns, Q16).
+
+All calls go through the C ABI (libecho.so via the ctypes binding).  Small
+configurations compare every start/finish/step/digest; the full-size GPT-175B
+graphs compare sampled scenarios in full plus every step time the sample
+covers, in the same launch configuration the benchmark times.
+"""
+from __future__ import annotations
+
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from tests import tinygraph
+from tests.test_oracle_pins import _tiny_cases
+from tests.tinygraph import AG, AR, P2P, RS, Builder
+from workloads import configs, gpt1f1b, scenarios
+
+pytestmark = pytest.mark.gpu
+
+THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+@pytest.fixture(scope="module")
+def E():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2412_12487_amd as E
+    E.lib()      # fails loudly if libecho.so was not built
+    return E
+
+
+def gpu_run(E, g, sc, R, *, timelines=True, digest=True, graph=None):
+    G = graph or E.Graph(g, 0)
+    d, n = E.scenarios_to_device(sc)
+    out = G.compose(d, n, R, timelines=timelines, digest=digest)
+    res = {"step": out["step"].cpu().numpy()}
+    if digest:
+        res["digest"] = out["digest"].cpu().numpy().view(np.uint64)
+    if timelines:
+        res["start"] = out["start"].cpu().numpy()
+        res["finish"] = out["finish"].cpu().numpy()
+    if graph is None:
+        G.close()
+    return res
+
+
+def assert_same(gpu, ref, cols=None):
+    """gpu: [n_ops, n_scen] arrays; ref: oracle output [n_scen', n_ops] for scenarios `cols`."""
+    cols = list(range(ref["step"].shape[0])) if cols is None else list(cols)
+    np.testing.assert_array_equal(gpu["step"][cols], ref["step"])
+    if "digest" in gpu:
+        np.testing.assert_array_equal(gpu["digest"][cols], ref["digest"])
+    if "start" in gpu and "start" in ref:
+        for j, c in enumerate(cols):
+            np.testing.assert_array_equal(gpu["start"][:, c], ref["start"][j], err_msg=f"start, scenario {c}")
+            np.testing.assert_array_equal(gpu["finish"][:, c], ref["finish"][j], err_msg=f"finish, scenario {c}")
+
+
+# ---------------------------------------------------------------- small graphs, everything compared
+TINY = _tiny_cases()
+
+
+@pytest.mark.parametrize("name", sorted(TINY))
+@pytest.mark.parametrize("R", [0, 1, 2])
+def test_tiny_graphs(E, name, R):
+    g = TINY[name]
+    sc = scenarios.draw(3, np.random.default_rng(7), bw_inter=(20000, 90000), alpha=(0, 5000),
+                        ar_algo_random=True, slowdown=(65536, 140000))
+    assert_same(gpu_run(E, g, sc, R), oracle.run(g, sc, R))
+
+
+def _random_graph(rng, n_ranks, ops_per_rank, n_coll):
+    b = Builder(n_ranks, gpus_per_node=int(rng.integers(1, 5)))
+    colls = []
+    for _ in range(n_coll):
+        t = int(rng.integers(0, 4 if n_ranks > 1 else 3))
+        k = 2 if t == P2P else int(rng.integers(1, n_ranks + 1))
+        members = sorted(rng.choice(n_ranks, size=min(k, n_ranks), replace=False).tolist())
+        if t == P2P and len(members) < 2:
+            continue
+        colls.append((b.collective(t, int(rng.integers(0, 64 << 20))), members, int(rng.integers(1, 5))))
+    # every rank issues its collectives in collective-id order on a per-collective stream
+    for r in range(n_ranks):
+        ids = []
+        mine = [(c, s) for c, m, s in colls if r in m]
+        for k in range(ops_per_rank):
+            preds = [int(u) for u in ids[-6:] if rng.random() < 0.25]
+            if mine and rng.random() < 0.3:
+                c, s = mine.pop(0)
+                ids.append(b.comm(r, c, stream=s, preds=preds))
+            elif rng.random() < 0.1:
+                ids.append(b.op(r, stream=5, kind=2, dur=int(rng.integers(0, 4000)), preds=preds))
+            else:
+                ids.append(b.compute(r, int(rng.integers(0, 90000)), stream=int(rng.integers(0, 2)) * 6,
+                                     cls=int(rng.integers(0, 8)), preds=preds))
+        for c, s in mine:
+            b.comm(r, c, stream=s, preds=ids[-1:])
+    return b.graph()
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_graphs(E, seed):
+    rng = np.random.default_rng(1000 + seed)
+    g = _random_graph(rng, int(rng.integers(1, 17)), int(rng.integers(5, 60)), int(rng.integers(0, 30)))
+    n = [1, 5, 64, 70, 130][seed % 5]
+    sc = scenarios.draw(n, rng, bw_inter=(20000, 400000), bw_intra=(50000, 400000), alpha=(0, 20000),
+                        ar_algo_random=True, slowdown=(65536, 150000),
+                        jitter=(int(rng.integers(0, 20000)), int(seed)) if seed % 2 else None)
+    try:
+        ref = {R: oracle.run(g, sc, R, threads=THREADS) for R in (0, 1, 2)}
+    except oracle.OracleError as e:      # generator made a deadlock: the library must agree
+        assert e.code == -4
+        with pytest.raises(E.EchoError) as x:
+            E.Graph(g, 0)
+        assert x.value.code in (E.ECHO_ERR_CYCLE, E.ECHO_ERR_MATCH)
+        return
+    G = E.Graph(g, 0)
+    for R in (0, 1, 2):
+        assert_same(gpu_run(E, g, sc, R, graph=G), ref[R])
+    G.close()
+
+
+def test_1f1b_pipeline_closed_form(E):
+    g = tinygraph.pipeline_1f1b(8, 16, 1000, 2100)
+    sc = scenarios.default_scenarios(2)
+    sc["alpha_ns"][:] = 0
+    res = gpu_run(E, g, sc, 1)
+    assert (res["step"] == (16 + 8 - 1) * 3100).all()
+
+
+# ---------------------------------------------------------------- benchmark configurations
+@pytest.mark.parametrize("R", [0, 1, 2])
+def test_config1_tiny(E, R):
+    g, sc = configs.graph(1), configs.scenario_batch(1)
+    assert_same(gpu_run(E, g, sc, R), oracle.run(g, sc, R))
+
+
+def test_config4_enumeration_4096(E):
+    g, sc = configs.graph(4), configs.scenario_batch(4)
+    assert_same(gpu_run(E, g, sc, 1), oracle.run(g, sc, 1, threads=THREADS))
+
+
+def test_config2_gpt175b_96ranks(E):
+    g, sc = configs.graph(2), configs.scenario_batch(2)
+    ref = oracle.run(g, sc, 1, threads=THREADS)
+    assert_same(gpu_run(E, g, sc, 1), ref)
+
+
+def _sampled(E, g, sc, R, cols):
+    """Compose every scenario on the GPU; compare the sampled columns in full."""
+    import torch
+    G = E.Graph(g, 0)
+    d, n = E.scenarios_to_device(sc)
+    out = G.compose(d, n, R, timelines=True, digest=True)
+    idx = torch.tensor(cols, device=out["start"].device)
+    gpu = {"step": out["step"].cpu().numpy(), "digest": out["digest"].cpu().numpy().view(np.uint64),
+           "start": out["start"].index_select(1, idx).cpu().numpy(),
+           "finish": out["finish"].index_select(1, idx).cpu().numpy()}
+    del out
+    G.close()
+    ref = oracle.run(g, scenarios.take(sc, cols), R, threads=min(THREADS, len(cols)))
+    np.testing.assert_array_equal(gpu["step"][cols], ref["step"])
+    np.testing.assert_array_equal(gpu["digest"][cols], ref["digest"])
+    for j, c in enumerate(cols):
+        np.testing.assert_array_equal(gpu["start"][:, j], ref["start"][j], err_msg=f"start, scenario {c}")
+        np.testing.assert_array_equal(gpu["finish"][:, j], ref["finish"][j], err_msg=f"finish, scenario {c}")
+    return gpu
+
+
+def test_config3_gpt175b_1024ranks_sampled(E):
+    g, sc = configs.graph(3), configs.scenario_batch(3)
+    n = scenarios.count(sc)
+    cols = sorted({0, n - 1, *np.random.default_rng(3).choice(n, 2, replace=False).tolist()})
+    gpu = _sampled(E, g, sc, 1, cols)
+    assert (gpu["step"] > 0).all()
+
+
+@pytest.mark.parametrize("index", [0, 3] if not os.environ.get("ECHO_FULL") else list(range(16)))
+def test_config5_extrapolation_sampled(E, index):
+    g, sc = configs.graph(5, index), configs.scenario_batch(5, index)
+    _sampled(E, g, sc, 1, [0, scenarios.count(sc) - 1])
+
+
+# ---------------------------------------------------------------- properties and edge cases
+def test_batch_invariance(E):
+    """A scenario composes to the same timeline alone or inside a wide batch."""
+    g = configs.graph(1)
+    sc = scenarios.draw(200, np.random.default_rng(9), bw_inter=(50000, 400000), slowdown=(65536, 91750),
+                        jitter=(6554, 3), ar_algo_random=True)
+    full = gpu_run(E, g, sc, 1)
+    for cols in ([0], [199], [63, 64, 65], list(range(120, 200))):
+        part = gpu_run(E, g, scenarios.take(sc, cols), 1)
+        for j, c in enumerate(cols):
+            np.testing.assert_array_equal(part["finish"][:, j], full["finish"][:, c])
+            assert part["digest"][j] == full["digest"][c]
+
+
+@pytest.mark.parametrize("n", [1, 63, 65, 127])
+def test_ragged_scenario_counts(E, n):
+    g = configs.graph(1)
+    sc = scenarios.take(configs.scenario_batch(4), slice(0, n))
+    assert_same(gpu_run(E, g, sc, 1), oracle.run(g, sc, 1, threads=THREADS))
+
+
+def test_outputs_without_timelines(E):
+    g = configs.graph(1)
+    sc = scenarios.take(configs.scenario_batch(4), slice(0, 100))
+    a = gpu_run(E, g, sc, 1, timelines=False)
+    ref = oracle.run(g, sc, 1, threads=THREADS, timelines=False)
+    np.testing.assert_array_equal(a["step"], ref["step"])
+    np.testing.assert_array_equal(a["digest"], ref["digest"])
+
+
+def test_cc_costs_match_oracle(E):
+    for cfg in (2, 4):
+        g, sc = configs.graph(cfg), configs.scenario_batch(cfg)
+        sc = scenarios.take(sc, slice(0, 64))
+        G = E.Graph(g, 0)
+        d, n = E.scenarios_to_device(sc)
+        cost = G.cc_cost(d, n).cpu().numpy()
+        G.close()
+        ref = oracle.run(g, sc, 0, threads=THREADS, timelines=False, costs=True)
+        np.testing.assert_array_equal(cost.T, ref["cost"])
+
+
+def test_graph_without_ops(E):
+    g = Builder(4).graph()
+    res = gpu_run(E, g, scenarios.default_scenarios(3), 1)
+    assert (res["step"] == 0).all()
+
+
+def test_single_member_collectives_and_empty_ranks(E):
+    b = Builder(5, gpus_per_node=2)
+    c = b.collective(AR, 5 << 20)
+    d = b.collective(AG, 0)
+    w = b.compute(1, 400)
+    v = b.comm(1, c, preds=[w])
+    b.compute(1, 30, preds=[v])
+    b.comm(3, d)
+    b.compute(3, 7)
+    g = b.graph()
+    sc = scenarios.default_scenarios(2)
+    assert_same(gpu_run(E, g, sc, 1), oracle.run(g, sc, 1))
+
+
+def test_out_of_range_scenario_reported(E):
+    g = configs.graph(1)
+    sc = scenarios.default_scenarios(4)
+    sc["bw_inter_MBps"][2] = 0
+    G = E.Graph(g, 0)
+    d, n = E.scenarios_to_device(sc)
+    with pytest.raises(E.EchoError) as x:
+        G.compose(d, n, 1)
+    assert x.value.code == E.ECHO_ERR_RANGE
+    sc["bw_inter_MBps"][2] = 1000          # the graph stays usable afterwards
+    d, n = E.scenarios_to_device(sc)
+    G.compose(d, n, 1)
+    G.close()
+
+
+def test_time_limit_reported(E):
+    big = (1 << 50) - 1
+    b = Builder(2)
+    c1, c2 = b.collective(AR, big), b.collective(AR, big)
+    for r in range(2):
+        b.comm(r, c1)
+        b.comm(r, c2)
+    sc = scenarios.default_scenarios(1)
+    for k in ("bw_intra_MBps", "bw_inter_MBps", "reduce_MBps"):
+        sc[k][:] = 1
+    G = E.Graph(b.graph(), 0)
+    d, n = E.scenarios_to_device(sc)
+    with pytest.raises(E.EchoError) as x:
+        G.compose(d, n, 0)
+    assert x.value.code == E.ECHO_ERR_RANGE
+    G.close()

@@ -10,6 +10,8 @@ a dict of numpy arrays, one entry per field (structure of arrays):
     bw_inter_MBps  int64  [n]        inter-server bandwidth per GPU (MB/s)
     reduce_MBps    int64  [n]        reduction throughput of the collective kernel (MB/s)
     jitter_seed    uint64 [n]        seed of the per-op duration jitter stream
+    jitter_stream  uint32 [n]        which SplitMix64 sub-stream the scenario draws from
+                                     (its index in the batch it was drawn in)
     jitter_amp_q16 int32  [n]        jitter amplitude A in Q16 (0 = no jitter)
     ar_algo        uint8  [n]        all-reduce algorithm: 0 ring, 1 tree
     slowdown_q16   uint32 [n, 8, 4]  slowdown factor per (kernel class, collective type), Q16
@@ -46,7 +48,7 @@ DEFAULTS = dict(
 )
 
 FIELDS = ("alpha_ns", "bw_intra_MBps", "bw_inter_MBps", "reduce_MBps",
-          "jitter_seed", "jitter_amp_q16", "ar_algo", "slowdown_q16")
+          "jitter_seed", "jitter_stream", "jitter_amp_q16", "ar_algo", "slowdown_q16")
 
 
 def default_scenarios(n: int) -> dict:
@@ -57,6 +59,7 @@ def default_scenarios(n: int) -> dict:
         "bw_inter_MBps": np.full(n, DEFAULTS["bw_inter_MBps"], np.int64),
         "reduce_MBps": np.full(n, DEFAULTS["reduce_MBps"], np.int64),
         "jitter_seed": np.zeros(n, np.uint64),
+        "jitter_stream": np.arange(n, dtype=np.uint32),
         "jitter_amp_q16": np.zeros(n, np.int32),
         "ar_algo": np.full(n, RING, np.uint8),
         "slowdown_q16": np.broadcast_to(PAPER_SLOWDOWN_Q16[None, :, None], (n, 8, 4)).copy(),
