@@ -354,7 +354,15 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
     std::vector<int32_t> far;
     {
         std::vector<int32_t> latest(kStreams);
+        std::vector<int64_t> busy(kStreams);
+        int slot[kStreams];
         for (int64_t r = 0; r < R; ++r) {
+            // slot 0 = the stream with the most compute/memcpy ops; the rest keep their order
+            std::fill(busy.begin(), busy.end(), 0);
+            for (int64_t i = rank_off[r]; i < rank_off[r + 1]; ++i)
+                if (d->op_kind[i] != ECHO_COMM) ++busy[d->op_stream[i]];
+            const int top = int(std::max_element(busy.begin(), busy.end()) - busy.begin());
+            for (int k = 0, next = 1; k < kStreams; ++k) slot[k] = k == top ? 0 : next++;
             std::fill(latest.begin(), latest.end(), -1);
             for (int64_t i = rank_off[r]; i < rank_off[r + 1]; ++i) {
                 const int32_t v = order[i];
@@ -362,18 +370,23 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
                 const int64_t f0 = (int64_t)far.size();
                 for (int32_t j = poff[v]; j < poff[v + 1]; ++j) {
                     const int32_t u = preds[j];
-                    if (latest[d->op_stream[u]] == u) mask |= 1u << d->op_stream[u];
+                    const int su = slot[d->op_stream[u]];
+                    if (latest[su] == u) mask |= 1u << su;
                     else far.push_back(u);
                 }
-                latest[d->op_stream[v]] = v;
+                const int sv = slot[d->op_stream[v]];
+                const int32_t prev = latest[sv];
+                latest[sv] = v;
+                const bool fast = d->op_kind[v] != ECHO_COMM && sv == 0 && (mask & ~1u) == 0 &&
+                                  (int64_t)far.size() == f0 && (prev < 0 || d->op_kind[prev] != ECHO_COMM);
                 WalkItem &it = items[i];
                 it.op = v;
-                it.meta = (uint32_t)d->op_kind[v] | ((uint32_t)d->op_stream[v] << 2) |
-                          ((uint32_t)d->op_class[v] << 5) | (mask << 8);
+                it.meta = (uint32_t)d->op_kind[v] | ((uint32_t)sv << 2) | ((uint32_t)d->op_class[v] << 5) |
+                          (mask << 8) | (fast ? kFast : 0u);
                 it.nfar = (int32_t)((int64_t)far.size() - f0);
                 it.far_off = (int32_t)f0;
                 it.coll = d->op_kind[v] == ECHO_COMM ? (int32_t)d->op_coll[v] : -1;
-                it.pad = 0;
+                it.aux = 0;
                 it.dur = d->op_kind[v] == ECHO_COMM ? 0 : d->op_dur_ns[v];
             }
         }
@@ -390,18 +403,25 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
         cl_off[k + 1] += cl_off[k];
         cp_off[k + 1] += cp_off[k];
     }
-    std::vector<int32_t> cl(cl_off.back()), cp(cp_off.back());
-    std::vector<uint8_t> cl_type(cl_off.back()), cp_class(cp_off.back());
+    std::vector<int32_t> cl(cl_off.back());
+    std::vector<uint8_t> cl_type(cl_off.back());
+    std::vector<ComputeRec> cp(cp_off.back());
     {
         std::vector<int64_t> fl(cl_off.begin(), cl_off.end() - 1), fp(cp_off.begin(), cp_off.end() - 1);
+        std::vector<int32_t> prev_on_stream(R * kStreams, -1);
         for (int64_t v = 0; v < n; ++v) {
             const int64_t k = (int64_t)d->op_rank[v] * kStreams + d->op_stream[v];
+            const int32_t prev = prev_on_stream[k];
+            prev_on_stream[k] = (int32_t)v;
             if (d->op_kind[v] == ECHO_COMM) {
                 cl_type[fl[k]] = d->coll_type[d->op_coll[v]];
                 cl[fl[k]++] = (int32_t)v;
             } else if (d->op_kind[v] == ECHO_COMPUTE) {
-                cp_class[fp[k]] = d->op_class[v];
-                cp[fp[k]++] = (int32_t)v;
+                // chained: the only predecessor is the previous op of the stream, a compute op
+                const bool chained = prev >= 0 && d->op_kind[prev] == ECHO_COMPUTE && poff[v + 1] - poff[v] == 1 &&
+                                     preds[poff[v]] == prev;
+                cp[fp[k]++] = ComputeRec{(int32_t)v, (uint32_t)d->op_class[v] | (chained ? kChained : 0u),
+                                         d->op_dur_ns[v]};
             }
         }
     }
@@ -459,7 +479,6 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
     UP(dg.cl_type, cl_type);
     UP(dg.cp_off, cp_off);
     UP(dg.cp, cp);
-    UP(dg.cp_class, cp_class);
     UP(dg.status, std::vector<unsigned>(1, 0u));
 #undef UP
     e = walk_capacity(device, &g->capacity);
@@ -516,8 +535,8 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
     const int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, g->capacity / g->n_ranks));
     for (int32_t p = 0; p <= n_refine; ++p) {
         if (p > 0) {
-            OverlapArgs o{g->dg.cl_off, g->dg.cp_off, g->dg.cl, g->dg.cp, g->dg.cl_type, g->dg.cp_class,
-                          d_scen, start, finish, g->factor, n_scen, n_tiles};
+            OverlapArgs o{g->dg.cl_off, g->dg.cp_off, g->dg.cl, g->dg.cl_type, g->dg.cp,
+                          d_scen, start, finish, g->factor, n_scen, n_tiles, p > 1};
             TIMED(ECHO_K_OVERLAP, launch_overlap(o, g->n_ranks, stream), "overlap kernel");
             TIMED(ECHO_K_CLEAR, launch_clear(g->arrive, n_arrive, g->count, n_count, stream), "clear kernel");
         }

@@ -29,22 +29,39 @@ constexpr unsigned kStatusOverflow = 2u;         // a time reached 2^62
 constexpr unsigned kStatusTimeout = 4u;          // a barrier wait exceeded the spin limit
 constexpr unsigned kStatusAbort = 8u;            // stop all waits (set with timeout)
 
-// One entry of a rank's walk list (32 bytes, read wave-uniformly).
+// One entry of a rank's walk list (32 bytes, read wave-uniformly).  Streams
+// are renumbered per rank into "slots": slot 0 is the rank's busiest
+// compute/memcpy stream, so most items only touch slot 0.
 struct WalkItem {
     int32_t op;         // op id: row of the [op][scenario] outputs
-    uint32_t meta;      // kind | stream << 2 | class << 5 | regmask << 8
-    int32_t nfar;       // predecessors read back from memory ...
-    int32_t far_off;    // ... listed at far[far_off .. far_off + nfar)
+    uint32_t meta;      // kind | slot << 2 | class << 5 | regmask << 8 | fast << 16
+    int32_t far_off;    // predecessors read back from memory: far[far_off .. +nfar)
     int32_t coll;       // collective of a comm op, -1 otherwise
-    int32_t pad;
     int64_t dur;        // base duration of compute / memcpy ops
+    int32_t nfar;
+    int32_t aux;
 };
 static_assert(sizeof(WalkItem) == 32, "walk item must stay 32 bytes");
+
+// A "fast" item is a compute/memcpy op on slot 0 whose only predecessor is
+// the previous op of slot 0, itself not a comm op: its start is that op's finish.
+constexpr uint32_t kFast = 1u << 16;
 
 __host__ __device__ inline int item_kind(uint32_t m) { return int(m & 3u); }
 __host__ __device__ inline int item_stream(uint32_t m) { return int((m >> 2) & 7u); }
 __host__ __device__ inline int item_class(uint32_t m) { return int((m >> 5) & 7u); }
 __host__ __device__ inline unsigned item_regmask(uint32_t m) { return (m >> 8) & 0xffu; }
+
+// Compute op of a (rank, stream) list for overlap detection (16 bytes).
+struct ComputeRec {
+    int32_t op;
+    uint32_t meta;      // class | kChained
+    int64_t dur;        // base duration
+};
+static_assert(sizeof(ComputeRec) == 16, "compute record must stay 16 bytes");
+// Compute op whose only predecessor is the previous compute op of its stream:
+// it starts exactly when that op finishes.
+constexpr uint32_t kChained = 0x80;
 
 // Device copy of a loaded graph (all pointers are device memory).
 struct DeviceGraph {
@@ -65,8 +82,7 @@ struct DeviceGraph {
     int32_t *cl = nullptr;
     uint8_t *cl_type = nullptr;      // collective type of each listed comm op
     int64_t *cp_off = nullptr;       // [n_ranks * 8 + 1]
-    int32_t *cp = nullptr;
-    uint8_t *cp_class = nullptr;
+    ComputeRec *cp = nullptr;
     unsigned *status = nullptr;      // device status word
 };
 
@@ -90,14 +106,17 @@ struct WalkArgs {
     int32_t final_pass;              // accumulate step time (and digest)
 };
 
+
 struct OverlapArgs {
     const int64_t *cl_off, *cp_off;
-    const int32_t *cl, *cp;
-    const uint8_t *cl_type, *cp_class;
+    const int32_t *cl;
+    const uint8_t *cl_type;
+    const ComputeRec *cp;
     const echo_scenario *scen;
     const int64_t *start, *finish;
-    uint32_t *factor;
+    uint32_t *factor;                // in: factors of the previous pass (if it was refined), out: new ones
     int32_t n_scen, n_tiles;
+    int32_t prev_refined;            // the previous pass inflated its compute ops by `factor`
 };
 
 // Kernel launchers (echo_kernels.hip).  All enqueue on `stream`.

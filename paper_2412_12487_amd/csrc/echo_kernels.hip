@@ -11,6 +11,8 @@
 //
 // Everything is int64 nanoseconds and Q16 factors, bit-exact by construction:
 // max, add, 64-bit multiply and shifts only (no floating point on the path).
+#include <algorithm>
+
 #include "echo_internal.h"
 
 namespace echo {
@@ -21,6 +23,8 @@ constexpr uint64_t kMixA = 0xBF58476D1CE4E5B9ull;    // SplitMix64 output functi
 constexpr uint64_t kMixB = 0x94D049BB133111EBull;
 constexpr int64_t kKnobLimit = int64_t(1) << 40;
 constexpr int64_t kInf = INT64_MAX;
+// s_waitcnt immediate for "vmcnt(0)" on gfx9-family targets (expcnt and lgkmcnt left at their maxima)
+constexpr int kWaitVm0 = 0x0F70;
 
 __device__ __forceinline__ uint64_t mix64(uint64_t z) {
     z = (z ^ (z >> 30)) * kMixA;
@@ -152,24 +156,34 @@ __device__ bool wait_arrivals(const unsigned *cnt, unsigned need, unsigned *stat
     }
 }
 
+constexpr int kBlock = 32;   // walk items fetched (and factors staged) per round
+
+// One wavefront walks one rank's list for one 64-scenario tile.  REFINED: the
+// pass inflates compute ops by the factors of the previous pass's overlaps.
+// FINAL: the pass produces the step time (and DIGEST: the timeline digest).
+template <bool REFINED, bool FINAL, bool DIGEST>
 __global__ __launch_bounds__(64) void k_walk(WalkArgs a) {
+    __shared__ uint32_t fstage[REFINED ? kBlock * kLanes : 1];
     const int lane = threadIdx.x;
     const int32_t r = blockIdx.x / a.tiles;
     const int32_t tile = a.tile0 + blockIdx.x % a.tiles;
     const int32_t sig0 = tile * kLanes + lane;
     const bool active = sig0 < a.n_scen;
-    const int32_t sigma = active ? sig0 : a.n_scen - 1;   // idle lanes mirror the last scenario
+    // Idle lanes of the last tile mirror its last scenario: they compute the same
+    // values and store them to the same places; only active lanes issue atomics.
+    const int32_t col = active ? lane : a.n_scen - 1 - tile * kLanes;
+    const bool mirror = (tile + 1) * kLanes > a.n_scen;
+    const int32_t sigma = tile * kLanes + col;
     const int64_t ns = a.n_scen;
     const echo_scenario *sc = a.scen + sigma;
     const uint64_t jseed = sc->jitter_seed;
     const uint32_t jstream = sc->jitter_stream;
     const int32_t amp = sc->jitter_amp_q16;
-    const bool use_factor = a.factor != nullptr;
-    const bool final_pass = a.final_pass != 0;
-    const bool want_digest = final_pass && a.digest != nullptr;
+    int64_t *const sbase = a.start + (int64_t)tile * kLanes;    // row v of tile: sbase + v * ns
+    int64_t *const fbase = a.finish + (int64_t)tile * kLanes;
     const unsigned *tile_count = a.count + tile;
 
-    // Per stream: finish of the latest op, or a comm op still waiting for its barrier.
+    // Per slot: finish of the latest op, or a comm op still waiting for its barrier.
     int64_t lf[kStreams], ps[kStreams];
     int32_t pc[kStreams], pv[kStreams];
 #pragma unroll
@@ -179,56 +193,74 @@ __global__ __launch_bounds__(64) void k_walk(WalkArgs a) {
         pc[j] = -1;
         pv[j] = 0;
     }
-    int64_t smax = 0;
     uint64_t dig = 0;
+    uint32_t hi_or = 0;          // OR of the high words of every time: bit 30 set <=> some time >= 2^62
     unsigned err = 0;
     const int64_t beg = a.rank_off[r], end = a.rank_off[r + 1];
+    // lane j < 32 holds the first half of item j of the round, lane 32 + j its second half
     const int4 *items4 = reinterpret_cast<const int4 *>(a.items);
-    int4 nlo = make_int4(0, 0, 0, 0), nhi = nlo;
-    if (beg + lane < end) {
-        nlo = items4[2 * (beg + lane)];
-        nhi = items4[2 * (beg + lane) + 1];
-    }
+    const int half = lane >> 5, slotl = lane & 31;
+    // lanes past the end of the list hold op 0, so staged factor loads stay in bounds
+    int4 nxt = beg + slotl < end ? items4[2 * (beg + slotl) + half] : make_int4(0, 0, 0, 0);
 
-// Finish of the comm op pending on stream j: barrier (latest member launch) + cost.
+// Finish of the comm op pending on slot j: barrier (latest member launch) + cost.
 #define RESOLVE(j)                                                                               \
     if (pc[j] >= 0) {                                                                            \
         const int64_t c_ = pc[j];                                                                \
         if (!wait_arrivals(tile_count + c_ * a.n_tiles, (unsigned)a.c_N[c_], a.status,           \
                            a.spin_limit))                                                        \
             goto out;                                                                            \
-        const uint64_t b_ = __hip_atomic_fetch_max(a.arrive + c_ * ns + sigma, 0ull,             \
-                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  \
+        uint64_t b_ = 0;                                                                         \
+        if (active)                                                                              \
+            b_ = __hip_atomic_fetch_max(a.arrive + c_ * ns + sigma, 0ull, __ATOMIC_RELAXED,      \
+                                        __HIP_MEMORY_SCOPE_AGENT);                               \
+        b_ = mirror ? (uint64_t)__shfl((long long)b_, col) : b_;                                 \
         const int64_t f_ = (int64_t)b_ + a.cost[c_ * ns + sigma];                                \
-        err |= f_ >= kTimeLimit ? kStatusOverflow : 0u;                                          \
-        if (active) a.finish[(int64_t)pv[j] * ns + sigma] = f_;                                  \
-        if (final_pass) {                                                                        \
-            smax = f_ > smax ? f_ : smax;                                                        \
-            if (want_digest) dig += mix64(mix64((uint64_t)pv[j] ^ (uint64_t)ps[j]) ^ (uint64_t)f_); \
-        }                                                                                        \
+        hi_or |= (uint32_t)((uint64_t)f_ >> 32);                                                 \
+        (fbase + (int64_t)pv[j] * ns)[col] = f_;                                                 \
+        if (DIGEST) dig += mix64(mix64((uint64_t)pv[j] ^ (uint64_t)ps[j]) ^ (uint64_t)f_);       \
         lf[j] = f_;                                                                              \
         pc[j] = -1;                                                                              \
     }
 
-    for (int64_t blk = beg; blk < end; blk += kLanes) {
-        // lane j holds item blk + j; the next block is fetched while this one runs
-        const int4 clo = nlo, chi = nhi;
-        if (blk + kLanes + lane < end) {
-            nlo = items4[2 * (blk + kLanes + lane)];
-            nhi = items4[2 * (blk + kLanes + lane) + 1];
+    for (int64_t blk = beg; blk < end; blk += kBlock) {
+        const int4 cur = nxt;
+        const int nb = end - blk < kBlock ? int(end - blk) : kBlock;
+        nxt = blk + kBlock + slotl < end ? items4[2 * (blk + kBlock + slotl) + half] : make_int4(0, 0, 0, 0);
+        if (REFINED) {
+            // stage this round's slowdown factors: one load per item, one wait per round
+            uint32_t fv[kBlock];
+#pragma unroll
+            for (int j = 0; j < kBlock; ++j) {
+                const int32_t opj = __builtin_amdgcn_readlane(cur.x, j);
+                fv[j] = a.factor[(int64_t)opj * ns + sigma];
+            }
+#pragma unroll
+            for (int j = 0; j < kBlock; ++j) fstage[j * kLanes + lane] = fv[j];
         }
-        const int nb = end - blk < kLanes ? int(end - blk) : kLanes;
         for (int j = 0; j < nb; ++j) {
-            const int32_t op = __builtin_amdgcn_readlane(clo.x, j);
-            const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(clo.y, j);
-            const int32_t nfar = __builtin_amdgcn_readlane(clo.z, j);
-            const int32_t far_off = __builtin_amdgcn_readlane(clo.w, j);
-            const int32_t coll = __builtin_amdgcn_readlane(chi.x, j);
-            const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(chi.w, j) << 32) |
-                                          (uint32_t)__builtin_amdgcn_readlane(chi.z, j));
-            const int kind = item_kind(meta), st = item_stream(meta);
+            const int32_t op = __builtin_amdgcn_readlane(cur.x, j);
+            const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);
+            const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) |
+                                          (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32));
+            const int kind = item_kind(meta);
+            if (meta & kFast) {
+                // compute/memcpy op right after the previous op of slot 0
+                int64_t d = amp != 0 ? jittered(dur, op, jseed, jstream, amp) : dur;
+                if (REFINED && kind == ECHO_COMPUTE) d = q16(d, fstage[j * kLanes + lane]);
+                const int64_t s0 = lf[0], f = s0 + d;
+                (sbase + (int64_t)op * ns)[col] = s0;
+                (fbase + (int64_t)op * ns)[col] = f;
+                hi_or |= (uint32_t)((uint64_t)f >> 32);
+                if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)s0) ^ (uint64_t)f);
+                lf[0] = f;
+                continue;
+            }
+            const int32_t far_off = __builtin_amdgcn_readlane(cur.z, j);
+            const int32_t coll = __builtin_amdgcn_readlane(cur.w, j);
+            const int32_t nfar = __builtin_amdgcn_readlane(cur.z, j + 32);
+            const int st = item_stream(meta);
             const unsigned mask = item_regmask(meta);
-
             int64_t ready = 0;
 #pragma unroll
             for (int q = 0; q < kStreams; ++q) {
@@ -239,18 +271,15 @@ __global__ __launch_bounds__(64) void k_walk(WalkArgs a) {
             }
             for (int32_t q = 0; q < nfar; ++q) {
                 const int64_t u = a.far[far_off + q];
-                const int64_t fu = a.finish[u * ns + sigma];
+                const int64_t fu = (fbase + u * ns)[col];
                 ready = fu > ready ? fu : ready;
             }
-            const int64_t row = (int64_t)op * ns + sigma;
+            (sbase + (int64_t)op * ns)[col] = ready;
             if (kind == ECHO_COMM) {
                 // launch: publish this member's launch time, then count the arrival
-                if (active) {
-                    a.start[row] = ready;
-                    __hip_atomic_fetch_max(a.arrive + (int64_t)coll * ns + sigma,
-                                           (unsigned long long)ready, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-                }
+                if (active)
+                    __hip_atomic_fetch_max(a.arrive + (int64_t)coll * ns + sigma, (unsigned long long)ready,
+                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
                 if (lane == 0)
                     __hip_atomic_fetch_add(a.count + (int64_t)coll * a.n_tiles + tile, 1u,
@@ -264,54 +293,96 @@ __global__ __launch_bounds__(64) void k_walk(WalkArgs a) {
                     }
             } else {
                 int64_t d = amp != 0 ? jittered(dur, op, jseed, jstream, amp) : dur;
-                if (use_factor && kind == ECHO_COMPUTE) d = q16(d, a.factor[row]);
+                if (REFINED && kind == ECHO_COMPUTE) d = q16(d, fstage[j * kLanes + lane]);
                 const int64_t f = ready + d;
-                err |= f >= kTimeLimit ? kStatusOverflow : 0u;
-                if (active) {
-                    a.start[row] = ready;
-                    a.finish[row] = f;
-                }
+                hi_or |= (uint32_t)((uint64_t)f >> 32);
+                (fbase + (int64_t)op * ns)[col] = f;
+                if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)ready) ^ (uint64_t)f);
 #pragma unroll
                 for (int q = 0; q < kStreams; ++q)
                     if (q == st) lf[q] = f;
-                if (final_pass) {
-                    smax = f > smax ? f : smax;
-                    if (want_digest) dig += mix64(mix64((uint64_t)op ^ (uint64_t)ready) ^ (uint64_t)f);
-                }
             }
         }
     }
 #pragma unroll
     for (int q = 0; q < kStreams; ++q) { RESOLVE(q) }
 #undef RESOLVE
-out:
-    if (active) {
-        if (err) __hip_atomic_fetch_or(a.status, err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (final_pass) {
-            __hip_atomic_fetch_max(reinterpret_cast<unsigned long long *>(a.step) + sigma,
-                                   (unsigned long long)smax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (want_digest)
-                __hip_atomic_fetch_add(reinterpret_cast<unsigned long long *>(a.digest) + sigma,
-                                       (unsigned long long)dig, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
+    if (hi_or >> 30) err |= kStatusOverflow;
+    if (active && err) __hip_atomic_fetch_or(a.status, err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (FINAL && active) {
+        // finishes along a FIFO stream never decrease: the last op of each slot holds its maximum
+        int64_t smax = 0;
+#pragma unroll
+        for (int q = 0; q < kStreams; ++q) smax = lf[q] > smax ? lf[q] : smax;
+        __hip_atomic_fetch_max(reinterpret_cast<unsigned long long *>(a.step) + sigma, (unsigned long long)smax,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (DIGEST)
+            __hip_atomic_fetch_add(reinterpret_cast<unsigned long long *>(a.digest) + sigma,
+                                   (unsigned long long)dig, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    return;
+out:
+    if (active && err) __hip_atomic_fetch_or(a.status, err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+using WalkKernel = void (*)(WalkArgs);
+WalkKernel walk_kernel(bool refined, bool final_pass, bool digest) {
+    if (!final_pass) return refined ? k_walk<true, false, false> : k_walk<false, false, false>;
+    if (digest) return refined ? k_walk<true, true, true> : k_walk<false, true, true>;
+    return refined ? k_walk<true, true, false> : k_walk<false, true, false>;
 }
 
 // ------------------------------------------------------------------ overlap detection
 // One wavefront per (rank, tile).  Compute ops of one stream run back to back,
 // and so do the comm ops of one stream, so for each comm stream a cursor that
 // only moves forward finds every comm op overlapping the current compute op.
+// After compute op v the cursor of each comm stream sits on the first comm op
+// that ends after v started; for the next compute op v', "that comm op starts
+// at or after v' ends" proves both "no overlap" and "cursor stays" -- one
+// compare per comm stream in the common case.  A compute op's interval is
+// rebuilt rather than read: a chained op starts where the previous compute op
+// of its stream finished, and every finish is start + base duration (the same
+// jitter draw as the composer pass, inflated by the factor that pass used);
+// only unchained ops read their start.
 __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     const int lane = threadIdx.x;
     const int32_t r = blockIdx.x / a.n_tiles;
     const int32_t tile = blockIdx.x % a.n_tiles;
-    const int32_t sig0 = tile * kLanes + lane;
-    const bool active = sig0 < a.n_scen;
-    const int32_t sigma = active ? sig0 : a.n_scen - 1;
+    const bool active = tile * kLanes + lane < a.n_scen;
+    const int32_t col = active ? lane : a.n_scen - 1 - tile * kLanes;
+    const int32_t sigma = tile * kLanes + col;
     const int64_t ns = a.n_scen;
-    const uint32_t *slow = &a.scen[sigma].slowdown_q16[0][0];
+    const int64_t *const sbase = a.start + (int64_t)tile * kLanes;
+    const int64_t *const fbase = a.finish + (int64_t)tile * kLanes;
+    uint32_t *const obase = a.factor + (int64_t)tile * kLanes;
+    const echo_scenario *sc = a.scen + sigma;
+    const uint32_t *slow = &sc->slowdown_q16[0][0];
+    const uint64_t jseed = sc->jitter_seed;
+    const uint32_t jstream = sc->jitter_stream;
+    const int32_t amp = sc->jitter_amp_q16;
     const int64_t *cl_off = a.cl_off + (int64_t)r * kStreams;
     const int64_t *cp_off = a.cp_off + (int64_t)r * kStreams;
+
+    // comm streams of this rank that carry comm ops, packed to the front
+    int64_t kb[kStreams];
+    int32_t nk[kStreams];
+    int ncs = 0;
+#pragma unroll
+    for (int k = 0; k < kStreams; ++k) {
+        kb[k] = 0;
+        nk[k] = 0;
+    }
+    for (int k = 0; k < kStreams; ++k) {
+        const int64_t b = cl_off[k], n = cl_off[k + 1] - b;
+        if (n == 0) continue;
+#pragma unroll
+        for (int q = 0; q < kStreams; ++q)
+            if (q == ncs) {
+                kb[q] = b;
+                nk[q] = (int32_t)n;
+            }
+        ++ncs;
+    }
 
     for (int s = 0; s < kStreams; ++s) {
         const int64_t b0 = cp_off[s], b1 = cp_off[s + 1];
@@ -323,49 +394,73 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
             p[k] = 0;
             cs[k] = kInf;
             cf[k] = kInf;
-            if (cl_off[k + 1] > cl_off[k]) {
-                const int64_t c = a.cl[cl_off[k]];
-                cs[k] = a.start[c * ns + sigma];
-                cf[k] = a.finish[c * ns + sigma];
+            if (k < ncs) {
+                const int64_t c = a.cl[kb[k]];
+                cs[k] = (sbase + c * ns)[col];
+                cf[k] = (fbase + c * ns)[col];
             }
         }
-        for (int64_t i = b0; i < b1; ++i) {
-            const int64_t v = a.cp[i];
-            const int cls = a.cp_class[i];
-            const int64_t sv = a.start[v * ns + sigma], fv = a.finish[v * ns + sigma];
-            uint32_t F = 65536u;
-#pragma unroll
-            for (int k = 0; k < kStreams; ++k) {
-                const int64_t kb = cl_off[k];
-                const int32_t nk = (int32_t)(cl_off[k + 1] - kb);
-                if (nk == 0) continue;
-                while (cf[k] <= sv) {                  // ends before v starts: never again
-                    ++p[k];
-                    if (p[k] < nk) {
-                        const int64_t c = a.cl[kb + p[k]];
-                        cs[k] = a.start[c * ns + sigma];
-                        cf[k] = a.finish[c * ns + sigma];
-                    } else {
-                        cs[k] = kInf;
-                        cf[k] = kInf;
+        int64_t fprev = 0;
+        // lane j holds compute record i0 + j of the current round of 64
+        const int4 *recs = reinterpret_cast<const int4 *>(a.cp);
+        int4 nxt = b0 + lane < b1 ? recs[b0 + lane] : make_int4(0, 0, 0, 0);
+        for (int64_t i0 = b0; i0 < b1; i0 += kLanes) {
+            const int4 cur = nxt;
+            // settle the round's records here, once, so the per-op loop below carries
+            // no memory wait (a wait there would also wait for the previous op's store)
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);
+            nxt = i0 + kLanes + lane < b1 ? recs[i0 + kLanes + lane] : make_int4(0, 0, 0, 0);
+            const int nr = b1 - i0 < kLanes ? int(b1 - i0) : kLanes;
+            for (int j = 0; j < nr; ++j) {
+                const int64_t v = __builtin_amdgcn_readlane(cur.x, j);
+                const int meta = __builtin_amdgcn_readlane(cur.y, j);
+                const int64_t d0 = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.w, j) << 32) |
+                                             (uint32_t)__builtin_amdgcn_readlane(cur.z, j));
+                const int64_t sv = (meta & kChained) ? fprev : (sbase + v * ns)[col];
+                int64_t d = amp != 0 ? jittered(d0, (int32_t)v, jseed, jstream, amp) : d0;
+                if (a.prev_refined) d = q16(d, (obase + v * ns)[col]);   // the previous pass's duration
+                const int64_t fv = sv + d;
+                fprev = fv;
+                bool busy = false;
+    #pragma unroll
+                for (int k = 0; k < kStreams; ++k)
+                    if (k < ncs) busy |= cs[k] < fv;
+                uint32_t F = 65536u;
+                if (busy) {
+                    const int cls = meta & 7;
+    #pragma unroll
+                    for (int k = 0; k < kStreams; ++k) {
+                        if (k >= ncs) break;
+                        if (!(cs[k] < fv)) continue;
+                        while (cf[k] <= sv) {              // ends before v starts: never again
+                            ++p[k];
+                            if (p[k] < nk[k]) {
+                                const int64_t c = a.cl[kb[k] + p[k]];
+                                cs[k] = (sbase + c * ns)[col];
+                                cf[k] = (fbase + c * ns)[col];
+                            } else {
+                                cs[k] = kInf;
+                                cf[k] = kInf;
+                            }
+                        }
+                        int32_t q = p[k];
+                        int64_t qs = cs[k], qf = cf[k];
+                        while (qs < fv) {
+                            const int64_t lo = sv > qs ? sv : qs, hi = fv < qf ? fv : qf;
+                            if (lo < hi) {
+                                const uint32_t x = slow[cls * kTypes + a.cl_type[kb[k] + q]];
+                                F = x > F ? x : F;
+                            }
+                            if (qf >= fv) break;           // the next one starts after v ends
+                            if (++q >= nk[k]) break;
+                            const int64_t c = a.cl[kb[k] + q];
+                            qs = (sbase + c * ns)[col];
+                            qf = (fbase + c * ns)[col];
+                        }
                     }
                 }
-                int32_t q = p[k];
-                int64_t qs = cs[k], qf = cf[k];
-                while (qs < fv) {
-                    const int64_t lo = sv > qs ? sv : qs, hi = fv < qf ? fv : qf;
-                    if (lo < hi) {
-                        const uint32_t x = slow[cls * kTypes + a.cl_type[kb + q]];
-                        F = x > F ? x : F;
-                    }
-                    if (qf >= fv) break;               // the next one starts after v ends
-                    if (++q >= nk) break;
-                    const int64_t c = a.cl[kb + q];
-                    qs = a.start[c * ns + sigma];
-                    qf = a.finish[c * ns + sigma];
-                }
+                (obase + v * ns)[col] = F;
             }
-            if (active) a.factor[v * ns + sigma] = F;
         }
     }
 }
@@ -408,8 +503,9 @@ hipError_t launch_cc_cost(const DeviceGraph &g, const echo_scenario *scen, int32
 hipError_t launch_walk(const WalkArgs &a, int32_t n_ranks, hipStream_t stream) {
     WalkArgs args = a;
     void *params[] = {&args};
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k_walk),
-                                      dim3((unsigned)(n_ranks * a.tiles)), dim3(kLanes), params, 0, stream);
+    const WalkKernel k = walk_kernel(a.factor != nullptr, a.final_pass != 0, a.digest != nullptr);
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k), dim3((unsigned)(n_ranks * a.tiles)),
+                                      dim3(kLanes), params, 0, stream);
 }
 
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
@@ -418,13 +514,18 @@ hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t str
 }
 
 hipError_t walk_capacity(int device, int64_t *waves) {
-    int per_cu = 0, cus = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(k_walk),
-                                                                kLanes, 0);
+    int cus = 0;
+    hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
     if (e != hipSuccess) return e;
-    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
-    if (e != hipSuccess) return e;
-    *waves = (int64_t)per_cu * cus;
+    int64_t least = INT64_MAX;
+    for (int v = 0; v < 8; ++v) {
+        int per_cu = 0;
+        const WalkKernel k = walk_kernel(v & 1, v & 2, v & 4);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(k), kLanes, 0);
+        if (e != hipSuccess) return e;
+        least = std::min<int64_t>(least, (int64_t)per_cu * cus);
+    }
+    *waves = least;
     return hipSuccess;
 }
 
