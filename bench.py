@@ -86,6 +86,8 @@ def main():
     ap.add_argument("--config", type=int, default=3, help="workload 1-4 (see workloads/configs.py)")
     ap.add_argument("--refine", type=int, default=1)
     ap.add_argument("--cpu-sample", type=int, default=8, help="scenarios the CPU oracle composes (0 = skip)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only copy MIB MiB device-to-device once (calibrates HBM byte counters) and exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -95,6 +97,16 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n}), flush=True)
+        return
 
     import paper_2412_12487_amd as E
     from workloads import configs

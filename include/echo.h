@@ -121,7 +121,7 @@ typedef struct {
  * Validate a graph, match its collectives, merge each collective into one
  * barrier node, order the merged graph by topological level and upload it
  * to device `hip_device` (the analogue of the simulator's initialisation,
- * Sec. 7.5 and Table 8).  Matching rule (Sec. 4.2: predefined matching rules
+ * Sec. 8.5, Table 8).  Matching rule (Sec. 4.2: predefined matching rules
  * plus a user API): within one communicator -- the set of (rank, stream) of a
  * collective's members -- every member rank issues that communicator's
  * collectives in the same order.  Errors: ARG (malformed arrays), RANGE,

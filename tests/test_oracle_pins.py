@@ -58,8 +58,10 @@ def test_cc_cost_hand_values(row):
 @pytest.mark.parametrize("S,N,M,K", [(4194304, 8, 1, 8), (26214400, 4, 4, 1), (50331648, 16, 2, 8),
                                      (123456789, 24, 3, 8), (1, 2, 2, 1)])
 def test_ring_allreduce_is_reduce_scatter_plus_all_gather(S, N, M, K):
-    """A ring all-reduce is a reduce-scatter followed by an all-gather over the same
-    ring (Sec. 5.1); with one connection set-up, T_AR = T_RS + T_AG - alpha."""
+    """Eq. 4 (ring AR) carries 2(N-1) slow hops per round where Eq. 3 (ring RS)
+    carries N-1, and Eq. 2 (ring AG) is exactly those N-1 hops: a ring all-reduce
+    is a reduce-scatter plus an all-gather with one connection set-up, so
+    T_AR = T_RS + T_AG - alpha.  A dropped or doubled term breaks this."""
     kw = dict(alpha=7000, bw_intra=300000, bw_inter=40000, reduce=150000)
     ar = oracle.cc_time(AR, S, N, M, K, **kw)
     rs = oracle.cc_time(RS, S, N, M, K, **kw)
