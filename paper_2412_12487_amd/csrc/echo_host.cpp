@@ -9,6 +9,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -56,6 +57,28 @@ int64_t table6_chunk(int64_t S) {
     return 288000;
 }
 
+// Host side of a CollTable: the per-collective inputs of the CC model.
+struct HostCollTable {
+    int64_t n;
+    std::vector<int64_t> bytes, chunk, eta_ring, eta_chunks;
+    std::vector<int32_t> N, M, K;
+    std::vector<uint8_t> type;
+    explicit HostCollTable(int64_t count)
+        : n(count), bytes(count), chunk(count), eta_ring(count), eta_chunks(count), N(count), M(count), K(count),
+          type(count) {}
+    void set(int64_t i, int t, int64_t S, int32_t members, int32_t servers, int32_t per_server) {
+        const int64_t ch = table6_chunk(S);
+        type[i] = (uint8_t)t;
+        bytes[i] = S;
+        chunk[i] = ch;
+        eta_ring[i] = (S + (int64_t)members * ch - 1) / ((int64_t)members * ch);   // ring rounds
+        eta_chunks[i] = (S + ch - 1) / ch;                                       // pipelined chunks
+        N[i] = members;
+        M[i] = servers;
+        K[i] = per_server;
+    }
+};
+
 template <class T>
 hipError_t upload(T **dst, const std::vector<T> &src) {
     *dst = nullptr;
@@ -72,13 +95,16 @@ struct echo_graph_s {
     int device = 0;
     int64_t n_ops = 0, n_colls = 0, n_levels = 0;
     int32_t n_ranks = 0;
-    int64_t capacity = 0;              // co-resident walk wavefronts
+    int64_t capacity[8] = {};          // co-resident walk workgroups per kernel variant
+    bool need_coll_cost = false;       // some comm op reads its cost per collective
     int64_t spin_limit = kDefaultSpinNs / 10;   // 100 MHz ticks
     DeviceGraph dg;
     std::vector<void *> owned;         // device allocations of the graph
     // workspace, grown on demand
     int64_t *cost = nullptr;
     size_t cost_n = 0;
+    int64_t *class_cost = nullptr;
+    size_t class_cost_n = 0;
     unsigned long long *arrive = nullptr;
     size_t arrive_n = 0;
     unsigned *count = nullptr;
@@ -103,6 +129,7 @@ void free_graph(echo_graph g) {
     (void)hipDeviceSynchronize();
     for (void *p : g->owned) (void)hipFree(p);
     (void)hipFree(g->cost);
+    (void)hipFree(g->class_cost);
     (void)hipFree(g->arrive);
     (void)hipFree(g->count);
     (void)hipFree(g->factor);
@@ -259,9 +286,10 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
     // matching rule: within one communicator (the (rank, stream) set of the
     // members) every member rank issues the communicator's collectives in the
     // same order -- so each collective sits at the same position everywhere.
+    std::vector<int32_t> cid(nc);                  // communicator of each collective
+    std::vector<int32_t> pos(nc, -1);              // its position in the communicator's issue order
     {
         std::map<std::vector<int64_t>, int32_t> comm_id;
-        std::vector<int32_t> cid(nc);
         std::vector<int64_t> key;
         for (int64_t c = 0; c < nc; ++c) {
             key.clear();
@@ -271,7 +299,6 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
             cid[c] = it->second;
         }
         std::unordered_map<uint64_t, int32_t> issued;   // (communicator, rank) -> collectives so far
-        std::vector<int32_t> pos(nc, -1);
         for (int64_t v = 0; v < n; ++v) {
             if (d->op_kind[v] != ECHO_COMM) continue;
             const int64_t c = d->op_coll[v];
@@ -283,6 +310,84 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
                             "collective %lld: rank %d issues it as call %d of its communicator, "
                             "another member as call %d",
                             (long long)c, d->op_rank[v], p, pos[c]);
+        }
+    }
+
+    // cost classes: collectives with the same (type, S, N, M, K) cost the same in every scenario
+    std::vector<int32_t> ccls(nc);
+    std::vector<std::array<int64_t, 5>> classes;
+    {
+        std::map<std::array<int64_t, 5>, int32_t> cls_id;
+        for (int64_t c = 0; c < nc; ++c) {
+            const std::array<int64_t, 5> k{d->coll_type[c], d->coll_bytes[c], cN[c], cM[c], cK[c]};
+            auto it = cls_id.emplace(k, (int32_t)classes.size());
+            if (it.second) classes.push_back(k);
+            ccls[c] = it.first->second;
+        }
+    }
+    // rank blocks: the most used classes of a block get its LDS cost slots;
+    // collectives whose members all sit in one block meet in that block's LDS
+    const int64_t nblk = (R + kBlockRanks - 1) / kBlockRanks;
+    std::vector<int32_t> block_class(nblk * kClassSlots, -1);
+    std::vector<uint32_t> coll_aux(nc, 0);          // channel part of the aux word (local collectives)
+    std::vector<uint8_t> op_slot(n, (uint8_t)kNoSlot);
+    {
+        std::vector<int64_t> first_op(nblk + 1, n);
+        for (int64_t v = n - 1; v >= 0; --v) first_op[d->op_rank[v] / kBlockRanks] = v;
+        for (int64_t b = nblk - 1; b >= 0; --b)
+            if (first_op[b] > first_op[b + 1]) first_op[b] = first_op[b + 1];
+        std::unordered_map<int32_t, int64_t> use;
+        std::vector<std::pair<int64_t, int32_t>> order;
+        for (int64_t b = 0; b < nblk; ++b) {
+            use.clear();
+            for (int64_t v = first_op[b]; v < first_op[b + 1]; ++v)
+                if (d->op_kind[v] == ECHO_COMM) ++use[ccls[d->op_coll[v]]];
+            order.clear();
+            for (auto &kv : use) order.emplace_back(-kv.second, kv.first);
+            std::sort(order.begin(), order.end());
+            std::unordered_map<int32_t, int32_t> slot_of;
+            for (int i = 0; i < kClassSlots && i < (int)order.size(); ++i) {
+                block_class[b * kClassSlots + i] = order[i].second;
+                slot_of[order[i].second] = i;
+            }
+            for (int64_t v = first_op[b]; v < first_op[b + 1]; ++v)
+                if (d->op_kind[v] == ECHO_COMM) {
+                    auto it = slot_of.find(ccls[d->op_coll[v]]);
+                    if (it != slot_of.end()) op_slot[v] = (uint8_t)it->second;
+                }
+        }
+        // channels: one per communicator of a block whose collectives are all local
+        std::map<std::pair<int64_t, int32_t>, int32_t> channel;   // (block, communicator) -> channel
+        std::vector<int32_t> used(nblk, 0);
+        for (int64_t c = 0; c < nc; ++c) {
+            const int64_t b0 = d->op_rank[mem[moff[c]]] / kBlockRanks;
+            bool local = true;
+            for (int64_t j = moff[c]; j < moff[c + 1]; ++j)
+                local = local && d->op_rank[mem[j]] / kBlockRanks == b0;
+            const int64_t expected = (int64_t)cN[c] * (pos[c] / 2 + 1);
+            if (!local || expected >= (int64_t(1) << kExpectedBits)) continue;
+            auto it = channel.find({b0, cid[c]});
+            if (it == channel.end()) {
+                if (used[b0] >= kChannels) continue;                 // out of channels: meet globally
+                it = channel.emplace(std::make_pair(b0, cid[c]), used[b0]++).first;
+            }
+            coll_aux[c] = kAuxLocal | ((uint32_t)it->second << 1) | ((uint32_t)(pos[c] & 1) << 4) |
+                          ((uint32_t)expected << 9);
+        }
+        // a communicator is local for all its collectives or none: drop channels whose
+        // communicator also has a collective that could not be met locally
+        std::map<std::pair<int64_t, int32_t>, bool> ok;
+        for (int64_t c = 0; c < nc; ++c) {
+            const int64_t b0 = d->op_rank[mem[moff[c]]] / kBlockRanks;
+            auto it = channel.find({b0, cid[c]});
+            if (it == channel.end()) continue;
+            auto &flag = ok.emplace(std::make_pair(b0, cid[c]), true).first->second;
+            if (!(coll_aux[c] & kAuxLocal)) flag = false;
+        }
+        for (int64_t c = 0; c < nc; ++c) {
+            const int64_t b0 = d->op_rank[mem[moff[c]]] / kBlockRanks;
+            auto it = ok.find({b0, cid[c]});
+            if (it != ok.end() && !it->second) coll_aux[c] = 0;
         }
     }
 
@@ -386,7 +491,9 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
                 it.nfar = (int32_t)((int64_t)far.size() - f0);
                 it.far_off = (int32_t)f0;
                 it.coll = d->op_kind[v] == ECHO_COMM ? (int32_t)d->op_coll[v] : -1;
-                it.aux = 0;
+                it.aux = d->op_kind[v] == ECHO_COMM
+                             ? coll_aux[d->op_coll[v]] | ((uint32_t)op_slot[v] << 5)
+                             : 0u;
                 it.dur = d->op_kind[v] == ECHO_COMM ? 0 : d->op_dur_ns[v];
             }
         }
@@ -425,16 +532,13 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
             }
         }
     }
-    std::vector<int64_t> c_bytes(nc), c_chunk(nc), c_eta_ring(nc), c_eta_chunks(nc);
-    std::vector<uint8_t> c_type(nc);
-    for (int64_t c = 0; c < nc; ++c) {
-        const int64_t S = d->coll_bytes[c], ch = table6_chunk(S);
-        c_bytes[c] = S;
-        c_chunk[c] = ch;
-        c_eta_ring[c] = (S + (int64_t)cN[c] * ch - 1) / ((int64_t)cN[c] * ch);   // ring rounds
-        c_eta_chunks[c] = (S + ch - 1) / ch;                                   // pipelined chunks
-        c_type[c] = d->coll_type[c];
-    }
+    HostCollTable colls(nc), cls((int64_t)classes.size());
+    for (int64_t c = 0; c < nc; ++c) colls.set(c, d->coll_type[c], d->coll_bytes[c], cN[c], cM[c], cK[c]);
+    for (size_t k = 0; k < classes.size(); ++k)
+        cls.set((int64_t)k, (int)classes[k][0], classes[k][1], (int32_t)classes[k][2], (int32_t)classes[k][3],
+                (int32_t)classes[k][4]);
+    bool need_coll_cost = false;
+    for (int64_t v = 0; v < n; ++v) need_coll_cost = need_coll_cost || (d->op_kind[v] == ECHO_COMM && op_slot[v] == kNoSlot);
 
     // upload
     echo_graph g = new (std::nothrow) echo_graph_s();
@@ -453,6 +557,8 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
     dg.n_ops = n;
     dg.n_colls = nc;
     dg.n_ranks = (int32_t)R;
+    dg.n_blocks = (int32_t)nblk;
+    g->need_coll_cost = need_coll_cost;
 #define UP(dst, src)                                                        \
     do {                                                                    \
         e = upload(&dst, src);                                              \
@@ -466,14 +572,20 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
     UP(dg.items, items);
     UP(dg.rank_off, rank_off);
     UP(dg.far, far);
-    UP(dg.c_bytes, c_bytes);
-    UP(dg.c_chunk, c_chunk);
-    UP(dg.c_eta_ring, c_eta_ring);
-    UP(dg.c_eta_chunks, c_eta_chunks);
-    UP(dg.c_N, cN);
-    UP(dg.c_M, cM);
-    UP(dg.c_K, cK);
-    UP(dg.c_type, c_type);
+    for (int t = 0; t < 2; ++t) {
+        HostCollTable &h = t == 0 ? colls : cls;
+        CollTable &dt = t == 0 ? dg.colls : dg.classes;
+        dt.n = h.n;
+        UP(dt.bytes, h.bytes);
+        UP(dt.chunk, h.chunk);
+        UP(dt.eta_ring, h.eta_ring);
+        UP(dt.eta_chunks, h.eta_chunks);
+        UP(dt.N, h.N);
+        UP(dt.M, h.M);
+        UP(dt.K, h.K);
+        UP(dt.type, h.type);
+    }
+    UP(dg.block_class, block_class);
     UP(dg.cl_off, cl_off);
     UP(dg.cl, cl);
     UP(dg.cl_type, cl_type);
@@ -481,16 +593,19 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
     UP(dg.cp, cp);
     UP(dg.status, std::vector<unsigned>(1, 0u));
 #undef UP
-    e = walk_capacity(device, &g->capacity);
+    e = walk_capacity(device, g->capacity);
     if (e != hipSuccess) {
         free_graph(g);
         return hip_fail(e, "occupancy query");
     }
-    if (g->capacity < R) {
-        const int64_t cap = g->capacity;
+    int64_t least = INT64_MAX;
+    for (int v = 0; v < 8; ++v) least = std::min(least, g->capacity[v]);
+    if (least < nblk) {
+        const int64_t cap = least;
         free_graph(g);
-        return fail(ECHO_ERR_RANGE, "%lld ranks exceed the %lld co-resident walk wavefronts of the device",
-                    (long long)R, (long long)cap);
+        return fail(ECHO_ERR_RANGE,
+                    "%lld ranks need %lld co-resident walk workgroups of %d ranks; the device holds %lld",
+                    (long long)R, (long long)nblk, kBlockRanks, (long long)cap);
     }
     *out = g;
     return ECHO_OK;
@@ -507,6 +622,7 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
     const int32_t n_tiles = (int32_t)((ns + kLanes - 1) / kLanes);
     int rc;
     if ((rc = ensure(&g->cost, &g->cost_n, (size_t)(g->n_colls * ns), "cost"))) return rc;
+    if ((rc = ensure(&g->class_cost, &g->class_cost_n, (size_t)(g->dg.classes.n * ns), "class cost"))) return rc;
     if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->n_colls * ns), "arrivals"))) return rc;
     if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * n_tiles), "arrival counts"))) return rc;
     if (n_refine > 0 && (rc = ensure(&g->factor, &g->factor_n, (size_t)(g->n_ops * ns), "factors"))) return rc;
@@ -529,11 +645,16 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
     } while (0)
     TIMED(ECHO_K_INIT, launch_init(g->dg, d_scen, n_scen, g->arrive, n_arrive, g->count, n_count, step, d_digest,
                                    stream), "init kernel");
-    TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg, d_scen, n_scen, g->cost, stream), "cc_cost kernel");
+    TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.classes, d_scen, n_scen, g->class_cost, g->dg.status, stream),
+          "cc_cost kernel");
+    if (g->need_coll_cost)
+        TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.colls, d_scen, n_scen, g->cost, g->dg.status, stream),
+              "cc_cost kernel");
 
-    // tiles per walk launch: every rank of a tile must be co-resident
-    const int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, g->capacity / g->n_ranks));
     for (int32_t p = 0; p <= n_refine; ++p) {
+        // tiles per walk launch: every rank block of a tile must be co-resident
+        const int64_t cap = g->capacity[walk_variant(p > 0, p == n_refine, d_digest != nullptr)];
+        const int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, cap / g->dg.n_blocks));
         if (p > 0) {
             OverlapArgs o{g->dg.cl_off, g->dg.cp_off, g->dg.cl, g->dg.cl_type, g->dg.cp,
                           d_scen, start, finish, g->factor, n_scen, n_tiles, p > 1};
@@ -545,9 +666,11 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
             a.items = g->dg.items;
             a.rank_off = g->dg.rank_off;
             a.far = g->dg.far;
-            a.c_N = g->dg.c_N;
+            a.c_N = g->dg.colls.N;
+            a.block_class = g->dg.block_class;
             a.scen = d_scen;
             a.cost = g->cost;
+            a.class_cost = g->class_cost;
             a.factor = p > 0 ? g->factor : nullptr;
             a.start = start;
             a.finish = finish;
@@ -561,9 +684,10 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
             a.n_tiles = n_tiles;
             a.tile0 = (int32_t)t0;
             a.tiles = (int32_t)std::min<int64_t>(per_launch, n_tiles - t0);
+            a.n_ranks = g->n_ranks;
             a.final_pass = p == n_refine;
             if (g->n_ranks == 0 || g->n_ops == 0) continue;
-            TIMED(ECHO_K_WALK, launch_walk(a, g->n_ranks, stream), "walk kernel");
+            TIMED(ECHO_K_WALK, launch_walk(a, g->dg.n_blocks, stream), "walk kernel");
         }
     }
 #undef TIMED
@@ -603,7 +727,8 @@ int echo_cc_cost(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int6
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     if ((e = launch_init(g->dg, d_scen, n_scen, nullptr, 0, nullptr, 0, nullptr, nullptr, s)))
         return hip_fail(e, "init kernel");
-    if ((e = launch_cc_cost(g->dg, d_scen, n_scen, d_cost, s))) return hip_fail(e, "cc_cost kernel");
+    if ((e = launch_cc_cost(g->dg.colls, d_scen, n_scen, d_cost, g->dg.status, s)))
+        return hip_fail(e, "cc_cost kernel");
     return ECHO_OK;
 }
 

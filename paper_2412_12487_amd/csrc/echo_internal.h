@@ -47,6 +47,25 @@ static_assert(sizeof(WalkItem) == 32, "walk item must stay 32 bytes");
 // the previous op of slot 0, itself not a comm op: its start is that op's finish.
 constexpr uint32_t kFast = 1u << 16;
 
+// Workgroups walk kBlockRanks consecutive ranks (one wavefront each) for one
+// scenario tile.  A collective whose members all sit in one block is met in
+// LDS: each communicator of the block owns a channel with two alternating
+// slots (max of launch times per lane, arrival count).  Collective costs are
+// looked up per cost class -- the (type, S, N, M, K) tuple that fixes T(c, s)
+// for a scenario -- and a block stages its most used classes in LDS.
+constexpr int kBlockRanks = 8;
+constexpr int kChannels = 8;          // LDS barrier channels per block
+constexpr int kClassSlots = 8;        // LDS cost classes per block
+constexpr uint32_t kNoSlot = 15;
+// Comm item aux word: bit 0 local barrier | channel << 1 | slot parity << 4 |
+// class slot << 5 (kNoSlot: read the cost from global memory) | expected count << 9.
+constexpr uint32_t kAuxLocal = 1u;
+constexpr int kExpectedBits = 23;
+__host__ __device__ inline int aux_channel(uint32_t x) { return int((x >> 1) & 7u); }
+__host__ __device__ inline int aux_parity(uint32_t x) { return int((x >> 4) & 1u); }
+__host__ __device__ inline int aux_slot(uint32_t x) { return int((x >> 5) & 15u); }
+__host__ __device__ inline unsigned aux_expected(uint32_t x) { return x >> 9; }
+
 __host__ __device__ inline int item_kind(uint32_t m) { return int(m & 3u); }
 __host__ __device__ inline int item_stream(uint32_t m) { return int((m >> 2) & 7u); }
 __host__ __device__ inline int item_class(uint32_t m) { return int((m >> 5) & 7u); }
@@ -63,20 +82,27 @@ static_assert(sizeof(ComputeRec) == 16, "compute record must stay 16 bytes");
 // it starts exactly when that op finishes.
 constexpr uint32_t kChained = 0x80;
 
+// Inputs of the CC model for a table of collectives (or of cost classes).
+struct CollTable {
+    int64_t n = 0;
+    int64_t *bytes = nullptr;        // S
+    int64_t *chunk = nullptr;        // chunk size (Table 6)
+    int64_t *eta_ring = nullptr;     // ceil(S / (N * chunk))
+    int64_t *eta_chunks = nullptr;   // ceil(S / chunk)
+    int32_t *N = nullptr, *M = nullptr, *K = nullptr;
+    uint8_t *type = nullptr;
+};
+
 // Device copy of a loaded graph (all pointers are device memory).
 struct DeviceGraph {
     int64_t n_ops = 0, n_colls = 0;
-    int32_t n_ranks = 0;
+    int32_t n_ranks = 0, n_blocks = 0;
     WalkItem *items = nullptr;       // walk lists, rank-major
     int64_t *rank_off = nullptr;     // [n_ranks + 1] offsets into items
     int32_t *far = nullptr;          // far predecessor op ids
-    // collectives
-    int64_t *c_bytes = nullptr;      // S
-    int64_t *c_chunk = nullptr;      // chunk size (Table 6)
-    int64_t *c_eta_ring = nullptr;   // ceil(S / (N * chunk))
-    int64_t *c_eta_chunks = nullptr; // ceil(S / chunk)
-    int32_t *c_N = nullptr, *c_M = nullptr, *c_K = nullptr;
-    uint8_t *c_type = nullptr;
+    CollTable colls;                 // every collective
+    CollTable classes;               // every cost class
+    int32_t *block_class = nullptr;  // [n_blocks][kClassSlots] class staged in each LDS slot, -1 = none
     // overlap detection: comm / compute ops of each (rank, stream), program order
     int64_t *cl_off = nullptr;       // [n_ranks * 8 + 1]
     int32_t *cl = nullptr;
@@ -91,8 +117,10 @@ struct WalkArgs {
     const int64_t *rank_off;
     const int32_t *far;
     const int32_t *c_N;
+    const int32_t *block_class;
     const echo_scenario *scen;
     const int64_t *cost;             // [coll][scen]
+    const int64_t *class_cost;       // [class][scen]
     const uint32_t *factor;          // [op][scen] slowdown factors, or null (pass 1)
     int64_t *start, *finish;         // [op][scen]
     unsigned long long *arrive;      // [coll][scen] latest member launch
@@ -103,6 +131,7 @@ struct WalkArgs {
     int64_t spin_limit;              // wall-clock ticks (100 MHz) before a wait gives up
     int32_t n_scen, n_tiles;
     int32_t tile0, tiles;            // tiles handled by this launch
+    int32_t n_ranks;
     int32_t final_pass;              // accumulate step time (and digest)
 };
 
@@ -125,11 +154,15 @@ hipError_t launch_init(const DeviceGraph &g, const echo_scenario *scen, int32_t 
                        int64_t n_count, int64_t *step, uint64_t *digest, hipStream_t stream);
 hipError_t launch_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *count,
                         int64_t n_count, hipStream_t stream);
-hipError_t launch_cc_cost(const DeviceGraph &g, const echo_scenario *scen, int32_t n_scen,
-                          int64_t *cost, hipStream_t stream);
-hipError_t launch_walk(const WalkArgs &a, int32_t n_ranks, hipStream_t stream);
+hipError_t launch_cc_cost(const CollTable &t, const echo_scenario *scen, int32_t n_scen, int64_t *cost,
+                          unsigned *status, hipStream_t stream);
+hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream);
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream);
-// Co-resident walk wavefronts the device can hold (one wavefront per block).
-hipError_t walk_capacity(int device, int64_t *waves);
+// Co-resident walk workgroups (kBlockRanks wavefronts each) the device can hold,
+// for each of the 8 kernel variants (bit 0 refined, bit 1 final, bit 2 digest).
+hipError_t walk_capacity(int device, int64_t workgroups[8]);
+inline int walk_variant(bool refined, bool final_pass, bool digest) {
+    return (refined ? 1 : 0) | (final_pass ? 2 : 0) | (digest ? 4 : 0);
+}
 
 }  // namespace echo

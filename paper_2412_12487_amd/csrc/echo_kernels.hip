@@ -33,18 +33,22 @@ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
 }
 
 // (d * f + 2^15) >> 16 in unsigned 64-bit: d < 2^44 and f < 2^20 never wrap.
-__device__ __forceinline__ int64_t q16(int64_t d, uint64_t f) {
-    return int64_t(((uint64_t)d * f + 32768ull) >> 16);
+__device__ __forceinline__ int64_t q16(int64_t d, uint32_t f) {
+    return int64_t(((uint64_t)d * (uint64_t)f + 32768ull) >> 16);
 }
 
-// Base duration with uniform jitter of amplitude amp (Q16) from the
-// (jstream * 2^36 + v + 1)-th SplitMix64 output of the scenario's seed.
-__device__ __forceinline__ int64_t jittered(int64_t d0, int32_t v, uint64_t seed, uint32_t jstream,
-                                            int32_t amp) {
-    const uint64_t k = ((uint64_t)jstream << 36) + (uint64_t)(uint32_t)v + 1ull;
-    const uint64_t u = mix64(seed + k * kGolden);
-    const int64_t J = (int64_t)(((u >> 32) * (uint64_t)(2 * amp + 1)) >> 32) - amp;
-    return q16(d0, (uint64_t)(65536 + J));
+// Base duration with uniform jitter of amplitude amp (Q16) from the k-th
+// SplitMix64 output of the scenario's seed, k = jstream * 2^36 + v + 1.  The
+// SplitMix64 state seed + k * golden is split into a per-scenario part
+// (jbase = seed + jstream * 2^36 * golden) and a per-op part ((v + 1) * golden,
+// the same for every lane).
+__device__ __forceinline__ uint64_t jitter_base(uint64_t seed, uint32_t jstream) {
+    return seed + ((uint64_t)jstream << 36) * kGolden;
+}
+__device__ __forceinline__ int64_t jittered(int64_t d0, int32_t v, uint64_t jbase, int32_t amp) {
+    const uint64_t u = mix64(jbase + ((uint64_t)(uint32_t)v + 1ull) * kGolden);
+    const uint32_t f = (uint32_t)(65536 - amp) + __umulhi((uint32_t)(u >> 32), (uint32_t)(2 * amp + 1));
+    return q16(d0, f);
 }
 
 __device__ __forceinline__ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -93,15 +97,15 @@ __global__ void k_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *
 }
 
 // ------------------------------------------------------------------ CC estimator
-// One block per collective; lanes stride over scenarios.
-__global__ __launch_bounds__(64) void k_cc_cost(DeviceGraph g, const echo_scenario *scen,
-                                                int32_t n_scen, int64_t *cost) {
+// One block per collective (or cost class); lanes stride over scenarios.
+__global__ __launch_bounds__(64) void k_cc_cost(CollTable t, const echo_scenario *scen, int32_t n_scen,
+                                                int64_t *cost, unsigned *status) {
     const int64_t c = blockIdx.x;
-    const int type = g.c_type[c];
-    const int64_t S = g.c_bytes[c], chunk = g.c_chunk[c];
-    const int64_t N = g.c_N[c], M = g.c_M[c], K = g.c_K[c];
-    const unsigned __int128 eta_ring = (unsigned __int128)g.c_eta_ring[c];
-    const unsigned __int128 eta_chunks = (unsigned __int128)g.c_eta_chunks[c];
+    const int type = t.type[c];
+    const int64_t S = t.bytes[c], chunk = t.chunk[c];
+    const int64_t N = t.N[c], M = t.M[c], K = t.K[c];
+    const unsigned __int128 eta_ring = (unsigned __int128)t.eta_ring[c];
+    const unsigned __int128 eta_chunks = (unsigned __int128)t.eta_chunks[c];
     const unsigned __int128 n1 = (unsigned __int128)(N - 1);
     for (int32_t s = threadIdx.x; s < n_scen; s += blockDim.x) {
         const echo_scenario &sc = scen[s];
@@ -130,7 +134,7 @@ __global__ __launch_bounds__(64) void k_cc_cost(DeviceGraph g, const echo_scenar
             T = alpha + eta_chunks * hop;
         }
         if (T >= (unsigned __int128)kTimeLimit) {
-            __hip_atomic_fetch_or(g.status, kStatusOverflow, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_or(status, kStatusOverflow, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             T = (unsigned __int128)(kTimeLimit - 1);
         }
         cost[c * n_scen + s] = (int64_t)T;
@@ -157,42 +161,85 @@ __device__ bool wait_arrivals(const unsigned *cnt, unsigned need, unsigned *stat
 }
 
 constexpr int kBlock = 32;   // walk items fetched (and factors staged) per round
+// s_waitcnt immediate for "lgkmcnt(0)" on gfx9-family targets (vmcnt and expcnt left at their maxima)
+constexpr int kWaitLgkm0 = 0xC07F;
 
-// One wavefront walks one rank's list for one 64-scenario tile.  REFINED: the
-// pass inflates compute ops by the factors of the previous pass's overlaps.
-// FINAL: the pass produces the step time (and DIGEST: the timeline digest).
+// Wait until `need` members have arrived at an LDS barrier slot of this block.
+__device__ __forceinline__ unsigned ld_local(const unsigned *p) {
+    return __builtin_amdgcn_readfirstlane(__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
+}
+
+__device__ bool wait_local(const unsigned *cnt, unsigned need, unsigned *status, int64_t limit) {
+    if (ld_local(cnt) >= need) return true;
+    const uint64_t t0 = wall_clock64();
+    for (unsigned it = 1;; ++it) {
+        __builtin_amdgcn_s_sleep(1);
+        if (ld_local(cnt) >= need) return true;
+        if ((it & 255) == 0) {
+            if (__builtin_amdgcn_readfirstlane(ld_relaxed(status)) & kStatusAbort) return false;
+            if ((int64_t)(wall_clock64() - t0) > limit) {
+                __hip_atomic_fetch_or(status, kStatusTimeout | kStatusAbort, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+                return false;
+            }
+        }
+    }
+}
+
+// A workgroup of kBlockRanks wavefronts walks the ranks of one block for one
+// 64-scenario tile; wavefront w walks rank block * kBlockRanks + w.  REFINED:
+// the pass inflates compute ops by the factors of the previous pass's
+// overlaps.  FINAL: the pass produces the step time (and DIGEST: the digest).
 template <bool REFINED, bool FINAL, bool DIGEST>
-__global__ __launch_bounds__(64) void k_walk(WalkArgs a) {
-    __shared__ uint32_t fstage[REFINED ? kBlock * kLanes : 1];
-    const int lane = threadIdx.x;
-    const int32_t r = blockIdx.x / a.tiles;
+__global__ __launch_bounds__(kBlockRanks * 64) void k_walk(WalkArgs a) {
+    __shared__ uint32_t fstage[REFINED ? kBlockRanks * kBlock * kLanes : 1];
+    __shared__ unsigned long long lbar[kChannels][2][kLanes];   // per channel and slot: latest launch per lane
+    __shared__ unsigned lcnt[kChannels][2];                      // per channel and slot: members arrived
+    __shared__ int64_t ccost[kClassSlots][kLanes];               // staged class costs of this tile
+    __shared__ int32_t pinfo[kBlockRanks][kStreams][3];          // per wave and slot: pending collective, op, aux
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform within a wavefront
+    const int32_t blk = blockIdx.x / a.tiles;
     const int32_t tile = a.tile0 + blockIdx.x % a.tiles;
-    const int32_t sig0 = tile * kLanes + lane;
-    const bool active = sig0 < a.n_scen;
+    const int32_t r = blk * kBlockRanks + wave;
+    const bool active = tile * kLanes + lane < a.n_scen;
     // Idle lanes of the last tile mirror its last scenario: they compute the same
-    // values and store them to the same places; only active lanes issue atomics.
+    // values and store them to the same places; only active lanes issue global atomics.
     const int32_t col = active ? lane : a.n_scen - 1 - tile * kLanes;
     const bool mirror = (tile + 1) * kLanes > a.n_scen;
     const int32_t sigma = tile * kLanes + col;
     const int64_t ns = a.n_scen;
+
+    // block set-up: clear the barrier channels, stage the block's class costs
+    for (int i = threadIdx.x; i < kChannels * 2 * kLanes; i += blockDim.x) (&lbar[0][0][0])[i] = 0;
+    if (threadIdx.x < kChannels * 2) (&lcnt[0][0])[threadIdx.x] = 0;
+    if (wave < kClassSlots) {
+        const int32_t cls = a.block_class[(int64_t)blk * kClassSlots + wave];
+        ccost[wave][lane] = cls >= 0 ? a.class_cost[(int64_t)cls * ns + sigma] : 0;
+    }
+    __syncthreads();
+    if (r >= a.n_ranks) return;
+
     const echo_scenario *sc = a.scen + sigma;
-    const uint64_t jseed = sc->jitter_seed;
-    const uint32_t jstream = sc->jitter_stream;
+    const uint64_t jbase = jitter_base(sc->jitter_seed, sc->jitter_stream);
     const int32_t amp = sc->jitter_amp_q16;
     int64_t *const sbase = a.start + (int64_t)tile * kLanes;    // row v of tile: sbase + v * ns
     int64_t *const fbase = a.finish + (int64_t)tile * kLanes;
     const unsigned *tile_count = a.count + tile;
+    uint32_t *const fst = fstage + (REFINED ? wave * kBlock * kLanes : 0);
 
-    // Per slot: finish of the latest op, or a comm op still waiting for its barrier.
-    int64_t lf[kStreams], ps[kStreams];
-    int32_t pc[kStreams], pv[kStreams];
+    // Per slot: finish of the latest op, or (bit j of `pending`) a comm op still
+    // waiting for its barrier, described in this wave's row of pinfo.
+    int64_t lf[kStreams];
 #pragma unroll
-    for (int j = 0; j < kStreams; ++j) {
-        lf[j] = 0;
-        ps[j] = 0;
-        pc[j] = -1;
-        pv[j] = 0;
-    }
+    for (int j = 0; j < kStreams; ++j) lf[j] = 0;
+    uint32_t pending = 0;
+    int32_t (*const pend)[3] = pinfo[wave];
+    // A wait that gave up (timeout or abort) marks the wave dead: it finishes its
+    // list without waiting again; the times it writes are meaningless and the
+    // status word already reports the failure.
+    bool dead = false;
     uint64_t dig = 0;
     uint32_t hi_or = 0;          // OR of the high words of every time: bit 30 set <=> some time >= 2^62
     unsigned err = 0;
@@ -205,60 +252,94 @@ __global__ __launch_bounds__(64) void k_walk(WalkArgs a) {
 
 // Finish of the comm op pending on slot j: barrier (latest member launch) + cost.
 #define RESOLVE(j)                                                                               \
-    if (pc[j] >= 0) {                                                                            \
-        const int64_t c_ = pc[j];                                                                \
-        if (!wait_arrivals(tile_count + c_ * a.n_tiles, (unsigned)a.c_N[c_], a.status,           \
-                           a.spin_limit))                                                        \
-            goto out;                                                                            \
+    if (pending & (1u << j)) {                                                                   \
+        const int64_t c_ = __builtin_amdgcn_readfirstlane(pend[j][0]);                          \
+        const int32_t v_ = __builtin_amdgcn_readfirstlane(pend[j][1]);                          \
+        const uint32_t x_ = (uint32_t)__builtin_amdgcn_readfirstlane(pend[j][2]);               \
         uint64_t b_ = 0;                                                                         \
-        if (active)                                                                              \
-            b_ = __hip_atomic_fetch_max(a.arrive + c_ * ns + sigma, 0ull, __ATOMIC_RELAXED,      \
-                                        __HIP_MEMORY_SCOPE_AGENT);                               \
-        b_ = mirror ? (uint64_t)__shfl((long long)b_, col) : b_;                                 \
-        const int64_t f_ = (int64_t)b_ + a.cost[c_ * ns + sigma];                                \
+        if (x_ & kAuxLocal) {                                                                    \
+            const int ch_ = aux_channel(x_), par_ = aux_parity(x_);                              \
+            if (!dead && !__builtin_amdgcn_readfirstlane(                                        \
+                             wait_local(&lcnt[ch_][par_], aux_expected(x_), a.status, a.spin_limit))) \
+                dead = true;                                                                     \
+            b_ = lbar[ch_][par_][lane];                                                          \
+        } else {                                                                                 \
+            if (!dead && !__builtin_amdgcn_readfirstlane(wait_arrivals(tile_count + c_ * a.n_tiles, \
+                                                                       (unsigned)a.c_N[c_], a.status, \
+                                                                       a.spin_limit)))           \
+                dead = true;                                                                     \
+            if (active)                                                                          \
+                b_ = __hip_atomic_fetch_max(a.arrive + c_ * ns + sigma, 0ull, __ATOMIC_RELAXED,  \
+                                            __HIP_MEMORY_SCOPE_AGENT);                           \
+            b_ = mirror ? (uint64_t)__shfl((long long)b_, col) : b_;                             \
+        }                                                                                        \
+        const int sl_ = aux_slot(x_);                                                            \
+        /* distinct load kinds keep the two reads from merging into one flat load */            \
+        const int64_t t_ = sl_ < kClassSlots ? ccost[sl_][lane]                                  \
+                                             : __hip_atomic_load(a.cost + c_ * ns + sigma,         \
+                                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); \
+        const int64_t f_ = (int64_t)b_ + t_;                                                     \
         hi_or |= (uint32_t)((uint64_t)f_ >> 32);                                                 \
-        (fbase + (int64_t)pv[j] * ns)[col] = f_;                                                 \
-        if (DIGEST) dig += mix64(mix64((uint64_t)pv[j] ^ (uint64_t)ps[j]) ^ (uint64_t)f_);       \
+        (fbase + (int64_t)v_ * ns)[col] = f_;                                                    \
+        if (DIGEST) {                                                                            \
+            const int64_t s_ = (sbase + (int64_t)v_ * ns)[col];                                  \
+            dig += mix64(mix64((uint64_t)v_ ^ (uint64_t)s_) ^ (uint64_t)f_);                     \
+        }                                                                                        \
         lf[j] = f_;                                                                              \
-        pc[j] = -1;                                                                              \
+        pending &= ~(1u << j);                                                                   \
     }
 
-    for (int64_t blk = beg; blk < end; blk += kBlock) {
+    for (int64_t blk0 = beg; blk0 < end; blk0 += kBlock) {
         const int4 cur = nxt;
-        const int nb = end - blk < kBlock ? int(end - blk) : kBlock;
-        nxt = blk + kBlock + slotl < end ? items4[2 * (blk + kBlock + slotl) + half] : make_int4(0, 0, 0, 0);
+        const int nb = end - blk0 < kBlock ? int(end - blk0) : kBlock;
+        nxt = blk0 + kBlock + slotl < end ? items4[2 * (blk0 + kBlock + slotl) + half] : make_int4(0, 0, 0, 0);
         if (REFINED) {
-            // stage this round's slowdown factors: one load per item, one wait per round
-            uint32_t fv[kBlock];
+            // stage this round's slowdown factors, half a round per memory round trip
 #pragma unroll
-            for (int j = 0; j < kBlock; ++j) {
-                const int32_t opj = __builtin_amdgcn_readlane(cur.x, j);
-                fv[j] = a.factor[(int64_t)opj * ns + sigma];
+            for (int h = 0; h < kBlock; h += kBlock / 2) {
+                uint32_t fv[kBlock / 2];
+#pragma unroll
+                for (int j = 0; j < kBlock / 2; ++j) {
+                    const int32_t opj = __builtin_amdgcn_readlane(cur.x, h + j);
+                    fv[j] = a.factor[(int64_t)opj * ns + sigma];
+                }
+#pragma unroll
+                for (int j = 0; j < kBlock / 2; ++j) fst[(h + j) * kLanes + lane] = fv[j];
             }
-#pragma unroll
-            for (int j = 0; j < kBlock; ++j) fstage[j * kLanes + lane] = fv[j];
         }
-        for (int j = 0; j < nb; ++j) {
+        // fast flags of the round, one bit per item
+        const uint64_t fast_bits = __builtin_amdgcn_read_exec() &
+                                   __ballot((lane < nb) && (lane < 32) && (cur.y & kFast));
+        int j = 0;
+        while (j < nb) {
+            // a run of fast items: compute/memcpy ops right after the previous op of slot 0
+            int64_t s0 = lf[0];
+            while (j < nb && ((fast_bits >> j) & 1)) {
+                const int32_t op = __builtin_amdgcn_readlane(cur.x, j);
+                const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);
+                const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) |
+                                              (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32));
+                int64_t d = amp != 0 ? jittered(dur, op, jbase, amp) : dur;
+                if (REFINED && item_kind(meta) == ECHO_COMPUTE) d = q16(d, fst[j * kLanes + lane]);
+                const int64_t f = s0 + d;
+                (sbase + (int64_t)op * ns)[col] = s0;
+                (fbase + (int64_t)op * ns)[col] = f;
+                hi_or |= (uint32_t)((uint64_t)f >> 32);
+                if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)s0) ^ (uint64_t)f);
+                s0 = f;
+                ++j;
+            }
+            lf[0] = s0;
+            if (j >= nb) break;
             const int32_t op = __builtin_amdgcn_readlane(cur.x, j);
             const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);
             const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) |
                                           (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32));
             const int kind = item_kind(meta);
-            if (meta & kFast) {
-                // compute/memcpy op right after the previous op of slot 0
-                int64_t d = amp != 0 ? jittered(dur, op, jseed, jstream, amp) : dur;
-                if (REFINED && kind == ECHO_COMPUTE) d = q16(d, fstage[j * kLanes + lane]);
-                const int64_t s0 = lf[0], f = s0 + d;
-                (sbase + (int64_t)op * ns)[col] = s0;
-                (fbase + (int64_t)op * ns)[col] = f;
-                hi_or |= (uint32_t)((uint64_t)f >> 32);
-                if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)s0) ^ (uint64_t)f);
-                lf[0] = f;
-                continue;
-            }
             const int32_t far_off = __builtin_amdgcn_readlane(cur.z, j);
             const int32_t coll = __builtin_amdgcn_readlane(cur.w, j);
             const int32_t nfar = __builtin_amdgcn_readlane(cur.z, j + 32);
+            const uint32_t aux = (uint32_t)__builtin_amdgcn_readlane(cur.w, j + 32);
             const int st = item_stream(meta);
             const unsigned mask = item_regmask(meta);
             int64_t ready = 0;
@@ -277,23 +358,31 @@ __global__ __launch_bounds__(64) void k_walk(WalkArgs a) {
             (sbase + (int64_t)op * ns)[col] = ready;
             if (kind == ECHO_COMM) {
                 // launch: publish this member's launch time, then count the arrival
-                if (active)
-                    __hip_atomic_fetch_max(a.arrive + (int64_t)coll * ns + sigma, (unsigned long long)ready,
-                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-                if (lane == 0)
-                    __hip_atomic_fetch_add(a.count + (int64_t)coll * a.n_tiles + tile, 1u,
-                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-#pragma unroll
-                for (int q = 0; q < kStreams; ++q)
-                    if (q == st) {
-                        pc[q] = coll;
-                        pv[q] = op;
-                        ps[q] = ready;
-                    }
+                if (aux & kAuxLocal) {
+                    const int ch = aux_channel(aux), par = aux_parity(aux);
+                    __hip_atomic_fetch_max(&lbar[ch][par][lane], (unsigned long long)ready, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WORKGROUP);
+                    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+                    if (lane == 0)
+                        __hip_atomic_fetch_add(&lcnt[ch][par], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                } else {
+                    if (active)
+                        __hip_atomic_fetch_max(a.arrive + (int64_t)coll * ns + sigma, (unsigned long long)ready,
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                    if (lane == 0)
+                        __hip_atomic_fetch_add(a.count + (int64_t)coll * a.n_tiles + tile, 1u, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+                }
+                if (lane == 0) {
+                    pend[st][0] = coll;
+                    pend[st][1] = op;
+                    pend[st][2] = (int32_t)aux;
+                }
+                pending |= 1u << st;
             } else {
-                int64_t d = amp != 0 ? jittered(dur, op, jseed, jstream, amp) : dur;
-                if (REFINED && kind == ECHO_COMPUTE) d = q16(d, fstage[j * kLanes + lane]);
+                int64_t d = amp != 0 ? jittered(dur, op, jbase, amp) : dur;
+                if (REFINED && kind == ECHO_COMPUTE) d = q16(d, fst[j * kLanes + lane]);
                 const int64_t f = ready + d;
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 (fbase + (int64_t)op * ns)[col] = f;
@@ -302,6 +391,7 @@ __global__ __launch_bounds__(64) void k_walk(WalkArgs a) {
                 for (int q = 0; q < kStreams; ++q)
                     if (q == st) lf[q] = f;
             }
+            ++j;
         }
     }
 #pragma unroll
@@ -309,7 +399,7 @@ __global__ __launch_bounds__(64) void k_walk(WalkArgs a) {
 #undef RESOLVE
     if (hi_or >> 30) err |= kStatusOverflow;
     if (active && err) __hip_atomic_fetch_or(a.status, err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (FINAL && active) {
+    if (FINAL && active && !dead) {
         // finishes along a FIFO stream never decrease: the last op of each slot holds its maximum
         int64_t smax = 0;
 #pragma unroll
@@ -320,9 +410,6 @@ __global__ __launch_bounds__(64) void k_walk(WalkArgs a) {
             __hip_atomic_fetch_add(reinterpret_cast<unsigned long long *>(a.digest) + sigma,
                                    (unsigned long long)dig, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    return;
-out:
-    if (active && err) __hip_atomic_fetch_or(a.status, err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 using WalkKernel = void (*)(WalkArgs);
@@ -357,8 +444,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     uint32_t *const obase = a.factor + (int64_t)tile * kLanes;
     const echo_scenario *sc = a.scen + sigma;
     const uint32_t *slow = &sc->slowdown_q16[0][0];
-    const uint64_t jseed = sc->jitter_seed;
-    const uint32_t jstream = sc->jitter_stream;
+    const uint64_t jbase = jitter_base(sc->jitter_seed, sc->jitter_stream);
     const int32_t amp = sc->jitter_amp_q16;
     const int64_t *cl_off = a.cl_off + (int64_t)r * kStreams;
     const int64_t *cp_off = a.cp_off + (int64_t)r * kStreams;
@@ -417,7 +503,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 const int64_t d0 = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.w, j) << 32) |
                                              (uint32_t)__builtin_amdgcn_readlane(cur.z, j));
                 const int64_t sv = (meta & kChained) ? fprev : (sbase + v * ns)[col];
-                int64_t d = amp != 0 ? jittered(d0, (int32_t)v, jseed, jstream, amp) : d0;
+                int64_t d = amp != 0 ? jittered(d0, (int32_t)v, jbase, amp) : d0;
                 if (a.prev_refined) d = q16(d, (obase + v * ns)[col]);   // the previous pass's duration
                 const int64_t fv = sv + d;
                 fprev = fv;
@@ -493,19 +579,19 @@ hipError_t launch_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *
     return hipGetLastError();
 }
 
-hipError_t launch_cc_cost(const DeviceGraph &g, const echo_scenario *scen, int32_t n_scen, int64_t *cost,
-                          hipStream_t stream) {
-    if (g.n_colls == 0 || n_scen == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_cc_cost, dim3((unsigned)g.n_colls), dim3(64), 0, stream, g, scen, n_scen, cost);
+hipError_t launch_cc_cost(const CollTable &t, const echo_scenario *scen, int32_t n_scen, int64_t *cost,
+                          unsigned *status, hipStream_t stream) {
+    if (t.n == 0 || n_scen == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_cc_cost, dim3((unsigned)t.n), dim3(64), 0, stream, t, scen, n_scen, cost, status);
     return hipGetLastError();
 }
 
-hipError_t launch_walk(const WalkArgs &a, int32_t n_ranks, hipStream_t stream) {
+hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream) {
     WalkArgs args = a;
     void *params[] = {&args};
     const WalkKernel k = walk_kernel(a.factor != nullptr, a.final_pass != 0, a.digest != nullptr);
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k), dim3((unsigned)(n_ranks * a.tiles)),
-                                      dim3(kLanes), params, 0, stream);
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k), dim3((unsigned)(n_blocks * a.tiles)),
+                                      dim3(kBlockRanks * kLanes), params, 0, stream);
 }
 
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
@@ -513,19 +599,18 @@ hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t str
     return hipGetLastError();
 }
 
-hipError_t walk_capacity(int device, int64_t *waves) {
+hipError_t walk_capacity(int device, int64_t workgroups[8]) {
     int cus = 0;
     hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
     if (e != hipSuccess) return e;
-    int64_t least = INT64_MAX;
     for (int v = 0; v < 8; ++v) {
         int per_cu = 0;
         const WalkKernel k = walk_kernel(v & 1, v & 2, v & 4);
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(k), kLanes, 0);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(k),
+                                                         kBlockRanks * kLanes, 0);
         if (e != hipSuccess) return e;
-        least = std::min<int64_t>(least, (int64_t)per_cu * cus);
+        workgroups[v] = (int64_t)per_cu * cus;
     }
-    *waves = least;
     return hipSuccess;
 }
 
