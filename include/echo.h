@@ -132,6 +132,18 @@ typedef struct {
  */
 int echo_load_graph(const echo_graph_desc *desc, int hip_device, echo_graph *out);
 
+/*
+ * echo_load_graph with an explicit walker width.  The composer walks each
+ * scenario tile with one wavefront per "walker" -- `ranks_per_walker`
+ * consecutive ranks whose ops it visits in level order -- and every walker of
+ * a tile must be resident on the device at once.  0 picks the fewest ranks
+ * per walker that fit (one, unless the graph has more ranks than the device
+ * holds wavefronts); a positive value asks for at least that many (up to 16).
+ * Results do not depend on it.  Errors: as echo_load_graph; ARG for a value
+ * outside [0, 16]; RANGE when the graph does not fit at 16 ranks per walker.
+ */
+int echo_load_graph_ex(const echo_graph_desc *desc, int hip_device, int32_t ranks_per_walker, echo_graph *out);
+
 /* Sizes of a loaded graph: ops, collectives and topological levels of the merged graph. */
 int echo_graph_info(echo_graph g, int64_t *n_ops, int64_t *n_colls, int64_t *n_levels);
 

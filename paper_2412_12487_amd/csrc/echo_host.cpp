@@ -4,7 +4,8 @@
 // it validates the per-rank graphs, matches collectives (Sec. 4.2 matching
 // rules), merges every collective into one barrier node, levels the merged
 // graph with Kahn's algorithm (a cycle is a deadlocked job), and lays out one
-// level-ordered walk list per rank for the device.  echo_compose_batch is the
+// level-ordered walk list per walker (a group of consecutive ranks walked by one
+// wavefront) for the device.  echo_compose_batch is the
 // execution step: it only enqueues kernels.
 #include <hip/hip_runtime.h>
 
@@ -45,6 +46,7 @@ int hip_fail(hipError_t e, const char *what) {
 constexpr int64_t kDurLimit = int64_t(1) << 43;
 constexpr int64_t kBytesLimit = int64_t(1) << 50;
 constexpr int64_t kI32Max = INT32_MAX;
+constexpr int kMaxRanksPerWalker = 16;
 constexpr int64_t kDefaultSpinNs = 20LL * 1000 * 1000 * 1000;   // 20 s
 
 // Table 6 (all-reduce breakdown): NCCL chunk size by tensor size.  The size
@@ -94,7 +96,7 @@ hipError_t upload(T **dst, const std::vector<T> &src) {
 struct echo_graph_s {
     int device = 0;
     int64_t n_ops = 0, n_colls = 0, n_levels = 0;
-    int32_t n_ranks = 0;
+    int32_t n_ranks = 0, n_walkers = 0;
     int64_t capacity[8] = {};          // co-resident walk workgroups per kernel variant
     bool need_coll_cost = false;       // some comm op reads its cost per collective
     int64_t spin_limit = kDefaultSpinNs / 10;   // 100 MHz ticks
@@ -177,8 +179,10 @@ struct Timed {
 };
 
 // ------------------------------------------------------------------ loader
-int load(const echo_graph_desc *d, int device, echo_graph *out) {
+int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out) {
     if (!d || !out) return fail(ECHO_ERR_ARG, "null descriptor or output handle");
+    if (min_rpw < 0 || min_rpw > kMaxRanksPerWalker)
+        return fail(ECHO_ERR_ARG, "ranks_per_walker %d outside [0, %d]", min_rpw, kMaxRanksPerWalker);
     *out = nullptr;
     const int64_t n = d->n_ops, nc = d->n_colls;
     const int64_t R = d->n_ranks;
@@ -325,72 +329,6 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
             ccls[c] = it.first->second;
         }
     }
-    // rank blocks: the most used classes of a block get its LDS cost slots;
-    // collectives whose members all sit in one block meet in that block's LDS
-    const int64_t nblk = (R + kBlockRanks - 1) / kBlockRanks;
-    std::vector<int32_t> block_class(nblk * kClassSlots, -1);
-    std::vector<uint32_t> coll_aux(nc, 0);          // channel part of the aux word (local collectives)
-    std::vector<uint8_t> op_slot(n, (uint8_t)kNoSlot);
-    {
-        std::vector<int64_t> first_op(nblk + 1, n);
-        for (int64_t v = n - 1; v >= 0; --v) first_op[d->op_rank[v] / kBlockRanks] = v;
-        for (int64_t b = nblk - 1; b >= 0; --b)
-            if (first_op[b] > first_op[b + 1]) first_op[b] = first_op[b + 1];
-        std::unordered_map<int32_t, int64_t> use;
-        std::vector<std::pair<int64_t, int32_t>> order;
-        for (int64_t b = 0; b < nblk; ++b) {
-            use.clear();
-            for (int64_t v = first_op[b]; v < first_op[b + 1]; ++v)
-                if (d->op_kind[v] == ECHO_COMM) ++use[ccls[d->op_coll[v]]];
-            order.clear();
-            for (auto &kv : use) order.emplace_back(-kv.second, kv.first);
-            std::sort(order.begin(), order.end());
-            std::unordered_map<int32_t, int32_t> slot_of;
-            for (int i = 0; i < kClassSlots && i < (int)order.size(); ++i) {
-                block_class[b * kClassSlots + i] = order[i].second;
-                slot_of[order[i].second] = i;
-            }
-            for (int64_t v = first_op[b]; v < first_op[b + 1]; ++v)
-                if (d->op_kind[v] == ECHO_COMM) {
-                    auto it = slot_of.find(ccls[d->op_coll[v]]);
-                    if (it != slot_of.end()) op_slot[v] = (uint8_t)it->second;
-                }
-        }
-        // channels: one per communicator of a block whose collectives are all local
-        std::map<std::pair<int64_t, int32_t>, int32_t> channel;   // (block, communicator) -> channel
-        std::vector<int32_t> used(nblk, 0);
-        for (int64_t c = 0; c < nc; ++c) {
-            const int64_t b0 = d->op_rank[mem[moff[c]]] / kBlockRanks;
-            bool local = true;
-            for (int64_t j = moff[c]; j < moff[c + 1]; ++j)
-                local = local && d->op_rank[mem[j]] / kBlockRanks == b0;
-            const int64_t expected = (int64_t)cN[c] * (pos[c] / 2 + 1);
-            if (!local || expected >= (int64_t(1) << kExpectedBits)) continue;
-            auto it = channel.find({b0, cid[c]});
-            if (it == channel.end()) {
-                if (used[b0] >= kChannels) continue;                 // out of channels: meet globally
-                it = channel.emplace(std::make_pair(b0, cid[c]), used[b0]++).first;
-            }
-            coll_aux[c] = kAuxLocal | ((uint32_t)it->second << 1) | ((uint32_t)(pos[c] & 1) << 4) |
-                          ((uint32_t)expected << 9);
-        }
-        // a communicator is local for all its collectives or none: drop channels whose
-        // communicator also has a collective that could not be met locally
-        std::map<std::pair<int64_t, int32_t>, bool> ok;
-        for (int64_t c = 0; c < nc; ++c) {
-            const int64_t b0 = d->op_rank[mem[moff[c]]] / kBlockRanks;
-            auto it = channel.find({b0, cid[c]});
-            if (it == channel.end()) continue;
-            auto &flag = ok.emplace(std::make_pair(b0, cid[c]), true).first->second;
-            if (!(coll_aux[c] & kAuxLocal)) flag = false;
-        }
-        for (int64_t c = 0; c < nc; ++c) {
-            const int64_t b0 = d->op_rank[mem[moff[c]]] / kBlockRanks;
-            auto it = ok.find({b0, cid[c]});
-            if (it != ok.end() && !it->second) coll_aux[c] = 0;
-        }
-    }
-
     // Kahn levels of the merged graph: node v for a compute/memcpy op,
     // node n + c for collective c (all its member ops).
     const int64_t nn = n + nc;
@@ -435,8 +373,94 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
     std::vector<int64_t>().swap(succ);
     std::vector<int64_t>().swap(soff);
 
-    // walk lists: each rank's ops by (key, program order), key = level for
-    // compute/memcpy, the launch level for a comm op
+    // walkers: every walk workgroup of a scenario tile must be co-resident, so a
+    // graph with more ranks than the device holds wavefronts walks several
+    // consecutive ranks per wavefront
+    hipError_t e = hipSetDevice(device);
+    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+    int64_t capacity[8];
+    e = walk_capacity(device, capacity);
+    if (e != hipSuccess) return hip_fail(e, "occupancy query");
+    const int64_t least = *std::min_element(capacity, capacity + 8);
+    int64_t rpw = std::max<int64_t>(1, min_rpw);       // ranks per walker
+    while (rpw <= kMaxRanksPerWalker &&
+           ((R + rpw - 1) / rpw + kBlockWalkers - 1) / kBlockWalkers > least)
+        ++rpw;
+    if (rpw > kMaxRanksPerWalker)
+        return fail(ECHO_ERR_RANGE, "%lld ranks do not fit %lld co-resident walk workgroups of %d wavefronts "
+                    "at %d ranks per wavefront", (long long)R, (long long)least, kBlockWalkers, kMaxRanksPerWalker);
+    const int64_t W = (R + rpw - 1) / rpw;             // walkers
+    const int64_t rpb = rpw * kBlockWalkers;           // ranks per workgroup
+
+    // rank blocks (the ranks of one workgroup): the most used classes of a block
+    // get its LDS cost slots; collectives whose members all sit in one block meet
+    // in that block's LDS
+    const int64_t nblk = (W + kBlockWalkers - 1) / kBlockWalkers;
+    std::vector<int32_t> block_class(nblk * kClassSlots, -1);
+    std::vector<uint32_t> coll_aux(nc, 0);          // channel part of the aux word (local collectives)
+    std::vector<uint8_t> op_slot(n, (uint8_t)kNoSlot);
+    {
+        std::vector<int64_t> first_op(nblk + 1, n);
+        for (int64_t v = n - 1; v >= 0; --v) first_op[d->op_rank[v] / rpb] = v;
+        for (int64_t b = nblk - 1; b >= 0; --b)
+            if (first_op[b] > first_op[b + 1]) first_op[b] = first_op[b + 1];
+        std::unordered_map<int32_t, int64_t> use;
+        std::vector<std::pair<int64_t, int32_t>> order;
+        for (int64_t b = 0; b < nblk; ++b) {
+            use.clear();
+            for (int64_t v = first_op[b]; v < first_op[b + 1]; ++v)
+                if (d->op_kind[v] == ECHO_COMM) ++use[ccls[d->op_coll[v]]];
+            order.clear();
+            for (auto &kv : use) order.emplace_back(-kv.second, kv.first);
+            std::sort(order.begin(), order.end());
+            std::unordered_map<int32_t, int32_t> slot_of;
+            for (int i = 0; i < kClassSlots && i < (int)order.size(); ++i) {
+                block_class[b * kClassSlots + i] = order[i].second;
+                slot_of[order[i].second] = i;
+            }
+            for (int64_t v = first_op[b]; v < first_op[b + 1]; ++v)
+                if (d->op_kind[v] == ECHO_COMM) {
+                    auto it = slot_of.find(ccls[d->op_coll[v]]);
+                    if (it != slot_of.end()) op_slot[v] = (uint8_t)it->second;
+                }
+        }
+        // channels: one per communicator of a block whose collectives are all local
+        std::map<std::pair<int64_t, int32_t>, int32_t> channel;   // (block, communicator) -> channel
+        std::vector<int32_t> used(nblk, 0);
+        for (int64_t c = 0; c < nc; ++c) {
+            const int64_t b0 = d->op_rank[mem[moff[c]]] / rpb;
+            bool local = true;
+            for (int64_t j = moff[c]; j < moff[c + 1]; ++j)
+                local = local && d->op_rank[mem[j]] / rpb == b0;
+            const int64_t expected = (int64_t)cN[c] * (pos[c] / 2 + 1);
+            if (!local || expected >= (int64_t(1) << kExpectedBits)) continue;
+            auto it = channel.find({b0, cid[c]});
+            if (it == channel.end()) {
+                if (used[b0] >= kChannels) continue;                 // out of channels: meet globally
+                it = channel.emplace(std::make_pair(b0, cid[c]), used[b0]++).first;
+            }
+            coll_aux[c] = kAuxLocal | ((uint32_t)it->second << 1) | ((uint32_t)(pos[c] & 1) << 4) |
+                          ((uint32_t)expected << 9);
+        }
+        // a communicator is local for all its collectives or none: drop channels whose
+        // communicator also has a collective that could not be met locally
+        std::map<std::pair<int64_t, int32_t>, bool> ok;
+        for (int64_t c = 0; c < nc; ++c) {
+            const int64_t b0 = d->op_rank[mem[moff[c]]] / rpb;
+            auto it = channel.find({b0, cid[c]});
+            if (it == channel.end()) continue;
+            auto &flag = ok.emplace(std::make_pair(b0, cid[c]), true).first->second;
+            if (!(coll_aux[c] & kAuxLocal)) flag = false;
+        }
+        for (int64_t c = 0; c < nc; ++c) {
+            const int64_t b0 = d->op_rank[mem[moff[c]]] / rpb;
+            auto it = ok.find({b0, cid[c]});
+            if (it != ok.end() && !it->second) coll_aux[c] = 0;
+        }
+    }
+
+    // walk lists: each walker's ops by (key, rank, program order), key = level
+    // for compute/memcpy, the launch level for a comm op
     std::vector<int32_t> key(n);
     for (int64_t v = 0; v < n; ++v) {
         if (d->op_kind[v] == ECHO_COMM) {
@@ -447,47 +471,113 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
             key[v] = level[v];
         }
     }
-    std::vector<int64_t> rank_off(R + 1, 0);
-    for (int64_t v = 0; v < n; ++v) ++rank_off[d->op_rank[v] + 1];
-    for (int64_t r = 0; r < R; ++r) rank_off[r + 1] += rank_off[r];
+    std::vector<int64_t> op_off(W + 1, 0);            // ops of walker w: [op_off[w], op_off[w + 1])
+    for (int64_t v = 0; v < n; ++v) ++op_off[d->op_rank[v] / rpw + 1];
+    for (int64_t w = 0; w < W; ++w) op_off[w + 1] += op_off[w];
     std::vector<int32_t> order(n);
     for (int64_t v = 0; v < n; ++v) order[v] = (int32_t)v;   // rank-major already
-    for (int64_t r = 0; r < R; ++r)
-        std::stable_sort(order.begin() + rank_off[r], order.begin() + rank_off[r + 1],
+    for (int64_t w = 0; w < W; ++w)
+        std::stable_sort(order.begin() + op_off[w], order.begin() + op_off[w + 1],
                          [&](int32_t x, int32_t y) { return key[x] < key[y]; });
-    std::vector<WalkItem> items(n);
+    std::vector<WalkItem> items;
+    items.reserve(n);
+    std::vector<int64_t> walk_off(W + 1, 0);
     std::vector<int32_t> far;
     {
+        const int npair = (int)(rpw * kStreams);       // (rank, stream) pairs of a walker
         std::vector<int32_t> latest(kStreams);
-        std::vector<int64_t> busy(kStreams);
-        int slot[kStreams];
-        for (int64_t r = 0; r < R; ++r) {
-            // slot 0 = the stream with the most compute/memcpy ops; the rest keep their order
+        std::vector<int64_t> busy(npair), total(npair);
+        std::vector<int> slot(npair);
+        std::vector<uint8_t> noreg(n, 0);
+        std::vector<int32_t> first_succ;                // walk position of the first successor
+        std::vector<int32_t> due;                       // kNoReg comm ops, by first successor
+        std::vector<std::pair<int32_t, int32_t>> sched;
+        auto pair_of = [&](int64_t v, int64_t r0) { return (int)((d->op_rank[v] - r0) * kStreams + d->op_stream[v]); };
+        auto emit_resolve = [&](int32_t v) {
+            WalkItem it{};
+            it.op = v;
+            it.meta = (uint32_t)kResolve | kNoReg;
+            it.far_off = (int32_t)far.size();
+            it.coll = (int32_t)d->op_coll[v];
+            it.dur = 0;
+            it.nfar = 0;
+            it.aux = coll_aux[d->op_coll[v]] | ((uint32_t)op_slot[v] << 5);
+            items.push_back(it);
+        };
+        for (int64_t w = 0; w < W; ++w) {
+            const int64_t r0 = w * rpw, lo = op_off[w], hi = op_off[w + 1];
+            // slot 0 = the pair with the most compute/memcpy ops; one rank per walker:
+            // the other streams keep their order; several: the busiest pairs get slots
             std::fill(busy.begin(), busy.end(), 0);
-            for (int64_t i = rank_off[r]; i < rank_off[r + 1]; ++i)
-                if (d->op_kind[i] != ECHO_COMM) ++busy[d->op_stream[i]];
+            std::fill(total.begin(), total.end(), 0);
+            for (int64_t i = lo; i < hi; ++i) {
+                ++total[pair_of(i, r0)];
+                if (d->op_kind[i] != ECHO_COMM) ++busy[pair_of(i, r0)];
+            }
             const int top = int(std::max_element(busy.begin(), busy.end()) - busy.begin());
-            for (int k = 0, next = 1; k < kStreams; ++k) slot[k] = k == top ? 0 : next++;
+            if (rpw == 1) {
+                for (int k = 0, next = 1; k < kStreams; ++k) slot[k] = k == top ? 0 : next++;
+            } else {
+                std::vector<int> rest;
+                for (int k = 0; k < npair; ++k)
+                    if (k != top && total[k] > 0) rest.push_back(k);
+                std::stable_sort(rest.begin(), rest.end(), [&](int x, int y) { return total[x] > total[y]; });
+                std::fill(slot.begin(), slot.end(), -1);
+                slot[top] = 0;
+                for (int k = 0; k < (int)rest.size(); ++k) slot[rest[k]] = k + 1 < kStreams ? k + 1 : -1;
+            }
+            for (int64_t i = lo; i < hi; ++i) noreg[i] = slot[pair_of(i, r0)] < 0;
+            // comm ops without a slot are finished by a resolve item placed before
+            // their first successor in the walk (or at its end)
+            sched.clear();
+            if (rpw > 1) {
+                if (first_succ.empty()) first_succ.assign(n, -1);
+                for (int64_t i = lo; i < hi; ++i) {
+                    const int32_t v = order[i];
+                    for (int32_t j = poff[v]; j < poff[v + 1]; ++j) {
+                        const int32_t u = preds[j];
+                        if (d->op_kind[u] == ECHO_COMM && noreg[u] && first_succ[u] < 0) {
+                            first_succ[u] = (int32_t)(i - lo);
+                            sched.emplace_back((int32_t)(i - lo), u);
+                        }
+                    }
+                }
+                for (int64_t i = lo; i < hi; ++i) {
+                    const int32_t v = order[i];
+                    if (d->op_kind[v] == ECHO_COMM && noreg[v] && first_succ[v] < 0)
+                        sched.emplace_back((int32_t)(hi - lo), v);
+                }
+                std::stable_sort(sched.begin(), sched.end(),
+                                 [](const std::pair<int32_t, int32_t> &x, const std::pair<int32_t, int32_t> &y) {
+                                     return x.first < y.first;
+                                 });
+            }
+            size_t next_due = 0;
             std::fill(latest.begin(), latest.end(), -1);
-            for (int64_t i = rank_off[r]; i < rank_off[r + 1]; ++i) {
+            for (int64_t i = lo; i < hi; ++i) {
+                while (next_due < sched.size() && sched[next_due].first == i - lo) emit_resolve(sched[next_due++].second);
                 const int32_t v = order[i];
                 unsigned mask = 0;
                 const int64_t f0 = (int64_t)far.size();
                 for (int32_t j = poff[v]; j < poff[v + 1]; ++j) {
                     const int32_t u = preds[j];
-                    const int su = slot[d->op_stream[u]];
-                    if (latest[su] == u) mask |= 1u << su;
+                    const int su = slot[pair_of(u, r0)];
+                    if (su >= 0 && latest[su] == u) mask |= 1u << su;
                     else far.push_back(u);
                 }
-                const int sv = slot[d->op_stream[v]];
-                const int32_t prev = latest[sv];
-                latest[sv] = v;
+                const int sv = slot[pair_of(v, r0)];
+                int32_t prev = -1;
+                if (sv >= 0) {
+                    prev = latest[sv];
+                    latest[sv] = v;
+                }
                 const bool fast = d->op_kind[v] != ECHO_COMM && sv == 0 && (mask & ~1u) == 0 &&
                                   (int64_t)far.size() == f0 && (prev < 0 || d->op_kind[prev] != ECHO_COMM);
-                WalkItem &it = items[i];
+                WalkItem it{};
                 it.op = v;
-                it.meta = (uint32_t)d->op_kind[v] | ((uint32_t)sv << 2) | ((uint32_t)d->op_class[v] << 5) |
-                          (mask << 8) | (fast ? kFast : 0u);
+                it.meta = (uint32_t)d->op_kind[v] | ((uint32_t)(sv >= 0 ? sv : 0) << 2) |
+                          ((uint32_t)d->op_class[v] << 5) | (mask << 8) | (fast ? kFast : 0u) |
+                          (sv < 0 ? kNoReg : 0u);
                 it.nfar = (int32_t)((int64_t)far.size() - f0);
                 it.far_off = (int32_t)f0;
                 it.coll = d->op_kind[v] == ECHO_COMM ? (int32_t)d->op_coll[v] : -1;
@@ -495,9 +585,14 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
                              ? coll_aux[d->op_coll[v]] | ((uint32_t)op_slot[v] << 5)
                              : 0u;
                 it.dur = d->op_kind[v] == ECHO_COMM ? 0 : d->op_dur_ns[v];
+                items.push_back(it);
             }
+            while (next_due < sched.size()) emit_resolve(sched[next_due++].second);
+            walk_off[w + 1] = (int64_t)items.size();
         }
     }
+    if ((int64_t)far.size() > kI32Max || (int64_t)items.size() > kI32Max)
+        return fail(ECHO_ERR_RANGE, "walk lists exceed 2^31 entries");
 
     // per (rank, stream) comm and compute op lists in program order
     std::vector<int64_t> cl_off(R * kStreams + 1, 0), cp_off(R * kStreams + 1, 0);
@@ -548,15 +643,13 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
     g->n_colls = nc;
     g->n_levels = n_levels;
     g->n_ranks = (int32_t)R;
-    hipError_t e = hipSetDevice(device);
-    if (e != hipSuccess) {
-        delete g;
-        return hip_fail(e, "hipSetDevice");
-    }
+    g->n_walkers = (int32_t)W;
+    std::copy(capacity, capacity + 8, g->capacity);
     DeviceGraph &dg = g->dg;
     dg.n_ops = n;
     dg.n_colls = nc;
     dg.n_ranks = (int32_t)R;
+    dg.n_walkers = (int32_t)W;
     dg.n_blocks = (int32_t)nblk;
     g->need_coll_cost = need_coll_cost;
 #define UP(dst, src)                                                        \
@@ -570,7 +663,7 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
         }                                                                   \
     } while (0)
     UP(dg.items, items);
-    UP(dg.rank_off, rank_off);
+    UP(dg.walk_off, walk_off);
     UP(dg.far, far);
     for (int t = 0; t < 2; ++t) {
         HostCollTable &h = t == 0 ? colls : cls;
@@ -593,20 +686,6 @@ int load(const echo_graph_desc *d, int device, echo_graph *out) {
     UP(dg.cp, cp);
     UP(dg.status, std::vector<unsigned>(1, 0u));
 #undef UP
-    e = walk_capacity(device, g->capacity);
-    if (e != hipSuccess) {
-        free_graph(g);
-        return hip_fail(e, "occupancy query");
-    }
-    int64_t least = INT64_MAX;
-    for (int v = 0; v < 8; ++v) least = std::min(least, g->capacity[v]);
-    if (least < nblk) {
-        const int64_t cap = least;
-        free_graph(g);
-        return fail(ECHO_ERR_RANGE,
-                    "%lld ranks need %lld co-resident walk workgroups of %d ranks; the device holds %lld",
-                    (long long)R, (long long)nblk, kBlockRanks, (long long)cap);
-    }
     *out = g;
     return ECHO_OK;
 }
@@ -664,7 +743,7 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
         for (int64_t t0 = 0; t0 < n_tiles; t0 += per_launch) {
             WalkArgs a;
             a.items = g->dg.items;
-            a.rank_off = g->dg.rank_off;
+            a.walk_off = g->dg.walk_off;
             a.far = g->dg.far;
             a.c_N = g->dg.colls.N;
             a.block_class = g->dg.block_class;
@@ -684,7 +763,7 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
             a.n_tiles = n_tiles;
             a.tile0 = (int32_t)t0;
             a.tiles = (int32_t)std::min<int64_t>(per_launch, n_tiles - t0);
-            a.n_ranks = g->n_ranks;
+            a.n_walkers = g->n_walkers;
             a.final_pass = p == n_refine;
             if (g->n_ranks == 0 || g->n_ops == 0) continue;
             TIMED(ECHO_K_WALK, launch_walk(a, g->dg.n_blocks, stream), "walk kernel");
@@ -698,15 +777,19 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
 
 extern "C" {
 
-int echo_load_graph(const echo_graph_desc *desc, int hip_device, echo_graph *out) {
+int echo_load_graph_ex(const echo_graph_desc *desc, int hip_device, int32_t ranks_per_walker, echo_graph *out) {
     g_last_error.clear();
     try {
-        return load(desc, hip_device, out);
+        return load(desc, hip_device, ranks_per_walker, out);
     } catch (const std::bad_alloc &) {
         return fail(ECHO_ERR_NOMEM, "host allocation failed while loading the graph");
     } catch (...) {
         return fail(ECHO_ERR_ARG, "unexpected exception while loading the graph");
     }
+}
+
+int echo_load_graph(const echo_graph_desc *desc, int hip_device, echo_graph *out) {
+    return echo_load_graph_ex(desc, hip_device, 0, out);
 }
 
 int echo_graph_info(echo_graph g, int64_t *n_ops, int64_t *n_colls, int64_t *n_levels) {

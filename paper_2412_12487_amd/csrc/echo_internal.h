@@ -1,13 +1,16 @@
 // echo_internal.h -- device data layout and kernel launchers of libecho.so.
 //
-// The loader turns the caller's per-rank graphs into one "walk list" per rank:
-// that rank's ops ordered by (key, program order) where key is the op's
+// The loader turns the caller's per-rank graphs into one "walk list" per
+// walker: a walker is a group of consecutive ranks (one rank unless the graph
+// has more ranks than the device holds co-resident wavefronts), and its list
+// holds their ops ordered by (key, rank, program order) where key is the op's
 // topological level in the merged graph (a collective merged into one barrier
 // node) -- for a comm op, the level at which it can launch.  A wavefront walks
-// one rank for 64 scenarios (one lane each); predecessors that are the latest
-// op of their stream stay in registers, the rest are read back from the
-// finish array.  Collective barriers are met through per-(collective,
-// scenario) arrival maxima and per-(collective, scenario tile) arrival counts.
+// one walker for 64 scenarios (one lane each); predecessors that are the
+// latest op of a register slot stay in registers, the rest are read back from
+// the finish array.  Collective barriers are met through per-(collective,
+// scenario) arrival maxima and per-(collective, scenario tile) arrival counts,
+// or in LDS when every member sits in one workgroup.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -29,12 +32,16 @@ constexpr unsigned kStatusOverflow = 2u;         // a time reached 2^62
 constexpr unsigned kStatusTimeout = 4u;          // a barrier wait exceeded the spin limit
 constexpr unsigned kStatusAbort = 8u;            // stop all waits (set with timeout)
 
-// One entry of a rank's walk list (32 bytes, read wave-uniformly).  Streams
-// are renumbered per rank into "slots": slot 0 is the rank's busiest
-// compute/memcpy stream, so most items only touch slot 0.
+// One entry of a walk list (32 bytes, read wave-uniformly).  The (rank,
+// stream) pairs of a walker are mapped to eight register "slots": slot 0 is
+// its busiest compute/memcpy stream, so most items only touch slot 0.  Pairs
+// left without a slot (a walker of several ranks) keep nothing in registers:
+// their ops carry kNoReg, their successors read them back from memory, and a
+// comm op among them is finished by a resolve item placed before its first
+// successor.
 struct WalkItem {
     int32_t op;         // op id: row of the [op][scenario] outputs
-    uint32_t meta;      // kind | slot << 2 | class << 5 | regmask << 8 | fast << 16
+    uint32_t meta;      // kind | slot << 2 | class << 5 | regmask << 8 | fast << 16 | noreg << 17
     int32_t far_off;    // predecessors read back from memory: far[far_off .. +nfar)
     int32_t coll;       // collective of a comm op, -1 otherwise
     int64_t dur;        // base duration of compute / memcpy ops
@@ -46,14 +53,19 @@ static_assert(sizeof(WalkItem) == 32, "walk item must stay 32 bytes");
 // A "fast" item is a compute/memcpy op on slot 0 whose only predecessor is
 // the previous op of slot 0, itself not a comm op: its start is that op's finish.
 constexpr uint32_t kFast = 1u << 16;
+// The op's (rank, stream) pair has no register slot.
+constexpr uint32_t kNoReg = 1u << 17;
+// Item kind (besides compute/comm/memcpy) that finishes a kNoReg comm op:
+// wait for its barrier, then write its finish.
+constexpr int kResolve = 3;
 
-// Workgroups walk kBlockRanks consecutive ranks (one wavefront each) for one
-// scenario tile.  A collective whose members all sit in one block is met in
+// Workgroups walk kBlockWalkers consecutive walkers (one wavefront each) for
+// one scenario tile.  A collective whose members all sit in one block is met in
 // LDS: each communicator of the block owns a channel with two alternating
 // slots (max of launch times per lane, arrival count).  Collective costs are
 // looked up per cost class -- the (type, S, N, M, K) tuple that fixes T(c, s)
 // for a scenario -- and a block stages its most used classes in LDS.
-constexpr int kBlockRanks = 8;
+constexpr int kBlockWalkers = 8;
 constexpr int kChannels = 8;          // LDS barrier channels per block
 constexpr int kClassSlots = 8;        // LDS cost classes per block
 constexpr uint32_t kNoSlot = 15;
@@ -96,9 +108,9 @@ struct CollTable {
 // Device copy of a loaded graph (all pointers are device memory).
 struct DeviceGraph {
     int64_t n_ops = 0, n_colls = 0;
-    int32_t n_ranks = 0, n_blocks = 0;
-    WalkItem *items = nullptr;       // walk lists, rank-major
-    int64_t *rank_off = nullptr;     // [n_ranks + 1] offsets into items
+    int32_t n_ranks = 0, n_walkers = 0, n_blocks = 0;
+    WalkItem *items = nullptr;       // walk lists, walker-major
+    int64_t *walk_off = nullptr;     // [n_walkers + 1] offsets into items
     int32_t *far = nullptr;          // far predecessor op ids
     CollTable colls;                 // every collective
     CollTable classes;               // every cost class
@@ -114,7 +126,7 @@ struct DeviceGraph {
 
 struct WalkArgs {
     const WalkItem *items;
-    const int64_t *rank_off;
+    const int64_t *walk_off;
     const int32_t *far;
     const int32_t *c_N;
     const int32_t *block_class;
@@ -131,7 +143,7 @@ struct WalkArgs {
     int64_t spin_limit;              // wall-clock ticks (100 MHz) before a wait gives up
     int32_t n_scen, n_tiles;
     int32_t tile0, tiles;            // tiles handled by this launch
-    int32_t n_ranks;
+    int32_t n_walkers;
     int32_t final_pass;              // accumulate step time (and digest)
 };
 
@@ -158,7 +170,7 @@ hipError_t launch_cc_cost(const CollTable &t, const echo_scenario *scen, int32_t
                           unsigned *status, hipStream_t stream);
 hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream);
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream);
-// Co-resident walk workgroups (kBlockRanks wavefronts each) the device can hold,
+// Co-resident walk workgroups (kBlockWalkers wavefronts each) the device can hold,
 // for each of the 8 kernel variants (bit 0 refined, bit 1 final, bit 2 digest).
 hipError_t walk_capacity(int device, int64_t workgroups[8]);
 inline int walk_variant(bool refined, bool final_pass, bool digest) {

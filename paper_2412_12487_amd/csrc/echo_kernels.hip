@@ -4,8 +4,8 @@
 //   k_clear    clear barrier state between passes
 //   k_cc_cost  CC estimator (Sec. 5.3, Eq. 2-5): one lane per (collective, scenario)
 //   k_walk     timeline composer (Sec. 4.2) with the collective synchronisation
-//              rule (Sec. 5.2): one wavefront per (rank, 64-scenario tile) walks
-//              the rank's ops in level order, max-plus relaxation in registers
+//              rule (Sec. 5.2): one wavefront per (walker, 64-scenario tile) walks
+//              the ops of its ranks in level order, max-plus relaxation in registers
 //   k_overlap  validator input (Sec. 6): per compute op and scenario, the largest
 //              slowdown factor over the comm ops of its rank that overlap it
 //
@@ -186,23 +186,23 @@ __device__ bool wait_local(const unsigned *cnt, unsigned need, unsigned *status,
     }
 }
 
-// A workgroup of kBlockRanks wavefronts walks the ranks of one block for one
-// 64-scenario tile; wavefront w walks rank block * kBlockRanks + w.  REFINED:
+// A workgroup of kBlockWalkers wavefronts walks the walkers of one block for
+// one 64-scenario tile; wavefront w walks walker block * kBlockWalkers + w.  REFINED:
 // the pass inflates compute ops by the factors of the previous pass's
 // overlaps.  FINAL: the pass produces the step time (and DIGEST: the digest).
 template <bool REFINED, bool FINAL, bool DIGEST>
-__global__ __launch_bounds__(kBlockRanks * 64) void k_walk(WalkArgs a) {
-    __shared__ uint32_t fstage[REFINED ? kBlockRanks * kBlock * kLanes : 1];
+__global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
+    __shared__ uint32_t fstage[REFINED ? kBlockWalkers * kBlock * kLanes : 1];
     __shared__ unsigned long long lbar[kChannels][2][kLanes];   // per channel and slot: latest launch per lane
     __shared__ unsigned lcnt[kChannels][2];                      // per channel and slot: members arrived
     __shared__ int64_t ccost[kClassSlots][kLanes];               // staged class costs of this tile
-    __shared__ int32_t pinfo[kBlockRanks][kStreams][3];          // per wave and slot: pending collective, op, aux
+    __shared__ int32_t pinfo[kBlockWalkers][kStreams][3];          // per wave and slot: pending collective, op, aux
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform within a wavefront
     const int32_t blk = blockIdx.x / a.tiles;
     const int32_t tile = a.tile0 + blockIdx.x % a.tiles;
-    const int32_t r = blk * kBlockRanks + wave;
+    const int32_t w = blk * kBlockWalkers + wave;
     const bool active = tile * kLanes + lane < a.n_scen;
     // Idle lanes of the last tile mirror its last scenario: they compute the same
     // values and store them to the same places; only active lanes issue global atomics.
@@ -219,7 +219,7 @@ __global__ __launch_bounds__(kBlockRanks * 64) void k_walk(WalkArgs a) {
         ccost[wave][lane] = cls >= 0 ? a.class_cost[(int64_t)cls * ns + sigma] : 0;
     }
     __syncthreads();
-    if (r >= a.n_ranks) return;
+    if (w >= a.n_walkers) return;
 
     const echo_scenario *sc = a.scen + sigma;
     const uint64_t jbase = jitter_base(sc->jitter_seed, sc->jitter_stream);
@@ -240,52 +240,59 @@ __global__ __launch_bounds__(kBlockRanks * 64) void k_walk(WalkArgs a) {
     // list without waiting again; the times it writes are meaningless and the
     // status word already reports the failure.
     bool dead = false;
+    int64_t xmax = 0;            // latest finish among ops kept out of the register slots
     uint64_t dig = 0;
     uint32_t hi_or = 0;          // OR of the high words of every time: bit 30 set <=> some time >= 2^62
     unsigned err = 0;
-    const int64_t beg = a.rank_off[r], end = a.rank_off[r + 1];
+    const int64_t beg = a.walk_off[w], end = a.walk_off[w + 1];
     // lane j < 32 holds the first half of item j of the round, lane 32 + j its second half
     const int4 *items4 = reinterpret_cast<const int4 *>(a.items);
     const int half = lane >> 5, slotl = lane & 31;
     // lanes past the end of the list hold op 0, so staged factor loads stay in bounds
     int4 nxt = beg + slotl < end ? items4[2 * (beg + slotl) + half] : make_int4(0, 0, 0, 0);
 
-// Finish of the comm op pending on slot j: barrier (latest member launch) + cost.
-#define RESOLVE(j)                                                                               \
-    if (pending & (1u << j)) {                                                                   \
-        const int64_t c_ = __builtin_amdgcn_readfirstlane(pend[j][0]);                          \
-        const int32_t v_ = __builtin_amdgcn_readfirstlane(pend[j][1]);                          \
-        const uint32_t x_ = (uint32_t)__builtin_amdgcn_readfirstlane(pend[j][2]);               \
+// Finish f_ of comm op v_ (collective c_, aux word x_): its barrier -- the
+// latest member launch -- plus the collective's cost; written to the finish array.
+#define MEET(c_, v_, x_, f_)                                                                     \
+    {                                                                                            \
         uint64_t b_ = 0;                                                                         \
-        if (x_ & kAuxLocal) {                                                                    \
+        if ((x_) & kAuxLocal) {                                                                  \
             const int ch_ = aux_channel(x_), par_ = aux_parity(x_);                              \
             if (!dead && !__builtin_amdgcn_readfirstlane(                                        \
                              wait_local(&lcnt[ch_][par_], aux_expected(x_), a.status, a.spin_limit))) \
                 dead = true;                                                                     \
             b_ = lbar[ch_][par_][lane];                                                          \
         } else {                                                                                 \
-            if (!dead && !__builtin_amdgcn_readfirstlane(wait_arrivals(tile_count + c_ * a.n_tiles, \
+            if (!dead && !__builtin_amdgcn_readfirstlane(wait_arrivals(tile_count + (int64_t)(c_) * a.n_tiles, \
                                                                        (unsigned)a.c_N[c_], a.status, \
                                                                        a.spin_limit)))           \
                 dead = true;                                                                     \
             if (active)                                                                          \
-                b_ = __hip_atomic_fetch_max(a.arrive + c_ * ns + sigma, 0ull, __ATOMIC_RELAXED,  \
-                                            __HIP_MEMORY_SCOPE_AGENT);                           \
+                b_ = __hip_atomic_fetch_max(a.arrive + (int64_t)(c_) * ns + sigma, 0ull,         \
+                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);         \
             b_ = mirror ? (uint64_t)__shfl((long long)b_, col) : b_;                             \
         }                                                                                        \
         const int sl_ = aux_slot(x_);                                                            \
         /* distinct load kinds keep the two reads from merging into one flat load */            \
         const int64_t t_ = sl_ < kClassSlots ? ccost[sl_][lane]                                  \
-                                             : __hip_atomic_load(a.cost + c_ * ns + sigma,         \
+                                             : __hip_atomic_load(a.cost + (int64_t)(c_) * ns + sigma, \
                                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); \
-        const int64_t f_ = (int64_t)b_ + t_;                                                     \
-        hi_or |= (uint32_t)((uint64_t)f_ >> 32);                                                 \
-        (fbase + (int64_t)v_ * ns)[col] = f_;                                                    \
+        f_ = (int64_t)b_ + t_;                                                                   \
+        hi_or |= (uint32_t)((uint64_t)(f_) >> 32);                                               \
+        (fbase + (int64_t)(v_) * ns)[col] = f_;                                                  \
         if (DIGEST) {                                                                            \
-            const int64_t s_ = (sbase + (int64_t)v_ * ns)[col];                                  \
-            dig += mix64(mix64((uint64_t)v_ ^ (uint64_t)s_) ^ (uint64_t)f_);                     \
+            const int64_t s_ = (sbase + (int64_t)(v_) * ns)[col];                                \
+            dig += mix64(mix64((uint64_t)(v_) ^ (uint64_t)s_) ^ (uint64_t)(f_));                 \
         }                                                                                        \
-        lf[j] = f_;                                                                              \
+    }
+
+// Finish of the comm op pending on slot j.
+#define RESOLVE(j)                                                                               \
+    if (pending & (1u << j)) {                                                                   \
+        const int32_t pc_ = __builtin_amdgcn_readfirstlane(pend[j][0]);                          \
+        const int32_t pv_ = __builtin_amdgcn_readfirstlane(pend[j][1]);                          \
+        const uint32_t px_ = (uint32_t)__builtin_amdgcn_readfirstlane(pend[j][2]);               \
+        MEET(pc_, pv_, px_, lf[j])                                                               \
         pending &= ~(1u << j);                                                                   \
     }
 
@@ -340,6 +347,14 @@ __global__ __launch_bounds__(kBlockRanks * 64) void k_walk(WalkArgs a) {
             const int32_t coll = __builtin_amdgcn_readlane(cur.w, j);
             const int32_t nfar = __builtin_amdgcn_readlane(cur.z, j + 32);
             const uint32_t aux = (uint32_t)__builtin_amdgcn_readlane(cur.w, j + 32);
+            if (kind == kResolve) {
+                // a comm op without a register slot: its barrier is due before its first successor
+                int64_t f;
+                MEET(coll, op, aux, f)
+                xmax = f > xmax ? f : xmax;
+                ++j;
+                continue;
+            }
             const int st = item_stream(meta);
             const unsigned mask = item_regmask(meta);
             int64_t ready = 0;
@@ -374,12 +389,14 @@ __global__ __launch_bounds__(kBlockRanks * 64) void k_walk(WalkArgs a) {
                         __hip_atomic_fetch_add(a.count + (int64_t)coll * a.n_tiles + tile, 1u, __ATOMIC_RELAXED,
                                                __HIP_MEMORY_SCOPE_AGENT);
                 }
-                if (lane == 0) {
-                    pend[st][0] = coll;
-                    pend[st][1] = op;
-                    pend[st][2] = (int32_t)aux;
+                if (!(meta & kNoReg)) {
+                    if (lane == 0) {
+                        pend[st][0] = coll;
+                        pend[st][1] = op;
+                        pend[st][2] = (int32_t)aux;
+                    }
+                    pending |= 1u << st;
                 }
-                pending |= 1u << st;
             } else {
                 int64_t d = amp != 0 ? jittered(dur, op, jbase, amp) : dur;
                 if (REFINED && kind == ECHO_COMPUTE) d = q16(d, fst[j * kLanes + lane]);
@@ -387,9 +404,13 @@ __global__ __launch_bounds__(kBlockRanks * 64) void k_walk(WalkArgs a) {
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 (fbase + (int64_t)op * ns)[col] = f;
                 if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)ready) ^ (uint64_t)f);
+                if (meta & kNoReg) {
+                    xmax = f > xmax ? f : xmax;
+                } else {
 #pragma unroll
-                for (int q = 0; q < kStreams; ++q)
-                    if (q == st) lf[q] = f;
+                    for (int q = 0; q < kStreams; ++q)
+                        if (q == st) lf[q] = f;
+                }
             }
             ++j;
         }
@@ -397,11 +418,13 @@ __global__ __launch_bounds__(kBlockRanks * 64) void k_walk(WalkArgs a) {
 #pragma unroll
     for (int q = 0; q < kStreams; ++q) { RESOLVE(q) }
 #undef RESOLVE
+#undef MEET
     if (hi_or >> 30) err |= kStatusOverflow;
     if (active && err) __hip_atomic_fetch_or(a.status, err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (FINAL && active && !dead) {
-        // finishes along a FIFO stream never decrease: the last op of each slot holds its maximum
-        int64_t smax = 0;
+        // finishes along a FIFO stream never decrease: the last op of each slot holds its
+        // maximum; ops without a slot went into xmax
+        int64_t smax = xmax;
 #pragma unroll
         for (int q = 0; q < kStreams; ++q) smax = lf[q] > smax ? lf[q] : smax;
         __hip_atomic_fetch_max(reinterpret_cast<unsigned long long *>(a.step) + sigma, (unsigned long long)smax,
@@ -591,7 +614,7 @@ hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream) 
     void *params[] = {&args};
     const WalkKernel k = walk_kernel(a.factor != nullptr, a.final_pass != 0, a.digest != nullptr);
     return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k), dim3((unsigned)(n_blocks * a.tiles)),
-                                      dim3(kBlockRanks * kLanes), params, 0, stream);
+                                      dim3(kBlockWalkers * kLanes), params, 0, stream);
 }
 
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
@@ -607,7 +630,7 @@ hipError_t walk_capacity(int device, int64_t workgroups[8]) {
         int per_cu = 0;
         const WalkKernel k = walk_kernel(v & 1, v & 2, v & 4);
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(k),
-                                                         kBlockRanks * kLanes, 0);
+                                                         kBlockWalkers * kLanes, 0);
         if (e != hipSuccess) return e;
         workgroups[v] = (int64_t)per_cu * cus;
     }

@@ -20,7 +20,7 @@ ECHO_OK, ECHO_ERR_ARG, ECHO_ERR_RANGE, ECHO_ERR_MATCH = 0, -1, -2, -3
 ECHO_ERR_CYCLE, ECHO_ERR_NOMEM, ECHO_ERR_HIP, ECHO_ERR_DEVICE = -4, -5, -6, -7
 ERROR_NAMES = {0: "OK", -1: "ARG", -2: "RANGE", -3: "MATCH", -4: "CYCLE", -5: "NOMEM", -6: "HIP",
                -7: "DEVICE"}
-EXPORTS = ("echo_load_graph", "echo_graph_info", "echo_free_graph", "echo_cc_cost",
+EXPORTS = ("echo_load_graph", "echo_load_graph_ex", "echo_graph_info", "echo_free_graph", "echo_cc_cost",
            "echo_compose_batch", "echo_sync_status", "echo_set_timing", "echo_kernel_times",
            "echo_last_error")
 KERNEL_KINDS = {0: "init", 1: "cc_cost", 2: "walk", 3: "overlap", 4: "clear"}
@@ -65,6 +65,8 @@ def lib():
     P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     L.echo_load_graph.argtypes = [ctypes.POINTER(_Desc), ctypes.c_int, ctypes.POINTER(P)]
     L.echo_load_graph.restype = ctypes.c_int
+    L.echo_load_graph_ex.argtypes = [ctypes.POINTER(_Desc), ctypes.c_int, ctypes.c_int32, ctypes.POINTER(P)]
+    L.echo_load_graph_ex.restype = ctypes.c_int
     L.echo_graph_info.argtypes = [P, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64)]
     L.echo_graph_info.restype = ctypes.c_int
     L.echo_free_graph.argtypes = [P]
@@ -118,7 +120,7 @@ def _stream_ptr(device):
 class Graph:
     """A loaded graph: validated, matched, levelled and resident on one GPU."""
 
-    def __init__(self, arrays: dict, device: int = 0):
+    def __init__(self, arrays: dict, device: int = 0, ranks_per_walker: int = 0):
         L = lib()
         self._keep = {
             "op_rank": np.ascontiguousarray(arrays["op_rank"], np.int32),
@@ -142,7 +144,7 @@ class Graph:
                   ptr(k["op_dur"]), ptr(k["op_coll"]), ptr(k["pred_off"]), ptr(k["pred_idx"]),
                   k["coll_type"].shape[0], ptr(k["coll_type"]), ptr(k["coll_bytes"]))
         h = ctypes.c_void_p()
-        _check(L.echo_load_graph(ctypes.byref(d), int(device), ctypes.byref(h)))
+        _check(L.echo_load_graph_ex(ctypes.byref(d), int(device), int(ranks_per_walker), ctypes.byref(h)))
         self._keep = None
         self.handle = h
         self.device = int(device)

@@ -145,3 +145,11 @@ def test_generated_graphs_all_load(E):
     """Every config's generator output is acyclic and matches (config 5: the smaller graphs)."""
     for cfg, idx in [(1, 0), (2, 0), (5, 0), (5, 3), (5, 8), (5, 11)]:
         assert _load_code(E, configs.graph(cfg, idx)) == _valid_code(E), (cfg, idx)
+
+
+def test_walker_width_out_of_range_is_an_argument_error(E):
+    g = configs.graph(1)
+    for bad in (-1, 17):
+        with pytest.raises(E.EchoError) as x:
+            E.Graph(g, 0, ranks_per_walker=bad)
+        assert x.value.code == E.ECHO_ERR_ARG

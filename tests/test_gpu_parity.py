@@ -123,6 +123,46 @@ def test_random_graphs(E, seed):
     G.close()
 
 
+# ---------------------------------------------------------------- several ranks per wavefront
+# A graph with more ranks than the device holds wavefronts is walked with
+# several ranks per wavefront; these tests force that layout on small graphs.
+@pytest.mark.parametrize("rpw", [2, 3, 8])
+def test_walkers_of_several_ranks_tiny(E, rpw):
+    sc = scenarios.draw(3, np.random.default_rng(8), bw_inter=(20000, 90000), alpha=(0, 5000),
+                        ar_algo_random=True, slowdown=(65536, 140000), jitter=(3000, 5))
+    for name in sorted(TINY):
+        g = TINY[name]
+        G = E.Graph(g, 0, ranks_per_walker=rpw)
+        for R in (0, 2):
+            assert_same(gpu_run(E, g, sc, R, graph=G), oracle.run(g, sc, R))
+        G.close()
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("rpw", [2, 5, 16])
+def test_walkers_of_several_ranks_random(E, seed, rpw):
+    rng = np.random.default_rng(2000 + seed)
+    g = _random_graph(rng, int(rng.integers(2, 40)), int(rng.integers(5, 60)), int(rng.integers(0, 40)))
+    sc = scenarios.draw(70, rng, bw_inter=(20000, 400000), bw_intra=(50000, 400000), alpha=(0, 20000),
+                        ar_algo_random=True, slowdown=(65536, 150000), jitter=(5000, seed))
+    try:
+        ref = oracle.run(g, sc, 1, threads=THREADS)
+    except oracle.OracleError as e:
+        assert e.code == -4
+        return
+    G = E.Graph(g, 0, ranks_per_walker=rpw)
+    assert_same(gpu_run(E, g, sc, 1, graph=G), ref)
+    G.close()
+
+
+@pytest.mark.parametrize("rpw", [2, 3])
+def test_walkers_of_several_ranks_config1(E, rpw):
+    g, sc = configs.graph(1), scenarios.take(configs.scenario_batch(4), slice(0, 130))
+    G = E.Graph(g, 0, ranks_per_walker=rpw)
+    assert_same(gpu_run(E, g, sc, 1, graph=G), oracle.run(g, sc, 1, threads=THREADS))
+    G.close()
+
+
 def test_1f1b_pipeline_closed_form(E):
     g = tinygraph.pipeline_1f1b(8, 16, 1000, 2100)
     sc = scenarios.default_scenarios(2)
@@ -178,7 +218,9 @@ def test_config3_gpt175b_1024ranks_sampled(E):
     assert (gpu["step"] > 0).all()
 
 
-@pytest.mark.parametrize("index", [0, 3] if not os.environ.get("ECHO_FULL") else list(range(16)))
+# graph 6 has 8192 ranks: more than the device holds wavefronts, so it is walked
+# with several ranks per wavefront
+@pytest.mark.parametrize("index", [0, 3, 6] if not os.environ.get("ECHO_FULL") else list(range(16)))
 def test_config5_extrapolation_sampled(E, index):
     g, sc = configs.graph(5, index), configs.scenario_batch(5, index)
     _sampled(E, g, sc, 1, [0, scenarios.count(sc) - 1])
