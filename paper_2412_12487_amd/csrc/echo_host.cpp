@@ -593,6 +593,26 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     }
     if ((int64_t)far.size() > kI32Max || (int64_t)items.size() > kI32Max)
         return fail(ECHO_ERR_RANGE, "walk lists exceed 2^31 entries");
+    {
+        // what a pass without caller-visible timelines must still store
+        std::vector<uint32_t> need(n, 0);
+        for (int32_t u : far) need[u] |= kNeedF;
+        std::vector<int32_t> prev_on_stream(R * kStreams, -1);
+        for (int64_t v = 0; v < n; ++v) {
+            const int64_t k = (int64_t)d->op_rank[v] * kStreams + d->op_stream[v];
+            const int32_t prev = prev_on_stream[k];
+            prev_on_stream[k] = (int32_t)v;
+            if (d->op_kind[v] == ECHO_COMM) {
+                need[v] |= kNeedS | kNeedF;
+            } else if (d->op_kind[v] == ECHO_COMPUTE) {
+                const bool chained = prev >= 0 && d->op_kind[prev] == ECHO_COMPUTE && poff[v + 1] - poff[v] == 1 &&
+                                     preds[poff[v]] == prev;
+                if (!chained) need[v] |= kNeedS;
+            }
+        }
+        for (WalkItem &it : items)
+            if (item_kind(it.meta) != kResolve) it.meta |= need[it.op];
+    }
 
     // per (rank, stream) comm and compute op lists in program order
     std::vector<int64_t> cl_off(R * kStreams + 1, 0), cp_off(R * kStreams + 1, 0);
@@ -765,6 +785,7 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
             a.tiles = (int32_t)std::min<int64_t>(per_launch, n_tiles - t0);
             a.n_walkers = g->n_walkers;
             a.final_pass = p == n_refine;
+            a.store_all = p == n_refine && (d_start || d_finish);
             if (g->n_ranks == 0 || g->n_ops == 0) continue;
             TIMED(ECHO_K_WALK, launch_walk(a, g->dg.n_blocks, stream), "walk kernel");
         }

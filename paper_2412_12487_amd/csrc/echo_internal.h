@@ -42,6 +42,7 @@ constexpr unsigned kStatusAbort = 8u;            // stop all waits (set with tim
 struct WalkItem {
     int32_t op;         // op id: row of the [op][scenario] outputs
     uint32_t meta;      // kind | slot << 2 | class << 5 | regmask << 8 | fast << 16 | noreg << 17
+                        // | need start << 18 | need finish << 19
     int32_t far_off;    // predecessors read back from memory: far[far_off .. +nfar)
     int32_t coll;       // collective of a comm op, -1 otherwise
     int64_t dur;        // base duration of compute / memcpy ops
@@ -55,6 +56,13 @@ static_assert(sizeof(WalkItem) == 32, "walk item must stay 32 bytes");
 constexpr uint32_t kFast = 1u << 16;
 // The op's (rank, stream) pair has no register slot.
 constexpr uint32_t kNoReg = 1u << 17;
+// A pass that does not produce the caller's timelines stores only what later
+// steps read back: the start (kNeedS) of comm ops and of compute ops that do not
+// simply follow the previous compute op of their stream (overlap detection
+// rebuilds the others), and the finish (kNeedF) of comm ops and of ops read as
+// far predecessors.
+constexpr uint32_t kNeedS = 1u << 18;
+constexpr uint32_t kNeedF = 1u << 19;
 // Item kind (besides compute/comm/memcpy) that finishes a kNoReg comm op:
 // wait for its barrier, then write its finish.
 constexpr int kResolve = 3;
@@ -145,6 +153,7 @@ struct WalkArgs {
     int32_t tile0, tiles;            // tiles handled by this launch
     int32_t n_walkers;
     int32_t final_pass;              // accumulate step time (and digest)
+    int32_t store_all;               // store every start and finish (else only kNeedS / kNeedF)
 };
 
 

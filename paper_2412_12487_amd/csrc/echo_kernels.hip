@@ -245,6 +245,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     uint32_t hi_or = 0;          // OR of the high words of every time: bit 30 set <=> some time >= 2^62
     unsigned err = 0;
     const int64_t beg = a.walk_off[w], end = a.walk_off[w + 1];
+    const uint32_t keep = a.store_all ? (kNeedS | kNeedF) : 0u;    // stores beyond each item's own needs
     // lane j < 32 holds the first half of item j of the round, lane 32 + j its second half
     const int4 *items4 = reinterpret_cast<const int4 *>(a.items);
     const int half = lane >> 5, slotl = lane & 31;
@@ -329,8 +330,8 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 int64_t d = amp != 0 ? jittered(dur, op, jbase, amp) : dur;
                 if (REFINED && item_kind(meta) == ECHO_COMPUTE) d = q16(d, fst[j * kLanes + lane]);
                 const int64_t f = s0 + d;
-                (sbase + (int64_t)op * ns)[col] = s0;
-                (fbase + (int64_t)op * ns)[col] = f;
+                if ((meta | keep) & kNeedS) (sbase + (int64_t)op * ns)[col] = s0;
+                if ((meta | keep) & kNeedF) (fbase + (int64_t)op * ns)[col] = f;
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)s0) ^ (uint64_t)f);
                 s0 = f;
@@ -370,7 +371,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 const int64_t fu = (fbase + u * ns)[col];
                 ready = fu > ready ? fu : ready;
             }
-            (sbase + (int64_t)op * ns)[col] = ready;
+            if ((meta | keep) & kNeedS) (sbase + (int64_t)op * ns)[col] = ready;
             if (kind == ECHO_COMM) {
                 // launch: publish this member's launch time, then count the arrival
                 if (aux & kAuxLocal) {
@@ -402,7 +403,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 if (REFINED && kind == ECHO_COMPUTE) d = q16(d, fst[j * kLanes + lane]);
                 const int64_t f = ready + d;
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
-                (fbase + (int64_t)op * ns)[col] = f;
+                if ((meta | keep) & kNeedF) (fbase + (int64_t)op * ns)[col] = f;
                 if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)ready) ^ (uint64_t)f);
                 if (meta & kNoReg) {
                     xmax = f > xmax ? f : xmax;
