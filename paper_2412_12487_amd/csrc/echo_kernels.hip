@@ -526,9 +526,20 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 const int meta = __builtin_amdgcn_readlane(cur.y, j);
                 const int64_t d0 = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.w, j) << 32) |
                                              (uint32_t)__builtin_amdgcn_readlane(cur.z, j));
-                const int64_t sv = (meta & kChained) ? fprev : (sbase + v * ns)[col];
+                // Loads in this loop are waited for on their own path (explicit vmcnt(0)):
+                // left pending, they would make the compiler wait at the next join, on
+                // every path, for the previous op's store as well.
+                int64_t sv = fprev;
+                if (!(meta & kChained)) {
+                    sv = (sbase + v * ns)[col];
+                    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                }
                 int64_t d = amp != 0 ? jittered(d0, (int32_t)v, jbase, amp) : d0;
-                if (a.prev_refined) d = q16(d, (obase + v * ns)[col]);   // the previous pass's duration
+                if (a.prev_refined) {                                     // the previous pass's duration
+                    const uint32_t f_old = (obase + v * ns)[col];
+                    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                    d = q16(d, f_old);
+                }
                 const int64_t fv = sv + d;
                 fprev = fv;
                 bool busy = false;
@@ -568,6 +579,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                             qf = (fbase + c * ns)[col];
                         }
                     }
+                    __builtin_amdgcn_s_waitcnt(kWaitVm0);
                 }
                 (obase + v * ns)[col] = F;
             }
