@@ -52,11 +52,11 @@ def walk_bytes(g, n_scen, n_refine):
     """Algorithmic bytes of the composer passes (edge-relaxation model):
     per pass and scenario, 16 B written per op (start, finish), 8 B read per
     merged predecessor, 8 B per collective cost; a refined pass also reads a
-    4 B slowdown factor per compute op."""
+    1 B overlap mask per compute op."""
     preds = merged_pred_counts(g)
     per_pass = (16 * len(preds) + 8 * int(preds.sum()) + 8 * len(g["coll_type"])) * n_scen
     n_compute = int((g["op_kind"] == 0).sum())
-    passes = [per_pass] + [per_pass + 4 * n_compute * n_scen] * n_refine
+    passes = [per_pass] + [per_pass + 1 * n_compute * n_scen] * n_refine
     return passes
 
 

@@ -111,8 +111,8 @@ struct echo_graph_s {
     size_t arrive_n = 0;
     unsigned *count = nullptr;
     size_t count_n = 0;
-    uint32_t *factor = nullptr;
-    size_t factor_n = 0;
+    uint8_t *tmask = nullptr;
+    size_t tmask_n = 0;
     int64_t *tmp_start = nullptr, *tmp_finish = nullptr;
     size_t tmp_start_n = 0, tmp_finish_n = 0;
     int64_t *tmp_step = nullptr;
@@ -134,7 +134,7 @@ void free_graph(echo_graph g) {
     (void)hipFree(g->class_cost);
     (void)hipFree(g->arrive);
     (void)hipFree(g->count);
-    (void)hipFree(g->factor);
+    (void)hipFree(g->tmask);
     (void)hipFree(g->tmp_start);
     (void)hipFree(g->tmp_finish);
     (void)hipFree(g->tmp_step);
@@ -724,7 +724,7 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
     if ((rc = ensure(&g->class_cost, &g->class_cost_n, (size_t)(g->dg.classes.n * ns), "class cost"))) return rc;
     if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->n_colls * ns), "arrivals"))) return rc;
     if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * n_tiles), "arrival counts"))) return rc;
-    if (n_refine > 0 && (rc = ensure(&g->factor, &g->factor_n, (size_t)(g->n_ops * ns), "factors"))) return rc;
+    if (n_refine > 0 && (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(g->n_ops * ns), "overlap masks"))) return rc;
     if (!d_start && (rc = ensure(&g->tmp_start, &g->tmp_start_n, (size_t)(g->n_ops * ns), "start"))) return rc;
     if (!d_finish && (rc = ensure(&g->tmp_finish, &g->tmp_finish_n, (size_t)(g->n_ops * ns), "finish")))
         return rc;
@@ -756,7 +756,7 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
         const int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, cap / g->dg.n_blocks));
         if (p > 0) {
             OverlapArgs o{g->dg.cl_off, g->dg.cp_off, g->dg.cl, g->dg.cl_type, g->dg.cp,
-                          d_scen, start, finish, g->factor, n_scen, n_tiles, p > 1};
+                          d_scen, start, finish, g->tmask, n_scen, n_tiles, p > 1};
             TIMED(ECHO_K_OVERLAP, launch_overlap(o, g->n_ranks, stream), "overlap kernel");
             TIMED(ECHO_K_CLEAR, launch_clear(g->arrive, n_arrive, g->count, n_count, stream), "clear kernel");
         }
@@ -770,7 +770,7 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
             a.scen = d_scen;
             a.cost = g->cost;
             a.class_cost = g->class_cost;
-            a.factor = p > 0 ? g->factor : nullptr;
+            a.tmask = p > 0 ? g->tmask : nullptr;
             a.start = start;
             a.finish = finish;
             a.arrive = g->arrive;

@@ -91,6 +91,10 @@ __host__ __device__ inline int item_stream(uint32_t m) { return int((m >> 2) & 7
 __host__ __device__ inline int item_class(uint32_t m) { return int((m >> 5) & 7u); }
 __host__ __device__ inline unsigned item_regmask(uint32_t m) { return (m >> 8) & 0xffu; }
 
+// Overlap detection records, per compute op and scenario, which collective
+// types overlap it as a 4-bit mask (bit t: some comm op of type t on the same
+// rank overlaps).  The slowdown factor is the largest table entry
+// slowdown_q16[class][t] over the set bits, 65536 for an empty mask.
 // Compute op of a (rank, stream) list for overlap detection (16 bytes).
 struct ComputeRec {
     int32_t op;
@@ -141,7 +145,7 @@ struct WalkArgs {
     const echo_scenario *scen;
     const int64_t *cost;             // [coll][scen]
     const int64_t *class_cost;       // [class][scen]
-    const uint32_t *factor;          // [op][scen] slowdown factors, or null (pass 1)
+    const uint8_t *tmask;            // [op][scen] overlap type masks of compute ops, or null (pass 1)
     int64_t *start, *finish;         // [op][scen]
     unsigned long long *arrive;      // [coll][scen] latest member launch
     unsigned *count;                 // [coll][tile] members arrived
@@ -164,7 +168,7 @@ struct OverlapArgs {
     const ComputeRec *cp;
     const echo_scenario *scen;
     const int64_t *start, *finish;
-    uint32_t *factor;                // in: factors of the previous pass (if it was refined), out: new ones
+    uint8_t *tmask;                  // in: masks of the previous pass (if it was refined), out: new ones
     int32_t n_scen, n_tiles;
     int32_t prev_refined;            // the previous pass inflated its compute ops by `factor`
 };

@@ -6,8 +6,8 @@
 //   k_walk     timeline composer (Sec. 4.2) with the collective synchronisation
 //              rule (Sec. 5.2): one wavefront per (walker, 64-scenario tile) walks
 //              the ops of its ranks in level order, max-plus relaxation in registers
-//   k_overlap  validator input (Sec. 6): per compute op and scenario, the largest
-//              slowdown factor over the comm ops of its rank that overlap it
+//   k_overlap  validator input (Sec. 6): per compute op and scenario, the mask of
+//              collective types among the comm ops of its rank that overlap it
 //
 // Everything is int64 nanoseconds and Q16 factors, bit-exact by construction:
 // max, add, 64-bit multiply and shifts only (no floating point on the path).
@@ -160,7 +160,23 @@ __device__ bool wait_arrivals(const unsigned *cnt, unsigned need, unsigned *stat
     }
 }
 
-constexpr int kBlock = 32;   // walk items fetched (and factors staged) per round
+constexpr int kBlock = 32;   // walk items fetched (and overlap masks staged) per round
+
+// Duration d inflated by the slowdown factor of overlap mask m (Sec. 6): the
+// largest entry of the op's class row over the collective types in m; an empty
+// mask is factor 65536, which q16 maps to d itself.  tbl: the lane's table in
+// LDS, entry e at tbl[e * 64 + lane].
+__device__ __forceinline__ int64_t inflate(int64_t d, uint32_t m, const uint32_t *tbl, int cls, int lane) {
+    if (m == 0) return d;
+    uint32_t F = 65536u;
+#pragma unroll
+    for (int t = 0; t < kTypes; ++t)
+        if ((m >> t) & 1u) {
+            const uint32_t x = tbl[(cls * kTypes + t) * kLanes + lane];
+            F = x > F ? x : F;
+        }
+    return q16(d, F);
+}
 // s_waitcnt immediate for "lgkmcnt(0)" on gfx9-family targets (vmcnt and expcnt left at their maxima)
 constexpr int kWaitLgkm0 = 0xC07F;
 
@@ -192,11 +208,13 @@ __device__ bool wait_local(const unsigned *cnt, unsigned need, unsigned *status,
 // overlaps.  FINAL: the pass produces the step time (and DIGEST: the digest).
 template <bool REFINED, bool FINAL, bool DIGEST>
 __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
-    __shared__ uint32_t fstage[REFINED ? kBlockWalkers * kBlock * kLanes : 1];
+    __shared__ uint8_t fstage[REFINED ? kBlockWalkers * kBlock * kLanes : 1];   // staged overlap masks
     __shared__ unsigned long long lbar[kChannels][2][kLanes];   // per channel and slot: latest launch per lane
     __shared__ unsigned lcnt[kChannels][2];                      // per channel and slot: members arrived
     __shared__ int64_t ccost[kClassSlots][kLanes];               // staged class costs of this tile
     __shared__ int32_t pinfo[kBlockWalkers][kStreams][3];          // per wave and slot: pending collective, op, aux
+    __shared__ uint32_t slow[REFINED ? kClasses * kTypes * kLanes : 1];   // slowdown table of each lane's scenario
+    static_assert(kBlockWalkers * 4 == kClasses * kTypes, "one 16-byte table slice per wavefront");
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform within a wavefront
@@ -218,6 +236,14 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
         const int32_t cls = a.block_class[(int64_t)blk * kClassSlots + wave];
         ccost[wave][lane] = cls >= 0 ? a.class_cost[(int64_t)cls * ns + sigma] : 0;
     }
+    if (REFINED) {
+        // entry e of the table for lane l at slow[e * 64 + l]: lanes hit distinct banks
+        const uint4 t4 = reinterpret_cast<const uint4 *>(&a.scen[sigma].slowdown_q16[0][0])[wave];
+        slow[(4 * wave + 0) * kLanes + lane] = t4.x;
+        slow[(4 * wave + 1) * kLanes + lane] = t4.y;
+        slow[(4 * wave + 2) * kLanes + lane] = t4.z;
+        slow[(4 * wave + 3) * kLanes + lane] = t4.w;
+    }
     __syncthreads();
     if (w >= a.n_walkers) return;
 
@@ -227,7 +253,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     int64_t *const sbase = a.start + (int64_t)tile * kLanes;    // row v of tile: sbase + v * ns
     int64_t *const fbase = a.finish + (int64_t)tile * kLanes;
     const unsigned *tile_count = a.count + tile;
-    uint32_t *const fst = fstage + (REFINED ? wave * kBlock * kLanes : 0);
+    uint8_t *const fst = fstage + (REFINED ? wave * kBlock * kLanes : 0);
 
     // Per slot: finish of the latest op, or (bit j of `pending`) a comm op still
     // waiting for its barrier, described in this wave's row of pinfo.
@@ -302,17 +328,17 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
         const int nb = end - blk0 < kBlock ? int(end - blk0) : kBlock;
         nxt = blk0 + kBlock + slotl < end ? items4[2 * (blk0 + kBlock + slotl) + half] : make_int4(0, 0, 0, 0);
         if (REFINED) {
-            // stage this round's slowdown factors, half a round per memory round trip
+            // stage this round's overlap masks, half a round per memory round trip
 #pragma unroll
             for (int h = 0; h < kBlock; h += kBlock / 2) {
-                uint32_t fv[kBlock / 2];
+                uint32_t mv[kBlock / 2];
 #pragma unroll
                 for (int j = 0; j < kBlock / 2; ++j) {
                     const int32_t opj = __builtin_amdgcn_readlane(cur.x, h + j);
-                    fv[j] = a.factor[(int64_t)opj * ns + sigma];
+                    mv[j] = a.tmask[(int64_t)opj * ns + sigma];
                 }
 #pragma unroll
-                for (int j = 0; j < kBlock / 2; ++j) fst[(h + j) * kLanes + lane] = fv[j];
+                for (int j = 0; j < kBlock / 2; ++j) fst[(h + j) * kLanes + lane] = (uint8_t)mv[j];
             }
         }
         // fast flags of the round, one bit per item
@@ -328,7 +354,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) |
                                               (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32));
                 int64_t d = amp != 0 ? jittered(dur, op, jbase, amp) : dur;
-                if (REFINED && item_kind(meta) == ECHO_COMPUTE) d = q16(d, fst[j * kLanes + lane]);
+                if (REFINED && item_kind(meta) == ECHO_COMPUTE) d = inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane);
                 const int64_t f = s0 + d;
                 if ((meta | keep) & kNeedS) (sbase + (int64_t)op * ns)[col] = s0;
                 if ((meta | keep) & kNeedF) (fbase + (int64_t)op * ns)[col] = f;
@@ -400,7 +426,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 }
             } else {
                 int64_t d = amp != 0 ? jittered(dur, op, jbase, amp) : dur;
-                if (REFINED && kind == ECHO_COMPUTE) d = q16(d, fst[j * kLanes + lane]);
+                if (REFINED && kind == ECHO_COMPUTE) d = inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane);
                 const int64_t f = ready + d;
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 if ((meta | keep) & kNeedF) (fbase + (int64_t)op * ns)[col] = f;
@@ -465,7 +491,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     const int64_t ns = a.n_scen;
     const int64_t *const sbase = a.start + (int64_t)tile * kLanes;
     const int64_t *const fbase = a.finish + (int64_t)tile * kLanes;
-    uint32_t *const obase = a.factor + (int64_t)tile * kLanes;
+    uint8_t *const obase = a.tmask + (int64_t)tile * kLanes;
     const echo_scenario *sc = a.scen + sigma;
     const uint32_t *slow = &sc->slowdown_q16[0][0];
     const uint64_t jbase = jitter_base(sc->jitter_seed, sc->jitter_stream);
@@ -536,9 +562,17 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 }
                 int64_t d = amp != 0 ? jittered(d0, (int32_t)v, jbase, amp) : d0;
                 if (a.prev_refined) {                                     // the previous pass's duration
-                    const uint32_t f_old = (obase + v * ns)[col];
+                    const uint32_t m_old = (obase + v * ns)[col];
                     __builtin_amdgcn_s_waitcnt(kWaitVm0);
-                    d = q16(d, f_old);
+                    if (m_old != 0) {
+                        uint32_t F = 65536u;
+                        for (int t = 0; t < kTypes; ++t)
+                            if ((m_old >> t) & 1u) {
+                                const uint32_t x = slow[(meta & 7) * kTypes + t];
+                                F = x > F ? x : F;
+                            }
+                        d = q16(d, F);
+                    }
                 }
                 const int64_t fv = sv + d;
                 fprev = fv;
@@ -546,9 +580,8 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     #pragma unroll
                 for (int k = 0; k < kStreams; ++k)
                     if (k < ncs) busy |= cs[k] < fv;
-                uint32_t F = 65536u;
+                uint32_t m = 0;                            // types of the comm ops overlapping v
                 if (busy) {
-                    const int cls = meta & 7;
     #pragma unroll
                     for (int k = 0; k < kStreams; ++k) {
                         if (k >= ncs) break;
@@ -568,10 +601,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                         int64_t qs = cs[k], qf = cf[k];
                         while (qs < fv) {
                             const int64_t lo = sv > qs ? sv : qs, hi = fv < qf ? fv : qf;
-                            if (lo < hi) {
-                                const uint32_t x = slow[cls * kTypes + a.cl_type[kb[k] + q]];
-                                F = x > F ? x : F;
-                            }
+                            if (lo < hi) m |= 1u << a.cl_type[kb[k] + q];
                             if (qf >= fv) break;           // the next one starts after v ends
                             if (++q >= nk[k]) break;
                             const int64_t c = a.cl[kb[k] + q];
@@ -581,7 +611,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                     }
                     __builtin_amdgcn_s_waitcnt(kWaitVm0);
                 }
-                (obase + v * ns)[col] = F;
+                (obase + v * ns)[col] = (uint8_t)m;
             }
         }
     }
@@ -625,7 +655,7 @@ hipError_t launch_cc_cost(const CollTable &t, const echo_scenario *scen, int32_t
 hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream) {
     WalkArgs args = a;
     void *params[] = {&args};
-    const WalkKernel k = walk_kernel(a.factor != nullptr, a.final_pass != 0, a.digest != nullptr);
+    const WalkKernel k = walk_kernel(a.tmask != nullptr, a.final_pass != 0, a.digest != nullptr);
     return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k), dim3((unsigned)(n_blocks * a.tiles)),
                                       dim3(kBlockWalkers * kLanes), params, 0, stream);
 }
