@@ -8,6 +8,11 @@ Table 8 of the paper).
 
 Prints one JSON line with the metric, a roofline entry for the composer
 (walk) kernel, and the CPU oracle timed on a bounded sample of the same work.
+
+--replica times the data-parallel symmetry reduction instead (Sec. 8.5, DDP
+mode): one DP replica of a graph whose replicas share their durations,
+composed alone, against the sweep over every replica; the value counts the
+whole job's ops.
 """
 from __future__ import annotations
 
@@ -83,7 +88,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--config", type=int, default=3, help="workload 1-4 (see workloads/configs.py)")
+    ap.add_argument("--config", type=int, default=3, help="workload 1-5 (see workloads/configs.py)")
+    ap.add_argument("--index", type=int, default=0, help="graph of config 5 (0-15)")
+    ap.add_argument("--scenarios", type=int, default=0,
+                    help="batch size drawn with the config's recipe (0 = the config's own)")
+    ap.add_argument("--replica", action="store_true",
+                    help="time one DP replica composed alone against the sweep over every replica")
     ap.add_argument("--refine", type=int, default=1)
     ap.add_argument("--cpu-sample", type=int, default=8, help="scenarios the CPU oracle composes (0 = skip)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -109,14 +119,47 @@ def main():
         return
 
     import paper_2412_12487_amd as E
-    from workloads import configs
+    from workloads import configs, gpt1f1b
 
     E.lib()
+    if args.replica:
+        return replica_mode(args, E, configs, gpt1f1b)
     t = time.perf_counter()
-    g = configs.graph(args.config)
-    sc = configs.scenario_batch(args.config)
+    g = configs.graph(args.config, args.index)
+    sc = configs.scenario_batch(args.config, args.index, args.scenarios or None)
     log(f"graph: config {args.config} {configs.NAMES[args.config]}: {len(g['op_rank'])} ops, "
         f"{len(g['coll_type'])} collectives, {g['n_ranks']} ranks ({time.perf_counter() - t:.1f} s)")
+    r = time_compose(E, g, sc, args)
+    line = {
+        "metric": "op-evaluations/sec (ops x scenarios composed), 1 GPU",
+        "value": round(r["value"], 1),
+        "unit": "op-evals/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r["ms_per_step"], 4),
+        "gpu_ms_per_step": round(r["gpu_ms"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": f"config {args.config}: {configs.NAMES[args.config]}, "
+                               f"{r['n_ops']} ops x {r['n_scen']} scenarios, {args.refine} refinement(s)",
+                   "n_ops": r["n_ops"], "n_scenarios": r["n_scen"], "n_refine": args.refine,
+                   "ranks": int(g["n_ranks"]), "levels": r["levels"], "load_s": round(r["load_s"], 2)},
+        "kernels_ms": r["kernels_ms"],
+        "roofline": roofline(g, r, args, args.config),
+    }
+    if args.cpu_sample > 0:
+        log(f"cpu baseline: oracle on {args.cpu_sample} scenario(s) ...")
+        line["cpu_baseline"] = cpu_baseline(g, sc, args.refine, args.cpu_sample)
+    print(json.dumps(line), flush=True)
+
+
+def time_compose(E, g, sc, args):
+    """Load g, compose the batch warmup + steps times; wall and per-kernel timings."""
+    import torch
     t = time.perf_counter()
     G = E.Graph(g, 0)
     load_s = time.perf_counter() - t
@@ -149,48 +192,75 @@ def main():
     wall = time.perf_counter() - t0
     G.sync_status()
     ms_per_step = wall * 1000.0 / args.steps
-    value = G.n_ops * n_scen / (ms_per_step / 1000.0)
+    n_walk = sum(1 for k, _ in G.kernel_times() if k == "walk")
+    res = {"n_ops": G.n_ops, "n_scen": n_scen, "levels": G.n_levels, "load_s": load_s,
+           "ms_per_step": ms_per_step, "gpu_ms": float(np.median(step_ms)),
+           "value": G.n_ops * n_scen / (ms_per_step / 1000.0),
+           "walk_avg_ms": float(np.mean(walk_ms)) / max(n_walk, 1), "n_walk": n_walk,
+           "kernels_ms": {k: round(float(np.mean(v)), 4) for k, v in kernels.items()}}
+    del out
+    G.close()
+    return res
 
-    passes = walk_bytes(g, n_scen, args.refine)
-    n_walk_launches = sum(1 for k, _ in G.kernel_times() if k == "walk")
-    walk_avg_ms = float(np.mean(walk_ms)) / max(n_walk_launches, 1)
-    bytes_per_launch = sum(passes) / max(n_walk_launches, 1)
-    achieved = bytes_per_launch / (walk_avg_ms / 1000.0) / 1e9
+
+def roofline(g, r, args, traffic_config):
+    passes = walk_bytes(g, r["n_scen"], args.refine)
+    bytes_per_launch = sum(passes) / max(r["n_walk"], 1)
+    achieved = bytes_per_launch / (r["walk_avg_ms"] / 1000.0) / 1e9
     traffic = None
-    if os.path.exists(TRAFFIC_FILE):
+    if traffic_config is not None and os.path.exists(TRAFFIC_FILE):
         tr = json.load(open(TRAFFIC_FILE))
-        if tr.get("kernel_source_sha") == source_hash() and tr.get("config") == args.config:
+        if tr.get("kernel_source_sha") == source_hash() and tr.get("config") == traffic_config:
             traffic = tr.get("bytes_per_launch")
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "k_walk", "avg_launch_ms": round(walk_avg_ms, 4),
-                "algorithmic_bytes_per_launch": int(bytes_per_launch)}
+    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "kernel": "k_walk", "avg_launch_ms": round(r["walk_avg_ms"], 4),
+            "algorithmic_bytes_per_launch": int(bytes_per_launch)}
+
+
+def replica_mode(args, E, configs, gpt1f1b):
+    """Symmetry reduction (one DP replica composed alone) against the sweep over
+    every replica, on a graph whose replicas share their durations."""
+    params = configs.graph_params(args.config, args.index)
+    t = time.perf_counter()
+    g = gpt1f1b.gpt_graph(**params, replica_invariant=True)
+    rg, _ = gpt1f1b.dp_replica(g, params["tp"], params["dp"])
+    sc = configs.scenario_batch(args.config, args.index, args.scenarios or None)
+    name = f"config {args.config}" + (f" graph {args.index + 1}" if args.config == 5 else "") + \
+        f" (TP{params['tp']} x PP{params['pp']} x DP{params['dp']}, replica-invariant durations)"
+    log(f"graphs: {name}: {len(g['op_rank'])} ops, replica {len(rg['op_rank'])} ops "
+        f"({time.perf_counter() - t:.1f} s)")
+    n_scen = len(sc["alpha_ns"])
+    # the sweep over every replica needs start + finish + masks for all of the job's ops
+    full_fits = len(g["op_rank"]) * n_scen * 17 < 200 * 10**9
+    full = time_compose(E, g, sc, args) if full_fits else None
+    red = time_compose(E, rg, sc, args)
     line = {
-        "metric": "op-evaluations/sec (ops x scenarios composed), 1 GPU",
-        "value": round(value, 1),
+        "metric": "op-evaluations/sec (ops x scenarios of the whole job, composed through one DP replica), 1 GPU",
+        "value": round(len(g["op_rank"]) * red["n_scen"] / (red["ms_per_step"] / 1000.0), 1),
         "unit": "op-evals/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
-        "gpu_ms_per_step": round(float(np.median(step_ms)), 4),
+        "ms_per_step": round(red["ms_per_step"], 4),
+        "gpu_ms_per_step": round(red["gpu_ms"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int64",
         "data": "synthetic",
-        "config": {"workload": f"config {args.config}: {configs.NAMES[args.config]}, "
-                               f"{G.n_ops} ops x {n_scen} scenarios, {args.refine} refinement(s)",
-                   "n_ops": G.n_ops, "n_scenarios": n_scen, "n_refine": args.refine,
-                   "ranks": int(g["n_ranks"]), "levels": G.n_levels, "load_s": round(load_s, 2)},
-        "kernels_ms": {k: round(float(np.mean(v)), 4) for k, v in kernels.items()},
-        "roofline": roofline,
+        "config": {"workload": f"{name}, DP-replica mode: {red['n_ops']} of {len(g['op_rank'])} ops x "
+                               f"{red['n_scen']} scenarios, {args.refine} refinement(s)",
+                   "n_ops_job": len(g["op_rank"]), "n_ops_replica": red["n_ops"], "n_scenarios": red["n_scen"],
+                   "n_refine": args.refine,
+                   "full_sweep_ms_per_step": round(full["ms_per_step"], 4) if full else None,
+                   "speedup_vs_full_sweep": round(full["ms_per_step"] / red["ms_per_step"], 2) if full else None},
+        "kernels_ms": red["kernels_ms"],
+        "roofline": roofline(rg, red, args, None),
     }
-    del out
-    G.close()
     if args.cpu_sample > 0:
-        log(f"cpu baseline: oracle on {args.cpu_sample} scenario(s) ...")
-        line["cpu_baseline"] = cpu_baseline(g, sc, args.refine, args.cpu_sample)
+        log(f"cpu baseline: oracle on {args.cpu_sample} scenario(s) of the replica ...")
+        line["cpu_baseline"] = cpu_baseline(rg, sc, args.refine, args.cpu_sample)
     print(json.dumps(line), flush=True)
 
 

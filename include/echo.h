@@ -72,6 +72,20 @@ typedef struct echo_graph_s *echo_graph;
  *   coll_type[c]   ECHO_AR, ECHO_AG, ECHO_RS or ECHO_P2P
  *   coll_bytes[c]  message size S, 0 <= S < 2^50 (AG/RS: the full buffer)
  *   gpus_per_node  ranks per server: node(rank) = rank / gpus_per_node
+ *   coll_N[c], coll_M[c], coll_K[c]
+ *                  optional (all three or none; NULL = derived from the members):
+ *                  the membership the cost of collective c is computed with --
+ *                  N members, M distinct servers, K most members on one server --
+ *                  when some members are not part of this graph.  This is the
+ *                  symmetry reduction of data-parallel training (Sec. 8.5, DDP
+ *                  mode: one copy of the workload per DP group): simulate one DP
+ *                  replica, give each collective its whole group's N, M, K, and
+ *                  its barrier is met by the member ops present (a DP collective
+ *                  with one local member becomes a self-barrier).  When every
+ *                  replica has the same durations (no jitter) the result equals
+ *                  the sweep over all replicas op for op.  Requires
+ *                  1 <= M <= N, 1 <= K <= N, M*K >= N, N >= the members present,
+ *                  N = 2 for P2P; else ECHO_ERR_ARG.
  *
  * Collective membership is explicit (op_coll): every rank in a group joins
  * with exactly one comm op.  P2P collectives have exactly two members.
@@ -88,6 +102,7 @@ typedef struct {
     int64_t n_colls;
     const uint8_t *coll_type;
     const int64_t *coll_bytes;
+    const int32_t *coll_N, *coll_M, *coll_K;
 } echo_graph_desc;
 
 /*

@@ -49,7 +49,7 @@ def _load():
     P = ctypes.c_void_p
     i64, i32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
     lib.oracle_run.restype = ctypes.c_int
-    lib.oracle_run.argtypes = [i64, i32, i32] + [P] * 8 + [i64, P, P, i32] + [P] * 9 + [i32, i32] \
+    lib.oracle_run.argtypes = [i64, i32, i32] + [P] * 8 + [i64, P, P, P, P, P, i32] + [P] * 9 + [i32, i32] \
         + [P] * 6 + [ctypes.c_char_p, i64]
     lib.oracle_chunk_bytes.restype = i64
     lib.oracle_chunk_bytes.argtypes = [i64]
@@ -97,6 +97,10 @@ def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelin
     coll_type = _c(g["coll_type"], np.uint8)
     coll_bytes = _c(g["coll_bytes"], np.int64)
     n_ops, n_colls = op_rank.shape[0], coll_type.shape[0]
+    # optional membership the costs use (one DP replica simulated alone)
+    given = [None if graph.get(k) is None else _c(graph[k], np.int32) for k in ("coll_N", "coll_M", "coll_K")]
+    if any(x is not None and x.shape[0] != n_colls for x in given):
+        raise OracleError(-1, "coll_N, coll_M and coll_K must have n_colls entries")
     if pred_off.shape[0] != n_ops + 1:
         raise OracleError(-1, "pred_off must have n_ops + 1 entries")
     n = int(np.asarray(scen["alpha_ns"]).shape[0])
@@ -123,7 +127,7 @@ def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelin
     rc = lib.oracle_run(
         n_ops, int(graph["n_ranks"]), int(graph["gpus_per_node"]),
         _p(op_rank), _p(op_stream), _p(op_kind), _p(op_class), _p(op_dur), _p(op_coll),
-        _p(pred_off), _p(pred_idx), n_colls, _p(coll_type), _p(coll_bytes),
+        _p(pred_off), _p(pred_idx), n_colls, _p(coll_type), _p(coll_bytes), *[_p(x) for x in given],
         n, _p(alpha), _p(bwa), _p(bwe), _p(red), _p(jseed), _p(jstream), _p(jamp), _p(algo), _p(slow),
         int(n_refine), int(max(1, threads)),
         _p(out.get("start")), _p(out.get("finish")), _p(out["step"]), _p(out["digest"]),

@@ -73,6 +73,9 @@ typedef struct {
     int64_t n_colls;
     const uint8_t *coll_type;
     const int64_t *coll_bytes;
+    /* optional membership each collective is costed with (Sec. 8.5, DDP mode: one
+       DP replica simulated alone, its collectives keeping their whole group's size) */
+    const int32_t *coll_N, *coll_M, *coll_K;
 } graph_t;
 
 typedef struct {
@@ -91,7 +94,9 @@ typedef struct {
     int64_t *succ;
     int64_t *mem_off;        /* members of each collective (CSR), program order  */
     int64_t *mem;
-    int64_t *cN, *cM, *cK;   /* members, distinct servers, max members per server */
+    int64_t *cN;             /* member ops present: the arrivals that complete a barrier */
+    int64_t *cM, *cK;        /* distinct servers, max members per server (of those present) */
+    int64_t *tN, *tM, *tK;   /* N, M, K the cost formulas use (given, else cN, cM, cK) */
     int64_t *cl_off;         /* comm ops of each (rank, stream), program order   */
     int64_t *cl;
 } derived_t;
@@ -430,7 +435,7 @@ static int check_scen(const scen_t *sc, char *err, int64_t errlen) {
 
 static void free_derived(derived_t *d) {
     free(d->npred); free(d->succ_off); free(d->succ); free(d->mem_off); free(d->mem);
-    free(d->cN); free(d->cM); free(d->cK); free(d->cl_off); free(d->cl);
+    free(d->cN); free(d->cM); free(d->cK); free(d->tN); free(d->tM); free(d->tK); free(d->cl_off); free(d->cl);
 }
 
 static int cmp_i64(const void *a, const void *b) {
@@ -466,9 +471,12 @@ static int derive(const graph_t *g, derived_t *d, char *err, int64_t errlen) {
     d->cN = calloc((size_t)nc + 1, sizeof(int64_t));
     d->cM = calloc((size_t)nc + 1, sizeof(int64_t));
     d->cK = calloc((size_t)nc + 1, sizeof(int64_t));
+    d->tN = calloc((size_t)nc + 1, sizeof(int64_t));
+    d->tM = calloc((size_t)nc + 1, sizeof(int64_t));
+    d->tK = calloc((size_t)nc + 1, sizeof(int64_t));
     d->cl_off = calloc((size_t)R * NSTREAM + 2, sizeof(int64_t));
     if (!stream_prev || !last || !buf || !d->npred || !d->succ_off || !d->mem_off || !d->cN || !d->cM
-        || !d->cK || !d->cl_off) goto nomem;
+        || !d->cK || !d->tN || !d->tM || !d->tK || !d->cl_off) goto nomem;
     for (int64_t i = 0; i < R * NSTREAM; i++) last[i] = -1;
     for (int64_t v = 0; v < n; v++) {
         const int64_t key = (int64_t)g->op_rank[v] * NSTREAM + g->op_stream[v];
@@ -526,6 +534,23 @@ static int derive(const graph_t *g, derived_t *d, char *err, int64_t errlen) {
             free(stream_prev); free(last); free(buf); free_derived(d);
             return E_MATCH;
         }
+        d->tN[c] = d->cN[c];
+        d->tM[c] = d->cM[c];
+        d->tK[c] = d->cK[c];
+        if (g->coll_N) {
+            /* the whole group: at least the members present, M servers of at most K each */
+            const int64_t N = g->coll_N[c], M = g->coll_M[c], K = g->coll_K[c];
+            if (N < d->cN[c] || M < 1 || M > N || K < 1 || K > N || M * K < N
+                || (g->coll_type[c] == P2P && N != 2)) {
+                set_err(err, errlen, "collective %lld: given membership inconsistent (N %lld)", (long long)c,
+                        (long long)N);
+                free(stream_prev); free(last); free(buf); free_derived(d);
+                return E_ARG;
+            }
+            d->tN[c] = N;
+            d->tM[c] = M;
+            d->tK[c] = K;
+        }
     }
     /* comm ops per (rank, stream), program order */
     for (int64_t v = 0; v < n; v++)
@@ -576,7 +601,7 @@ static int run_scenario(job_t *jb, int32_t si, work_t *w, int64_t *s, int64_t *f
     if (rc) return rc;
     /* CC estimator */
     for (int64_t c = 0; c < g->n_colls; c++) {
-        cost[c] = cc_time(g->coll_type[c], g->coll_bytes[c], dv->cN[c], dv->cM[c], dv->cK[c], &sc);
+        cost[c] = cc_time(g->coll_type[c], g->coll_bytes[c], dv->tN[c], dv->tM[c], dv->tK[c], &sc);
         if (cost[c] < 0) {
             snprintf(jb->msg, sizeof jb->msg, "collective %lld costs >= 2^62 ns", (long long)c);
             return E_RANGE;
@@ -657,14 +682,19 @@ int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int3
                const uint8_t *op_stream, const uint8_t *op_kind, const uint8_t *op_class,
                const int64_t *op_dur, const int64_t *op_coll, const int64_t *pred_off,
                const int32_t *pred_idx, int64_t n_colls, const uint8_t *coll_type,
-               const int64_t *coll_bytes, int32_t n_scen, const int64_t *alpha,
+               const int64_t *coll_bytes, const int32_t *coll_N, const int32_t *coll_M,
+               const int32_t *coll_K, int32_t n_scen, const int64_t *alpha,
                const int64_t *bw_intra, const int64_t *bw_inter, const int64_t *reduce,
                const uint64_t *jseed, const uint32_t *jstream, const int32_t *jamp,
                const uint8_t *algo, const uint32_t *slow, int32_t n_refine, int32_t n_threads,
                int64_t *start, int64_t *finish, int64_t *step, uint64_t *digest, int64_t *cost,
                uint32_t *factor, char *err, int64_t errlen) {
     graph_t g = {n_ops, n_ranks, gpus_per_node, op_rank, op_stream, op_kind, op_class, op_dur,
-                 op_coll, pred_off, pred_idx, n_colls, coll_type, coll_bytes};
+                 op_coll, pred_off, pred_idx, n_colls, coll_type, coll_bytes, coll_N, coll_M, coll_K};
+    if ((coll_N || coll_M || coll_K) && !(coll_N && coll_M && coll_K)) {
+        set_err(err, errlen, "coll_N, coll_M and coll_K go together", 0, 0);
+        return E_ARG;
+    }
     if (err && errlen > 0) err[0] = 0;
     if (n_scen < 0 || n_refine < 0 || n_threads < 1) {
         set_err(err, errlen, "bad n_scen %lld / n_refine %lld", (long long)n_scen, (long long)n_refine);

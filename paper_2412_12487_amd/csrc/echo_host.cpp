@@ -262,7 +262,11 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
         for (int64_t v = 0; v < n; ++v)
             if (d->op_kind[v] == ECHO_COMM) mem[fill[d->op_coll[v]]++] = (int32_t)v;
     }
-    std::vector<int32_t> cN(nc), cM(nc), cK(nc);
+    const bool given = d->coll_N || d->coll_M || d->coll_K;
+    if (given && !(d->coll_N && d->coll_M && d->coll_K))
+        return fail(ECHO_ERR_ARG, "coll_N, coll_M and coll_K must be given together");
+    std::vector<int32_t> cN(nc), cM(nc), cK(nc);   // members present, and the cost's N, M, K
+    std::vector<int32_t> kN(nc), kM(nc), kK(nc);
     for (int64_t c = 0; c < nc; ++c) {
         const int64_t N = moff[c + 1] - moff[c];
         if (N == 0) return fail(ECHO_ERR_MATCH, "collective %lld has no member op", (long long)c);
@@ -285,6 +289,20 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
         cN[c] = (int32_t)N;
         cM[c] = servers;
         cK[c] = best;
+        kN[c] = (int32_t)N;
+        kM[c] = servers;
+        kK[c] = best;
+        if (given) {
+            const int64_t gN = d->coll_N[c], gM = d->coll_M[c], gK = d->coll_K[c];
+            if (gN < N || gM < 1 || gM > gN || gK < 1 || gK > gN || gM * gK < gN ||
+                (d->coll_type[c] == ECHO_P2P && gN != 2))
+                return fail(ECHO_ERR_ARG,
+                            "collective %lld: membership N=%lld M=%lld K=%lld is inconsistent with its %lld "
+                            "member op(s)", (long long)c, (long long)gN, (long long)gM, (long long)gK, (long long)N);
+            kN[c] = (int32_t)gN;
+            kM[c] = (int32_t)gM;
+            kK[c] = (int32_t)gK;
+        }
     }
 
     // matching rule: within one communicator (the (rank, stream) set of the
@@ -323,7 +341,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     {
         std::map<std::array<int64_t, 5>, int32_t> cls_id;
         for (int64_t c = 0; c < nc; ++c) {
-            const std::array<int64_t, 5> k{d->coll_type[c], d->coll_bytes[c], cN[c], cM[c], cK[c]};
+            const std::array<int64_t, 5> k{d->coll_type[c], d->coll_bytes[c], kN[c], kM[c], kK[c]};
             auto it = cls_id.emplace(k, (int32_t)classes.size());
             if (it.second) classes.push_back(k);
             ccls[c] = it.first->second;
@@ -648,7 +666,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
         }
     }
     HostCollTable colls(nc), cls((int64_t)classes.size());
-    for (int64_t c = 0; c < nc; ++c) colls.set(c, d->coll_type[c], d->coll_bytes[c], cN[c], cM[c], cK[c]);
+    for (int64_t c = 0; c < nc; ++c) colls.set(c, d->coll_type[c], d->coll_bytes[c], kN[c], kM[c], kK[c]);
     for (size_t k = 0; k < classes.size(); ++k)
         cls.set((int64_t)k, (int)classes[k][0], classes[k][1], (int32_t)classes[k][2], (int32_t)classes[k][3],
                 (int32_t)classes[k][4]);
@@ -698,6 +716,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
         UP(dt.K, h.K);
         UP(dt.type, h.type);
     }
+    UP(dg.members, cN);
     UP(dg.block_class, block_class);
     UP(dg.cl_off, cl_off);
     UP(dg.cl, cl);
@@ -765,7 +784,7 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
             a.items = g->dg.items;
             a.walk_off = g->dg.walk_off;
             a.far = g->dg.far;
-            a.c_N = g->dg.colls.N;
+            a.c_N = g->dg.members;
             a.block_class = g->dg.block_class;
             a.scen = d_scen;
             a.cost = g->cost;

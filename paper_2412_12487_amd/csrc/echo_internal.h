@@ -125,6 +125,7 @@ struct DeviceGraph {
     int64_t *walk_off = nullptr;     // [n_walkers + 1] offsets into items
     int32_t *far = nullptr;          // far predecessor op ids
     CollTable colls;                 // every collective
+    int32_t *members = nullptr;      // [n_colls] member ops present: arrivals that complete a barrier
     CollTable classes;               // every cost class
     int32_t *block_class = nullptr;  // [n_blocks][kClassSlots] class staged in each LDS slot, -1 = none
     // overlap detection: comm / compute ops of each (rank, stream), program order
@@ -140,7 +141,7 @@ struct WalkArgs {
     const WalkItem *items;
     const int64_t *walk_off;
     const int32_t *far;
-    const int32_t *c_N;
+    const int32_t *c_N;              // [coll] member ops present (arrivals that complete the barrier)
     const int32_t *block_class;
     const echo_scenario *scen;
     const int64_t *cost;             // [coll][scen]

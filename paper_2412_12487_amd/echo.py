@@ -48,6 +48,7 @@ class _Desc(ctypes.Structure):
         ("op_class", ctypes.c_void_p), ("op_dur_ns", ctypes.c_void_p), ("op_coll", ctypes.c_void_p),
         ("pred_off", ctypes.c_void_p), ("pred_idx", ctypes.c_void_p), ("n_colls", ctypes.c_int64),
         ("coll_type", ctypes.c_void_p), ("coll_bytes", ctypes.c_void_p),
+        ("coll_N", ctypes.c_void_p), ("coll_M", ctypes.c_void_p), ("coll_K", ctypes.c_void_p),
     ]
 
 
@@ -134,15 +135,23 @@ class Graph:
             "coll_type": np.ascontiguousarray(arrays["coll_type"], np.uint8),
             "coll_bytes": np.ascontiguousarray(arrays["coll_bytes"], np.int64),
         }
+        nc = self._keep["coll_type"].shape[0]
+        for key in ("coll_N", "coll_M", "coll_K"):       # optional: membership of partial collectives
+            if arrays.get(key) is not None:
+                self._keep[key] = np.ascontiguousarray(arrays[key], np.int32)
+                if self._keep[key].shape[0] != nc:
+                    raise EchoError(ECHO_ERR_ARG, f"{key} must have n_colls entries")
         k = self._keep
         n = k["op_rank"].shape[0]
         if k["pred_off"].shape[0] != n + 1:
             raise EchoError(ECHO_ERR_ARG, "pred_off must have n_ops + 1 entries")
         ptr = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+        opt = lambda key: ptr(k[key]) if key in k else None
         d = _Desc(n, int(arrays["n_ranks"]), int(arrays["gpus_per_node"]),
                   ptr(k["op_rank"]), ptr(k["op_stream"]), ptr(k["op_kind"]), ptr(k["op_class"]),
                   ptr(k["op_dur"]), ptr(k["op_coll"]), ptr(k["pred_off"]), ptr(k["pred_idx"]),
-                  k["coll_type"].shape[0], ptr(k["coll_type"]), ptr(k["coll_bytes"]))
+                  nc, ptr(k["coll_type"]), ptr(k["coll_bytes"]),
+                  opt("coll_N"), opt("coll_M"), opt("coll_K"))
         h = ctypes.c_void_p()
         _check(L.echo_load_graph_ex(ctypes.byref(d), int(device), int(ranks_per_walker), ctypes.byref(h)))
         self._keep = None

@@ -153,3 +153,33 @@ def test_walker_width_out_of_range_is_an_argument_error(E):
         with pytest.raises(E.EchoError) as x:
             E.Graph(g, 0, ranks_per_walker=bad)
         assert x.value.code == E.ECHO_ERR_ARG
+
+
+def _replica_graph():
+    from workloads import gpt1f1b
+    p = dict(configs.TINY, tp=2, pp=2, dp=2, microbatches=2, seed=0)
+    rg, _ = gpt1f1b.dp_replica(gpt1f1b.gpt_graph(**p, replica_invariant=True), 2, 2)
+    return {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in rg.items()}
+
+
+def test_replica_graph_with_group_membership_passes_validation(E):
+    assert _load_code(E, _replica_graph()) == _valid_code(E)
+
+
+@pytest.mark.parametrize("what", ["partial", "N_below_members", "M_zero", "MK_short", "p2p_not_two"])
+def test_inconsistent_group_membership_is_an_argument_error(E, what):
+    g = _replica_graph()
+    c = int(np.flatnonzero(g["coll_type"] != P2P)[0])
+    if what == "partial":
+        g["coll_K"] = None
+    elif what == "N_below_members":
+        q = int(np.flatnonzero(g["coll_type"] == P2P)[0])
+        g["coll_N"][q], g["coll_M"][q], g["coll_K"][q] = 1, 1, 1
+    elif what == "M_zero":
+        g["coll_M"][c] = 0
+    elif what == "MK_short":
+        g["coll_N"][c], g["coll_M"][c], g["coll_K"][c] = 9, 2, 4
+    else:
+        q = int(np.flatnonzero(g["coll_type"] == P2P)[0])
+        g["coll_N"][q], g["coll_M"][q], g["coll_K"][q] = 4, 2, 2
+    assert _load_code(E, g) == E.ECHO_ERR_ARG

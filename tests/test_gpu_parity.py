@@ -319,3 +319,65 @@ def test_time_limit_reported(E):
         G.compose(d, n, 0)
     assert x.value.code == E.ECHO_ERR_RANGE
     G.close()
+
+
+# ---------------------------------------------------------------- DP-replica symmetry reduction
+# One data-parallel replica composed alone (collectives costed at their whole
+# group's size, barriers met by the members present) against the oracle, and
+# against the GPU's own sweep over every replica.
+from tests.test_oracle_pins import REPLICA_CASES, _replica_scen   # noqa: E402
+
+
+def _replica_pair(params):
+    g = gpt1f1b.gpt_graph(**params, replica_invariant=True)
+    rg, op_map = gpt1f1b.dp_replica(g, params["tp"], params["dp"])
+    return g, rg, op_map
+
+
+def _full_vs_replica(E, g, rg, op_map, sc, R):
+    """GPU sweep over all replicas and over one replica; the replica's rows must agree."""
+    import torch
+    d, n = E.scenarios_to_device(sc)
+    Gf, Gr = E.Graph(g, 0), E.Graph(rg, 0)
+    full = Gf.compose(d, n, R, timelines=True)
+    red = Gr.compose(d, n, R, timelines=True)
+    idx = torch.as_tensor(op_map, device=full["finish"].device)
+    np.testing.assert_array_equal(full["step"].cpu().numpy(), red["step"].cpu().numpy())
+    for key in ("start", "finish"):
+        assert torch.equal(full[key].index_select(0, idx), red[key]), key
+    Gf.close()
+    Gr.close()
+    return {"step": red["step"].cpu().numpy(), "start": red["start"].cpu().numpy(),
+            "finish": red["finish"].cpu().numpy()}
+
+
+@pytest.mark.parametrize("case", range(len(REPLICA_CASES)))
+def test_dp_replica_small(E, case):
+    g, rg, op_map = _replica_pair(REPLICA_CASES[case])
+    sc = _replica_scen(case, 70)
+    for R in (0, 1, 2):
+        red = _full_vs_replica(E, g, rg, op_map, sc, R)
+        assert_same(red, oracle.run(rg, sc, R, threads=THREADS))
+
+
+def test_dp_replica_gpt175b_tp8pp4dp3(E):
+    p = configs.graph_params(2)
+    g, rg, op_map = _replica_pair(p)
+    sc = configs.scenario_batch(2)
+    red = _full_vs_replica(E, g, rg, op_map, sc, 1)
+    assert_same(red, oracle.run(rg, sc, 1, threads=THREADS))
+
+
+def test_dp_replica_gpt175b_8192_ranks(E):
+    """GPT-175B TP8 x PP16 x DP64 (8192 ranks): the full sweep needs two ranks per
+    wavefront; its DP replica has 128 ranks."""
+    p = configs.graph_params(5, 15)
+    g, rg, op_map = _replica_pair(p)
+    sc = configs.scenario_batch(5, 15)
+    red = _full_vs_replica(E, g, rg, op_map, sc, 1)
+    cols = [0, scenarios.count(sc) - 1]
+    ref = oracle.run(rg, scenarios.take(sc, cols), 1, threads=2)
+    np.testing.assert_array_equal(red["step"][cols], ref["step"])
+    for j, c in enumerate(cols):
+        np.testing.assert_array_equal(red["finish"][:, c], ref["finish"][j])
+        np.testing.assert_array_equal(red["start"][:, c], ref["start"][j])

@@ -474,3 +474,93 @@ def test_all_benchmark_graphs_small_enough_compose():
         g = configs.graph(cfg)
         r = oracle.run(g, scenarios.take(configs.scenario_batch(cfg), slice(0, 2)), 1, timelines=False)
         assert (r["step"] > 0).all()
+
+
+# ---------------------------------------------------------------- DP-replica symmetry reduction
+# Sec. 8.5 (DDP mode): one copy of the workload per DP group.  Simulating one
+# replica, with every collective costed at its whole group's size and its
+# barrier met by the members present, must reproduce the sweep over all
+# replicas op for op when every replica has the same durations.
+REPLICA_CASES = [
+    dict(configs.TINY, tp=2, pp=2, dp=2, microbatches=4, seed=0),
+    dict(configs.TINY, tp=2, pp=2, dp=4, microbatches=3, seed=1, gpus_per_node=2),   # DP groups span servers
+    dict(configs.TINY | dict(n_layers=4), tp=1, pp=4, dp=3, microbatches=4, seed=2, gpus_per_node=1),
+    dict(configs.TINY, tp=2, pp=2, dp=3, microbatches=2, seed=3, distopt=True, gpus_per_node=2),   # RS + AG
+]
+
+
+def _replica_scen(seed, n=6):
+    return scenarios.draw(n, np.random.default_rng(seed), bw_inter=(20000, 400000), bw_intra=(50000, 400000),
+                          alpha=(0, 20000), ar_algo_random=True, slowdown=(65536, 150000))
+
+
+@pytest.mark.parametrize("case", range(len(REPLICA_CASES)))
+def test_dp_replica_equals_full_sweep(case):
+    p = REPLICA_CASES[case]
+    g = gpt1f1b.gpt_graph(**p, replica_invariant=True)
+    rg, op_map = gpt1f1b.dp_replica(g, p["tp"], p["dp"])
+    assert len(rg["op_rank"]) * p["dp"] == len(g["op_rank"])
+    # precondition: the replicas are copies of each other, placement (hence costs) included
+    for k in range(1, p["dp"]):
+        rk, _ = gpt1f1b.dp_replica(g, p["tp"], p["dp"], replica=k)
+        for key, val in rg.items():
+            np.testing.assert_array_equal(np.asarray(rk[key]), np.asarray(val), err_msg=key)
+    sc = _replica_scen(case)
+    for R in (0, 1, 2):
+        full, red = oracle.run(g, sc, R), oracle.run(rg, sc, R)
+        np.testing.assert_array_equal(full["step"], red["step"])
+        np.testing.assert_array_equal(full["start"][:, op_map], red["start"])
+        np.testing.assert_array_equal(full["finish"][:, op_map], red["finish"])
+    # every replica runs the same timeline
+    for k in range(1, p["dp"]):
+        _, m_k = gpt1f1b.dp_replica(g, p["tp"], p["dp"], replica=k)
+        np.testing.assert_array_equal(full["finish"][:, m_k], red["finish"])
+
+
+def test_dp_replica_of_asymmetric_placement_differs():
+    """Replicas placed differently (a pipeline hop inside a server for one replica,
+    across servers for another) are not copies: the reduction does not apply."""
+    p = dict(configs.TINY | dict(n_layers=4), tp=1, pp=4, dp=3, microbatches=4, seed=2, gpus_per_node=4)
+    g = gpt1f1b.gpt_graph(**p, replica_invariant=True)
+    r0, _ = gpt1f1b.dp_replica(g, 1, 3, replica=0)
+    r1, _ = gpt1f1b.dp_replica(g, 1, 3, replica=1)
+    assert (r0["coll_M"] != r1["coll_M"]).any()
+    sc = _replica_scen(2)
+    assert (oracle.run(g, sc, 1)["step"] != oracle.run(r0, sc, 1)["step"]).any()
+
+
+def test_dp_replica_needs_the_whole_group_membership():
+    """Costing the replica's collectives at their local size (or drawing durations per
+    replica) changes the result: the reduction is exact only as specified."""
+    p = REPLICA_CASES[1]
+    g = gpt1f1b.gpt_graph(**p, replica_invariant=True)
+    rg, op_map = gpt1f1b.dp_replica(g, p["tp"], p["dp"])
+    sc = _replica_scen(11)
+    full = oracle.run(g, sc, 1)
+    local = {k: v for k, v in rg.items() if k not in ("coll_N", "coll_M", "coll_K")}
+    assert (oracle.run(local, sc, 1)["step"] != full["step"]).any()
+    g2 = gpt1f1b.gpt_graph(**p)                       # durations differ between replicas
+    rg2, _ = gpt1f1b.dp_replica(g2, p["tp"], p["dp"])
+    assert (oracle.run(rg2, sc, 1)["step"] != oracle.run(g2, sc, 1)["step"]).any()
+
+
+@pytest.mark.parametrize("bad", [dict(N=0), dict(M=0), dict(K=0), dict(MK=True), dict(P2P=3)])
+def test_inconsistent_group_membership_rejected(bad):
+    p = REPLICA_CASES[0]
+    rg, _ = gpt1f1b.dp_replica(gpt1f1b.gpt_graph(**p, replica_invariant=True), p["tp"], p["dp"])
+    rg = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in rg.items()}
+    c = int(np.flatnonzero(rg["coll_type"] != P2P)[0])
+    if "N" in bad:
+        rg["coll_N"][c] = 0
+    if "M" in bad:
+        rg["coll_M"][c] = 0
+    if "K" in bad:
+        rg["coll_K"][c] = 0
+    if "MK" in bad:
+        rg["coll_N"][c], rg["coll_M"][c], rg["coll_K"][c] = 8, 2, 3
+    if "P2P" in bad:
+        q = int(np.flatnonzero(rg["coll_type"] == P2P)[0])
+        rg["coll_N"][q], rg["coll_M"][q], rg["coll_K"][q] = 3, 1, 3
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.run(rg, scenarios.default_scenarios(1), 1)
+    assert e.value.code == -1

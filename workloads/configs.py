@@ -72,10 +72,11 @@ def graph(config: int, index: int = 0) -> dict:
     return gpt1f1b.gpt_graph(**graph_params(config, index))
 
 
-def scenario_batch(config: int, index: int = 0) -> dict:
-    """The seeded scenario batch of a config (index: config-5 graph)."""
+def scenario_batch(config: int, index: int = 0, n: int | None = None) -> dict:
+    """The seeded scenario batch of a config (index: config-5 graph; n: another
+    batch size drawn with the same recipe)."""
     rng = np.random.default_rng(1000 + config)
-    n = N_SCEN[config]
+    n = N_SCEN[config] if n is None else int(n)
     if config == 1:
         return scenarios.default_scenarios(n)
     if config == 2:

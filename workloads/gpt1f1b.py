@@ -284,8 +284,12 @@ def _build_stage(p, P, tp, dp, m, n_layers, h, seq, distopt):
 
 
 def gpt_graph(*, n_layers, hidden, seq, tp, pp, dp, microbatches, seed,
-              distopt=False, gpus_per_node=8):
-    """Build the execution graphs of all TP*PP*DP ranks of one training step."""
+              distopt=False, gpus_per_node=8, replica_invariant=False):
+    """Build the execution graphs of all TP*PP*DP ranks of one training step.
+
+    replica_invariant: every data-parallel replica gets the same durations (one
+    draw per pipeline stage, tensor-parallel rank and op), as when a single
+    replica is traced and copied."""
     if n_layers % pp:
         raise ValueError("n_layers must be divisible by pp")
     P, T, D, m = pp, tp, dp, microbatches
@@ -347,7 +351,11 @@ def gpt_graph(*, n_layers, hidden, seq, tp, pp, dp, microbatches, seed,
     n_ops = base
     durk = np.concatenate(parts["durk"])
     rng = np.random.default_rng(seed)
-    z = rng.standard_normal(n_ops)
+    if replica_invariant:
+        z = np.concatenate([np.tile(rng.standard_normal((T, len(s.kind))), (D, 1)).reshape(-1) for s in stages]) \
+            if n_ops else np.zeros(0)
+    else:
+        z = rng.standard_normal(n_ops)
     med = np.where(durk == _DUR_MEMCPY, MEMCPY_MEDIAN_NS, COMPUTE_MEDIAN_NS)
     dur = np.maximum(np.rint(med * np.exp(LOG_SIGMA * z)), 1.0).astype(np.int64)
     dur[durk == _DUR_NONE] = 0
@@ -368,3 +376,61 @@ def gpt_graph(*, n_layers, hidden, seq, tp, pp, dp, microbatches, seed,
         "n_ranks": P * T * D,
         "gpus_per_node": gpus_per_node,
     }
+
+
+def dp_replica(graph: dict, tp: int, dp: int, replica: int = 0):
+    """The graph of one data-parallel replica, as Echo's DDP mode simulates it
+    (Sec. 8.5: one copy of the workload per DP group).
+
+    Keeps the ranks with data-parallel index `replica` (rank = tp + TP*(dp + DP*pp)),
+    renumbered tp + TP*pp, and every collective with a member among them.  Each
+    kept collective carries the membership of its whole group -- coll_N members,
+    coll_M distinct servers, coll_K most members on one server, from the full
+    placement -- so its cost is unchanged while its barrier only involves the
+    members kept.  Returns (replica graph, op_map) with op_map[new op] = old op.
+    """
+    rank = graph["op_rank"].astype(np.int64)
+    keep = (rank // tp) % dp == replica
+    op_map = np.flatnonzero(keep)
+    new_id = np.full(rank.shape[0], -1, np.int64)
+    new_id[op_map] = np.arange(op_map.shape[0])
+    comm = graph["op_kind"] == KIND_COMM
+    coll = graph["op_coll"]
+    n_colls = graph["coll_type"].shape[0]
+    # whole-group membership of every collective
+    node = rank // int(graph["gpus_per_node"])
+    cm = coll[comm]
+    N = np.bincount(cm, minlength=n_colls)
+    pairs, cnt = np.unique(np.stack([cm, node[comm]], 1), axis=0, return_counts=True) if cm.size else \
+        (np.zeros((0, 2), np.int64), np.zeros(0, np.int64))
+    M = np.bincount(pairs[:, 0], minlength=n_colls)
+    K = np.zeros(n_colls, np.int64)
+    np.maximum.at(K, pairs[:, 0], cnt)
+    kept_colls = np.unique(coll[keep & comm])
+    cmap = np.full(n_colls, -1, np.int64)
+    cmap[kept_colls] = np.arange(kept_colls.shape[0])
+    # dependencies: same-rank, so every predecessor of a kept op is kept
+    pcount = np.diff(graph["pred_off"])[op_map]
+    src = np.repeat(np.arange(rank.shape[0]), np.diff(graph["pred_off"]))
+    pidx = graph["pred_idx"][keep[src]]
+    pred_off = np.zeros(op_map.shape[0] + 1, np.int64)
+    np.cumsum(pcount, out=pred_off[1:])
+    r = rank[op_map]
+    out = {
+        "op_rank": ((r % tp) + tp * (r // (tp * dp))).astype(np.int32),
+        "op_stream": graph["op_stream"][op_map],
+        "op_kind": graph["op_kind"][op_map],
+        "op_class": graph["op_class"][op_map],
+        "op_dur": graph["op_dur"][op_map],
+        "op_coll": np.where(coll[op_map] >= 0, cmap[np.maximum(coll[op_map], 0)], -1).astype(np.int64),
+        "pred_off": pred_off,
+        "pred_idx": new_id[pidx].astype(np.int32),
+        "coll_type": graph["coll_type"][kept_colls],
+        "coll_bytes": graph["coll_bytes"][kept_colls],
+        "coll_N": N[kept_colls].astype(np.int32),
+        "coll_M": M[kept_colls].astype(np.int32),
+        "coll_K": K[kept_colls].astype(np.int32),
+        "n_ranks": int(graph["n_ranks"]) // dp,
+        "gpus_per_node": int(graph["gpus_per_node"]),
+    }
+    return out, op_map
