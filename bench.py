@@ -94,7 +94,11 @@ def main():
                     help="batch size drawn with the config's recipe (0 = the config's own)")
     ap.add_argument("--replica", action="store_true",
                     help="time one DP replica composed alone against the sweep over every replica")
-    ap.add_argument("--refine", type=int, default=1)
+    ap.add_argument("--refine", type=int, default=1, help="refinements (the most, with --until-stable)")
+    ap.add_argument("--until-stable", action="store_true",
+                    help="validator variant: refine until no duration changes (at most --refine times)")
+    ap.add_argument("--prorate", action="store_true",
+                    help="validator variant: inflate only the overlapped part of a compute op")
     ap.add_argument("--cpu-sample", type=int, default=8, help="scenarios the CPU oracle composes (0 = skip)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device once (calibrates HBM byte counters) and exit")
@@ -145,16 +149,25 @@ def main():
         "dtype": "int64",
         "data": "synthetic",
         "config": {"workload": f"config {args.config}: {configs.NAMES[args.config]}, "
-                               f"{r['n_ops']} ops x {r['n_scen']} scenarios, {args.refine} refinement(s)",
+                               f"{r['n_ops']} ops x {r['n_scen']} scenarios, " + validator_name(args),
                    "n_ops": r["n_ops"], "n_scenarios": r["n_scen"], "n_refine": args.refine,
                    "ranks": int(g["n_ranks"]), "levels": r["levels"], "load_s": round(r["load_s"], 2)},
         "kernels_ms": r["kernels_ms"],
-        "roofline": roofline(g, r, args, args.config),
+        "roofline": roofline(g, r, args, args.config if not (args.until_stable or args.prorate) else None),
     }
+    if "refinements" in r:
+        line["config"]["refinements"] = r["refinements"]
     if args.cpu_sample > 0:
         log(f"cpu baseline: oracle on {args.cpu_sample} scenario(s) ...")
         line["cpu_baseline"] = cpu_baseline(g, sc, args.refine, args.cpu_sample)
     print(json.dumps(line), flush=True)
+
+
+def validator_name(args):
+    if not (args.until_stable or args.prorate):
+        return f"{args.refine} refinement(s)"
+    kind = " + ".join(x for x, on in (("until stable", args.until_stable), ("prorated", args.prorate)) if on)
+    return f"validator {kind}, at most {args.refine} refinement(s)"
 
 
 def time_compose(E, g, sc, args):
@@ -170,8 +183,10 @@ def time_compose(E, g, sc, args):
            "start": torch.empty((G.n_ops, n_scen), dtype=torch.int64, device=dev),
            "finish": torch.empty((G.n_ops, n_scen), dtype=torch.int64, device=dev)}
     G.set_timing(True)
+    variant = dict(until_stable=args.until_stable, prorate=args.prorate,
+                   refinements=args.until_stable or args.prorate)
     for i in range(args.warmup):
-        G.compose(d_scen, n_scen, args.refine, out=out)
+        G.compose(d_scen, n_scen, args.refine, out=out, **variant)
         log(f"warmup {i}: {G.kernel_times()}")
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream(dev)
@@ -180,7 +195,7 @@ def time_compose(E, g, sc, args):
     for i in range(args.steps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        G.compose(d_scen, n_scen, args.refine, out=out, check=False)
+        last = G.compose(d_scen, n_scen, args.refine, out=out, check=False, **variant)
         e1.record(stream)
         torch.cuda.synchronize()
         step_ms.append(e0.elapsed_time(e1))
@@ -192,19 +207,26 @@ def time_compose(E, g, sc, args):
     wall = time.perf_counter() - t0
     G.sync_status()
     ms_per_step = wall * 1000.0 / args.steps
-    n_walk = sum(1 for k, _ in G.kernel_times() if k == "walk")
+    # walk launches that ran (a pass past every scenario's fixed point returns at once)
+    lw = [ms for k, ms in G.kernel_times() if k == "walk"]
+    ran = [ms for ms in lw if ms > 0.02 * max(lw, default=0.0)]
+    n_walk = len(ran)
     res = {"n_ops": G.n_ops, "n_scen": n_scen, "levels": G.n_levels, "load_s": load_s,
            "ms_per_step": ms_per_step, "gpu_ms": float(np.median(step_ms)),
            "value": G.n_ops * n_scen / (ms_per_step / 1000.0),
-           "walk_avg_ms": float(np.mean(walk_ms)) / max(n_walk, 1), "n_walk": n_walk,
+           "walk_avg_ms": float(np.mean(walk_ms)) * (sum(ran) / max(sum(lw), 1e-9)) / max(n_walk, 1),
+           "n_walk": n_walk,
            "kernels_ms": {k: round(float(np.mean(v)), 4) for k, v in kernels.items()}}
+    if args.steps and "refinements" in last:
+        rf = last["refinements"].cpu().numpy()
+        res["refinements"] = {"min": int(rf.min()), "mean": round(float(rf.mean()), 3), "max": int(rf.max())}
     del out
     G.close()
     return res
 
 
 def roofline(g, r, args, traffic_config):
-    passes = walk_bytes(g, r["n_scen"], args.refine)
+    passes = walk_bytes(g, r["n_scen"], max(r["n_walk"] - 1, 0))
     bytes_per_launch = sum(passes) / max(r["n_walk"], 1)
     achieved = bytes_per_launch / (r["walk_avg_ms"] / 1000.0) / 1e9
     traffic = None

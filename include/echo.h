@@ -200,6 +200,38 @@ int echo_compose_batch(echo_graph g, const echo_scenario *d_scen, int32_t n_scen
                        void *hip_stream);
 
 /*
+ * Validator options (Sec. 3 and Sec. 6 give the model -- overlapped
+ * computation runs slower -- but no iteration rule).
+ *   max_refine    at most this many refinements (0..64)
+ *   until_stable  nonzero: stop refining a scenario once a refinement would
+ *                 leave every duration unchanged (the timeline is then a fixed
+ *                 point: one more refinement reproduces it)
+ *   prorate       nonzero: inflate only the overlapped part of a compute op:
+ *                 duration D - o + q16(o, F), o = the time of [start, finish)
+ *                 covered by the union of the overlapping comm ops' intervals
+ *                 on the previous timeline, capped at D; zero: q16(D, F)
+ */
+typedef struct {
+    int32_t max_refine;
+    int32_t until_stable;
+    int32_t prorate;
+} echo_validator;
+
+/*
+ * echo_compose_batch with validator options.  d_refinements (device, n_scen
+ * int32, or NULL) receives the refinements composed per scenario: with
+ * until_stable, those that changed some duration; else max_refine.  Passes
+ * past the point where every scenario is stable are skipped on the device
+ * (no host synchronisation).  With prorate, the extra time of one op,
+ * q16(o, F) - o, must stay below 2^32 - 1 ns (else ECHO_ERR_RANGE from
+ * echo_sync_status).  Errors and ownership as echo_compose_batch; ARG for a
+ * NULL options pointer or max_refine outside 0..64.
+ */
+int echo_compose_validated(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const echo_validator *opts,
+                           int64_t *d_start, int64_t *d_finish, int64_t *d_step, uint64_t *d_digest,
+                           int32_t *d_refinements, void *hip_stream);
+
+/*
  * Wait for `hip_stream` and report the device-side status of the graph's
  * launches since the previous call: ECHO_OK, ECHO_ERR_RANGE (a scenario knob
  * out of range or a time >= 2^62) or ECHO_ERR_DEVICE (a wait for a collective

@@ -49,8 +49,8 @@ def _load():
     P = ctypes.c_void_p
     i64, i32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
     lib.oracle_run.restype = ctypes.c_int
-    lib.oracle_run.argtypes = [i64, i32, i32] + [P] * 8 + [i64, P, P, P, P, P, i32] + [P] * 9 + [i32, i32] \
-        + [P] * 6 + [ctypes.c_char_p, i64]
+    lib.oracle_run.argtypes = [i64, i32, i32] + [P] * 8 + [i64, P, P, P, P, P, i32] + [P] * 9 \
+        + [i32, i32, i32, i32] + [P] * 7 + [ctypes.c_char_p, i64]
     lib.oracle_chunk_bytes.restype = i64
     lib.oracle_chunk_bytes.argtypes = [i64]
     lib.oracle_cc_time.restype = i64
@@ -74,13 +74,17 @@ def _p(a):
 
 
 def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelines: bool = True,
-        costs: bool = False, factors: bool = False, jitter_stream=None) -> dict:
+        costs: bool = False, factors: bool = False, jitter_stream=None, until_stable: bool = False,
+        prorate: bool = False) -> dict:
     """Compose every scenario of `scen` on `graph`.
 
     Returns a dict with 'step' [n_scen] int64 and 'digest' [n_scen] uint64, plus
     'start'/'finish' [n_scen, n_ops] int64 (timelines=True), 'cost'
     [n_scen, n_colls] int64 (costs=True) and 'factor' [n_scen, n_ops] uint32
-    (factors=True).  jitter_stream defaults to the scenario's index in `scen`.
+    (factors=True), and 'refinements' [n_scen] int32: the refined passes composed.
+    until_stable: refine until a refinement would change no duration (at most
+    n_refine times); prorate: inflate only the overlapped part of a compute op.
+    jitter_stream defaults to the scenario's index in `scen`.
     Raises OracleError on invalid input or a deadlocked graph.
     """
     lib = _load()
@@ -115,7 +119,8 @@ def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelin
     jamp = _c(scen["jitter_amp_q16"], np.int32)
     algo = _c(scen["ar_algo"], np.uint8)
     slow = _c(scen["slowdown_q16"], np.uint32).reshape(n, 8, 4)
-    out = {"step": np.zeros(n, np.int64), "digest": np.zeros(n, np.uint64)}
+    out = {"step": np.zeros(n, np.int64), "digest": np.zeros(n, np.uint64),
+           "refinements": np.zeros(n, np.int32)}
     if timelines:
         out["start"] = np.zeros((n, n_ops), np.int64)
         out["finish"] = np.zeros((n, n_ops), np.int64)
@@ -129,9 +134,9 @@ def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelin
         _p(op_rank), _p(op_stream), _p(op_kind), _p(op_class), _p(op_dur), _p(op_coll),
         _p(pred_off), _p(pred_idx), n_colls, _p(coll_type), _p(coll_bytes), *[_p(x) for x in given],
         n, _p(alpha), _p(bwa), _p(bwe), _p(red), _p(jseed), _p(jstream), _p(jamp), _p(algo), _p(slow),
-        int(n_refine), int(max(1, threads)),
+        int(n_refine), int(bool(until_stable)), int(bool(prorate)), int(max(1, threads)),
         _p(out.get("start")), _p(out.get("finish")), _p(out["step"]), _p(out["digest"]),
-        _p(out.get("cost")), _p(out.get("factor")), err, 512)
+        _p(out.get("cost")), _p(out.get("factor")), _p(out["refinements"]), err, 512)
     if rc != 0:
         raise OracleError(rc, err.value.decode(errors="replace"))
     return out

@@ -319,13 +319,16 @@ overflow:
 /* Sec. 6: overlap with communication -> slowdown factor per compute op */
 /* ------------------------------------------------------------------ */
 static void overlap_factors(const graph_t *g, const derived_t *dv, const scen_t *sc,
-                            const int64_t *s, const int64_t *f, uint32_t *F) {
+                            const int64_t *s, const int64_t *f, uint32_t *F, int64_t *O, int64_t *lo_buf,
+                            int64_t *hi_buf) {
     for (int64_t v = 0; v < g->n_ops; v++) {
         F[v] = Q16_ONE;
+        O[v] = 0;
         if (g->op_kind[v] != COMPUTE) continue;
         const int64_t r = g->op_rank[v], sv = s[v], fv = f[v];
         const uint32_t *row = sc->slow + 4 * g->op_class[v];
         uint32_t best = Q16_ONE;
+        int64_t n_iv = 0;           /* overlapping comm intervals, clipped to [sv, fv) */
         for (int k = 0; k < NSTREAM; k++) {
             const int64_t lo0 = dv->cl_off[r * NSTREAM + k], hi0 = dv->cl_off[r * NSTREAM + k + 1];
             /* Comm ops of one stream are FIFO, so their finish times are sorted:
@@ -342,11 +345,44 @@ static void overlap_factors(const graph_t *g, const derived_t *dv, const scen_t 
                 if (a < b) {
                     const uint32_t x = row[g->coll_type[g->op_coll[c]]];
                     if (x > best) best = x;
+                    lo_buf[n_iv] = a;
+                    hi_buf[n_iv] = b;
+                    n_iv++;
                 }
             }
         }
         F[v] = best;
+        /* length of the union of the clipped intervals: sort by start, then sweep */
+        for (int64_t i = 1; i < n_iv; i++) {
+            const int64_t a = lo_buf[i], b = hi_buf[i];
+            int64_t j = i - 1;
+            while (j >= 0 && lo_buf[j] > a) {
+                lo_buf[j + 1] = lo_buf[j];
+                hi_buf[j + 1] = hi_buf[j];
+                j--;
+            }
+            lo_buf[j + 1] = a;
+            hi_buf[j + 1] = b;
+        }
+        int64_t covered = 0, end = sv;
+        for (int64_t i = 0; i < n_iv; i++) {
+            const int64_t a = lo_buf[i] > end ? lo_buf[i] : end;
+            if (hi_buf[i] > a) {
+                covered += hi_buf[i] - a;
+                end = hi_buf[i];
+            }
+        }
+        O[v] = covered;
     }
+}
+
+/* Duration of compute op v in a refined pass (Sec. 6): the whole base duration
+ * D runs F times slower; prorated, only the overlapped part does -- the
+ * overlapped length measured on the previous timeline, capped at D. */
+static int64_t inflated(int64_t D, uint32_t F, int64_t overlapped, int prorate) {
+    if (!prorate) return q16_scale(D, F);
+    const int64_t o = overlapped < D ? overlapped : D;
+    return D - o + q16_scale(o, F);
 }
 
 /* ------------------------------------------------------------------ */
@@ -578,6 +614,7 @@ typedef struct {
     const graph_t *g;
     const derived_t *dv;
     int32_t n_scen, n_refine, n_threads, tid;
+    int32_t until_stable, prorate;
     const int64_t *alpha, *bw_intra, *bw_inter, *reduce;
     const uint64_t *jseed;
     const uint32_t *jstream;
@@ -587,12 +624,13 @@ typedef struct {
     int64_t *start, *finish, *step, *cost;
     uint64_t *digest;
     uint32_t *factor;
+    int32_t *refinements;
     int rc;
     char msg[256];
 } job_t;
 
 static int run_scenario(job_t *jb, int32_t si, work_t *w, int64_t *s, int64_t *f, int64_t *base,
-                        int64_t *cost, uint32_t *F) {
+                        int64_t *cost, uint32_t *F, int64_t *O, int64_t *lo_buf, int64_t *hi_buf) {
     const graph_t *g = jb->g;
     const derived_t *dv = jb->dv;
     scen_t sc = {jb->alpha[si], jb->bw_intra[si], jb->bw_inter[si], jb->reduce[si], jb->jseed[si],
@@ -615,14 +653,24 @@ static int run_scenario(job_t *jb, int32_t si, work_t *w, int64_t *s, int64_t *f
     }
     rc = compose(g, dv, w->dur, cost, s, f, w, jb->msg, sizeof jb->msg);
     if (rc) return rc;
-    /* validator: R refinements, each from the previous pass's timeline */
+    /* validator: R refinements, each from the previous pass's timeline; until_stable:
+       stop as soon as a refinement would leave every duration unchanged */
+    int32_t done = 0;
     for (int32_t p = 0; p < jb->n_refine; p++) {
-        overlap_factors(g, dv, &sc, s, f, F);
-        for (int64_t v = 0; v < g->n_ops; v++)
-            w->dur[v] = g->op_kind[v] == COMPUTE ? q16_scale(base[v], F[v]) : base[v];
+        overlap_factors(g, dv, &sc, s, f, F, O, lo_buf, hi_buf);
+        int changed = 0;
+        for (int64_t v = 0; v < g->n_ops; v++) {
+            if (g->op_kind[v] != COMPUTE) continue;
+            const int64_t d = inflated(base[v], F[v], O[v], jb->prorate);
+            changed |= d != w->dur[v];
+            w->dur[v] = d;
+        }
+        if (jb->until_stable && !changed) break;
         rc = compose(g, dv, w->dur, cost, s, f, w, jb->msg, sizeof jb->msg);
         if (rc) return rc;
+        done++;
     }
+    if (jb->refinements) jb->refinements[si] = done;
     /* step time and digest of the final timeline */
     int64_t step = 0;
     uint64_t dig = 0;
@@ -652,10 +700,13 @@ static void *worker(void *arg) {
     int64_t *f_tmp = jb->finish ? NULL : malloc(sizeof(int64_t) * (size_t)(n + 1));
     int64_t *c_tmp = jb->cost ? NULL : malloc(sizeof(int64_t) * (size_t)(nc + 1));
     uint32_t *F_tmp = jb->factor ? NULL : malloc(sizeof(uint32_t) * (size_t)(n + 1));
+    int64_t *O = malloc(sizeof(int64_t) * (size_t)(n + 1));
+    int64_t *lo_buf = malloc(sizeof(int64_t) * (size_t)(n + 1));
+    int64_t *hi_buf = malloc(sizeof(int64_t) * (size_t)(n + 1));
     jb->rc = OK;
     if (!w.pending || !w.ready || !w.dur || !w.arrived || !w.barrier || !w.heap.a || !base
         || (!jb->start && !s_tmp) || (!jb->finish && !f_tmp) || (!jb->cost && !c_tmp)
-        || (!jb->factor && !F_tmp)) {
+        || (!jb->factor && !F_tmp) || !O || !lo_buf || !hi_buf) {
         jb->rc = E_NOMEM;
         snprintf(jb->msg, sizeof jb->msg, "out of memory");
     }
@@ -664,10 +715,10 @@ static void *worker(void *arg) {
         int64_t *f = jb->finish ? jb->finish + (int64_t)si * n : f_tmp;
         int64_t *cost = jb->cost ? jb->cost + (int64_t)si * nc : c_tmp;
         uint32_t *F = jb->factor ? jb->factor + (int64_t)si * n : F_tmp;
-        jb->rc = run_scenario(jb, si, &w, s, f, base, cost, F);
+        jb->rc = run_scenario(jb, si, &w, s, f, base, cost, F, O, lo_buf, hi_buf);
     }
     free(w.pending); free(w.ready); free(w.dur); free(w.arrived); free(w.barrier); free(w.heap.a);
-    free(base); free(s_tmp); free(f_tmp); free(c_tmp); free(F_tmp);
+    free(base); free(s_tmp); free(f_tmp); free(c_tmp); free(F_tmp); free(O); free(lo_buf); free(hi_buf);
     return NULL;
 }
 
@@ -675,7 +726,11 @@ static void *worker(void *arg) {
  * Entry point.  Scenario fields are structure-of-arrays of length n_scen
  * (slowdown: n_scen x 8 x 4).  Outputs are scenario-major and any may be NULL:
  * start/finish/factor [n_scen][n_ops], cost [n_scen][n_colls], step/digest [n_scen].
- * factor receives the slowdown factor each op ran with in the final pass.
+ * factor receives the factor found on the timeline before the final pass.
+ * Validator options (Sec. 6): until_stable stops refining once a refinement
+ * would leave every duration unchanged (at most n_refine refinements;
+ * refinements[n_scen] receives how many ran); prorate inflates only the
+ * overlapped part of a compute op.
  * Returns 0 or a negative error code; err receives a message.
  */
 int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int32_t *op_rank,
@@ -686,9 +741,10 @@ int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int3
                const int32_t *coll_K, int32_t n_scen, const int64_t *alpha,
                const int64_t *bw_intra, const int64_t *bw_inter, const int64_t *reduce,
                const uint64_t *jseed, const uint32_t *jstream, const int32_t *jamp,
-               const uint8_t *algo, const uint32_t *slow, int32_t n_refine, int32_t n_threads,
-               int64_t *start, int64_t *finish, int64_t *step, uint64_t *digest, int64_t *cost,
-               uint32_t *factor, char *err, int64_t errlen) {
+               const uint8_t *algo, const uint32_t *slow, int32_t n_refine, int32_t until_stable,
+               int32_t prorate, int32_t n_threads, int64_t *start, int64_t *finish, int64_t *step,
+               uint64_t *digest, int64_t *cost, uint32_t *factor, int32_t *refinements, char *err,
+               int64_t errlen) {
     graph_t g = {n_ops, n_ranks, gpus_per_node, op_rank, op_stream, op_kind, op_class, op_dur,
                  op_coll, pred_off, pred_idx, n_colls, coll_type, coll_bytes, coll_N, coll_M, coll_K};
     if ((coll_N || coll_M || coll_K) && !(coll_N && coll_M && coll_K)) {
@@ -714,9 +770,9 @@ int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int3
         return E_NOMEM;
     }
     for (int32_t t = 0; t < n_threads; t++) {
-        jobs[t] = (job_t){&g, &dv, n_scen, n_refine, n_threads, t, alpha, bw_intra, bw_inter, reduce,
-                          jseed, jstream, jamp, algo, slow, start, finish, step, cost, digest, factor,
-                          OK, {0}};
+        jobs[t] = (job_t){&g, &dv, n_scen, n_refine, n_threads, t, until_stable != 0, prorate != 0, alpha,
+                          bw_intra, bw_inter, reduce, jseed, jstream, jamp, algo, slow, start, finish, step,
+                          cost, digest, factor, refinements, OK, {0}};
     }
     for (int32_t t = 1; t < n_threads; t++) pthread_create(&th[t], NULL, worker, &jobs[t]);
     worker(&jobs[0]);

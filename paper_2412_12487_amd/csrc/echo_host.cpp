@@ -97,7 +97,7 @@ struct echo_graph_s {
     int device = 0;
     int64_t n_ops = 0, n_colls = 0, n_levels = 0;
     int32_t n_ranks = 0, n_walkers = 0;
-    int64_t capacity[8] = {};          // co-resident walk workgroups per kernel variant
+    int64_t capacity[kWalkVariants] = {};   // co-resident walk workgroups per kernel variant
     bool need_coll_cost = false;       // some comm op reads its cost per collective
     int64_t spin_limit = kDefaultSpinNs / 10;   // 100 MHz ticks
     DeviceGraph dg;
@@ -113,6 +113,10 @@ struct echo_graph_s {
     size_t count_n = 0;
     uint8_t *tmask = nullptr;
     size_t tmask_n = 0;
+    uint32_t *ext = nullptr;           // prorated extra times
+    size_t ext_n = 0;
+    unsigned *chg = nullptr;           // per-scenario change flags + 1 stability word
+    size_t chg_n = 0;
     int64_t *tmp_start = nullptr, *tmp_finish = nullptr;
     size_t tmp_start_n = 0, tmp_finish_n = 0;
     int64_t *tmp_step = nullptr;
@@ -135,6 +139,8 @@ void free_graph(echo_graph g) {
     (void)hipFree(g->arrive);
     (void)hipFree(g->count);
     (void)hipFree(g->tmask);
+    (void)hipFree(g->ext);
+    (void)hipFree(g->chg);
     (void)hipFree(g->tmp_start);
     (void)hipFree(g->tmp_finish);
     (void)hipFree(g->tmp_step);
@@ -396,10 +402,10 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     // consecutive ranks per wavefront
     hipError_t e = hipSetDevice(device);
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
-    int64_t capacity[8];
+    int64_t capacity[kWalkVariants];
     e = walk_capacity(device, capacity);
     if (e != hipSuccess) return hip_fail(e, "occupancy query");
-    const int64_t least = *std::min_element(capacity, capacity + 8);
+    const int64_t least = *std::min_element(capacity, capacity + kWalkVariants);
     int64_t rpw = std::max<int64_t>(1, min_rpw);       // ranks per walker
     while (rpw <= kMaxRanksPerWalker &&
            ((R + rpw - 1) / rpw + kBlockWalkers - 1) / kBlockWalkers > least)
@@ -682,7 +688,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     g->n_levels = n_levels;
     g->n_ranks = (int32_t)R;
     g->n_walkers = (int32_t)W;
-    std::copy(capacity, capacity + 8, g->capacity);
+    std::copy(capacity, capacity + kWalkVariants, g->capacity);
     DeviceGraph &dg = g->dg;
     dg.n_ops = n;
     dg.n_colls = nc;
@@ -729,9 +735,12 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     return ECHO_OK;
 }
 
-int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n_refine, int64_t *d_start,
-            int64_t *d_finish, int64_t *d_step, uint64_t *d_digest, hipStream_t stream) {
+int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const echo_validator &val, int64_t *d_start,
+            int64_t *d_finish, int64_t *d_step, uint64_t *d_digest, int32_t *d_refinements, hipStream_t stream) {
     if (!g || !d_scen) return fail(ECHO_ERR_ARG, "null graph or scenario array");
+    const int32_t n_refine = val.max_refine;
+    const bool until_stable = val.until_stable != 0 && n_refine > 0;
+    const bool prorate = val.prorate != 0 && n_refine > 0;
     if (n_scen < 1 || n_refine < 0 || n_refine > 64)
         return fail(ECHO_ERR_ARG, "n_scen must be >= 1 and 0 <= n_refine <= 64 (got %d, %d)", n_scen, n_refine);
     hipError_t e = hipSetDevice(g->device);
@@ -743,7 +752,11 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
     if ((rc = ensure(&g->class_cost, &g->class_cost_n, (size_t)(g->dg.classes.n * ns), "class cost"))) return rc;
     if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->n_colls * ns), "arrivals"))) return rc;
     if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * n_tiles), "arrival counts"))) return rc;
-    if (n_refine > 0 && (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(g->n_ops * ns), "overlap masks"))) return rc;
+    if (n_refine > 0 && !prorate && (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(g->n_ops * ns), "overlap masks")))
+        return rc;
+    if (prorate && (rc = ensure(&g->ext, &g->ext_n, (size_t)(g->n_ops * ns), "prorated extra times"))) return rc;
+    if (until_stable && (rc = ensure(&g->chg, &g->chg_n, (size_t)(ns + 1), "change flags"))) return rc;
+    unsigned *stable = until_stable ? g->chg + ns : nullptr;
     if (!d_start && (rc = ensure(&g->tmp_start, &g->tmp_start_n, (size_t)(g->n_ops * ns), "start"))) return rc;
     if (!d_finish && (rc = ensure(&g->tmp_finish, &g->tmp_finish_n, (size_t)(g->n_ops * ns), "finish")))
         return rc;
@@ -768,15 +781,22 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
     if (g->need_coll_cost)
         TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.colls, d_scen, n_scen, g->cost, g->dg.status, stream),
               "cc_cost kernel");
+    if (until_stable && (e = launch_fill_i32(reinterpret_cast<int32_t *>(g->chg), ns + 1, 0, stream)))
+        return hip_fail(e, "fill kernel");
+    if (d_refinements && (e = launch_fill_i32(d_refinements, ns, until_stable ? 0 : n_refine, stream)))
+        return hip_fail(e, "fill kernel");
 
     for (int32_t p = 0; p <= n_refine; ++p) {
         // tiles per walk launch: every rank block of a tile must be co-resident
-        const int64_t cap = g->capacity[walk_variant(p > 0, p == n_refine, d_digest != nullptr)];
+        const int64_t cap = g->capacity[walk_variant(p > 0, p == n_refine, d_digest != nullptr, prorate)];
         const int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, cap / g->dg.n_blocks));
         if (p > 0) {
             OverlapArgs o{g->dg.cl_off, g->dg.cp_off, g->dg.cl, g->dg.cl_type, g->dg.cp,
-                          d_scen, start, finish, g->tmask, n_scen, n_tiles, p > 1};
+                          d_scen, start, finish, prorate ? nullptr : g->tmask, prorate ? g->ext : nullptr,
+                          until_stable ? g->chg : nullptr, stable, n_scen, n_tiles, p > 1, g->dg.status};
             TIMED(ECHO_K_OVERLAP, launch_overlap(o, g->n_ranks, stream), "overlap kernel");
+            if (until_stable && (e = launch_settle(g->chg, n_scen, d_refinements, stable, stream)))
+                return hip_fail(e, "settle kernel");
             TIMED(ECHO_K_CLEAR, launch_clear(g->arrive, n_arrive, g->count, n_count, stream), "clear kernel");
         }
         for (int64_t t0 = 0; t0 < n_tiles; t0 += per_launch) {
@@ -789,7 +809,9 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n
             a.scen = d_scen;
             a.cost = g->cost;
             a.class_cost = g->class_cost;
-            a.tmask = p > 0 ? g->tmask : nullptr;
+            a.tmask = p > 0 && !prorate ? g->tmask : nullptr;
+            a.ext = p > 0 && prorate ? g->ext : nullptr;
+            a.stable = p < n_refine ? stable : nullptr;     // the final pass always runs
             a.start = start;
             a.finish = finish;
             a.arrive = g->arrive;
@@ -860,7 +882,25 @@ int echo_compose_batch(echo_graph g, const echo_scenario *d_scen, int32_t n_scen
                        void *hip_stream) {
     g_last_error.clear();
     try {
-        return compose(g, d_scen, n_scen, n_refine, d_start, d_finish, d_step, d_digest,
+        if (n_refine < 0 || n_refine > 64)
+            return fail(ECHO_ERR_ARG, "n_refine must be in 0..64 (got %d)", n_refine);
+        const echo_validator val{n_refine, 0, 0};
+        return compose(g, d_scen, n_scen, val, d_start, d_finish, d_step, d_digest, nullptr,
+                       static_cast<hipStream_t>(hip_stream));
+    } catch (...) {
+        return fail(ECHO_ERR_NOMEM, "unexpected exception in compose");
+    }
+}
+
+int echo_compose_validated(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const echo_validator *opts,
+                           int64_t *d_start, int64_t *d_finish, int64_t *d_step, uint64_t *d_digest,
+                           int32_t *d_refinements, void *hip_stream) {
+    g_last_error.clear();
+    try {
+        if (!opts) return fail(ECHO_ERR_ARG, "null validator options");
+        if (opts->max_refine < 0 || opts->max_refine > 64)
+            return fail(ECHO_ERR_ARG, "max_refine must be in 0..64 (got %d)", opts->max_refine);
+        return compose(g, d_scen, n_scen, *opts, d_start, d_finish, d_step, d_digest, d_refinements,
                        static_cast<hipStream_t>(hip_stream));
     } catch (...) {
         return fail(ECHO_ERR_NOMEM, "unexpected exception in compose");

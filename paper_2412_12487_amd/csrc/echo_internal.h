@@ -147,6 +147,8 @@ struct WalkArgs {
     const int64_t *cost;             // [coll][scen]
     const int64_t *class_cost;       // [class][scen]
     const uint8_t *tmask;            // [op][scen] overlap type masks of compute ops, or null (pass 1)
+    const uint32_t *ext;             // [op][scen] prorated extra time of compute ops (prorating), or null
+    const unsigned *stable;          // non-null: skip the pass when *stable (every scenario at its fixed point)
     int64_t *start, *finish;         // [op][scen]
     unsigned long long *arrive;      // [coll][scen] latest member launch
     unsigned *count;                 // [coll][tile] members arrived
@@ -170,8 +172,12 @@ struct OverlapArgs {
     const echo_scenario *scen;
     const int64_t *start, *finish;
     uint8_t *tmask;                  // in: masks of the previous pass (if it was refined), out: new ones
+    uint32_t *ext;                   // prorating: in/out like tmask, the extra time q16(o, F) - o
+    unsigned *chg;                   // non-null: [scen] set when some duration changes
+    const unsigned *stable;          // non-null: skip when *stable
     int32_t n_scen, n_tiles;
-    int32_t prev_refined;            // the previous pass inflated its compute ops by `factor`
+    int32_t prev_refined;            // the previous pass inflated its compute ops
+    unsigned *status;
 };
 
 // Kernel launchers (echo_kernels.hip).  All enqueue on `stream`.
@@ -184,11 +190,20 @@ hipError_t launch_cc_cost(const CollTable &t, const echo_scenario *scen, int32_t
                           unsigned *status, hipStream_t stream);
 hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream);
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream);
+// After an overlap pass: count the refinement of every scenario whose durations changed,
+// clear the change flags, and set *stable when none changed.
+hipError_t launch_settle(unsigned *chg, int32_t n_scen, int32_t *refinements, unsigned *stable,
+                         hipStream_t stream);
+// Fill n int32 with v (a kernel, so the sequence stays capturable).
+hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream);
 // Co-resident walk workgroups (kBlockWalkers wavefronts each) the device can hold,
-// for each of the 8 kernel variants (bit 0 refined, bit 1 final, bit 2 digest).
-hipError_t walk_capacity(int device, int64_t workgroups[8]);
-inline int walk_variant(bool refined, bool final_pass, bool digest) {
-    return (refined ? 1 : 0) | (final_pass ? 2 : 0) | (digest ? 4 : 0);
+// for each kernel variant (bit 0 refined, bit 1 final, bit 2 digest, bit 3 prorated).
+constexpr int kWalkVariants = 16;
+hipError_t walk_capacity(int device, int64_t workgroups[kWalkVariants]);
+inline int walk_variant(bool refined, bool final_pass, bool digest, bool prorate) {
+    return (refined ? 1 : 0) | (final_pass ? 2 : 0) | (digest ? 4 : 0) | (refined && prorate ? 8 : 0);
 }
+// Largest prorated extra time an op may carry (its staging slot is 32 bits).
+constexpr uint32_t kExtLimit = 0xFFFFFFFFu;
 
 }  // namespace echo

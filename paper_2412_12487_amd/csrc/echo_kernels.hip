@@ -206,14 +206,16 @@ __device__ bool wait_local(const unsigned *cnt, unsigned need, unsigned *status,
 // one 64-scenario tile; wavefront w walks walker block * kBlockWalkers + w.  REFINED:
 // the pass inflates compute ops by the factors of the previous pass's
 // overlaps.  FINAL: the pass produces the step time (and DIGEST: the digest).
-template <bool REFINED, bool FINAL, bool DIGEST>
+// PRORATE (with REFINED): compute ops take their prorated extra time instead.
+template <bool REFINED, bool FINAL, bool DIGEST, bool PRORATE>
 __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
-    __shared__ uint8_t fstage[REFINED ? kBlockWalkers * kBlock * kLanes : 1];   // staged overlap masks
+    // staged per item and lane: overlap masks (one byte) or, prorating, extra times (32 bits)
+    __shared__ uint32_t fstage[REFINED ? kBlockWalkers * kBlock * kLanes / (PRORATE ? 1 : 4) : 1];
     __shared__ unsigned long long lbar[kChannels][2][kLanes];   // per channel and slot: latest launch per lane
     __shared__ unsigned lcnt[kChannels][2];                      // per channel and slot: members arrived
     __shared__ int64_t ccost[kClassSlots][kLanes];               // staged class costs of this tile
     __shared__ int32_t pinfo[kBlockWalkers][kStreams][3];          // per wave and slot: pending collective, op, aux
-    __shared__ uint32_t slow[REFINED ? kClasses * kTypes * kLanes : 1];   // slowdown table of each lane's scenario
+    __shared__ uint32_t slow[REFINED && !PRORATE ? kClasses * kTypes * kLanes : 1];   // lanes' slowdown tables
     static_assert(kBlockWalkers * 4 == kClasses * kTypes, "one 16-byte table slice per wavefront");
 
     const int lane = threadIdx.x & 63;
@@ -236,7 +238,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
         const int32_t cls = a.block_class[(int64_t)blk * kClassSlots + wave];
         ccost[wave][lane] = cls >= 0 ? a.class_cost[(int64_t)cls * ns + sigma] : 0;
     }
-    if (REFINED) {
+    if (REFINED && !PRORATE) {
         // entry e of the table for lane l at slow[e * 64 + l]: lanes hit distinct banks
         const uint4 t4 = reinterpret_cast<const uint4 *>(&a.scen[sigma].slowdown_q16[0][0])[wave];
         slow[(4 * wave + 0) * kLanes + lane] = t4.x;
@@ -246,6 +248,10 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     }
     __syncthreads();
     if (w >= a.n_walkers) return;
+    // every scenario reached its fixed point in an earlier pass: nothing left to refine
+    if (a.stable && __builtin_amdgcn_readfirstlane(__hip_atomic_load(a.stable, __ATOMIC_RELAXED,
+                                                                      __HIP_MEMORY_SCOPE_AGENT)))
+        return;
 
     const echo_scenario *sc = a.scen + sigma;
     const uint64_t jbase = jitter_base(sc->jitter_seed, sc->jitter_stream);
@@ -253,7 +259,8 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     int64_t *const sbase = a.start + (int64_t)tile * kLanes;    // row v of tile: sbase + v * ns
     int64_t *const fbase = a.finish + (int64_t)tile * kLanes;
     const unsigned *tile_count = a.count + tile;
-    uint8_t *const fst = fstage + (REFINED ? wave * kBlock * kLanes : 0);
+    uint8_t *const fst = reinterpret_cast<uint8_t *>(fstage) + (REFINED && !PRORATE ? wave * kBlock * kLanes : 0);
+    uint32_t *const fst32 = fstage + (REFINED && PRORATE ? wave * kBlock * kLanes : 0);
 
     // Per slot: finish of the latest op, or (bit j of `pending`) a comm op still
     // waiting for its barrier, described in this wave's row of pinfo.
@@ -328,17 +335,20 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
         const int nb = end - blk0 < kBlock ? int(end - blk0) : kBlock;
         nxt = blk0 + kBlock + slotl < end ? items4[2 * (blk0 + kBlock + slotl) + half] : make_int4(0, 0, 0, 0);
         if (REFINED) {
-            // stage this round's overlap masks, half a round per memory round trip
+            // stage this round's overlap masks (or extra times), half a round per memory round trip
 #pragma unroll
             for (int h = 0; h < kBlock; h += kBlock / 2) {
                 uint32_t mv[kBlock / 2];
 #pragma unroll
                 for (int j = 0; j < kBlock / 2; ++j) {
                     const int32_t opj = __builtin_amdgcn_readlane(cur.x, h + j);
-                    mv[j] = a.tmask[(int64_t)opj * ns + sigma];
+                    mv[j] = PRORATE ? a.ext[(int64_t)opj * ns + sigma] : a.tmask[(int64_t)opj * ns + sigma];
                 }
 #pragma unroll
-                for (int j = 0; j < kBlock / 2; ++j) fst[(h + j) * kLanes + lane] = (uint8_t)mv[j];
+                for (int j = 0; j < kBlock / 2; ++j) {
+                    if (PRORATE) fst32[(h + j) * kLanes + lane] = mv[j];
+                    else fst[(h + j) * kLanes + lane] = (uint8_t)mv[j];
+                }
             }
         }
         // fast flags of the round, one bit per item
@@ -354,7 +364,8 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) |
                                               (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32));
                 int64_t d = amp != 0 ? jittered(dur, op, jbase, amp) : dur;
-                if (REFINED && item_kind(meta) == ECHO_COMPUTE) d = inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane);
+                if (REFINED && item_kind(meta) == ECHO_COMPUTE)
+                    d = PRORATE ? d + fst32[j * kLanes + lane] : inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane);
                 const int64_t f = s0 + d;
                 if ((meta | keep) & kNeedS) (sbase + (int64_t)op * ns)[col] = s0;
                 if ((meta | keep) & kNeedF) (fbase + (int64_t)op * ns)[col] = f;
@@ -426,7 +437,8 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 }
             } else {
                 int64_t d = amp != 0 ? jittered(dur, op, jbase, amp) : dur;
-                if (REFINED && kind == ECHO_COMPUTE) d = inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane);
+                if (REFINED && kind == ECHO_COMPUTE)
+                    d = PRORATE ? d + fst32[j * kLanes + lane] : inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane);
                 const int64_t f = ready + d;
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 if ((meta | keep) & kNeedF) (fbase + (int64_t)op * ns)[col] = f;
@@ -463,10 +475,14 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
 }
 
 using WalkKernel = void (*)(WalkArgs);
-WalkKernel walk_kernel(bool refined, bool final_pass, bool digest) {
-    if (!final_pass) return refined ? k_walk<true, false, false> : k_walk<false, false, false>;
-    if (digest) return refined ? k_walk<true, true, true> : k_walk<false, true, true>;
-    return refined ? k_walk<true, true, false> : k_walk<false, true, false>;
+WalkKernel walk_kernel(bool refined, bool final_pass, bool digest, bool prorate) {
+    if (refined && prorate) {
+        if (!final_pass) return k_walk<true, false, false, true>;
+        return digest ? k_walk<true, true, true, true> : k_walk<true, true, false, true>;
+    }
+    if (!final_pass) return refined ? k_walk<true, false, false, false> : k_walk<false, false, false, false>;
+    if (digest) return refined ? k_walk<true, true, true, false> : k_walk<false, true, true, false>;
+    return refined ? k_walk<true, true, false, false> : k_walk<false, true, false, false>;
 }
 
 // ------------------------------------------------------------------ overlap detection
@@ -481,7 +497,26 @@ WalkKernel walk_kernel(bool refined, bool final_pass, bool digest) {
 // of its stream finished, and every finish is start + base duration (the same
 // jitter draw as the composer pass, inflated by the factor that pass used);
 // only unchained ops read their start.
+// Factor of a class-cls compute op overlapping the collective types in mask m:
+// the largest entry of the scenario's table row over them, 65536 for none.
+__device__ __forceinline__ uint32_t factor_of(uint32_t m, const uint32_t *slow, int cls) {
+    uint32_t F = 65536u;
+    for (int t = 0; t < kTypes; ++t)
+        if ((m >> t) & 1u) {
+            const uint32_t x = slow[cls * kTypes + t];
+            F = x > F ? x : F;
+        }
+    return F;
+}
+
+// PRORATE: also measure o, the part of [s_v, f_v) covered by the union of the
+// overlapping comm intervals (a merge of the per-stream interval lists in start
+// order), and record the extra time q16(min(o, D), F) - min(o, D) instead of a mask.
+template <bool PRORATE>
 __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
+    if (a.stable && __builtin_amdgcn_readfirstlane(__hip_atomic_load(a.stable, __ATOMIC_RELAXED,
+                                                                      __HIP_MEMORY_SCOPE_AGENT)))
+        return;                                  // every scenario is at its fixed point
     const int lane = threadIdx.x;
     const int32_t r = blockIdx.x / a.n_tiles;
     const int32_t tile = blockIdx.x % a.n_tiles;
@@ -492,12 +527,15 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     const int64_t *const sbase = a.start + (int64_t)tile * kLanes;
     const int64_t *const fbase = a.finish + (int64_t)tile * kLanes;
     uint8_t *const obase = a.tmask + (int64_t)tile * kLanes;
+    uint32_t *const ebase = a.ext + (int64_t)tile * kLanes;
     const echo_scenario *sc = a.scen + sigma;
     const uint32_t *slow = &sc->slowdown_q16[0][0];
     const uint64_t jbase = jitter_base(sc->jitter_seed, sc->jitter_stream);
     const int32_t amp = sc->jitter_amp_q16;
     const int64_t *cl_off = a.cl_off + (int64_t)r * kStreams;
     const int64_t *cp_off = a.cp_off + (int64_t)r * kStreams;
+    bool changed = false;                        // some duration differs from the previous pass's
+    bool ext_over = false;                       // a prorated extra time does not fit 32 bits
 
     // comm streams of this rank that carry comm ops, packed to the front
     int64_t kb[kStreams];
@@ -550,6 +588,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
             for (int j = 0; j < nr; ++j) {
                 const int64_t v = __builtin_amdgcn_readlane(cur.x, j);
                 const int meta = __builtin_amdgcn_readlane(cur.y, j);
+                const int cls = meta & 7;
                 const int64_t d0 = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.w, j) << 32) |
                                              (uint32_t)__builtin_amdgcn_readlane(cur.z, j));
                 // Loads in this loop are waited for on their own path (explicit vmcnt(0)):
@@ -560,18 +599,18 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                     sv = (sbase + v * ns)[col];
                     __builtin_amdgcn_s_waitcnt(kWaitVm0);
                 }
-                int64_t d = amp != 0 ? jittered(d0, (int32_t)v, jbase, amp) : d0;
-                if (a.prev_refined) {                                     // the previous pass's duration
-                    const uint32_t m_old = (obase + v * ns)[col];
-                    __builtin_amdgcn_s_waitcnt(kWaitVm0);
-                    if (m_old != 0) {
-                        uint32_t F = 65536u;
-                        for (int t = 0; t < kTypes; ++t)
-                            if ((m_old >> t) & 1u) {
-                                const uint32_t x = slow[(meta & 7) * kTypes + t];
-                                F = x > F ? x : F;
-                            }
-                        d = q16(d, F);
+                const int64_t D = amp != 0 ? jittered(d0, (int32_t)v, jbase, amp) : d0;
+                int64_t d = D;                   // the duration v ran with in the previous pass
+                uint32_t m_old = 0, e_old = 0;
+                if (a.prev_refined) {
+                    if (PRORATE) {
+                        e_old = (ebase + v * ns)[col];
+                        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                        d = D + e_old;
+                    } else {
+                        m_old = (obase + v * ns)[col];
+                        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                        if (m_old != 0) d = q16(D, factor_of(m_old, slow, cls));
                     }
                 }
                 const int64_t fv = sv + d;
@@ -581,6 +620,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 for (int k = 0; k < kStreams; ++k)
                     if (k < ncs) busy |= cs[k] < fv;
                 uint32_t m = 0;                            // types of the comm ops overlapping v
+                int64_t o = 0;                             // covered length (PRORATE)
                 if (busy) {
     #pragma unroll
                     for (int k = 0; k < kStreams; ++k) {
@@ -597,6 +637,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                                 cf[k] = kInf;
                             }
                         }
+                        if (PRORATE) continue;
                         int32_t q = p[k];
                         int64_t qs = cs[k], qf = cf[k];
                         while (qs < fv) {
@@ -609,12 +650,93 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                             qf = (fbase + c * ns)[col];
                         }
                     }
+                    if (PRORATE) {
+                        // merge the streams' overlapping intervals in start order; every one of
+                        // them ends after sv (each stream's intervals are disjoint and sorted)
+                        int32_t q[kStreams];
+                        int64_t qs[kStreams], qf[kStreams];
+    #pragma unroll
+                        for (int k = 0; k < kStreams; ++k) {
+                            q[k] = p[k];
+                            qs[k] = k < ncs ? cs[k] : kInf;
+                            qf[k] = k < ncs ? cf[k] : kInf;
+                        }
+                        int64_t t = sv;                    // covered up to here
+                        for (;;) {
+                            int bk = -1;
+                            int64_t bs = fv;
+    #pragma unroll
+                            for (int k = 0; k < kStreams; ++k)
+                                if (qs[k] < bs) {
+                                    bs = qs[k];
+                                    bk = k;
+                                }
+                            if (bk < 0) break;
+    #pragma unroll
+                            for (int k = 0; k < kStreams; ++k) {
+                                if (k != bk) continue;
+                                const int64_t lo = sv > qs[k] ? sv : qs[k], hi = fv < qf[k] ? fv : qf[k];
+                                if (lo < hi) {
+                                    m |= 1u << a.cl_type[kb[k] + q[k]];
+                                    const int64_t from = lo > t ? lo : t;
+                                    if (hi > from) {
+                                        o += hi - from;
+                                        t = hi;
+                                    }
+                                }
+                                if (++q[k] < nk[k]) {
+                                    const int64_t c = a.cl[kb[k] + q[k]];
+                                    qs[k] = (sbase + c * ns)[col];
+                                    qf[k] = (fbase + c * ns)[col];
+                                    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                                } else {
+                                    qs[k] = kInf;
+                                }
+                            }
+                        }
+                    }
                     __builtin_amdgcn_s_waitcnt(kWaitVm0);
                 }
-                (obase + v * ns)[col] = (uint8_t)m;
+                if (PRORATE) {
+                    uint32_t e = 0;
+                    if (m != 0) {
+                        const int64_t oc = o < D ? o : D;
+                        const int64_t x = q16(oc, factor_of(m, slow, cls)) - oc;
+                        ext_over |= x >= (int64_t)kExtLimit;
+                        e = x >= (int64_t)kExtLimit ? kExtLimit : (uint32_t)x;
+                    }
+                    changed |= e != e_old;
+                    (ebase + v * ns)[col] = e;
+                } else {
+                    if (a.chg && m != m_old)
+                        changed |= (m == 0 ? D : q16(D, factor_of(m, slow, cls))) != d;
+                    (obase + v * ns)[col] = (uint8_t)m;
+                }
             }
         }
     }
+    if (a.chg && active && changed) __hip_atomic_fetch_or(a.chg + sigma, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (active && ext_over) __hip_atomic_fetch_or(a.status, kStatusRange, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Count the refinement of each scenario whose durations changed; flag stability.
+__global__ __launch_bounds__(256) void k_settle(unsigned *chg, int32_t n_scen, int32_t *refinements,
+                                                 unsigned *stable) {
+    int any = 0;
+    for (int32_t i = threadIdx.x; i < n_scen; i += blockDim.x) {
+        if (chg[i]) {
+            any = 1;
+            if (refinements) refinements[i] += 1;
+            chg[i] = 0;
+        }
+    }
+    any = __syncthreads_or(any);
+    if (threadIdx.x == 0 && !any) *stable = 1u;
+}
+
+__global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
 }
 
 int grid_for(int64_t n, int block) {
@@ -655,23 +777,39 @@ hipError_t launch_cc_cost(const CollTable &t, const echo_scenario *scen, int32_t
 hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream) {
     WalkArgs args = a;
     void *params[] = {&args};
-    const WalkKernel k = walk_kernel(a.tmask != nullptr, a.final_pass != 0, a.digest != nullptr);
+    const WalkKernel k = walk_kernel(a.tmask != nullptr || a.ext != nullptr, a.final_pass != 0,
+                                     a.digest != nullptr, a.ext != nullptr);
     return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k), dim3((unsigned)(n_blocks * a.tiles)),
                                       dim3(kBlockWalkers * kLanes), params, 0, stream);
 }
 
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
-    hipLaunchKernelGGL(k_overlap, dim3((unsigned)(n_ranks * a.n_tiles)), dim3(kLanes), 0, stream, a);
+    if (a.ext)
+        hipLaunchKernelGGL(k_overlap<true>, dim3((unsigned)(n_ranks * a.n_tiles)), dim3(kLanes), 0, stream, a);
+    else
+        hipLaunchKernelGGL(k_overlap<false>, dim3((unsigned)(n_ranks * a.n_tiles)), dim3(kLanes), 0, stream, a);
     return hipGetLastError();
 }
 
-hipError_t walk_capacity(int device, int64_t workgroups[8]) {
+hipError_t launch_settle(unsigned *chg, int32_t n_scen, int32_t *refinements, unsigned *stable,
+                         hipStream_t stream) {
+    hipLaunchKernelGGL(k_settle, dim3(1), dim3(256), 0, stream, chg, n_scen, refinements, stable);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_fill_i32, dim3(grid_for(n, 256)), dim3(256), 0, stream, p, n, v);
+    return hipGetLastError();
+}
+
+hipError_t walk_capacity(int device, int64_t workgroups[kWalkVariants]) {
     int cus = 0;
     hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
     if (e != hipSuccess) return e;
-    for (int v = 0; v < 8; ++v) {
+    for (int v = 0; v < kWalkVariants; ++v) {
         int per_cu = 0;
-        const WalkKernel k = walk_kernel(v & 1, v & 2, v & 4);
+        const WalkKernel k = walk_kernel(v & 1, v & 2, v & 4, v & 8);
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(k),
                                                          kBlockWalkers * kLanes, 0);
         if (e != hipSuccess) return e;

@@ -21,7 +21,7 @@ ECHO_ERR_CYCLE, ECHO_ERR_NOMEM, ECHO_ERR_HIP, ECHO_ERR_DEVICE = -4, -5, -6, -7
 ERROR_NAMES = {0: "OK", -1: "ARG", -2: "RANGE", -3: "MATCH", -4: "CYCLE", -5: "NOMEM", -6: "HIP",
                -7: "DEVICE"}
 EXPORTS = ("echo_load_graph", "echo_load_graph_ex", "echo_graph_info", "echo_free_graph", "echo_cc_cost",
-           "echo_compose_batch", "echo_sync_status", "echo_set_timing", "echo_kernel_times",
+           "echo_compose_batch", "echo_compose_validated", "echo_sync_status", "echo_set_timing", "echo_kernel_times",
            "echo_last_error")
 KERNEL_KINDS = {0: "init", 1: "cc_cost", 2: "walk", 3: "overlap", 4: "clear"}
 
@@ -52,6 +52,10 @@ class _Desc(ctypes.Structure):
     ]
 
 
+class _Validator(ctypes.Structure):
+    _fields_ = [("max_refine", ctypes.c_int32), ("until_stable", ctypes.c_int32), ("prorate", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -76,6 +80,8 @@ def lib():
     L.echo_cc_cost.restype = ctypes.c_int
     L.echo_compose_batch.argtypes = [P, P, i32, i32, P, P, P, P, P]
     L.echo_compose_batch.restype = ctypes.c_int
+    L.echo_compose_validated.argtypes = [P, P, i32, ctypes.POINTER(_Validator), P, P, P, P, P, P]
+    L.echo_compose_validated.restype = ctypes.c_int
     L.echo_sync_status.argtypes = [P, P]
     L.echo_sync_status.restype = ctypes.c_int
     L.echo_set_timing.argtypes = [P, ctypes.c_int]
@@ -191,10 +197,14 @@ class Graph:
             self.sync_status()
         return out
 
-    def compose(self, d_scen, n_scen, n_refine=1, *, timelines=True, digest=False, out=None, check=True):
+    def compose(self, d_scen, n_scen, n_refine=1, *, timelines=True, digest=False, out=None, check=True,
+                until_stable=False, prorate=False, refinements=False):
         """Compose all scenarios.  Returns dict of torch tensors: 'step' [n_scen],
-        optional 'start'/'finish' [n_ops, n_scen] and 'digest' [n_scen] (uint64 bits
-        in an int64 tensor).  `out` may supply preallocated tensors of those names."""
+        optional 'start'/'finish' [n_ops, n_scen], 'digest' [n_scen] (uint64 bits
+        in an int64 tensor) and 'refinements' [n_scen] int32.  `out` may supply
+        preallocated tensors of those names.  until_stable / prorate select the
+        validator variants of echo_compose_validated (n_refine is then the most
+        refinements)."""
         import torch
         dev = torch.device("cuda", self.device)
         res = dict(out or {})
@@ -206,11 +216,20 @@ class Graph:
                     res[k] = torch.empty((self.n_ops, n_scen), dtype=torch.int64, device=dev)
         if digest and "digest" not in res:
             res["digest"] = torch.empty(n_scen, dtype=torch.int64, device=dev)
+        if refinements and "refinements" not in res:
+            res["refinements"] = torch.empty(n_scen, dtype=torch.int32, device=dev)
         p = lambda k: ctypes.c_void_p(res[k].data_ptr()) if k in res else ctypes.c_void_p(None)
-        _check(lib().echo_compose_batch(self.handle, ctypes.c_void_p(d_scen.data_ptr()), int(n_scen),
-                                        int(n_refine), p("start") if timelines else ctypes.c_void_p(None),
-                                        p("finish") if timelines else ctypes.c_void_p(None), p("step"),
-                                        p("digest") if digest else ctypes.c_void_p(None), _stream_ptr(dev)))
+        none = ctypes.c_void_p(None)
+        start, finish = (p("start"), p("finish")) if timelines else (none, none)
+        dig = p("digest") if digest else none
+        if until_stable or prorate or refinements:
+            opts = _Validator(int(n_refine), int(bool(until_stable)), int(bool(prorate)))
+            _check(lib().echo_compose_validated(self.handle, ctypes.c_void_p(d_scen.data_ptr()), int(n_scen),
+                                                ctypes.byref(opts), start, finish, p("step"), dig,
+                                                p("refinements") if refinements else none, _stream_ptr(dev)))
+        else:
+            _check(lib().echo_compose_batch(self.handle, ctypes.c_void_p(d_scen.data_ptr()), int(n_scen),
+                                            int(n_refine), start, finish, p("step"), dig, _stream_ptr(dev)))
         if check:
             self.sync_status()
         return res

@@ -88,3 +88,40 @@ def compose_validated(g, base, cost, slowdown, n_refine):
                       else int(base[v]) for v in range(len(base))], np.int64)
         s, f = compose(g, d, cost)
     return s, f
+
+
+def covered(g, s, f, v):
+    """Nanoseconds of [s_v, f_v) during which some comm op of v's rank runs, counted
+    one nanosecond at a time (tiny timelines only)."""
+    comm = [c for c in range(len(g["op_rank"]))
+            if g["op_kind"][c] == COMM and g["op_rank"][c] == g["op_rank"][v]]
+    return sum(1 for t in range(int(s[v]), int(f[v])) if any(s[c] <= t < f[c] for c in comm))
+
+
+def compose_variants(g, base, cost, slowdown, n_refine, *, until_stable=False, prorate=False):
+    """Validator variants: refine at most n_refine times, stopping early (until_stable) when
+    a refinement would change no duration; prorate inflates only the covered part of a
+    compute op (the covered time of the previous timeline, capped at the base duration).
+    Returns (s, f, refinements composed)."""
+    q16 = lambda d, F: (int(d) * int(F) + 32768) >> 16
+    n = len(base)
+    d = np.array(base, np.int64)
+    s, f = compose(g, d, cost)
+    done = 0
+    for _ in range(n_refine):
+        F = factors(g, s, f, slowdown)
+        new = d.copy()
+        for v in range(n):
+            if g["op_kind"][v] != COMPUTE:
+                continue
+            if prorate:
+                o = min(covered(g, s, f, v), int(base[v]))
+                new[v] = int(base[v]) - o + q16(o, F[v])
+            else:
+                new[v] = q16(base[v], F[v])
+        if until_stable and (new == d).all():
+            break
+        d = new
+        s, f = compose(g, d, cost)
+        done += 1
+    return s, f, done

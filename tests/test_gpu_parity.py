@@ -381,3 +381,95 @@ def test_dp_replica_gpt175b_8192_ranks(E):
     for j, c in enumerate(cols):
         np.testing.assert_array_equal(red["finish"][:, c], ref["finish"][j])
         np.testing.assert_array_equal(red["start"][:, c], ref["start"][j])
+
+
+# ---------------------------------------------------------------- validator variants
+def _variant_run(E, g, sc, R, until_stable, prorate, graph=None):
+    G = graph or E.Graph(g, 0)
+    d, n = E.scenarios_to_device(sc)
+    out = G.compose(d, n, R, timelines=True, digest=True, until_stable=until_stable, prorate=prorate,
+                    refinements=True)
+    res = {"step": out["step"].cpu().numpy(), "digest": out["digest"].cpu().numpy().view(np.uint64),
+           "start": out["start"].cpu().numpy(), "finish": out["finish"].cpu().numpy(),
+           "refinements": out["refinements"].cpu().numpy()}
+    if graph is None:
+        G.close()
+    return res
+
+
+VARIANTS = [(True, False), (False, True), (True, True)]
+
+
+@pytest.mark.parametrize("until_stable,prorate", VARIANTS)
+@pytest.mark.parametrize("seed", range(8))
+def test_validator_variants_random_graphs(E, seed, until_stable, prorate):
+    rng = np.random.default_rng(3000 + seed)
+    g = _random_graph(rng, int(rng.integers(2, 14)), int(rng.integers(10, 60)), int(rng.integers(3, 30)))
+    sc = scenarios.draw([1, 64, 70, 130][seed % 4], rng, bw_inter=(20000, 400000), alpha=(0, 20000),
+                        slowdown=(65536, 300000), jitter=(4000, seed) if seed % 2 else None)
+    try:
+        ref = oracle.run(g, sc, 8, threads=THREADS, until_stable=until_stable, prorate=prorate)
+    except oracle.OracleError as e:
+        assert e.code == -4
+        return
+    gpu = _variant_run(E, g, sc, 8, until_stable, prorate)
+    assert_same(gpu, ref)
+    np.testing.assert_array_equal(gpu["refinements"], ref["refinements"])
+
+
+@pytest.mark.parametrize("until_stable,prorate", VARIANTS)
+def test_validator_variants_tiny(E, until_stable, prorate):
+    sc = scenarios.draw(5, np.random.default_rng(21), bw_inter=(20000, 90000), alpha=(0, 5000),
+                        slowdown=(65536, 200000))
+    for name in sorted(TINY):
+        g = TINY[name]
+        ref = oracle.run(g, sc, 4, until_stable=until_stable, prorate=prorate)
+        gpu = _variant_run(E, g, sc, 4, until_stable, prorate)
+        assert_same(gpu, ref)
+        np.testing.assert_array_equal(gpu["refinements"], ref["refinements"])
+
+
+@pytest.mark.parametrize("until_stable,prorate", VARIANTS)
+def test_validator_variants_config1_and_2(E, until_stable, prorate):
+    g, sc = configs.graph(1), scenarios.take(configs.scenario_batch(4), slice(0, 130))
+    ref = oracle.run(g, sc, 10, threads=THREADS, until_stable=until_stable, prorate=prorate)
+    gpu = _variant_run(E, g, sc, 10, until_stable, prorate)
+    assert_same(gpu, ref)
+    np.testing.assert_array_equal(gpu["refinements"], ref["refinements"])
+    g, sc = configs.graph(2), configs.scenario_batch(2)
+    cols = [0, 1, 2, 63]
+    G = E.Graph(g, 0)
+    gpu = _variant_run(E, g, sc, 10, until_stable, prorate, graph=G)
+    G.close()
+    ref = oracle.run(g, scenarios.take(sc, cols), 10, threads=4, until_stable=until_stable, prorate=prorate,
+                     jitter_stream=cols)
+    np.testing.assert_array_equal(gpu["refinements"][cols], ref["refinements"])
+    np.testing.assert_array_equal(gpu["step"][cols], ref["step"])
+    np.testing.assert_array_equal(gpu["digest"][cols], ref["digest"])
+    for j, c in enumerate(cols):
+        np.testing.assert_array_equal(gpu["finish"][:, c], ref["finish"][j])
+
+
+def test_plain_refinement_reports_its_count(E):
+    g, sc = configs.graph(1), scenarios.default_scenarios(3)
+    res = _variant_run(E, g, sc, 3, False, False)
+    assert (res["refinements"] == 3).all()
+    assert_same(res, oracle.run(g, sc, 3))
+
+
+def test_prorated_extra_time_limit_reported(E):
+    """A prorated extra time of 2^32 ns or more does not fit its staging slot."""
+    b = Builder(2)
+    c = b.collective(AR, (1 << 50) - 1)
+    lead = b.compute(0, 10, stream=2)
+    b.comm(0, c, preds=[lead])
+    b.compute(0, (1 << 40), cls=0)
+    b.comm(1, c)
+    sc = scenarios.default_scenarios(1)
+    sc["slowdown_q16"][:] = 131072
+    G = E.Graph(b.graph(), 0)
+    d, n = E.scenarios_to_device(sc)
+    with pytest.raises(E.EchoError) as x:
+        G.compose(d, n, 1, prorate=True)
+    assert x.value.code == E.ECHO_ERR_RANGE
+    G.close()

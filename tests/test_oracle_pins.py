@@ -564,3 +564,116 @@ def test_inconsistent_group_membership_rejected(bad):
     with pytest.raises(oracle.OracleError) as e:
         oracle.run(rg, scenarios.default_scenarios(1), 1)
     assert e.value.code == -1
+
+
+# ---------------------------------------------------------------- validator variants
+# Sec. 3 / Sec. 6 give no iteration rule: besides R fixed refinements, refine until
+# the durations stop changing, and/or inflate only the overlapped part of an op.
+@pytest.mark.parametrize("name", sorted(TINY))
+@pytest.mark.parametrize("until_stable,prorate", [(True, False), (False, True), (True, True)])
+def test_validator_variants_match_brute_force(name, until_stable, prorate):
+    g = TINY[name]
+    rng = np.random.default_rng(13)
+    table = rng.integers(65536, 200000, (8, 4)).astype(np.uint32)
+    sc = _scen(1, alpha=2500)
+    sc["slowdown_q16"] = table[None].copy()
+    base, cost = _dur_cost(g, sc)
+    if int(max(cost.max(initial=0), base.max(initial=0))) * len(base) > 400_000:
+        pytest.skip("timeline too long for the per-nanosecond count")
+    s, f, done = bruteforce.compose_variants(g, base, cost, table, 4, until_stable=until_stable, prorate=prorate)
+    r = oracle.run(g, sc, 4, until_stable=until_stable, prorate=prorate)
+    np.testing.assert_array_equal(r["start"][0], s)
+    np.testing.assert_array_equal(r["finish"][0], f)
+    assert r["refinements"][0] == done
+
+
+def _overlap_pair(comm_start, comp_dur, coll_bytes):
+    """Rank 0: a compute op (stream 0) and an all-reduce (stream 1) launched after a
+    lead-in op of comm_start ns; rank 1 joins the all-reduce at once."""
+    b = Builder(2)
+    c = b.collective(AR, coll_bytes)
+    lead = b.compute(0, comm_start, stream=2)
+    b.comm(0, c, preds=[lead])
+    v = b.compute(0, comp_dur, cls=3)
+    b.comm(1, c)
+    return b.graph(), v
+
+
+def test_prorated_inflation_hand_value():
+    """A 1000 ns compute op starting at 0, with an all-reduce running from 700 ns on:
+    300 ns overlap; prorated d' = 700 + q16(300, F), whole-op d' = q16(1000, F)."""
+    g, v = _overlap_pair(700, 1000, 1 << 20)
+    sc = _scen(1)
+    F = 98304                                   # 1.5
+    sc["slowdown_q16"][:] = F
+    whole = oracle.run(g, sc, 1)
+    part = oracle.run(g, sc, 1, prorate=True)
+    assert whole["finish"][0][v] == (1000 * F + 32768) >> 16 == 1500
+    assert part["finish"][0][v] == 700 + ((300 * F + 32768) >> 16) == 1150
+
+
+def test_prorating_a_fully_overlapped_op_equals_whole_inflation():
+    g, v = _overlap_pair(0, 1000, 1 << 30)      # the all-reduce outlasts the compute op
+    sc = _scen(1)
+    sc["slowdown_q16"][:] = 80000
+    assert oracle.run(g, sc, 1, prorate=True)["finish"][0][v] == oracle.run(g, sc, 1)["finish"][0][v]
+
+
+def test_until_stable_equals_fixed_refinements_it_reports():
+    """The result after `refinements` rounds is the fixed point: plain refinement with that
+    many rounds, or one more, gives the same timeline."""
+    g = configs.graph(1)
+    sc = scenarios.draw(6, np.random.default_rng(17), bw_inter=(20000, 90000), slowdown=(65536, 200000),
+                        jitter=(6554, 1))
+    for prorate in (False, True):
+        r = oracle.run(g, sc, 8, until_stable=True, prorate=prorate)
+        assert (r["refinements"] >= 1).all()
+        for j in range(6):
+            k = int(r["refinements"][j])
+            one = scenarios.take(sc, [j])
+            for R in ({k, k + 1} if k < 8 else {k}):
+                fixed = oracle.run(g, one, R, prorate=prorate, jitter_stream=[j])
+                np.testing.assert_array_equal(fixed["finish"][0], r["finish"][j])
+
+
+def test_random_small_dags_validator_variants():
+    """Random tiny graphs with overlapping comm ops: the fixed-point and prorated validators
+    against brute force (per-nanosecond coverage, repeated full path enumeration)."""
+    rng = np.random.default_rng(321)
+    deep = 0
+    for trial in range(60):
+        n_ranks = int(rng.integers(1, 4))
+        b = Builder(n_ranks, gpus_per_node=int(rng.integers(1, 3)))
+        n_coll = int(rng.integers(1, 4))
+        colls = [b.collective(int(rng.integers(0, 3)), int(rng.integers(0, 256 << 10))) for _ in range(n_coll)]
+        for r in range(n_ranks):
+            ids = []
+            order = list(rng.permutation(n_coll))
+            for k in range(int(rng.integers(3, 7))):
+                preds = [int(u) for u in ids if rng.random() < 0.25]
+                if order and rng.random() < 0.4:
+                    ids.append(b.comm(r, colls[order.pop()], stream=int(rng.integers(1, 4)), preds=preds))
+                else:
+                    ids.append(b.compute(r, int(rng.integers(1, 600)), stream=int(rng.integers(0, 2)),
+                                         cls=int(rng.integers(0, 8)), preds=preds))
+            for c in order:
+                b.comm(r, colls[c], stream=int(rng.integers(1, 4)), preds=ids[-1:])
+        g = b.graph()
+        if len(g["op_rank"]) > 24:
+            continue
+        sc = _scen(1, alpha=int(rng.integers(0, 300)), bw_intra=400000, bw_inter=200000)
+        sc["slowdown_q16"] = rng.integers(65536, 260000, (1, 8, 4)).astype(np.uint32)
+        try:
+            base, cost = _dur_cost(g, sc)
+        except oracle.OracleError as e:
+            assert e.code == -4
+            continue
+        for until_stable, prorate in ((True, False), (False, True), (True, True)):
+            s, f, done = bruteforce.compose_variants(g, base, cost, sc["slowdown_q16"][0], 6,
+                                                     until_stable=until_stable, prorate=prorate)
+            r = oracle.run(g, sc, 6, until_stable=until_stable, prorate=prorate)
+            np.testing.assert_array_equal(r["start"][0], s)
+            np.testing.assert_array_equal(r["finish"][0], f)
+            assert r["refinements"][0] == done
+            deep += until_stable and done >= 2
+    assert deep >= 5          # the fixed point is often reached only after several rounds
