@@ -512,7 +512,8 @@ __device__ __forceinline__ uint32_t factor_of(uint32_t m, const uint32_t *slow, 
 // PRORATE: also measure o, the part of [s_v, f_v) covered by the union of the
 // overlapping comm intervals (a merge of the per-stream interval lists in start
 // order), and record the extra time q16(min(o, D), F) - min(o, D) instead of a mask.
-template <bool PRORATE>
+// DETECT: flag the scenarios whose durations change (fixed-point iteration).
+template <bool PRORATE, bool DETECT>
 __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     if (a.stable && __builtin_amdgcn_readfirstlane(__hip_atomic_load(a.stable, __ATOMIC_RELAXED,
                                                                       __HIP_MEMORY_SCOPE_AGENT)))
@@ -705,17 +706,18 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                         ext_over |= x >= (int64_t)kExtLimit;
                         e = x >= (int64_t)kExtLimit ? kExtLimit : (uint32_t)x;
                     }
-                    changed |= e != e_old;
+                    if (DETECT) changed |= e != e_old;
                     (ebase + v * ns)[col] = e;
                 } else {
-                    if (a.chg && m != m_old)
+                    if (DETECT && m != m_old)
                         changed |= (m == 0 ? D : q16(D, factor_of(m, slow, cls))) != d;
                     (obase + v * ns)[col] = (uint8_t)m;
                 }
             }
         }
     }
-    if (a.chg && active && changed) __hip_atomic_fetch_or(a.chg + sigma, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (DETECT && active && changed)
+        __hip_atomic_fetch_or(a.chg + sigma, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (active && ext_over) __hip_atomic_fetch_or(a.status, kStatusRange, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -784,10 +786,11 @@ hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream) 
 }
 
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
-    if (a.ext)
-        hipLaunchKernelGGL(k_overlap<true>, dim3((unsigned)(n_ranks * a.n_tiles)), dim3(kLanes), 0, stream, a);
-    else
-        hipLaunchKernelGGL(k_overlap<false>, dim3((unsigned)(n_ranks * a.n_tiles)), dim3(kLanes), 0, stream, a);
+    const dim3 grid((unsigned)(n_ranks * a.n_tiles)), block(kLanes);
+    if (a.ext && a.chg) hipLaunchKernelGGL((k_overlap<true, true>), grid, block, 0, stream, a);
+    else if (a.ext) hipLaunchKernelGGL((k_overlap<true, false>), grid, block, 0, stream, a);
+    else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((k_overlap<false, false>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 
