@@ -92,6 +92,9 @@ def main():
     ap.add_argument("--index", type=int, default=0, help="graph of config 5 (0-15)")
     ap.add_argument("--scenarios", type=int, default=0,
                     help="batch size drawn with the config's recipe (0 = the config's own)")
+    ap.add_argument("--cc", choices=["echo", "tables", "alpha-beta"], default="echo",
+                    help="collective cost model of every scenario: Eq. 2-5 from bandwidths, Eq. 2-5 from "
+                         "seeded CC parameter tables, or the alpha-beta baseline")
     ap.add_argument("--replica", action="store_true",
                     help="time one DP replica composed alone against the sweep over every replica")
     ap.add_argument("--refine", type=int, default=1, help="refinements (the most, with --until-stable)")
@@ -130,7 +133,7 @@ def main():
         return replica_mode(args, E, configs, gpt1f1b)
     t = time.perf_counter()
     g = configs.graph(args.config, args.index)
-    sc = configs.scenario_batch(args.config, args.index, args.scenarios or None)
+    sc = cc_variant(configs.scenario_batch(args.config, args.index, args.scenarios or None), args)
     log(f"graph: config {args.config} {configs.NAMES[args.config]}: {len(g['op_rank'])} ops, "
         f"{len(g['coll_type'])} collectives, {g['n_ranks']} ranks ({time.perf_counter() - t:.1f} s)")
     r = time_compose(E, g, sc, args)
@@ -151,9 +154,11 @@ def main():
         "config": {"workload": f"config {args.config}: {configs.NAMES[args.config]}, "
                                f"{r['n_ops']} ops x {r['n_scen']} scenarios, " + validator_name(args),
                    "n_ops": r["n_ops"], "n_scenarios": r["n_scen"], "n_refine": args.refine,
-                   "ranks": int(g["n_ranks"]), "levels": r["levels"], "load_s": round(r["load_s"], 2)},
+                   "ranks": int(g["n_ranks"]), "levels": r["levels"], "load_s": round(r["load_s"], 2),
+                   "cc_model": args.cc, "cc_cost_all_collectives_ms": r["cc_cost_all_ms"]},
         "kernels_ms": r["kernels_ms"],
-        "roofline": roofline(g, r, args, args.config if not (args.until_stable or args.prorate) else None),
+        "roofline": roofline(g, r, args, args.config if not (args.until_stable or args.prorate or args.cc != "echo")
+                             else None),
     }
     if "refinements" in r:
         line["config"]["refinements"] = r["refinements"]
@@ -170,11 +175,29 @@ def validator_name(args):
     return f"validator {kind}, at most {args.refine} refinement(s)"
 
 
+CC_TABLES = 8       # seeded tables for --cc tables
+
+
+def cc_variant(sc, args):
+    """Scenarios with the cost model --cc asks for."""
+    from workloads import scenarios
+    n = scenarios.count(sc)
+    sc = dict(sc)
+    if args.cc == "alpha-beta":
+        sc["cc_model"] = np.ones(n, np.uint8)
+    elif args.cc == "tables":
+        sc["cc_table"] = (np.arange(n) % CC_TABLES + 1).astype(np.int32)
+    return sc
+
+
 def time_compose(E, g, sc, args):
     """Load g, compose the batch warmup + steps times; wall and per-kernel timings."""
     import torch
+    from workloads import scenarios
     t = time.perf_counter()
     G = E.Graph(g, 0)
+    if args.cc == "tables":
+        G.set_cc_tables(scenarios.draw_cc_tables(CC_TABLES, np.random.default_rng(99)))
     load_s = time.perf_counter() - t
     log(f"loaded: {G.n_levels} levels in {load_s:.1f} s")
     d_scen, n_scen = E.scenarios_to_device(sc, "cuda:0")
@@ -220,6 +243,16 @@ def time_compose(E, g, sc, args):
     if args.steps and "refinements" in last:
         rf = last["refinements"].cpu().numpy()
         res["refinements"] = {"min": int(rf.min()), "mean": round(float(rf.mean()), 3), "max": int(rf.max())}
+    # the CC estimator alone over every collective (echo_cc_cost), per call
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    G.cc_cost(d_scen, n_scen)
+    e0.record(stream)
+    for _ in range(3):
+        costs = G.cc_cost(d_scen, n_scen, check=False)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    res["cc_cost_all_ms"] = round(e0.elapsed_time(e1) / 3, 4)
+    del costs
     del out
     G.close()
     return res
@@ -247,7 +280,7 @@ def replica_mode(args, E, configs, gpt1f1b):
     t = time.perf_counter()
     g = gpt1f1b.gpt_graph(**params, replica_invariant=True)
     rg, _ = gpt1f1b.dp_replica(g, params["tp"], params["dp"])
-    sc = configs.scenario_batch(args.config, args.index, args.scenarios or None)
+    sc = cc_variant(configs.scenario_batch(args.config, args.index, args.scenarios or None), args)
     name = f"config {args.config}" + (f" graph {args.index + 1}" if args.config == 5 else "") + \
         f" (TP{params['tp']} x PP{params['pp']} x DP{params['dp']}, replica-invariant durations)"
     log(f"graphs: {name}: {len(g['op_rank'])} ops, replica {len(rg['op_rank'])} ops "

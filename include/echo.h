@@ -118,9 +118,24 @@ typedef struct {
  *                     J = floor((u >> 32) * (2A+1) / 2^32) - A, u the k-th output of
  *                     SplitMix64 seeded with jitter_seed, k = jitter_stream*2^36 + v + 1
  *   ar_algo           ECHO_RING or ECHO_TREE for all-reduce collectives
+ *   cc_model          ECHO_CC_ECHO (0): the chunked model of Eq. 2-5;
+ *                     ECHO_CC_ALPHA_BETA (1): the alpha-beta baseline (see below)
+ *   cc_table          0: Eq. 2-5 take chunk sizes from Table 6 and beta, gamma and
+ *                     the reduce time from the three bandwidths above; k >= 1:
+ *                     they come from row set k-1 of the graph's CC parameter tables
+ *                     (echo_set_cc_tables), alpha included
  *   slowdown_q16[k][t] factor for a class-k compute op overlapping a type-t
  *                     collective, 65536 <= f < 2^20
  * q16(d, f) = (d*f + 32768) >> 16 in unsigned 64-bit arithmetic.
+ *
+ * Alpha-beta baseline (a what-if reference, not the paper's model): the
+ * latency-bandwidth cost of the ring and binomial-tree algorithms (Thakur,
+ * Rabenseifner and Gropp, IJHPCA 2005) with one rounding per step.  With
+ * B = bw_inter if the group spans servers else bw_intra, R = reduce,
+ * t_B(x) = ceil(x*1000 / B), t_R(x) = ceil(x*1000 / R), p = ceil(S / N),
+ * L = ceil(log2 N):  AG (N-1)(alpha + t_B(p));  RS (N-1)(alpha + t_B(p) + t_R(p));
+ * ring AR (N-1)(2 alpha + 2 t_B(p) + t_R(p));  tree AR L(2 alpha + 2 t_B(S) + t_R(S));
+ * P2P alpha + t_B(S).
  */
 typedef struct {
     int64_t alpha_ns, bw_intra_MBps, bw_inter_MBps, reduce_MBps;
@@ -128,9 +143,33 @@ typedef struct {
     uint32_t jitter_stream;
     int32_t jitter_amp_q16;
     uint8_t ar_algo;
-    uint8_t pad[15];
+    uint8_t cc_model;
+    uint8_t pad0[2];
+    int32_t cc_table;
+    uint8_t pad1[8];
     uint32_t slowdown_q16[8][4];
 } echo_scenario;
+
+enum { ECHO_CC_ECHO = 0, ECHO_CC_ALPHA_BETA = 1 };
+
+/*
+ * CC parameter table (Sec. 5.3 offline profiling: per chunk size, the
+ * connection set-up time, intra- and inter-server transmission times and the
+ * reduce throughput; Table 6 lists such rows by tensor size).  Row i serves
+ * collectives with S <= max_bytes[i] (the first such row; the last row also
+ * every larger S).  Per row: chunk size in bytes (1 <= chunk < 2^32), alpha,
+ * beta and gamma in ns (per chunk for beta and gamma, each in [0, 2^40)) and
+ * the reduce throughput in MB/s ([1, 2^40)).  max_bytes must not decrease.
+ */
+#define ECHO_CC_ROWS 7
+typedef struct {
+    int64_t max_bytes[ECHO_CC_ROWS];
+    int64_t chunk[ECHO_CC_ROWS];
+    int64_t alpha_ns[ECHO_CC_ROWS];
+    int64_t beta_ns[ECHO_CC_ROWS];
+    int64_t gamma_ns[ECHO_CC_ROWS];
+    int64_t reduce_MBps[ECHO_CC_ROWS];
+} echo_cc_table;
 
 /*
  * Validate a graph, match its collectives, merge each collective into one
@@ -164,6 +203,15 @@ int echo_graph_info(echo_graph g, int64_t *n_ops, int64_t *n_colls, int64_t *n_l
 
 /* Release a graph (waits for the device to be idle first).  NULL is allowed. */
 void echo_free_graph(echo_graph g);
+
+/*
+ * Give the graph n_tables CC parameter tables (host array, copied; n_tables = 0
+ * removes them).  Scenarios select one with cc_table = index + 1; a scenario
+ * naming a table the graph does not have is reported by echo_sync_status
+ * (ECHO_ERR_RANGE).  Errors: ARG (NULL with n_tables > 0, n_tables < 0,
+ * decreasing max_bytes), RANGE (a value outside its range), NOMEM, HIP.
+ */
+int echo_set_cc_tables(echo_graph g, const echo_cc_table *tables, int32_t n_tables);
 
 /*
  * CC estimator (Sec. 5.3): d_cost[c * n_scen + s] = running time of collective

@@ -49,12 +49,12 @@ def _load():
     P = ctypes.c_void_p
     i64, i32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
     lib.oracle_run.restype = ctypes.c_int
-    lib.oracle_run.argtypes = [i64, i32, i32] + [P] * 8 + [i64, P, P, P, P, P, i32] + [P] * 9 \
-        + [i32, i32, i32, i32] + [P] * 7 + [ctypes.c_char_p, i64]
+    lib.oracle_run.argtypes = [i64, i32, i32] + [P] * 8 + [i64, P, P, P, P, P, i32] + [P] * 8 \
+        + [P, P, i32, P] + [P] + [i32, i32, i32, i32] + [P] * 7 + [ctypes.c_char_p, i64]
     lib.oracle_chunk_bytes.restype = i64
     lib.oracle_chunk_bytes.argtypes = [i64]
     lib.oracle_cc_time.restype = i64
-    lib.oracle_cc_time.argtypes = [i32, i64, i64, i64, i64, i64, i64, i64, i64, i32]
+    lib.oracle_cc_time.argtypes = [i32, i64, i64, i64, i64, i64, i64, i64, i64, i32, i32, P]
     lib.oracle_splitmix64_at.restype = u64
     lib.oracle_splitmix64_at.argtypes = [u64, u64]
     lib.oracle_q16.restype = i64
@@ -75,7 +75,7 @@ def _p(a):
 
 def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelines: bool = True,
         costs: bool = False, factors: bool = False, jitter_stream=None, until_stable: bool = False,
-        prorate: bool = False) -> dict:
+        prorate: bool = False, cc_tables=None) -> dict:
     """Compose every scenario of `scen` on `graph`.
 
     Returns a dict with 'step' [n_scen] int64 and 'digest' [n_scen] uint64, plus
@@ -84,6 +84,8 @@ def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelin
     (factors=True), and 'refinements' [n_scen] int32: the refined passes composed.
     until_stable: refine until a refinement would change no duration (at most
     n_refine times); prorate: inflate only the overlapped part of a compute op.
+    cc_tables: int64 [n_tables, 6, 7] CC parameter tables that scenarios name with
+    cc_table = index + 1 (scenario fields cc_model / cc_table default to 0).
     jitter_stream defaults to the scenario's index in `scen`.
     Raises OracleError on invalid input or a deadlocked graph.
     """
@@ -118,6 +120,9 @@ def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelin
     jstream = _c(jitter_stream, np.uint32)
     jamp = _c(scen["jitter_amp_q16"], np.int32)
     algo = _c(scen["ar_algo"], np.uint8)
+    ccm = _c(scen["cc_model"], np.uint8) if "cc_model" in scen else np.zeros(n, np.uint8)
+    cct = _c(scen["cc_table"], np.int32) if "cc_table" in scen else np.zeros(n, np.int32)
+    tables = np.zeros((0, 6, 7), np.int64) if cc_tables is None else _c(cc_tables, np.int64).reshape(-1, 6, 7)
     slow = _c(scen["slowdown_q16"], np.uint32).reshape(n, 8, 4)
     out = {"step": np.zeros(n, np.int64), "digest": np.zeros(n, np.uint64),
            "refinements": np.zeros(n, np.int32)}
@@ -133,7 +138,8 @@ def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelin
         n_ops, int(graph["n_ranks"]), int(graph["gpus_per_node"]),
         _p(op_rank), _p(op_stream), _p(op_kind), _p(op_class), _p(op_dur), _p(op_coll),
         _p(pred_off), _p(pred_idx), n_colls, _p(coll_type), _p(coll_bytes), *[_p(x) for x in given],
-        n, _p(alpha), _p(bwa), _p(bwe), _p(red), _p(jseed), _p(jstream), _p(jamp), _p(algo), _p(slow),
+        n, _p(alpha), _p(bwa), _p(bwe), _p(red), _p(jseed), _p(jstream), _p(jamp), _p(algo), _p(ccm), _p(cct),
+        int(tables.shape[0]), _p(tables) if tables.shape[0] else None, _p(slow),
         int(n_refine), int(bool(until_stable)), int(bool(prorate)), int(max(1, threads)),
         _p(out.get("start")), _p(out.get("finish")), _p(out["step"]), _p(out["digest"]),
         _p(out.get("cost")), _p(out.get("factor")), _p(out["refinements"]), err, 512)
@@ -146,8 +152,11 @@ def chunk_bytes(S: int) -> int:
     return int(_load().oracle_chunk_bytes(S))
 
 
-def cc_time(ctype, S, N, M, K, *, alpha, bw_intra, bw_inter, reduce, algo=0) -> int:
-    return int(_load().oracle_cc_time(ctype, S, N, M, K, alpha, bw_intra, bw_inter, reduce, algo))
+def cc_time(ctype, S, N, M, K, *, alpha, bw_intra, bw_inter, reduce, algo=0, cc_model=0, table=None) -> int:
+    """Cost of one collective; table: an int64 [6, 7] CC parameter table or None."""
+    t = None if table is None else _c(table, np.int64).reshape(6, 7)
+    return int(_load().oracle_cc_time(ctype, S, N, M, K, alpha, bw_intra, bw_inter, reduce, algo, cc_model,
+                                      _p(t)))
 
 
 def splitmix64_at(seed: int, k: int) -> int:

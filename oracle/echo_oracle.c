@@ -78,12 +78,23 @@ typedef struct {
     const int32_t *coll_N, *coll_M, *coll_K;
 } graph_t;
 
+/* A CC parameter table (Sec. 5.3 offline profiling; rows like Table 6): per
+   row, the largest message it serves, chunk size, alpha, per-chunk beta and
+   gamma (ns) and reduce throughput (MB/s). */
+#define CC_ROWS 7
+typedef struct {
+    int64_t max_bytes[CC_ROWS], chunk[CC_ROWS], alpha[CC_ROWS], beta[CC_ROWS], gamma[CC_ROWS],
+        reduce[CC_ROWS];
+} cc_table_t;
+
 typedef struct {
     int64_t alpha, bw_intra, bw_inter, reduce;
     uint64_t jseed;
     uint32_t jstream;
     int32_t jamp;
     uint8_t algo;
+    uint8_t cc_model;        /* 0: Eq. 2-5; 1: alpha-beta baseline */
+    const cc_table_t *table; /* parameters of Eq. 2-5 from this table, or NULL: from bandwidths */
     const uint32_t *slow;    /* [8 classes][4 collective types] */
 } scen_t;
 
@@ -132,15 +143,55 @@ static int64_t ceil_log2(int64_t x) {
 /* Eq. 2 (ring all-gather), Eq. 3 (ring reduce-scatter), Eq. 4 (ring
  * all-reduce), Eq. 5 (tree all-reduce) and point-to-point as one chunked hop.
  * Returns -1 when the exact result is >= 2^62. */
+/* Alpha-beta baseline (not the paper's model; a what-if reference): the
+ * latency-bandwidth cost of the ring and binomial-tree algorithms after Thakur,
+ * Rabenseifner and Gropp (IJHPCA 2005), rounding each step up to a nanosecond.
+ * Ring steps move one N-th of the message, tree steps all of it. */
+static int64_t cc_time_alpha_beta(int type, int64_t S, int64_t N, int64_t M, const scen_t *sc) {
+    const int64_t B = M > 1 ? sc->bw_inter : sc->bw_intra;
+    const int64_t part = ceil_div(S, N);
+    const u128 alpha = (u128)sc->alpha, n1 = (u128)(N - 1);
+    const u128 t_part = (u128)ceil_div(part * 1000, B), r_part = (u128)ceil_div(part * 1000, sc->reduce);
+    const u128 t_all = (u128)ceil_div(S * 1000, B), r_all = (u128)ceil_div(S * 1000, sc->reduce);
+    u128 T;
+    switch (type) {
+    case AG: T = n1 * (alpha + t_part); break;                         /* N-1 steps */
+    case RS: T = n1 * (alpha + t_part + r_part); break;                /* N-1 steps, each reduces */
+    case AR:
+        if (sc->algo == TREE) T = (u128)ceil_log2(N) * (2 * alpha + 2 * t_all + r_all);  /* reduce + broadcast */
+        else T = n1 * (2 * alpha + 2 * t_part + r_part);              /* reduce-scatter + all-gather */
+        break;
+    default: T = alpha + t_all; break;                                 /* one hop */
+    }
+    if (T >= (u128)TIME_LIMIT) return -1;
+    return (int64_t)T;
+}
+
 static int64_t cc_time(int type, int64_t S, int64_t N, int64_t M, int64_t K, const scen_t *sc) {
-    const int64_t chunk = chunk_bytes(S);
-    const u128 alpha = (u128)sc->alpha;
-    const u128 beta = (u128)ceil_div(chunk * 1000, sc->bw_intra);   /* intra-server per chunk */
-    const u128 gamma = (u128)ceil_div(chunk * 1000, sc->bw_inter);  /* inter-server per chunk */
-    const u128 g = M > 1 ? gamma : beta;                             /* slowest hop in the group */
+    if (sc->cc_model == 1) return cc_time_alpha_beta(type, S, N, M, sc);
+    int64_t chunk, a, b, c, red;
+    if (sc->table) {
+        /* the first row whose bound covers S; the last row takes every larger S */
+        int i = 0;
+        while (i < CC_ROWS - 1 && S > sc->table->max_bytes[i]) i++;
+        chunk = sc->table->chunk[i];
+        a = sc->table->alpha[i];
+        b = sc->table->beta[i];
+        c = sc->table->gamma[i];
+        red = sc->table->reduce[i];
+    } else {
+        chunk = chunk_bytes(S);
+        a = sc->alpha;
+        b = ceil_div(chunk * 1000, sc->bw_intra);   /* intra-server per chunk */
+        c = ceil_div(chunk * 1000, sc->bw_inter);   /* inter-server per chunk */
+        red = sc->reduce;
+    }
+    const u128 alpha = (u128)a;
+    const u128 beta = (u128)b;
+    const u128 g = M > 1 ? (u128)c : beta;                           /* slowest hop in the group */
     const u128 eta_ring = (u128)ceil_div(S, N * chunk);              /* ring rounds */
     const u128 eta_chunks = (u128)ceil_div(S, chunk);                /* pipelined chunks */
-    const u128 reduce = (u128)ceil_div(S * 1000, sc->reduce);        /* delta * tensor_size */
+    const u128 reduce = (u128)ceil_div(S * 1000, red);               /* delta * tensor_size */
     const u128 n1 = (u128)(N - 1);
     u128 T;
     switch (type) {
@@ -457,7 +508,7 @@ static int check_graph(const graph_t *g, char *err, int64_t errlen) {
 static int check_scen(const scen_t *sc, char *err, int64_t errlen) {
     if (sc->alpha < 0 || sc->alpha >= KNOB_LIMIT || sc->bw_intra < 1 || sc->bw_intra >= KNOB_LIMIT
         || sc->bw_inter < 1 || sc->bw_inter >= KNOB_LIMIT || sc->reduce < 1 || sc->reduce >= KNOB_LIMIT
-        || sc->jamp < 0 || sc->jamp > 65535 || sc->algo > TREE) {
+        || sc->jamp < 0 || sc->jamp > 65535 || sc->algo > TREE || sc->cc_model > 1) {
         set_err(err, errlen, "scenario knob out of range", 0, 0);
         return E_RANGE;
     }
@@ -620,6 +671,10 @@ typedef struct {
     const uint32_t *jstream;
     const int32_t *jamp;
     const uint8_t *algo;
+    const uint8_t *cc_model;
+    const int32_t *cc_table;
+    int32_t n_tables;
+    const cc_table_t *tables;
     const uint32_t *slow;
     int64_t *start, *finish, *step, *cost;
     uint64_t *digest;
@@ -633,8 +688,14 @@ static int run_scenario(job_t *jb, int32_t si, work_t *w, int64_t *s, int64_t *f
                         int64_t *cost, uint32_t *F, int64_t *O, int64_t *lo_buf, int64_t *hi_buf) {
     const graph_t *g = jb->g;
     const derived_t *dv = jb->dv;
+    const int32_t tsel = jb->cc_table ? jb->cc_table[si] : 0;
+    if (tsel < 0 || tsel > jb->n_tables) {
+        snprintf(jb->msg, sizeof jb->msg, "scenario %d names CC table %d of %d", si, tsel, jb->n_tables);
+        return E_RANGE;
+    }
     scen_t sc = {jb->alpha[si], jb->bw_intra[si], jb->bw_inter[si], jb->reduce[si], jb->jseed[si],
-                 jb->jstream[si], jb->jamp[si], jb->algo[si], jb->slow + (int64_t)si * NCLASS * 4};
+                 jb->jstream[si], jb->jamp[si], jb->algo[si], jb->cc_model ? jb->cc_model[si] : 0,
+                 tsel > 0 ? jb->tables + (tsel - 1) : NULL, jb->slow + (int64_t)si * NCLASS * 4};
     int rc = check_scen(&sc, jb->msg, sizeof jb->msg);
     if (rc) return rc;
     /* CC estimator */
@@ -741,7 +802,8 @@ int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int3
                const int32_t *coll_K, int32_t n_scen, const int64_t *alpha,
                const int64_t *bw_intra, const int64_t *bw_inter, const int64_t *reduce,
                const uint64_t *jseed, const uint32_t *jstream, const int32_t *jamp,
-               const uint8_t *algo, const uint32_t *slow, int32_t n_refine, int32_t until_stable,
+               const uint8_t *algo, const uint8_t *cc_model, const int32_t *cc_table, int32_t n_tables,
+               const int64_t *tables, const uint32_t *slow, int32_t n_refine, int32_t until_stable,
                int32_t prorate, int32_t n_threads, int64_t *start, int64_t *finish, int64_t *step,
                uint64_t *digest, int64_t *cost, uint32_t *factor, int32_t *refinements, char *err,
                int64_t errlen) {
@@ -758,6 +820,25 @@ int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int3
     }
     int rc = check_graph(&g, err, errlen);
     if (rc) return rc;
+    const cc_table_t *tb = (const cc_table_t *)tables;
+    if (n_tables < 0 || (n_tables > 0 && !tables)) {
+        set_err(err, errlen, "bad CC table array", 0, 0);
+        return E_ARG;
+    }
+    for (int32_t k = 0; k < n_tables; k++)
+        for (int i = 0; i < CC_ROWS; i++) {
+            if (i > 0 && tb[k].max_bytes[i] < tb[k].max_bytes[i - 1]) {
+                set_err(err, errlen, "CC table %lld: max_bytes decreases at row %lld", k, i);
+                return E_ARG;
+            }
+            if (tb[k].chunk[i] < 1 || tb[k].chunk[i] >= ((int64_t)1 << 32) || tb[k].alpha[i] < 0
+                || tb[k].alpha[i] >= KNOB_LIMIT || tb[k].beta[i] < 0 || tb[k].beta[i] >= KNOB_LIMIT
+                || tb[k].gamma[i] < 0 || tb[k].gamma[i] >= KNOB_LIMIT || tb[k].reduce[i] < 1
+                || tb[k].reduce[i] >= KNOB_LIMIT) {
+                set_err(err, errlen, "CC table %lld row %lld out of range", k, i);
+                return E_RANGE;
+            }
+        }
     derived_t dv;
     rc = derive(&g, &dv, err, errlen);
     if (rc) return rc;
@@ -771,8 +852,8 @@ int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int3
     }
     for (int32_t t = 0; t < n_threads; t++) {
         jobs[t] = (job_t){&g, &dv, n_scen, n_refine, n_threads, t, until_stable != 0, prorate != 0, alpha,
-                          bw_intra, bw_inter, reduce, jseed, jstream, jamp, algo, slow, start, finish, step,
-                          cost, digest, factor, refinements, OK, {0}};
+                          bw_intra, bw_inter, reduce, jseed, jstream, jamp, algo, cc_model, cc_table, n_tables, tb,
+                          slow, start, finish, step, cost, digest, factor, refinements, OK, {0}};
     }
     for (int32_t t = 1; t < n_threads; t++) pthread_create(&th[t], NULL, worker, &jobs[t]);
     worker(&jobs[0]);
@@ -791,10 +872,12 @@ int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int3
 /* Exposed pieces for the pin tests (each is the oracle's own code above). */
 int64_t oracle_chunk_bytes(int64_t S) { return chunk_bytes(S); }
 int64_t oracle_cc_time(int32_t type, int64_t S, int64_t N, int64_t M, int64_t K, int64_t alpha,
-                       int64_t bw_intra, int64_t bw_inter, int64_t reduce, int32_t algo) {
+                       int64_t bw_intra, int64_t bw_inter, int64_t reduce, int32_t algo, int32_t cc_model,
+                       const int64_t *table) {
     uint32_t slow[32];
     for (int i = 0; i < 32; i++) slow[i] = Q16_ONE;
-    scen_t sc = {alpha, bw_intra, bw_inter, reduce, 0, 0, 0, (uint8_t)algo, slow};
+    scen_t sc = {alpha, bw_intra, bw_inter, reduce, 0, 0, 0, (uint8_t)algo, (uint8_t)cc_model,
+                 (const cc_table_t *)table, slow};
     return cc_time(type, S, N, M, K, &sc);
 }
 uint64_t oracle_splitmix64_at(uint64_t seed, uint64_t k) { return splitmix64_at(seed, k); }

@@ -47,6 +47,7 @@ constexpr int64_t kDurLimit = int64_t(1) << 43;
 constexpr int64_t kBytesLimit = int64_t(1) << 50;
 constexpr int64_t kI32Max = INT32_MAX;
 constexpr int kMaxRanksPerWalker = 16;
+constexpr int64_t kKnobLimitHost = int64_t(1) << 40;
 constexpr int64_t kDefaultSpinNs = 20LL * 1000 * 1000 * 1000;   // 20 s
 
 // Table 6 (all-reduce breakdown): NCCL chunk size by tensor size.  The size
@@ -139,6 +140,7 @@ void free_graph(echo_graph g) {
     (void)hipFree(g->arrive);
     (void)hipFree(g->count);
     (void)hipFree(g->tmask);
+    (void)hipFree(g->dg.cc_tables);
     (void)hipFree(g->ext);
     (void)hipFree(g->chg);
     (void)hipFree(g->tmp_start);
@@ -776,10 +778,10 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
     } while (0)
     TIMED(ECHO_K_INIT, launch_init(g->dg, d_scen, n_scen, g->arrive, n_arrive, g->count, n_count, step, d_digest,
                                    stream), "init kernel");
-    TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.classes, d_scen, n_scen, g->class_cost, g->dg.status, stream),
+    TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.classes, g->dg.cc_tables, d_scen, n_scen, g->class_cost, g->dg.status, stream),
           "cc_cost kernel");
     if (g->need_coll_cost)
-        TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.colls, d_scen, n_scen, g->cost, g->dg.status, stream),
+        TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.colls, g->dg.cc_tables, d_scen, n_scen, g->cost, g->dg.status, stream),
               "cc_cost kernel");
     if (until_stable && (e = launch_fill_i32(reinterpret_cast<int32_t *>(g->chg), ns + 1, 0, stream)))
         return hip_fail(e, "fill kernel");
@@ -872,7 +874,7 @@ int echo_cc_cost(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int6
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     if ((e = launch_init(g->dg, d_scen, n_scen, nullptr, 0, nullptr, 0, nullptr, nullptr, s)))
         return hip_fail(e, "init kernel");
-    if ((e = launch_cc_cost(g->dg.colls, d_scen, n_scen, d_cost, g->dg.status, s)))
+    if ((e = launch_cc_cost(g->dg.colls, g->dg.cc_tables, d_scen, n_scen, d_cost, g->dg.status, s)))
         return hip_fail(e, "cc_cost kernel");
     return ECHO_OK;
 }
@@ -905,6 +907,42 @@ int echo_compose_validated(echo_graph g, const echo_scenario *d_scen, int32_t n_
     } catch (...) {
         return fail(ECHO_ERR_NOMEM, "unexpected exception in compose");
     }
+}
+
+int echo_set_cc_tables(echo_graph g, const echo_cc_table *tables, int32_t n_tables) {
+    g_last_error.clear();
+    if (!g) return fail(ECHO_ERR_ARG, "null graph");
+    if (n_tables < 0 || (n_tables > 0 && !tables)) return fail(ECHO_ERR_ARG, "bad table array (n_tables %d)", n_tables);
+    constexpr int64_t kLim = kKnobLimitHost;
+    for (int32_t k = 0; k < n_tables; ++k) {
+        const echo_cc_table &t = tables[k];
+        for (int i = 0; i < ECHO_CC_ROWS; ++i) {
+            if (i > 0 && t.max_bytes[i] < t.max_bytes[i - 1])
+                return fail(ECHO_ERR_ARG, "table %d: max_bytes decreases at row %d", k, i);
+            if (t.chunk[i] < 1 || t.chunk[i] >= (int64_t(1) << 32) || t.alpha_ns[i] < 0 || t.alpha_ns[i] >= kLim ||
+                t.beta_ns[i] < 0 || t.beta_ns[i] >= kLim || t.gamma_ns[i] < 0 || t.gamma_ns[i] >= kLim ||
+                t.reduce_MBps[i] < 1 || t.reduce_MBps[i] >= kLim)
+                return fail(ECHO_ERR_RANGE, "table %d row %d: value out of range", k, i);
+        }
+    }
+    hipError_t e = hipSetDevice(g->device);
+    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+    echo_cc_table *d = nullptr;
+    if (n_tables > 0) {
+        e = hipMalloc(reinterpret_cast<void **>(&d), sizeof(echo_cc_table) * (size_t)n_tables);
+        if (e != hipSuccess) return fail(ECHO_ERR_NOMEM, "CC tables: %s", hipGetErrorString(e));
+        e = hipMemcpy(d, tables, sizeof(echo_cc_table) * (size_t)n_tables, hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            (void)hipFree(d);
+            return hip_fail(e, "CC tables upload");
+        }
+    }
+    // composes already enqueued may still read the old tables
+    (void)hipDeviceSynchronize();
+    (void)hipFree(g->dg.cc_tables);
+    g->dg.cc_tables = d;
+    g->dg.n_cc_tables = n_tables;
+    return ECHO_OK;
 }
 
 int echo_sync_status(echo_graph g, void *hip_stream) {

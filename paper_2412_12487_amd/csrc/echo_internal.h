@@ -135,6 +135,8 @@ struct DeviceGraph {
     int64_t *cp_off = nullptr;       // [n_ranks * 8 + 1]
     ComputeRec *cp = nullptr;
     unsigned *status = nullptr;      // device status word
+    echo_cc_table *cc_tables = nullptr;   // CC parameter tables (echo_set_cc_tables)
+    int32_t n_cc_tables = 0;
 };
 
 struct WalkArgs {
@@ -186,8 +188,8 @@ hipError_t launch_init(const DeviceGraph &g, const echo_scenario *scen, int32_t 
                        int64_t n_count, int64_t *step, uint64_t *digest, hipStream_t stream);
 hipError_t launch_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *count,
                         int64_t n_count, hipStream_t stream);
-hipError_t launch_cc_cost(const CollTable &t, const echo_scenario *scen, int32_t n_scen, int64_t *cost,
-                          unsigned *status, hipStream_t stream);
+hipError_t launch_cc_cost(const CollTable &t, const echo_cc_table *tables, const echo_scenario *scen,
+                          int32_t n_scen, int64_t *cost, unsigned *status, hipStream_t stream);
 hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream);
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream);
 // After an overlap pass: count the refinement of every scenario whose durations changed,

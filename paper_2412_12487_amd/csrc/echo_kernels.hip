@@ -66,7 +66,7 @@ __device__ __forceinline__ unsigned ld_relaxed(const unsigned *p) {
 // ------------------------------------------------------------------ set-up
 __global__ void k_init(const echo_scenario *scen, int32_t n_scen, unsigned long long *arrive,
                        int64_t n_arrive, unsigned *count, int64_t n_count, int64_t *step,
-                       uint64_t *digest, unsigned *status) {
+                       uint64_t *digest, int32_t n_tables, unsigned *status) {
     const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t nth = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = tid; i < n_arrive; i += nth) arrive[i] = 0;
@@ -79,7 +79,8 @@ __global__ void k_init(const echo_scenario *scen, int32_t n_scen, unsigned long 
                   s.bw_intra_MBps < kKnobLimit && s.bw_inter_MBps >= 1 &&
                   s.bw_inter_MBps < kKnobLimit && s.reduce_MBps >= 1 &&
                   s.reduce_MBps < kKnobLimit && s.jitter_amp_q16 >= 0 &&
-                  s.jitter_amp_q16 <= 65535 && s.ar_algo <= ECHO_TREE;
+                  s.jitter_amp_q16 <= 65535 && s.ar_algo <= ECHO_TREE && s.cc_model <= ECHO_CC_ALPHA_BETA &&
+                  s.cc_table >= 0 && s.cc_table <= n_tables;
         for (int k = 0; k < kClasses; ++k)
             for (int t = 0; t < kTypes; ++t) {
                 const uint32_t f = s.slowdown_q16[k][t];
@@ -98,14 +99,12 @@ __global__ void k_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *
 
 // ------------------------------------------------------------------ CC estimator
 // One block per collective (or cost class); lanes stride over scenarios.
-__global__ __launch_bounds__(64) void k_cc_cost(CollTable t, const echo_scenario *scen, int32_t n_scen,
-                                                int64_t *cost, unsigned *status) {
+__global__ __launch_bounds__(64) void k_cc_cost(CollTable t, const echo_cc_table *tables, const echo_scenario *scen,
+                                                int32_t n_scen, int64_t *cost, unsigned *status) {
     const int64_t c = blockIdx.x;
     const int type = t.type[c];
-    const int64_t S = t.bytes[c], chunk = t.chunk[c];
+    const int64_t S = t.bytes[c];
     const int64_t N = t.N[c], M = t.M[c], K = t.K[c];
-    const unsigned __int128 eta_ring = (unsigned __int128)t.eta_ring[c];
-    const unsigned __int128 eta_chunks = (unsigned __int128)t.eta_chunks[c];
     const unsigned __int128 n1 = (unsigned __int128)(N - 1);
     for (int32_t s = threadIdx.x; s < n_scen; s += blockDim.x) {
         const echo_scenario &sc = scen[s];
@@ -113,25 +112,67 @@ __global__ __launch_bounds__(64) void k_cc_cost(CollTable t, const echo_scenario
         const int64_t bwa = sc.bw_intra_MBps >= 1 ? sc.bw_intra_MBps : 1;
         const int64_t bwe = sc.bw_inter_MBps >= 1 ? sc.bw_inter_MBps : 1;
         const int64_t red = sc.reduce_MBps >= 1 ? sc.reduce_MBps : 1;
-        const unsigned __int128 alpha = (unsigned __int128)(sc.alpha_ns >= 0 ? sc.alpha_ns : 0);
-        const unsigned __int128 beta = (unsigned __int128)cdiv(chunk * 1000, bwa);
-        const unsigned __int128 gamma = (unsigned __int128)cdiv(chunk * 1000, bwe);
-        const unsigned __int128 hop = M > 1 ? gamma : beta;
-        const unsigned __int128 reduce = (unsigned __int128)cdiv(S * 1000, red);
+        unsigned __int128 alpha = (unsigned __int128)(sc.alpha_ns >= 0 ? sc.alpha_ns : 0);
         unsigned __int128 T;
-        if (type == ECHO_AG) {
-            T = alpha + hop * eta_ring * n1;                                    // Eq. 2
-        } else if (type == ECHO_RS) {
-            T = alpha + eta_ring * (n1 * beta + n1 * hop) + reduce;             // Eq. 3
-        } else if (type == ECHO_AR) {
-            if (sc.ar_algo == ECHO_TREE)                                        // Eq. 5
-                T = alpha + hop * (eta_chunks > 0 ? eta_chunks - 1 : 0) +
-                    2 * beta * (unsigned __int128)(K - 1) +
-                    2 * hop * (unsigned __int128)clog2(M) + reduce;
-            else                                                                // Eq. 4
-                T = alpha + eta_ring * (n1 * beta + 2 * n1 * hop) + reduce;
-        } else {                                                                // P2P
-            T = alpha + eta_chunks * hop;
+        if (sc.cc_model == ECHO_CC_ALPHA_BETA) {
+            // latency-bandwidth baseline: ring steps move ceil(S / N) bytes, tree steps all of S
+            const int64_t B = M > 1 ? bwe : bwa;
+            const int64_t part = cdiv(S, N);
+            const unsigned __int128 tbp = (unsigned __int128)cdiv(part * 1000, B);
+            const unsigned __int128 trp = (unsigned __int128)cdiv(part * 1000, red);
+            if (type == ECHO_AG) {
+                T = n1 * (alpha + tbp);
+            } else if (type == ECHO_RS) {
+                T = n1 * (alpha + tbp + trp);
+            } else if (type == ECHO_AR) {
+                if (sc.ar_algo == ECHO_TREE)
+                    T = (unsigned __int128)clog2(N) * (2 * alpha + 2 * (unsigned __int128)cdiv(S * 1000, B) +
+                                                       (unsigned __int128)cdiv(S * 1000, red));
+                else
+                    T = n1 * (2 * alpha + 2 * tbp + trp);
+            } else {
+                T = alpha + (unsigned __int128)cdiv(S * 1000, B);
+            }
+        } else {
+            int64_t chunk, eta_r, eta_t, b, g, r;
+            if (sc.cc_table > 0 && tables) {
+                // profiled parameters: the first row whose size bound covers S
+                const echo_cc_table &tb = tables[sc.cc_table - 1];
+                int i = 0;
+                while (i < ECHO_CC_ROWS - 1 && S > tb.max_bytes[i]) ++i;
+                chunk = tb.chunk[i] >= 1 ? tb.chunk[i] : 1;
+                eta_r = cdiv(S, N * chunk);
+                eta_t = cdiv(S, chunk);
+                alpha = (unsigned __int128)tb.alpha_ns[i];
+                b = tb.beta_ns[i];
+                g = tb.gamma_ns[i];
+                r = tb.reduce_MBps[i] >= 1 ? tb.reduce_MBps[i] : 1;
+            } else {
+                chunk = t.chunk[c];
+                eta_r = t.eta_ring[c];
+                eta_t = t.eta_chunks[c];
+                b = cdiv(chunk * 1000, bwa);
+                g = cdiv(chunk * 1000, bwe);
+                r = red;
+            }
+            const unsigned __int128 eta_ring = (unsigned __int128)eta_r, eta_chunks = (unsigned __int128)eta_t;
+            const unsigned __int128 beta = (unsigned __int128)b;
+            const unsigned __int128 hop = M > 1 ? (unsigned __int128)g : beta;
+            const unsigned __int128 reduce = (unsigned __int128)cdiv(S * 1000, r);
+            if (type == ECHO_AG) {
+                T = alpha + hop * eta_ring * n1;                                    // Eq. 2
+            } else if (type == ECHO_RS) {
+                T = alpha + eta_ring * (n1 * beta + n1 * hop) + reduce;             // Eq. 3
+            } else if (type == ECHO_AR) {
+                if (sc.ar_algo == ECHO_TREE)                                        // Eq. 5
+                    T = alpha + hop * (eta_chunks > 0 ? eta_chunks - 1 : 0) +
+                        2 * beta * (unsigned __int128)(K - 1) +
+                        2 * hop * (unsigned __int128)clog2(M) + reduce;
+                else                                                                // Eq. 4
+                    T = alpha + eta_ring * (n1 * beta + 2 * n1 * hop) + reduce;
+            } else {                                                                // P2P
+                T = alpha + eta_chunks * hop;
+            }
         }
         if (T >= (unsigned __int128)kTimeLimit) {
             __hip_atomic_fetch_or(status, kStatusOverflow, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -756,7 +797,7 @@ hipError_t launch_init(const DeviceGraph &g, const echo_scenario *scen, int32_t 
     int64_t n = n_arrive > n_count ? n_arrive : n_count;
     if (n_scen > n) n = n_scen;
     hipLaunchKernelGGL(k_init, dim3(grid_for(n, 256)), dim3(256), 0, stream, scen, n_scen, arrive,
-                       n_arrive, count, n_count, step, digest, g.status);
+                       n_arrive, count, n_count, step, digest, g.n_cc_tables, g.status);
     return hipGetLastError();
 }
 
@@ -769,10 +810,10 @@ hipError_t launch_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *
     return hipGetLastError();
 }
 
-hipError_t launch_cc_cost(const CollTable &t, const echo_scenario *scen, int32_t n_scen, int64_t *cost,
-                          unsigned *status, hipStream_t stream) {
+hipError_t launch_cc_cost(const CollTable &t, const echo_cc_table *tables, const echo_scenario *scen,
+                          int32_t n_scen, int64_t *cost, unsigned *status, hipStream_t stream) {
     if (t.n == 0 || n_scen == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_cc_cost, dim3((unsigned)t.n), dim3(64), 0, stream, t, scen, n_scen, cost, status);
+    hipLaunchKernelGGL(k_cc_cost, dim3((unsigned)t.n), dim3(64), 0, stream, t, tables, scen, n_scen, cost, status);
     return hipGetLastError();
 }
 

@@ -21,18 +21,20 @@ ECHO_ERR_CYCLE, ECHO_ERR_NOMEM, ECHO_ERR_HIP, ECHO_ERR_DEVICE = -4, -5, -6, -7
 ERROR_NAMES = {0: "OK", -1: "ARG", -2: "RANGE", -3: "MATCH", -4: "CYCLE", -5: "NOMEM", -6: "HIP",
                -7: "DEVICE"}
 EXPORTS = ("echo_load_graph", "echo_load_graph_ex", "echo_graph_info", "echo_free_graph", "echo_cc_cost",
-           "echo_compose_batch", "echo_compose_validated", "echo_sync_status", "echo_set_timing", "echo_kernel_times",
+           "echo_compose_batch", "echo_compose_validated", "echo_set_cc_tables", "echo_sync_status", "echo_set_timing", "echo_kernel_times",
            "echo_last_error")
 KERNEL_KINDS = {0: "init", 1: "cc_cost", 2: "walk", 3: "overlap", 4: "clear"}
 
 # echo_scenario (include/echo.h): 192 bytes.
 SCENARIO_DTYPE = np.dtype({
     "names": ["alpha_ns", "bw_intra_MBps", "bw_inter_MBps", "reduce_MBps", "jitter_seed",
-              "jitter_stream", "jitter_amp_q16", "ar_algo", "slowdown_q16"],
-    "formats": ["<i8", "<i8", "<i8", "<i8", "<u8", "<u4", "<i4", "u1", ("<u4", (8, 4))],
-    "offsets": [0, 8, 16, 24, 32, 40, 44, 48, 64],
+              "jitter_stream", "jitter_amp_q16", "ar_algo", "cc_model", "cc_table", "slowdown_q16"],
+    "formats": ["<i8", "<i8", "<i8", "<i8", "<u8", "<u4", "<i4", "u1", "u1", "<i4", ("<u4", (8, 4))],
+    "offsets": [0, 8, 16, 24, 32, 40, 44, 48, 49, 52, 64],
     "itemsize": 192,
 })
+CC_ROWS = 7           # rows of a CC parameter table; as int64 [6, CC_ROWS]: max_bytes, chunk,
+                      # alpha_ns, beta_ns, gamma_ns, reduce_MBps (the echo_cc_table layout)
 
 
 class EchoError(RuntimeError):
@@ -82,6 +84,8 @@ def lib():
     L.echo_compose_batch.restype = ctypes.c_int
     L.echo_compose_validated.argtypes = [P, P, i32, ctypes.POINTER(_Validator), P, P, P, P, P, P]
     L.echo_compose_validated.restype = ctypes.c_int
+    L.echo_set_cc_tables.argtypes = [P, P, i32]
+    L.echo_set_cc_tables.restype = ctypes.c_int
     L.echo_sync_status.argtypes = [P, P]
     L.echo_sync_status.restype = ctypes.c_int
     L.echo_set_timing.argtypes = [P, ctypes.c_int]
@@ -107,6 +111,9 @@ def pack_scenarios(sc: dict) -> np.ndarray:
               "jitter_amp_q16", "ar_algo"):
         rec[k] = sc[k]
     rec["jitter_stream"] = sc["jitter_stream"] if "jitter_stream" in sc else np.arange(n)
+    for k in ("cc_model", "cc_table"):
+        if k in sc:
+            rec[k] = sc[k]
     rec["slowdown_q16"] = np.asarray(sc["slowdown_q16"]).reshape(n, 8, 4)
     return rec
 
@@ -233,6 +240,14 @@ class Graph:
         if check:
             self.sync_status()
         return res
+
+    def set_cc_tables(self, tables):
+        """CC parameter tables: int64 array [n_tables, 6, 7] (max_bytes, chunk, alpha_ns,
+        beta_ns, gamma_ns, reduce_MBps per row); scenarios pick one with cc_table = index + 1."""
+        t = np.ascontiguousarray(tables, np.int64).reshape(-1, 6, CC_ROWS) if tables is not None and len(tables) \
+            else np.zeros((0, 6, CC_ROWS), np.int64)
+        _check(lib().echo_set_cc_tables(self.handle, t.ctypes.data_as(ctypes.c_void_p) if len(t) else None,
+                                        int(t.shape[0])))
 
     def set_timing(self, enable=True):
         _check(lib().echo_set_timing(self.handle, int(bool(enable))))

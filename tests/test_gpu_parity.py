@@ -473,3 +473,77 @@ def test_prorated_extra_time_limit_reported(E):
         G.compose(d, n, 1, prorate=True)
     assert x.value.code == E.ECHO_ERR_RANGE
     G.close()
+
+
+# ---------------------------------------------------------------- CC model variants
+def _mixed_cc_scenarios(sc, rng, n_tables):
+    n = scenarios.count(sc)
+    sc = dict(sc)
+    sc["cc_model"] = (rng.random(n) < 0.3).astype(np.uint8)
+    sc["cc_table"] = rng.integers(0, n_tables + 1, n).astype(np.int32)
+    return sc
+
+
+def test_cc_models_and_tables_costs(E):
+    rng = np.random.default_rng(77)
+    tables = scenarios.draw_cc_tables(3, rng)
+    for cfg in (2, 4):
+        g = configs.graph(cfg)
+        sc = _mixed_cc_scenarios(scenarios.take(configs.scenario_batch(cfg), slice(0, 70)), rng, 3)
+        G = E.Graph(g, 0)
+        G.set_cc_tables(tables)
+        d, n = E.scenarios_to_device(sc)
+        cost = G.cc_cost(d, n).cpu().numpy()
+        G.close()
+        ref = oracle.run(g, sc, 0, threads=THREADS, timelines=False, costs=True, cc_tables=tables)
+        np.testing.assert_array_equal(cost.T, ref["cost"])
+
+
+def test_cc_models_and_tables_compose(E):
+    rng = np.random.default_rng(78)
+    tables = scenarios.draw_cc_tables(4, rng)
+    g = configs.graph(1)
+    sc = _mixed_cc_scenarios(scenarios.take(configs.scenario_batch(4), slice(0, 130)), rng, 4)
+    G = E.Graph(g, 0)
+    G.set_cc_tables(tables)
+    assert_same(gpu_run(E, g, sc, 1, graph=G), oracle.run(g, sc, 1, threads=THREADS, cc_tables=tables))
+    G.close()
+    g, sc = configs.graph(2), _mixed_cc_scenarios(configs.scenario_batch(2), rng, 4)
+    G = E.Graph(g, 0)
+    G.set_cc_tables(tables)
+    gpu = gpu_run(E, g, sc, 1, graph=G)
+    G.close()
+    cols = [0, 5, 63]
+    ref = oracle.run(g, scenarios.take(sc, cols), 1, threads=3, cc_tables=tables, jitter_stream=cols)
+    np.testing.assert_array_equal(gpu["step"][cols], ref["step"])
+    np.testing.assert_array_equal(gpu["digest"][cols], ref["digest"])
+    for j, c in enumerate(cols):
+        np.testing.assert_array_equal(gpu["finish"][:, c], ref["finish"][j])
+
+
+def test_cc_table_errors_reported(E):
+    g = configs.graph(1)
+    G = E.Graph(g, 0)
+    bad = scenarios.draw_cc_tables(1, np.random.default_rng(1))
+    bad[0, 1, 2] = 0                                   # chunk 0
+    with pytest.raises(E.EchoError) as x:
+        G.set_cc_tables(bad)
+    assert x.value.code == E.ECHO_ERR_RANGE
+    bad = scenarios.draw_cc_tables(1, np.random.default_rng(1))
+    bad[0, 0, 5] = 0                                   # max_bytes decreases
+    with pytest.raises(E.EchoError) as x:
+        G.set_cc_tables(bad)
+    assert x.value.code == E.ECHO_ERR_ARG
+    G.set_cc_tables(scenarios.draw_cc_tables(2, np.random.default_rng(1)))
+    sc = dict(scenarios.default_scenarios(3), cc_table=np.array([0, 2, 3], np.int32))   # table 3 is missing
+    d, n = E.scenarios_to_device(sc)
+    with pytest.raises(E.EchoError) as x:
+        G.compose(d, n, 1)
+    assert x.value.code == E.ECHO_ERR_RANGE
+    G.set_cc_tables(None)
+    sc = dict(scenarios.default_scenarios(2), cc_table=np.array([0, 1], np.int32))
+    d, n = E.scenarios_to_device(sc)
+    with pytest.raises(E.EchoError) as x:
+        G.compose(d, n, 1)
+    assert x.value.code == E.ECHO_ERR_RANGE
+    G.close()

@@ -677,3 +677,82 @@ def test_random_small_dags_validator_variants():
             assert r["refinements"][0] == done
             deep += until_stable and done >= 2
     assert deep >= 5          # the fixed point is often reached only after several rounds
+
+
+# ---------------------------------------------------------------- CC model variants
+_AB = dict(alpha=10000, bw_intra=400000, bw_inter=50000, reduce=160000)
+
+
+@pytest.mark.parametrize("row", _rows("cc_alpha_beta.txt"), ids=lambda r: "-".join(r[:5]))
+def test_alpha_beta_hand_values(row):
+    t, algo, S, N, M, K, want = (int(x) for x in row)
+    assert oracle.cc_time(t, S, N, M, K, algo=algo, cc_model=1, **_AB) == want
+
+
+@pytest.mark.parametrize("S,N,M", [(1, 2, 1), (4 << 20, 8, 1), (5 << 20, 16, 2), (300 << 20, 64, 8), (12345, 3, 3)])
+def test_alpha_beta_ring_allreduce_is_reduce_scatter_plus_all_gather(S, N, M):
+    K = -(-N // M)
+    ar = oracle.cc_time(0, S, N, M, K, cc_model=1, **_AB)
+    assert ar == oracle.cc_time(2, S, N, M, K, cc_model=1, **_AB) + oracle.cc_time(1, S, N, M, K, cc_model=1, **_AB)
+
+
+def test_cc_table_equal_to_bandwidth_parameters_reproduces_every_cost():
+    rng = np.random.default_rng(8)
+    for _ in range(200):
+        kn = dict(alpha=int(rng.integers(0, 30000)), bw_intra=int(rng.integers(1000, 500000)),
+                  bw_inter=int(rng.integers(1000, 500000)), reduce=int(rng.integers(1000, 500000)))
+        table = scenarios.cc_table_from_bandwidths(kn["alpha"], kn["bw_intra"], kn["bw_inter"], kn["reduce"])
+        S = int(rng.choice([0, 1, 4 << 20, (4 << 20) + 1, 16 << 20, (128 << 20) + 7, 1 << 30,
+                            int(rng.integers(0, 1 << 31))]))
+        N = int(rng.integers(1, 300))
+        M = int(rng.integers(1, N + 1))
+        K = -(-N // M)
+        for t in range(4):
+            if t == 3 and N != 2:
+                continue
+            for algo in (0, 1):
+                assert oracle.cc_time(t, S, N, M, K, algo=algo, table=table, **kn) == \
+                    oracle.cc_time(t, S, N, M, K, algo=algo, **kn)
+
+
+def test_cc_table_row_selection_hand_values():
+    """Rows serve S up to their bound; the last row every larger S.  P2P inside one server:
+    alpha_row + ceil(S / chunk_row) * beta_row."""
+    table = scenarios.cc_table(chunk=np.arange(1, 8) * 1000, alpha=np.arange(1, 8) * 100,
+                               beta=np.arange(1, 8) * 10, gamma=np.arange(1, 8) * 50, reduce=100000)
+    p2p = lambda S: oracle.cc_time(3, S, 2, 1, 2, table=table, **_AB)
+    assert p2p(4 << 20) == 100 + 4195 * 10                 # row 0: ceil(4194304 / 1000) = 4195
+    assert p2p((4 << 20) + 1) == 200 + 2098 * 20           # row 1: ceil(4194305 / 2000) = 2098
+    assert p2p(300 << 20) == 700 + 44939 * 70              # past the last bound: row 6, ceil(314572800 / 7000)
+    # across servers the hop is gamma
+    assert oracle.cc_time(3, 1000, 2, 2, 1, table=table, **_AB) == 100 + 1 * 50
+
+
+def test_compose_with_cc_tables_and_models():
+    """A scenario whose table equals its bandwidth parameters composes exactly like the
+    table-less scenario; the alpha-beta model changes the result."""
+    g = configs.graph(1)
+    sc = scenarios.draw(4, np.random.default_rng(31), bw_inter=(20000, 90000), bw_intra=(50000, 400000),
+                        alpha=(0, 9000), ar_algo_random=True)
+    tables = np.stack([scenarios.cc_table_from_bandwidths(int(sc["alpha_ns"][i]), int(sc["bw_intra_MBps"][i]),
+                                                          int(sc["bw_inter_MBps"][i]), int(sc["reduce_MBps"][i]))
+                       for i in range(4)])
+    plain = oracle.run(g, sc, 1)
+    via = dict(sc, cc_table=np.arange(1, 5, dtype=np.int32))
+    r = oracle.run(g, via, 1, cc_tables=tables)
+    np.testing.assert_array_equal(r["finish"], plain["finish"])
+    ab = oracle.run(g, dict(sc, cc_model=np.ones(4, np.uint8)), 1)
+    assert (ab["step"] != plain["step"]).all()
+
+
+def test_cc_table_errors():
+    g = configs.graph(1)
+    sc = dict(scenarios.default_scenarios(1), cc_table=np.array([2], np.int32))
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.run(g, sc, 1, cc_tables=scenarios.draw_cc_tables(1, np.random.default_rng(0)))
+    assert e.value.code == -2
+    bad = scenarios.draw_cc_tables(1, np.random.default_rng(0))
+    bad[0, 0, 3] = bad[0, 0, 2] - 1                       # max_bytes decreases
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.run(g, scenarios.default_scenarios(1), 1, cc_tables=bad)
+    assert e.value.code == -1

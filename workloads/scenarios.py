@@ -14,7 +14,13 @@ a dict of numpy arrays, one entry per field (structure of arrays):
                                      (its index in the batch it was drawn in)
     jitter_amp_q16 int32  [n]        jitter amplitude A in Q16 (0 = no jitter)
     ar_algo        uint8  [n]        all-reduce algorithm: 0 ring, 1 tree
+    cc_model       uint8  [n]        collective cost model: 0 Echo (chunked), 1 alpha-beta baseline
+    cc_table       int32  [n]        0: parameters from the bandwidths; k: CC parameter table k-1
     slowdown_q16   uint32 [n, 8, 4]  slowdown factor per (kernel class, collective type), Q16
+
+CC parameter tables (int64 [6, 7]: per row max_bytes, chunk, alpha_ns,
+beta_ns, gamma_ns, reduce_MBps) are inputs too; `cc_table_from_bandwidths`
+writes the table equal to a scenario's bandwidth-derived parameters.
 
 Only input values live here; no formula of the method is evaluated.
 """
@@ -48,7 +54,11 @@ DEFAULTS = dict(
 )
 
 FIELDS = ("alpha_ns", "bw_intra_MBps", "bw_inter_MBps", "reduce_MBps",
-          "jitter_seed", "jitter_stream", "jitter_amp_q16", "ar_algo", "slowdown_q16")
+          "jitter_seed", "jitter_stream", "jitter_amp_q16", "ar_algo", "cc_model", "cc_table", "slowdown_q16")
+
+# Table 6 of the paper: tensor-size bands (MB read as MiB) and NCCL's chunk size for each.
+TABLE6_MAX_BYTES = np.array([4, 8, 16, 32, 64, 128, 256], np.int64) << 20
+TABLE6_CHUNK = np.array([18000, 36000, 72000, 72000, 72000, 144000, 288000], np.int64)
 
 
 def default_scenarios(n: int) -> dict:
@@ -62,6 +72,8 @@ def default_scenarios(n: int) -> dict:
         "jitter_stream": np.arange(n, dtype=np.uint32),
         "jitter_amp_q16": np.zeros(n, np.int32),
         "ar_algo": np.full(n, RING, np.uint8),
+        "cc_model": np.zeros(n, np.uint8),
+        "cc_table": np.zeros(n, np.int32),
         "slowdown_q16": np.broadcast_to(PAPER_SLOWDOWN_Q16[None, :, None], (n, 8, 4)).copy(),
     }
 
@@ -103,3 +115,31 @@ def take(sc: dict, idx) -> dict:
 
 def count(sc: dict) -> int:
     return int(sc["alpha_ns"].shape[0])
+
+
+def cc_table(*, chunk, alpha, beta, gamma, reduce, max_bytes=TABLE6_MAX_BYTES) -> np.ndarray:
+    """One CC parameter table, int64 [6, 7]; each argument a scalar or 7 values."""
+    rows = [np.broadcast_to(np.asarray(x, np.int64), (7,)) for x in (max_bytes, chunk, alpha, beta, gamma, reduce)]
+    return np.stack(rows).astype(np.int64)
+
+
+def cc_table_from_bandwidths(alpha_ns, bw_intra_MBps, bw_inter_MBps, reduce_MBps) -> np.ndarray:
+    """The table holding exactly what a table-less scenario with these knobs uses:
+    Table 6 chunks, per-chunk times ceil(chunk * 1000 / bandwidth)."""
+    cdiv = lambda a, b: -(-a // b)
+    return cc_table(chunk=TABLE6_CHUNK, alpha=alpha_ns, beta=cdiv(TABLE6_CHUNK * 1000, bw_intra_MBps),
+                    gamma=cdiv(TABLE6_CHUNK * 1000, bw_inter_MBps), reduce=reduce_MBps)
+
+
+def draw_cc_tables(n: int, rng: np.random.Generator) -> np.ndarray:
+    """n seeded what-if tables, int64 [n, 6, 7]: Table 6 bands and chunks scaled by
+    1/2..2, alpha 2-20 us, per-chunk beta 20-400 ns and gamma 100-2000 ns (rising
+    with the chunk), reduce 100-400 GB/s."""
+    out = []
+    for _ in range(n):
+        scale = rng.integers(1, 5, 7) / 2.0
+        chunk = np.maximum(1, (TABLE6_CHUNK * scale).astype(np.int64))
+        out.append(cc_table(chunk=chunk, alpha=rng.integers(2_000, 20_001, 7),
+                            beta=np.sort(rng.integers(20, 401, 7)), gamma=np.sort(rng.integers(100, 2001, 7)),
+                            reduce=rng.integers(100_000, 400_001, 7)))
+    return np.stack(out) if out else np.zeros((0, 6, 7), np.int64)
