@@ -92,6 +92,8 @@ def main():
     ap.add_argument("--index", type=int, default=0, help="graph of config 5 (0-15)")
     ap.add_argument("--scenarios", type=int, default=0,
                     help="batch size drawn with the config's recipe (0 = the config's own)")
+    ap.add_argument("--forest", action="store_true",
+                    help="validator variant: slowdown factors predicted by a seeded 64-tree ensemble")
     ap.add_argument("--cc", choices=["echo", "tables", "alpha-beta"], default="echo",
                     help="collective cost model of every scenario: Eq. 2-5 from bandwidths, Eq. 2-5 from "
                          "seeded CC parameter tables, or the alpha-beta baseline")
@@ -157,8 +159,8 @@ def main():
                    "ranks": int(g["n_ranks"]), "levels": r["levels"], "load_s": round(r["load_s"], 2),
                    "cc_model": args.cc, "cc_cost_all_collectives_ms": r["cc_cost_all_ms"]},
         "kernels_ms": r["kernels_ms"],
-        "roofline": roofline(g, r, args, args.config if not (args.until_stable or args.prorate or args.cc != "echo")
-                             else None),
+        "roofline": roofline(g, r, args, args.config if not (args.until_stable or args.prorate or args.forest
+                                                             or args.cc != "echo") else None),
     }
     if "refinements" in r:
         line["config"]["refinements"] = r["refinements"]
@@ -169,9 +171,10 @@ def main():
 
 
 def validator_name(args):
-    if not (args.until_stable or args.prorate):
+    if not (args.until_stable or args.prorate or args.forest):
         return f"{args.refine} refinement(s)"
-    kind = " + ".join(x for x, on in (("until stable", args.until_stable), ("prorated", args.prorate)) if on)
+    kind = " + ".join(x for x, on in (("until stable", args.until_stable), ("prorated", args.prorate),
+                                      ("ensemble factors", args.forest)) if on)
     return f"validator {kind}, at most {args.refine} refinement(s)"
 
 
@@ -198,6 +201,9 @@ def time_compose(E, g, sc, args):
     G = E.Graph(g, 0)
     if args.cc == "tables":
         G.set_cc_tables(scenarios.draw_cc_tables(CC_TABLES, np.random.default_rng(99)))
+    if args.forest:
+        from workloads import slowdown_forest
+        G.set_forest(slowdown_forest.synthetic_forest(0))
     load_s = time.perf_counter() - t
     log(f"loaded: {G.n_levels} levels in {load_s:.1f} s")
     d_scen, n_scen = E.scenarios_to_device(sc, "cuda:0")
@@ -206,8 +212,8 @@ def time_compose(E, g, sc, args):
            "start": torch.empty((G.n_ops, n_scen), dtype=torch.int64, device=dev),
            "finish": torch.empty((G.n_ops, n_scen), dtype=torch.int64, device=dev)}
     G.set_timing(True)
-    variant = dict(until_stable=args.until_stable, prorate=args.prorate,
-                   refinements=args.until_stable or args.prorate)
+    variant = dict(until_stable=args.until_stable, prorate=args.prorate, forest=args.forest,
+                   refinements=args.until_stable or args.prorate or args.forest)
     for i in range(args.warmup):
         G.compose(d_scen, n_scen, args.refine, out=out, **variant)
         log(f"warmup {i}: {G.kernel_times()}")

@@ -258,12 +258,48 @@ int echo_compose_batch(echo_graph g, const echo_scenario *d_scen, int32_t n_scen
  *                 duration D - o + q16(o, F), o = the time of [start, finish)
  *                 covered by the union of the overlapping comm ops' intervals
  *                 on the previous timeline, capped at D; zero: q16(D, F)
+ *   forest        nonzero: F comes from the graph's tree ensemble
+ *                 (echo_set_forest) instead of the scenario's slowdown table
  */
 typedef struct {
     int32_t max_refine;
     int32_t until_stable;
     int32_t prorate;
+    int32_t forest;
 } echo_validator;
+
+/*
+ * Slowdown prediction by a gradient-boosted tree ensemble (Sec. 6: an
+ * XGBoost regressor over communication details and computation-kernel
+ * metrics, Table 4; trees at most 12 splits deep, Table 5).  For a compute op
+ * v overlapped by comm ops of collective type t, the feature vector is
+ *   x[0] kernel class   x[1] base duration d0 (ns; the profiled running time)
+ *   x[2] t              x[3] largest message S among the overlapping type-t ops
+ *   x[4] most members N among them (the N their cost uses)
+ *   x[5] the scenario's ar_algo   x[6] bw_intra_MBps   x[7] bw_inter_MBps
+ *   x[8..11] class_metrics[class][0..3] (kernel metrics of the class)
+ * and the prediction is base_q16 plus one leaf value per tree -- each tree
+ * walked from its root, left when x[feature] < threshold -- kept inside
+ * [65536, 2^20).  F(v) is the largest prediction over the collective types
+ * overlapping v.  Integer features, thresholds and leaves: bit-exact.
+ */
+typedef struct {
+    int32_t feature;    /* 0..11, or -1 for a leaf */
+    int32_t left, right;/* children: node indices */
+    int32_t value;      /* leaf: contribution to the factor (Q16) */
+    int64_t threshold;
+} echo_tree_node;
+#define ECHO_TREE_DEPTH 12
+
+/*
+ * Give the graph a tree ensemble (host arrays, copied): n_nodes nodes, the
+ * roots of n_trees trees, the base score (65536 <= base < 2^20) and
+ * class_metrics[8][4].  Every root-to-leaf path has at most ECHO_TREE_DEPTH
+ * splits.  n_trees = 0 removes the ensemble.  Errors: ARG (malformed trees or
+ * arrays), NOMEM, HIP.
+ */
+int echo_set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes, const int32_t *roots,
+                    int32_t n_trees, int32_t base_q16, const int64_t *class_metrics);
 
 /*
  * echo_compose_batch with validator options.  d_refinements (device, n_scen
@@ -273,7 +309,7 @@ typedef struct {
  * (no host synchronisation).  With prorate, the extra time of one op,
  * q16(o, F) - o, must stay below 2^32 - 1 ns (else ECHO_ERR_RANGE from
  * echo_sync_status).  Errors and ownership as echo_compose_batch; ARG for a
- * NULL options pointer or max_refine outside 0..64.
+ * NULL options pointer, max_refine outside 0..64 or forest without an ensemble.
  */
 int echo_compose_validated(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const echo_validator *opts,
                            int64_t *d_start, int64_t *d_finish, int64_t *d_step, uint64_t *d_digest,

@@ -50,7 +50,8 @@ def _load():
     i64, i32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
     lib.oracle_run.restype = ctypes.c_int
     lib.oracle_run.argtypes = [i64, i32, i32] + [P] * 8 + [i64, P, P, P, P, P, i32] + [P] * 8 \
-        + [P, P, i32, P] + [P] + [i32, i32, i32, i32] + [P] * 7 + [ctypes.c_char_p, i64]
+        + [P, P, i32, P] + [P] + [P, i64, P, i32, i32, P] + [i32, i32, i32, i32] + [P] * 7 \
+        + [ctypes.c_char_p, i64]
     lib.oracle_chunk_bytes.restype = i64
     lib.oracle_chunk_bytes.argtypes = [i64]
     lib.oracle_cc_time.restype = i64
@@ -65,6 +66,12 @@ def _load():
     return lib
 
 
+# One node of a tree ensemble (the oracle's tree_node_t): feature index (-1: leaf),
+# children, leaf value (Q16), threshold (left when x[feature] < threshold).
+TREE_NODE_DTYPE = np.dtype([("feature", "<i4"), ("left", "<i4"), ("right", "<i4"), ("value", "<i4"),
+                            ("threshold", "<i8")])
+
+
 def _c(a, dtype):
     return np.ascontiguousarray(a, dtype=dtype)
 
@@ -75,7 +82,7 @@ def _p(a):
 
 def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelines: bool = True,
         costs: bool = False, factors: bool = False, jitter_stream=None, until_stable: bool = False,
-        prorate: bool = False, cc_tables=None) -> dict:
+        prorate: bool = False, cc_tables=None, forest=None) -> dict:
     """Compose every scenario of `scen` on `graph`.
 
     Returns a dict with 'step' [n_scen] int64 and 'digest' [n_scen] uint64, plus
@@ -86,6 +93,9 @@ def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelin
     n_refine times); prorate: inflate only the overlapped part of a compute op.
     cc_tables: int64 [n_tables, 6, 7] CC parameter tables that scenarios name with
     cc_table = index + 1 (scenario fields cc_model / cc_table default to 0).
+    forest: a tree ensemble {'nodes': TREE_NODE_DTYPE array, 'roots': int32 [n_trees],
+    'base': Q16 base score, 'class_metrics': int64 [8, 4]} whose predictions replace
+    the scenario's slowdown table.
     jitter_stream defaults to the scenario's index in `scen`.
     Raises OracleError on invalid input or a deadlocked graph.
     """
@@ -123,6 +133,14 @@ def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelin
     ccm = _c(scen["cc_model"], np.uint8) if "cc_model" in scen else np.zeros(n, np.uint8)
     cct = _c(scen["cc_table"], np.int32) if "cc_table" in scen else np.zeros(n, np.int32)
     tables = np.zeros((0, 6, 7), np.int64) if cc_tables is None else _c(cc_tables, np.int64).reshape(-1, 6, 7)
+    if forest is not None:
+        f_nodes = np.ascontiguousarray(forest["nodes"], TREE_NODE_DTYPE)
+        f_roots = _c(forest["roots"], np.int32)
+        f_metrics = _c(forest["class_metrics"], np.int64).reshape(8, 4)
+        f_args = (_p(f_nodes), int(f_nodes.shape[0]), _p(f_roots), int(f_roots.shape[0]), int(forest["base"]),
+                  _p(f_metrics))
+    else:
+        f_args = (None, 0, None, 0, 0, None)
     slow = _c(scen["slowdown_q16"], np.uint32).reshape(n, 8, 4)
     out = {"step": np.zeros(n, np.int64), "digest": np.zeros(n, np.uint64),
            "refinements": np.zeros(n, np.int32)}
@@ -139,7 +157,7 @@ def run(graph: dict, scen: dict, n_refine: int = 1, *, threads: int = 1, timelin
         _p(op_rank), _p(op_stream), _p(op_kind), _p(op_class), _p(op_dur), _p(op_coll),
         _p(pred_off), _p(pred_idx), n_colls, _p(coll_type), _p(coll_bytes), *[_p(x) for x in given],
         n, _p(alpha), _p(bwa), _p(bwe), _p(red), _p(jseed), _p(jstream), _p(jamp), _p(algo), _p(ccm), _p(cct),
-        int(tables.shape[0]), _p(tables) if tables.shape[0] else None, _p(slow),
+        int(tables.shape[0]), _p(tables) if tables.shape[0] else None, _p(slow), *f_args,
         int(n_refine), int(bool(until_stable)), int(bool(prorate)), int(max(1, threads)),
         _p(out.get("start")), _p(out.get("finish")), _p(out["step"]), _p(out["digest"]),
         _p(out.get("cost")), _p(out.get("factor")), _p(out["refinements"]), err, 512)

@@ -87,6 +87,26 @@ typedef struct {
         reduce[CC_ROWS];
 } cc_table_t;
 
+/* A gradient-boosted tree ensemble predicting the slowdown factor (Sec. 6,
+   features after Table 4, trees of depth <= 12 after Table 5).  Node: feature
+   index (-1: leaf), children, leaf value (Q16 contribution), threshold (go
+   left when x[feature] < threshold). */
+#define NFEAT 12
+#define NMETRIC 4
+#define TREE_DEPTH 12
+typedef struct {
+    int32_t feature, left, right, value;
+    int64_t threshold;
+} tree_node_t;
+typedef struct {
+    const tree_node_t *nodes;
+    int64_t n_nodes;
+    const int32_t *roots;
+    int32_t n_trees;
+    int32_t base;                    /* base score (Q16) */
+    const int64_t *class_metrics;    /* [8 classes][NMETRIC] kernel metrics, features 8..11 */
+} forest_t;
+
 typedef struct {
     int64_t alpha, bw_intra, bw_inter, reduce;
     uint64_t jseed;
@@ -96,6 +116,7 @@ typedef struct {
     uint8_t cc_model;        /* 0: Eq. 2-5; 1: alpha-beta baseline */
     const cc_table_t *table; /* parameters of Eq. 2-5 from this table, or NULL: from bandwidths */
     const uint32_t *slow;    /* [8 classes][4 collective types] */
+    const forest_t *forest;  /* factors predicted by this ensemble instead of taken from slow */
 } scen_t;
 
 /* Structure derived once from the graph and shared by all scenarios. */
@@ -369,6 +390,40 @@ overflow:
 /* ------------------------------------------------------------------ */
 /* Sec. 6: overlap with communication -> slowdown factor per compute op */
 /* ------------------------------------------------------------------ */
+/* Factor predicted for a compute op from feature vector x: the base score plus one
+ * leaf value per tree, kept inside the factor range [65536, 2^20). */
+static uint32_t forest_predict(const forest_t *fo, const int64_t *x) {
+    int64_t sum = fo->base;
+    for (int32_t t = 0; t < fo->n_trees; t++) {
+        int32_t i = fo->roots[t];
+        while (fo->nodes[i].feature >= 0)
+            i = x[fo->nodes[i].feature] < fo->nodes[i].threshold ? fo->nodes[i].left : fo->nodes[i].right;
+        sum += fo->nodes[i].value;
+    }
+    if (sum < Q16_ONE) sum = Q16_ONE;
+    if (sum >= (1 << 20)) sum = (1 << 20) - 1;
+    return (uint32_t)sum;
+}
+
+/* Features of compute op v overlapped by comm ops of collective type t (after
+ * Table 4): kernel class, profiled running time (base duration, no jitter),
+ * collective type, largest message ("bucket size") and most members among the
+ * overlapping comm ops of that type, the scenario's all-reduce algorithm and
+ * bandwidths, and four per-class kernel metrics. */
+static void forest_features(const graph_t *g, const scen_t *sc, int64_t v, int t, int64_t smax, int64_t nmax,
+                            int64_t *x) {
+    const int cls = g->op_class[v];
+    x[0] = cls;
+    x[1] = g->op_dur[v];
+    x[2] = t;
+    x[3] = smax;
+    x[4] = nmax;
+    x[5] = sc->algo;
+    x[6] = sc->bw_intra;
+    x[7] = sc->bw_inter;
+    for (int k = 0; k < NMETRIC; k++) x[8 + k] = sc->forest->class_metrics[cls * NMETRIC + k];
+}
+
 static void overlap_factors(const graph_t *g, const derived_t *dv, const scen_t *sc,
                             const int64_t *s, const int64_t *f, uint32_t *F, int64_t *O, int64_t *lo_buf,
                             int64_t *hi_buf) {
@@ -380,6 +435,7 @@ static void overlap_factors(const graph_t *g, const derived_t *dv, const scen_t 
         const uint32_t *row = sc->slow + 4 * g->op_class[v];
         uint32_t best = Q16_ONE;
         int64_t n_iv = 0;           /* overlapping comm intervals, clipped to [sv, fv) */
+        int64_t smax[4] = {-1, -1, -1, -1}, nmax[4] = {0, 0, 0, 0};   /* per type, for the forest */
         for (int k = 0; k < NSTREAM; k++) {
             const int64_t lo0 = dv->cl_off[r * NSTREAM + k], hi0 = dv->cl_off[r * NSTREAM + k + 1];
             /* Comm ops of one stream are FIFO, so their finish times are sorted:
@@ -394,12 +450,27 @@ static void overlap_factors(const graph_t *g, const derived_t *dv, const scen_t 
                 if (s[c] >= fv) break;
                 const int64_t a = sv > s[c] ? sv : s[c], b = fv < f[c] ? fv : f[c];
                 if (a < b) {
-                    const uint32_t x = row[g->coll_type[g->op_coll[c]]];
+                    const int64_t cc = g->op_coll[c];
+                    const int ty = g->coll_type[cc];
+                    const uint32_t x = row[ty];
                     if (x > best) best = x;
+                    if (g->coll_bytes[cc] > smax[ty]) smax[ty] = g->coll_bytes[cc];
+                    if (dv->tN[cc] > nmax[ty]) nmax[ty] = dv->tN[cc];
                     lo_buf[n_iv] = a;
                     hi_buf[n_iv] = b;
                     n_iv++;
                 }
+            }
+        }
+        if (sc->forest) {
+            /* the ensemble's prediction for each overlapping collective type; the largest counts */
+            best = Q16_ONE;
+            for (int ty = 0; ty < 4; ty++) {
+                if (smax[ty] < 0) continue;
+                int64_t x[NFEAT];
+                forest_features(g, sc, v, ty, smax[ty], nmax[ty], x);
+                const uint32_t p = forest_predict(sc->forest, x);
+                if (p > best) best = p;
             }
         }
         F[v] = best;
@@ -676,6 +747,7 @@ typedef struct {
     int32_t n_tables;
     const cc_table_t *tables;
     const uint32_t *slow;
+    const forest_t *forest;
     int64_t *start, *finish, *step, *cost;
     uint64_t *digest;
     uint32_t *factor;
@@ -695,7 +767,7 @@ static int run_scenario(job_t *jb, int32_t si, work_t *w, int64_t *s, int64_t *f
     }
     scen_t sc = {jb->alpha[si], jb->bw_intra[si], jb->bw_inter[si], jb->reduce[si], jb->jseed[si],
                  jb->jstream[si], jb->jamp[si], jb->algo[si], jb->cc_model ? jb->cc_model[si] : 0,
-                 tsel > 0 ? jb->tables + (tsel - 1) : NULL, jb->slow + (int64_t)si * NCLASS * 4};
+                 tsel > 0 ? jb->tables + (tsel - 1) : NULL, jb->slow + (int64_t)si * NCLASS * 4, jb->forest};
     int rc = check_scen(&sc, jb->msg, sizeof jb->msg);
     if (rc) return rc;
     /* CC estimator */
@@ -803,7 +875,9 @@ int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int3
                const int64_t *bw_intra, const int64_t *bw_inter, const int64_t *reduce,
                const uint64_t *jseed, const uint32_t *jstream, const int32_t *jamp,
                const uint8_t *algo, const uint8_t *cc_model, const int32_t *cc_table, int32_t n_tables,
-               const int64_t *tables, const uint32_t *slow, int32_t n_refine, int32_t until_stable,
+               const int64_t *tables, const uint32_t *slow, const void *forest_nodes, int64_t n_nodes,
+               const int32_t *forest_roots, int32_t n_trees, int32_t forest_base, const int64_t *class_metrics,
+               int32_t n_refine, int32_t until_stable,
                int32_t prorate, int32_t n_threads, int64_t *start, int64_t *finish, int64_t *step,
                uint64_t *digest, int64_t *cost, uint32_t *factor, int32_t *refinements, char *err,
                int64_t errlen) {
@@ -839,6 +913,39 @@ int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int3
                 return E_RANGE;
             }
         }
+    /* the ensemble, if any: every tree at most TREE_DEPTH splits deep, indices in range */
+    forest_t fo = {(const tree_node_t *)forest_nodes, n_nodes, forest_roots, n_trees, forest_base, class_metrics};
+    if (n_trees > 0) {
+        if (!forest_nodes || !forest_roots || !class_metrics || n_nodes < 1 || forest_base < Q16_ONE
+            || forest_base >= (1 << 20)) {
+            set_err(err, errlen, "bad forest (%lld trees, %lld nodes)", n_trees, n_nodes);
+            return E_ARG;
+        }
+        int64_t stack_node[TREE_DEPTH + 2], stack_depth[TREE_DEPTH + 2];
+        for (int32_t t = 0; t < n_trees; t++) {
+            if (forest_roots[t] < 0 || forest_roots[t] >= n_nodes) {
+                set_err(err, errlen, "tree %lld: root %lld out of range", t, forest_roots[t]);
+                return E_ARG;
+            }
+            int sp = 0;
+            stack_node[sp] = forest_roots[t];
+            stack_depth[sp++] = 0;
+            while (sp > 0) {
+                const int64_t i = stack_node[--sp], dep = stack_depth[sp];
+                const tree_node_t *nd = fo.nodes + i;
+                if (nd->feature < 0) continue;
+                if (dep >= TREE_DEPTH || nd->feature >= NFEAT || nd->left < 0 || nd->left >= n_nodes
+                    || nd->right < 0 || nd->right >= n_nodes) {
+                    set_err(err, errlen, "tree %lld: node %lld is malformed or too deep", t, i);
+                    return E_ARG;
+                }
+                stack_node[sp] = nd->left;
+                stack_depth[sp++] = dep + 1;
+                stack_node[sp] = nd->right;
+                stack_depth[sp++] = dep + 1;
+            }
+        }
+    }
     derived_t dv;
     rc = derive(&g, &dv, err, errlen);
     if (rc) return rc;
@@ -853,7 +960,8 @@ int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int3
     for (int32_t t = 0; t < n_threads; t++) {
         jobs[t] = (job_t){&g, &dv, n_scen, n_refine, n_threads, t, until_stable != 0, prorate != 0, alpha,
                           bw_intra, bw_inter, reduce, jseed, jstream, jamp, algo, cc_model, cc_table, n_tables, tb,
-                          slow, start, finish, step, cost, digest, factor, refinements, OK, {0}};
+                          slow, n_trees > 0 ? &fo : NULL, start, finish, step, cost, digest, factor, refinements,
+                          OK, {0}};
     }
     for (int32_t t = 1; t < n_threads; t++) pthread_create(&th[t], NULL, worker, &jobs[t]);
     worker(&jobs[0]);
@@ -877,7 +985,7 @@ int64_t oracle_cc_time(int32_t type, int64_t S, int64_t N, int64_t M, int64_t K,
     uint32_t slow[32];
     for (int i = 0; i < 32; i++) slow[i] = Q16_ONE;
     scen_t sc = {alpha, bw_intra, bw_inter, reduce, 0, 0, 0, (uint8_t)algo, (uint8_t)cc_model,
-                 (const cc_table_t *)table, slow};
+                 (const cc_table_t *)table, slow, NULL};
     return cc_time(type, S, N, M, K, &sc);
 }
 uint64_t oracle_splitmix64_at(uint64_t seed, uint64_t k) { return splitmix64_at(seed, k); }

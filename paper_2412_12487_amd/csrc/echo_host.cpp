@@ -141,6 +141,9 @@ void free_graph(echo_graph g) {
     (void)hipFree(g->count);
     (void)hipFree(g->tmask);
     (void)hipFree(g->dg.cc_tables);
+    (void)hipFree(g->dg.forest_nodes);
+    (void)hipFree(g->dg.forest_roots);
+    (void)hipFree(g->dg.class_metrics);
     (void)hipFree(g->ext);
     (void)hipFree(g->chg);
     (void)hipFree(g->tmp_start);
@@ -651,7 +654,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
         cl_off[k + 1] += cl_off[k];
         cp_off[k + 1] += cp_off[k];
     }
-    std::vector<int32_t> cl(cl_off.back());
+    std::vector<int32_t> cl(cl_off.back()), cl_coll(cl_off.back());
     std::vector<uint8_t> cl_type(cl_off.back());
     std::vector<ComputeRec> cp(cp_off.back());
     {
@@ -663,6 +666,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
             prev_on_stream[k] = (int32_t)v;
             if (d->op_kind[v] == ECHO_COMM) {
                 cl_type[fl[k]] = d->coll_type[d->op_coll[v]];
+                cl_coll[fl[k]] = (int32_t)d->op_coll[v];
                 cl[fl[k]++] = (int32_t)v;
             } else if (d->op_kind[v] == ECHO_COMPUTE) {
                 // chained: the only predecessor is the previous op of the stream, a compute op
@@ -729,6 +733,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     UP(dg.cl_off, cl_off);
     UP(dg.cl, cl);
     UP(dg.cl_type, cl_type);
+    UP(dg.cl_coll, cl_coll);
     UP(dg.cp_off, cp_off);
     UP(dg.cp, cp);
     UP(dg.status, std::vector<unsigned>(1, 0u));
@@ -743,6 +748,9 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
     const int32_t n_refine = val.max_refine;
     const bool until_stable = val.until_stable != 0 && n_refine > 0;
     const bool prorate = val.prorate != 0 && n_refine > 0;
+    const bool forest = val.forest != 0 && n_refine > 0;
+    const bool ext = prorate || forest;             // refined passes add per-op extra times
+    if (forest && g->dg.n_trees == 0) return fail(ECHO_ERR_ARG, "forest factors requested, but the graph has no ensemble");
     if (n_scen < 1 || n_refine < 0 || n_refine > 64)
         return fail(ECHO_ERR_ARG, "n_scen must be >= 1 and 0 <= n_refine <= 64 (got %d, %d)", n_scen, n_refine);
     hipError_t e = hipSetDevice(g->device);
@@ -754,9 +762,9 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
     if ((rc = ensure(&g->class_cost, &g->class_cost_n, (size_t)(g->dg.classes.n * ns), "class cost"))) return rc;
     if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->n_colls * ns), "arrivals"))) return rc;
     if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * n_tiles), "arrival counts"))) return rc;
-    if (n_refine > 0 && !prorate && (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(g->n_ops * ns), "overlap masks")))
+    if (n_refine > 0 && !ext && (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(g->n_ops * ns), "overlap masks")))
         return rc;
-    if (prorate && (rc = ensure(&g->ext, &g->ext_n, (size_t)(g->n_ops * ns), "prorated extra times"))) return rc;
+    if (ext && (rc = ensure(&g->ext, &g->ext_n, (size_t)(g->n_ops * ns), "extra times"))) return rc;
     if (until_stable && (rc = ensure(&g->chg, &g->chg_n, (size_t)(ns + 1), "change flags"))) return rc;
     unsigned *stable = until_stable ? g->chg + ns : nullptr;
     if (!d_start && (rc = ensure(&g->tmp_start, &g->tmp_start_n, (size_t)(g->n_ops * ns), "start"))) return rc;
@@ -790,12 +798,37 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
 
     for (int32_t p = 0; p <= n_refine; ++p) {
         // tiles per walk launch: every rank block of a tile must be co-resident
-        const int64_t cap = g->capacity[walk_variant(p > 0, p == n_refine, d_digest != nullptr, prorate)];
+        const int64_t cap = g->capacity[walk_variant(p > 0, p == n_refine, d_digest != nullptr, ext)];
         const int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, cap / g->dg.n_blocks));
         if (p > 0) {
-            OverlapArgs o{g->dg.cl_off, g->dg.cp_off, g->dg.cl, g->dg.cl_type, g->dg.cp,
-                          d_scen, start, finish, prorate ? nullptr : g->tmask, prorate ? g->ext : nullptr,
-                          until_stable ? g->chg : nullptr, stable, n_scen, n_tiles, p > 1, g->dg.status};
+            OverlapArgs o{};
+            o.cl_off = g->dg.cl_off;
+            o.cp_off = g->dg.cp_off;
+            o.cl = g->dg.cl;
+            o.cl_type = g->dg.cl_type;
+            o.cp = g->dg.cp;
+            o.scen = d_scen;
+            o.start = start;
+            o.finish = finish;
+            o.tmask = ext ? nullptr : g->tmask;
+            o.ext = ext ? g->ext : nullptr;
+            o.chg = until_stable ? g->chg : nullptr;
+            o.stable = stable;
+            if (forest) {
+                o.cl_coll = g->dg.cl_coll;
+                o.coll_bytes = g->dg.colls.bytes;
+                o.coll_N = g->dg.colls.N;
+                o.forest_nodes = g->dg.forest_nodes;
+                o.forest_roots = g->dg.forest_roots;
+                o.class_metrics = g->dg.class_metrics;
+                o.n_trees = g->dg.n_trees;
+                o.forest_base = g->dg.forest_base;
+            }
+            o.prorate = prorate;
+            o.n_scen = n_scen;
+            o.n_tiles = n_tiles;
+            o.prev_refined = p > 1;
+            o.status = g->dg.status;
             TIMED(ECHO_K_OVERLAP, launch_overlap(o, g->n_ranks, stream), "overlap kernel");
             if (until_stable && (e = launch_settle(g->chg, n_scen, d_refinements, stable, stream)))
                 return hip_fail(e, "settle kernel");
@@ -811,8 +844,8 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
             a.scen = d_scen;
             a.cost = g->cost;
             a.class_cost = g->class_cost;
-            a.tmask = p > 0 && !prorate ? g->tmask : nullptr;
-            a.ext = p > 0 && prorate ? g->ext : nullptr;
+            a.tmask = p > 0 && !ext ? g->tmask : nullptr;
+            a.ext = p > 0 && ext ? g->ext : nullptr;
             a.stable = p < n_refine ? stable : nullptr;     // the final pass always runs
             a.start = start;
             a.finish = finish;
@@ -942,6 +975,55 @@ int echo_set_cc_tables(echo_graph g, const echo_cc_table *tables, int32_t n_tabl
     (void)hipFree(g->dg.cc_tables);
     g->dg.cc_tables = d;
     g->dg.n_cc_tables = n_tables;
+    return ECHO_OK;
+}
+
+int echo_set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes, const int32_t *roots,
+                    int32_t n_trees, int32_t base_q16, const int64_t *class_metrics) {
+    g_last_error.clear();
+    if (!g) return fail(ECHO_ERR_ARG, "null graph");
+    if (n_trees < 0) return fail(ECHO_ERR_ARG, "n_trees %d < 0", n_trees);
+    if (n_trees > 0) {
+        if (!nodes || !roots || !class_metrics || n_nodes < 1 || n_nodes > kI32Max)
+            return fail(ECHO_ERR_ARG, "null or empty ensemble arrays");
+        if (base_q16 < 65536 || base_q16 >= (1 << 20)) return fail(ECHO_ERR_ARG, "base %d outside [65536, 2^20)", base_q16);
+        // every path at most ECHO_TREE_DEPTH splits, indices and features in range
+        std::vector<std::pair<int32_t, int32_t>> stack;
+        for (int32_t t = 0; t < n_trees; ++t) {
+            if (roots[t] < 0 || roots[t] >= n_nodes) return fail(ECHO_ERR_ARG, "tree %d: root out of range", t);
+            stack.assign(1, {roots[t], 0});
+            while (!stack.empty()) {
+                const auto [i, depth] = stack.back();
+                stack.pop_back();
+                const echo_tree_node &nd = nodes[i];
+                if (nd.feature < 0) continue;
+                if (depth >= ECHO_TREE_DEPTH || nd.feature >= 12 || nd.left < 0 || nd.left >= n_nodes || nd.right < 0 ||
+                    nd.right >= n_nodes)
+                    return fail(ECHO_ERR_ARG, "tree %d: node %d is malformed or deeper than %d", t, i, ECHO_TREE_DEPTH);
+                stack.push_back({nd.left, depth + 1});
+                stack.push_back({nd.right, depth + 1});
+            }
+        }
+    }
+    hipError_t e = hipSetDevice(g->device);
+    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+    (void)hipDeviceSynchronize();                  // composes already enqueued may read the old ensemble
+    (void)hipFree(g->dg.forest_nodes);
+    (void)hipFree(g->dg.forest_roots);
+    (void)hipFree(g->dg.class_metrics);
+    g->dg.forest_nodes = nullptr;
+    g->dg.forest_roots = nullptr;
+    g->dg.class_metrics = nullptr;
+    g->dg.n_trees = 0;
+    if (n_trees == 0) return ECHO_OK;
+    std::vector<echo_tree_node> hn(nodes, nodes + n_nodes);
+    std::vector<int32_t> hr(roots, roots + n_trees);
+    std::vector<int64_t> hm(class_metrics, class_metrics + kClasses * kClassMetrics);
+    if ((e = upload(&g->dg.forest_nodes, hn)) || (e = upload(&g->dg.forest_roots, hr)) ||
+        (e = upload(&g->dg.class_metrics, hm)))
+        return fail(e == hipErrorOutOfMemory ? ECHO_ERR_NOMEM : ECHO_ERR_HIP, "ensemble upload: %s", hipGetErrorString(e));
+    g->dg.n_trees = n_trees;
+    g->dg.forest_base = base_q16;
     return ECHO_OK;
 }
 

@@ -137,7 +137,15 @@ struct DeviceGraph {
     unsigned *status = nullptr;      // device status word
     echo_cc_table *cc_tables = nullptr;   // CC parameter tables (echo_set_cc_tables)
     int32_t n_cc_tables = 0;
+    int32_t *cl_coll = nullptr;      // collective of each listed comm op (parallel to cl)
+    // slowdown ensemble (echo_set_forest)
+    echo_tree_node *forest_nodes = nullptr;
+    int32_t *forest_roots = nullptr;
+    int64_t *class_metrics = nullptr;  // [8][4]
+    int32_t n_trees = 0, forest_base = 65536;
 };
+
+constexpr int kClassMetrics = 4;
 
 struct WalkArgs {
     const WalkItem *items;
@@ -177,6 +185,15 @@ struct OverlapArgs {
     uint32_t *ext;                   // prorating: in/out like tmask, the extra time q16(o, F) - o
     unsigned *chg;                   // non-null: [scen] set when some duration changes
     const unsigned *stable;          // non-null: skip when *stable
+    // ensemble factors (forest_nodes non-null): features of the overlapping comm ops
+    const int32_t *cl_coll;
+    const int64_t *coll_bytes;       // S of each collective
+    const int32_t *coll_N;           // N its cost uses
+    const echo_tree_node *forest_nodes;
+    const int32_t *forest_roots;
+    const int64_t *class_metrics;
+    int32_t n_trees, forest_base;
+    int32_t prorate;                 // inflate only the overlapped part (extra times in ext)
     int32_t n_scen, n_tiles;
     int32_t prev_refined;            // the previous pass inflated its compute ops
     unsigned *status;

@@ -550,12 +550,77 @@ __device__ __forceinline__ uint32_t factor_of(uint32_t m, const uint32_t *slow, 
     return F;
 }
 
+// Factor predicted by the tree ensemble for a compute op (class cls, base
+// duration d0) overlapped by the collective types in mask m (Sec. 6): for each
+// type, the base score plus one leaf per tree, kept inside [65536, 2^20); the
+// largest over the types.  Trees are walked per lane from global memory (the
+// walk stops at a leaf; paths are at most ECHO_TREE_DEPTH splits long).
+constexpr int kForestLanes = 8;
+
+// feat: this wavefront's LDS feature rows, feature k of lane l at feat[k * 64 + l].
+__device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_t *smax, const int32_t *nmax,
+                                  int cls, int64_t d0, const echo_scenario *sc, int64_t *feat, int lane) {
+    const int64_t *met = a.class_metrics + cls * kClassMetrics;
+    feat[0 * kLanes + lane] = cls;
+    feat[1 * kLanes + lane] = d0;
+    feat[5 * kLanes + lane] = sc->ar_algo;
+    feat[6 * kLanes + lane] = sc->bw_intra_MBps;
+    feat[7 * kLanes + lane] = sc->bw_inter_MBps;
+#pragma unroll
+    for (int k = 0; k < kClassMetrics; ++k) feat[(8 + k) * kLanes + lane] = met[k];
+    uint32_t best = 65536u;
+#pragma unroll
+    for (int t = 0; t < kTypes; ++t) {
+        if (!((m >> t) & 1u)) continue;
+        feat[2 * kLanes + lane] = t;
+        feat[3 * kLanes + lane] = smax[t];
+        feat[4 * kLanes + lane] = nmax[t];
+        int64_t sum = a.forest_base;
+        // kForestLanes trees walked side by side: their node loads are independent
+        for (int32_t tr0 = 0; tr0 < a.n_trees; tr0 += kForestLanes) {
+            int32_t idx[kForestLanes];
+            bool live[kForestLanes];
+#pragma unroll
+            for (int q = 0; q < kForestLanes; ++q) {
+                live[q] = tr0 + q < a.n_trees;
+                idx[q] = live[q] ? a.forest_roots[tr0 + q] : 0;
+            }
+            for (int step = 0; step <= ECHO_TREE_DEPTH; ++step) {
+                echo_tree_node nd[kForestLanes];
+#pragma unroll
+                for (int q = 0; q < kForestLanes; ++q) nd[q] = a.forest_nodes[idx[q]];
+                bool more = false;
+#pragma unroll
+                for (int q = 0; q < kForestLanes; ++q) {
+                    if (!live[q] || nd[q].feature < 0) continue;
+                    const int64_t x = feat[nd[q].feature * kLanes + lane];
+                    idx[q] = x < nd[q].threshold ? nd[q].left : nd[q].right;
+                    more = true;
+                }
+                if (!more) {
+#pragma unroll
+                    for (int q = 0; q < kForestLanes; ++q)
+                        if (live[q]) sum += nd[q].value;
+                    break;
+                }
+            }
+        }
+        sum = sum < 65536 ? 65536 : sum;
+        sum = sum >= (int64_t(1) << 20) ? (int64_t(1) << 20) - 1 : sum;
+        best = (uint32_t)sum > best ? (uint32_t)sum : best;
+    }
+    return best;
+}
+
 // PRORATE: also measure o, the part of [s_v, f_v) covered by the union of the
 // overlapping comm intervals (a merge of the per-stream interval lists in start
 // order), and record the extra time q16(min(o, D), F) - min(o, D) instead of a mask.
 // DETECT: flag the scenarios whose durations change (fixed-point iteration).
-template <bool PRORATE, bool DETECT>
+// FOREST: the factor is the tree ensemble's prediction (recorded as an extra time).
+template <bool PRORATE, bool DETECT, bool FOREST>
 __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
+    constexpr bool EXT = PRORATE || FOREST;      // output: extra time per op instead of a mask
+    __shared__ int64_t feat[FOREST ? 12 * kLanes : 1];   // the ensemble's feature vectors, one per lane
     if (a.stable && __builtin_amdgcn_readfirstlane(__hip_atomic_load(a.stable, __ATOMIC_RELAXED,
                                                                       __HIP_MEMORY_SCOPE_AGENT)))
         return;                                  // every scenario is at its fixed point
@@ -645,7 +710,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 int64_t d = D;                   // the duration v ran with in the previous pass
                 uint32_t m_old = 0, e_old = 0;
                 if (a.prev_refined) {
-                    if (PRORATE) {
+                    if (EXT) {
                         e_old = (ebase + v * ns)[col];
                         __builtin_amdgcn_s_waitcnt(kWaitVm0);
                         d = D + e_old;
@@ -663,6 +728,24 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                     if (k < ncs) busy |= cs[k] < fv;
                 uint32_t m = 0;                            // types of the comm ops overlapping v
                 int64_t o = 0;                             // covered length (PRORATE)
+                int64_t smax[kTypes];                      // FOREST: largest S per overlapping type
+                int32_t nmax[kTypes];                      //         and most members
+    #pragma unroll
+                for (int tt = 0; tt < kTypes; ++tt) {
+                    smax[tt] = 0;
+                    nmax[tt] = 0;
+                }
+// note the comm op at list position x_ (type ty_) among v's overlaps, for the ensemble's features
+#define NOTE_FOREST(x_, ty_)                                                                     \
+    if (FOREST) {                                                                                \
+        const int32_t cc_ = a.cl_coll[x_];                                                       \
+        const int64_t S_ = a.coll_bytes[cc_];                                                    \
+        const int32_t N_ = a.coll_N[cc_];                                                        \
+        _Pragma("unroll") for (int tt = 0; tt < kTypes; ++tt) if (tt == (int)(ty_)) {            \
+            smax[tt] = S_ > smax[tt] ? S_ : smax[tt];                                            \
+            nmax[tt] = N_ > nmax[tt] ? N_ : nmax[tt];                                            \
+        }                                                                                        \
+    }
                 if (busy) {
     #pragma unroll
                     for (int k = 0; k < kStreams; ++k) {
@@ -684,7 +767,11 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                         int64_t qs = cs[k], qf = cf[k];
                         while (qs < fv) {
                             const int64_t lo = sv > qs ? sv : qs, hi = fv < qf ? fv : qf;
-                            if (lo < hi) m |= 1u << a.cl_type[kb[k] + q];
+                            if (lo < hi) {
+                                const uint32_t ty = a.cl_type[kb[k] + q];
+                                m |= 1u << ty;
+                                NOTE_FOREST(kb[k] + q, ty)
+                            }
                             if (qf >= fv) break;           // the next one starts after v ends
                             if (++q >= nk[k]) break;
                             const int64_t c = a.cl[kb[k] + q];
@@ -719,7 +806,9 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                                 if (k != bk) continue;
                                 const int64_t lo = sv > qs[k] ? sv : qs[k], hi = fv < qf[k] ? fv : qf[k];
                                 if (lo < hi) {
-                                    m |= 1u << a.cl_type[kb[k] + q[k]];
+                                    const uint32_t ty = a.cl_type[kb[k] + q[k]];
+                                    m |= 1u << ty;
+                                    NOTE_FOREST(kb[k] + q[k], ty)
                                     const int64_t from = lo > t ? lo : t;
                                     if (hi > from) {
                                         o += hi - from;
@@ -739,11 +828,14 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                     }
                     __builtin_amdgcn_s_waitcnt(kWaitVm0);
                 }
-                if (PRORATE) {
+#undef NOTE_FOREST
+                if (EXT) {
                     uint32_t e = 0;
                     if (m != 0) {
-                        const int64_t oc = o < D ? o : D;
-                        const int64_t x = q16(oc, factor_of(m, slow, cls)) - oc;
+                        const uint32_t F = FOREST ? forest_factor(a, m, smax, nmax, cls, d0, sc, feat, lane)
+                                                  : factor_of(m, slow, cls);
+                        const int64_t oc = PRORATE ? (o < D ? o : D) : D;
+                        const int64_t x = q16(oc, F) - oc;
                         ext_over |= x >= (int64_t)kExtLimit;
                         e = x >= (int64_t)kExtLimit ? kExtLimit : (uint32_t)x;
                     }
@@ -828,10 +920,17 @@ hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream) 
 
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
     const dim3 grid((unsigned)(n_ranks * a.n_tiles)), block(kLanes);
-    if (a.ext && a.chg) hipLaunchKernelGGL((k_overlap<true, true>), grid, block, 0, stream, a);
-    else if (a.ext) hipLaunchKernelGGL((k_overlap<true, false>), grid, block, 0, stream, a);
-    else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((k_overlap<false, false>), grid, block, 0, stream, a);
+    // a.ext: extra-time output (prorating and/or ensemble factors); a.forest_nodes: ensemble
+    const bool forest = a.forest_nodes != nullptr, prorate = a.prorate != 0;
+    if (forest) {
+        if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, true>), grid, block, 0, stream, a);
+        else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, true>), grid, block, 0, stream, a);
+        else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, true>), grid, block, 0, stream, a);
+        else hipLaunchKernelGGL((k_overlap<false, false, true>), grid, block, 0, stream, a);
+    } else if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, false>), grid, block, 0, stream, a);
+    else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, false>), grid, block, 0, stream, a);
+    else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, false>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((k_overlap<false, false, false>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 

@@ -21,7 +21,7 @@ ECHO_ERR_CYCLE, ECHO_ERR_NOMEM, ECHO_ERR_HIP, ECHO_ERR_DEVICE = -4, -5, -6, -7
 ERROR_NAMES = {0: "OK", -1: "ARG", -2: "RANGE", -3: "MATCH", -4: "CYCLE", -5: "NOMEM", -6: "HIP",
                -7: "DEVICE"}
 EXPORTS = ("echo_load_graph", "echo_load_graph_ex", "echo_graph_info", "echo_free_graph", "echo_cc_cost",
-           "echo_compose_batch", "echo_compose_validated", "echo_set_cc_tables", "echo_sync_status", "echo_set_timing", "echo_kernel_times",
+           "echo_compose_batch", "echo_compose_validated", "echo_set_cc_tables", "echo_set_forest", "echo_sync_status", "echo_set_timing", "echo_kernel_times",
            "echo_last_error")
 KERNEL_KINDS = {0: "init", 1: "cc_cost", 2: "walk", 3: "overlap", 4: "clear"}
 
@@ -55,7 +55,13 @@ class _Desc(ctypes.Structure):
 
 
 class _Validator(ctypes.Structure):
-    _fields_ = [("max_refine", ctypes.c_int32), ("until_stable", ctypes.c_int32), ("prorate", ctypes.c_int32)]
+    _fields_ = [("max_refine", ctypes.c_int32), ("until_stable", ctypes.c_int32), ("prorate", ctypes.c_int32),
+                ("forest", ctypes.c_int32)]
+
+
+# echo_tree_node: feature (-1 leaf), left, right, value (Q16), threshold (left when x < threshold)
+TREE_NODE_DTYPE = np.dtype([("feature", "<i4"), ("left", "<i4"), ("right", "<i4"), ("value", "<i4"),
+                            ("threshold", "<i8")])
 
 
 _lib = None
@@ -86,6 +92,8 @@ def lib():
     L.echo_compose_validated.restype = ctypes.c_int
     L.echo_set_cc_tables.argtypes = [P, P, i32]
     L.echo_set_cc_tables.restype = ctypes.c_int
+    L.echo_set_forest.argtypes = [P, P, i64, P, i32, i32, P]
+    L.echo_set_forest.restype = ctypes.c_int
     L.echo_sync_status.argtypes = [P, P]
     L.echo_sync_status.restype = ctypes.c_int
     L.echo_set_timing.argtypes = [P, ctypes.c_int]
@@ -205,7 +213,7 @@ class Graph:
         return out
 
     def compose(self, d_scen, n_scen, n_refine=1, *, timelines=True, digest=False, out=None, check=True,
-                until_stable=False, prorate=False, refinements=False):
+                until_stable=False, prorate=False, forest=False, refinements=False):
         """Compose all scenarios.  Returns dict of torch tensors: 'step' [n_scen],
         optional 'start'/'finish' [n_ops, n_scen], 'digest' [n_scen] (uint64 bits
         in an int64 tensor) and 'refinements' [n_scen] int32.  `out` may supply
@@ -229,8 +237,8 @@ class Graph:
         none = ctypes.c_void_p(None)
         start, finish = (p("start"), p("finish")) if timelines else (none, none)
         dig = p("digest") if digest else none
-        if until_stable or prorate or refinements:
-            opts = _Validator(int(n_refine), int(bool(until_stable)), int(bool(prorate)))
+        if until_stable or prorate or forest or refinements:
+            opts = _Validator(int(n_refine), int(bool(until_stable)), int(bool(prorate)), int(bool(forest)))
             _check(lib().echo_compose_validated(self.handle, ctypes.c_void_p(d_scen.data_ptr()), int(n_scen),
                                                 ctypes.byref(opts), start, finish, p("step"), dig,
                                                 p("refinements") if refinements else none, _stream_ptr(dev)))
@@ -248,6 +256,20 @@ class Graph:
             else np.zeros((0, 6, CC_ROWS), np.int64)
         _check(lib().echo_set_cc_tables(self.handle, t.ctypes.data_as(ctypes.c_void_p) if len(t) else None,
                                         int(t.shape[0])))
+
+    def set_forest(self, forest):
+        """Slowdown ensemble: {'nodes': TREE_NODE_DTYPE array, 'roots': int32 [n_trees],
+        'base': Q16 base score, 'class_metrics': int64 [8, 4]}, or None to remove it."""
+        L = lib()
+        if forest is None:
+            _check(L.echo_set_forest(self.handle, None, 0, None, 0, 65536, None))
+            return
+        nodes = np.ascontiguousarray(forest["nodes"], TREE_NODE_DTYPE)
+        roots = np.ascontiguousarray(forest["roots"], np.int32)
+        met = np.ascontiguousarray(forest["class_metrics"], np.int64).reshape(8, 4)
+        ptr = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+        _check(L.echo_set_forest(self.handle, ptr(nodes), int(nodes.shape[0]), ptr(roots), int(roots.shape[0]),
+                                 int(forest["base"]), ptr(met)))
 
     def set_timing(self, enable=True):
         _check(lib().echo_set_timing(self.handle, int(bool(enable))))

@@ -98,7 +98,47 @@ def covered(g, s, f, v):
     return sum(1 for t in range(int(s[v]), int(f[v])) if any(s[c] <= t < f[c] for c in comm))
 
 
-def compose_variants(g, base, cost, slowdown, n_refine, *, until_stable=False, prorate=False):
+def forest_predict(forest, x):
+    """Walk every tree from its root (left when x[feature] < threshold), add the leaves
+    to the base score, keep the sum inside [65536, 2^20)."""
+    nodes = forest["nodes"]
+    total = int(forest["base"])
+    for root in forest["roots"]:
+        i = int(root)
+        while nodes[i]["feature"] >= 0:
+            i = int(nodes[i]["left"] if x[nodes[i]["feature"]] < nodes[i]["threshold"] else nodes[i]["right"])
+        total += int(nodes[i]["value"])
+    return min(max(total, 65536), (1 << 20) - 1)
+
+
+def factors_forest(g, s, f, forest, knobs):
+    """Ensemble factors by checking every (compute, comm) pair of a rank: per collective
+    type overlapping v, the largest message and member count, then the largest prediction.
+    knobs: (ar_algo, bw_intra, bw_inter)."""
+    n = len(g["op_rank"])
+    coll, ctype = g["op_coll"], g["coll_type"]
+    members = np.bincount(coll[g["op_kind"] == COMM], minlength=len(ctype)) if len(ctype) else np.zeros(0, np.int64)
+    if g.get("coll_N") is not None:
+        members = np.asarray(g["coll_N"])
+    F = np.full(n, 65536, np.int64)
+    for v in range(n):
+        if g["op_kind"][v] != COMPUTE:
+            continue
+        smax, nmax = {}, {}
+        for c in range(n):
+            if g["op_kind"][c] == COMM and g["op_rank"][c] == g["op_rank"][v] and max(s[v], s[c]) < min(f[v], f[c]):
+                t = int(ctype[coll[c]])
+                smax[t] = max(smax.get(t, -1), int(g["coll_bytes"][coll[c]]))
+                nmax[t] = max(nmax.get(t, 0), int(members[coll[c]]))
+        cls = int(g["op_class"][v])
+        for t in smax:
+            x = [cls, int(g["op_dur"][v]), t, smax[t], nmax[t], *knobs] + [int(m) for m in forest["class_metrics"][cls]]
+            F[v] = max(F[v], forest_predict(forest, x))
+    return F
+
+
+def compose_variants(g, base, cost, slowdown, n_refine, *, until_stable=False, prorate=False, forest=None,
+                     knobs=(0, 400000, 50000)):
     """Validator variants: refine at most n_refine times, stopping early (until_stable) when
     a refinement would change no duration; prorate inflates only the covered part of a
     compute op (the covered time of the previous timeline, capped at the base duration).
@@ -109,7 +149,7 @@ def compose_variants(g, base, cost, slowdown, n_refine, *, until_stable=False, p
     s, f = compose(g, d, cost)
     done = 0
     for _ in range(n_refine):
-        F = factors(g, s, f, slowdown)
+        F = factors(g, s, f, slowdown) if forest is None else factors_forest(g, s, f, forest, knobs)
         new = d.copy()
         for v in range(n):
             if g["op_kind"][v] != COMPUTE:

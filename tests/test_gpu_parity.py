@@ -547,3 +547,92 @@ def test_cc_table_errors_reported(E):
         G.compose(d, n, 1)
     assert x.value.code == E.ECHO_ERR_RANGE
     G.close()
+
+
+# ---------------------------------------------------------------- tree-ensemble slowdown
+from workloads import slowdown_forest   # noqa: E402
+
+
+@pytest.mark.parametrize("until_stable,prorate", [(False, False), (True, False), (False, True)])
+@pytest.mark.parametrize("seed", range(6))
+def test_forest_random_graphs(E, seed, until_stable, prorate):
+    rng = np.random.default_rng(4000 + seed)
+    g = _random_graph(rng, int(rng.integers(2, 14)), int(rng.integers(10, 60)), int(rng.integers(3, 30)))
+    sc = scenarios.draw([1, 64, 70, 130][seed % 4], rng, bw_inter=(20000, 400000), bw_intra=(50000, 400000),
+                        alpha=(0, 20000), ar_algo_random=True, jitter=(4000, seed) if seed % 2 else None)
+    fo = slowdown_forest.synthetic_forest(seed)
+    try:
+        ref = oracle.run(g, sc, 6, threads=THREADS, until_stable=until_stable, prorate=prorate, forest=fo)
+    except oracle.OracleError as e:
+        assert e.code == -4
+        return
+    G = E.Graph(g, 0)
+    G.set_forest(fo)
+    d, n = E.scenarios_to_device(sc)
+    out = G.compose(d, n, 6, timelines=True, digest=True, until_stable=until_stable, prorate=prorate,
+                    forest=True, refinements=True)
+    gpu = {"step": out["step"].cpu().numpy(), "digest": out["digest"].cpu().numpy().view(np.uint64),
+           "start": out["start"].cpu().numpy(), "finish": out["finish"].cpu().numpy()}
+    G.close()
+    assert_same(gpu, ref)
+    np.testing.assert_array_equal(out["refinements"].cpu().numpy(), ref["refinements"])
+
+
+def test_forest_config1_and_2(E):
+    fo = slowdown_forest.synthetic_forest(7)
+    g, sc = configs.graph(1), scenarios.take(configs.scenario_batch(4), slice(0, 130))
+    G = E.Graph(g, 0)
+    G.set_forest(fo)
+    d, n = E.scenarios_to_device(sc)
+    out = G.compose(d, n, 2, timelines=True, digest=True, forest=True)
+    G.close()
+    gpu = {"step": out["step"].cpu().numpy(), "digest": out["digest"].cpu().numpy().view(np.uint64),
+           "start": out["start"].cpu().numpy(), "finish": out["finish"].cpu().numpy()}
+    assert_same(gpu, oracle.run(g, sc, 2, threads=THREADS, forest=fo))
+    g, sc = configs.graph(2), configs.scenario_batch(2)
+    G = E.Graph(g, 0)
+    G.set_forest(fo)
+    d, n = E.scenarios_to_device(sc)
+    out = G.compose(d, n, 1, timelines=True, digest=True, forest=True)
+    G.close()
+    cols = [0, 31, 63]
+    ref = oracle.run(g, scenarios.take(sc, cols), 1, threads=3, forest=fo, jitter_stream=cols)
+    np.testing.assert_array_equal(out["step"].cpu().numpy()[cols], ref["step"])
+    np.testing.assert_array_equal(out["digest"].cpu().numpy().view(np.uint64)[cols], ref["digest"])
+    fin = out["finish"].cpu().numpy()
+    for j, c in enumerate(cols):
+        np.testing.assert_array_equal(fin[:, c], ref["finish"][j])
+
+
+def test_forest_reproducing_the_table(E):
+    g = configs.graph(1)
+    rng = np.random.default_rng(12)
+    table = rng.integers(65536, 200000, (8, 4)).astype(np.uint32)
+    sc = scenarios.take(configs.scenario_batch(4), slice(0, 70))
+    sc["slowdown_q16"] = np.broadcast_to(table, (70, 8, 4)).copy()
+    G = E.Graph(g, 0)
+    G.set_forest(slowdown_forest.table_forest(table))
+    d, n = E.scenarios_to_device(sc)
+    a = G.compose(d, n, 2, timelines=True)
+    b = G.compose(d, n, 2, timelines=True, forest=True)
+    import torch
+    assert torch.equal(a["finish"], b["finish"]) and torch.equal(a["start"], b["start"])
+    G.close()
+
+
+def test_forest_errors(E):
+    g = configs.graph(1)
+    G = E.Graph(g, 0)
+    d, n = E.scenarios_to_device(scenarios.default_scenarios(2))
+    with pytest.raises(E.EchoError) as x:            # no ensemble yet
+        G.compose(d, n, 1, forest=True)
+    assert x.value.code == E.ECHO_ERR_ARG
+    deep = {"nodes": np.zeros(14, slowdown_forest.TREE_NODE_DTYPE), "roots": np.array([0], np.int32),
+            "base": 65536, "class_metrics": np.zeros((8, 4), np.int64)}
+    for i in range(13):
+        deep["nodes"][i] = (0, i + 1, i + 1, 0, 1)
+    deep["nodes"][13] = (-1, 0, 0, 5, 0)
+    with pytest.raises(E.EchoError) as x:
+        G.set_forest(deep)
+    assert x.value.code == E.ECHO_ERR_ARG
+    G.close()

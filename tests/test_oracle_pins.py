@@ -756,3 +756,100 @@ def test_cc_table_errors():
     with pytest.raises(oracle.OracleError) as e:
         oracle.run(g, scenarios.default_scenarios(1), 1, cc_tables=bad)
     assert e.value.code == -1
+
+
+# ---------------------------------------------------------------- tree-ensemble slowdown
+from workloads import slowdown_forest   # noqa: E402
+
+
+def _stump(values):
+    """One tree: AR (type 0) takes values[0], every other type values[1]."""
+    nodes = np.zeros(3, slowdown_forest.TREE_NODE_DTYPE)
+    nodes[0] = (2, 1, 2, 0, 1)
+    nodes[1] = (-1, 0, 0, values[0], 0)
+    nodes[2] = (-1, 0, 0, values[1], 0)
+    return {"nodes": nodes, "roots": np.array([0], np.int32), "base": 65536,
+            "class_metrics": np.zeros((8, 4), np.int64)}
+
+
+def test_forest_stump_hand_value():
+    g, v = _overlap_pair(700, 1000, 1 << 30)          # the all-reduce covers [700, ...)
+    sc = _scen(1)
+    r = oracle.run(g, sc, 1, forest=_stump([10000, 20000]))
+    assert r["finish"][0][v] == (1000 * 75536 + 32768) >> 16 == 1153
+    r = oracle.run(g, sc, 1, forest=_stump([10000, 20000]), prorate=True)
+    assert r["finish"][0][v] == 700 + ((300 * 75536 + 32768) >> 16) == 1046
+
+
+@pytest.mark.parametrize("prorate", [False, True])
+def test_forest_reproducing_the_table_equals_table_factors(prorate):
+    g = configs.graph(1)
+    rng = np.random.default_rng(5)
+    table = rng.integers(65536, 200000, (8, 4)).astype(np.uint32)
+    sc = scenarios.draw(5, rng, bw_inter=(20000, 90000), alpha=(0, 5000), jitter=(4000, 2))
+    sc["slowdown_q16"] = np.broadcast_to(table, (5, 8, 4)).copy()
+    for R in (1, 3):
+        a = oracle.run(g, sc, R, prorate=prorate)
+        b = oracle.run(g, sc, R, prorate=prorate, forest=slowdown_forest.table_forest(table))
+        np.testing.assert_array_equal(a["finish"], b["finish"])
+        np.testing.assert_array_equal(a["start"], b["start"])
+
+
+def test_forest_factors_match_brute_force_on_random_tiny_graphs():
+    rng = np.random.default_rng(654)
+    checked = 0
+    for trial in range(40):
+        n_ranks = int(rng.integers(1, 4))
+        b = Builder(n_ranks, gpus_per_node=int(rng.integers(1, 3)))
+        n_coll = int(rng.integers(1, 4))
+        colls = [b.collective(int(rng.integers(0, 3)), int(rng.integers(0, 256 << 10))) for _ in range(n_coll)]
+        for r in range(n_ranks):
+            ids = []
+            order = list(rng.permutation(n_coll))
+            for k in range(int(rng.integers(3, 7))):
+                preds = [int(u) for u in ids if rng.random() < 0.25]
+                if order and rng.random() < 0.4:
+                    ids.append(b.comm(r, colls[order.pop()], stream=int(rng.integers(1, 4)), preds=preds))
+                else:
+                    ids.append(b.compute(r, int(rng.integers(1, 600)), stream=int(rng.integers(0, 2)),
+                                         cls=int(rng.integers(0, 8)), preds=preds))
+            for c in order:
+                b.comm(r, colls[c], stream=int(rng.integers(1, 4)), preds=ids[-1:])
+        g = b.graph()
+        if len(g["op_rank"]) > 24:
+            continue
+        sc = _scen(1, alpha=int(rng.integers(0, 300)), bw_intra=400000, bw_inter=200000, ar_algo=int(trial % 2))
+        fo = slowdown_forest.synthetic_forest(trial, n_trees=8, max_depth=6, base=70000, leaf_mean=2000,
+                                              leaf_sd=6000)
+        try:
+            base, cost = _dur_cost(g, sc)
+        except oracle.OracleError as e:
+            assert e.code == -4
+            continue
+        for until_stable, prorate in ((False, False), (True, False), (False, True)):
+            s, f, done = bruteforce.compose_variants(g, base, cost, None, 4, until_stable=until_stable,
+                                                     prorate=prorate, forest=fo, knobs=(trial % 2, 400000, 200000))
+            r = oracle.run(g, sc, 4, until_stable=until_stable, prorate=prorate, forest=fo)
+            np.testing.assert_array_equal(r["start"][0], s)
+            np.testing.assert_array_equal(r["finish"][0], f)
+            assert r["refinements"][0] == done
+            checked += 1
+    assert checked >= 60
+
+
+def test_malformed_forests_rejected():
+    g = configs.graph(1)
+    sc = scenarios.default_scenarios(1)
+    deep = {"nodes": np.zeros(14, slowdown_forest.TREE_NODE_DTYPE), "roots": np.array([0], np.int32),
+            "base": 65536, "class_metrics": np.zeros((8, 4), np.int64)}
+    for i in range(13):                                   # a chain of 13 splits
+        deep["nodes"][i] = (0, i + 1, i + 1, 0, 1)
+    deep["nodes"][13] = (-1, 0, 0, 5, 0)
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.run(g, sc, 1, forest=deep)
+    assert e.value.code == -1
+    bad = _stump([1, 2])
+    bad["nodes"][0]["feature"] = 12
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.run(g, sc, 1, forest=bad)
+    assert e.value.code == -1
