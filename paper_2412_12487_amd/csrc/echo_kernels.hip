@@ -556,6 +556,7 @@ __device__ __forceinline__ uint32_t factor_of(uint32_t m, const uint32_t *slow, 
 // largest over the types.  Trees are walked per lane from global memory (the
 // walk stops at a leaf; paths are at most ECHO_TREE_DEPTH splits long).
 constexpr int kForestLanes = 8;
+constexpr int kPre = 8;          // unchained starts prefetched per round of overlap detection
 
 // feat: this wavefront's LDS feature rows, feature k of lane l at feat[k * 64 + l].
 __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_t *smax, const int32_t *nmax,
@@ -692,6 +693,24 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
             __builtin_amdgcn_s_waitcnt(kWaitVm0);
             nxt = i0 + kLanes + lane < b1 ? recs[i0 + kLanes + lane] : make_int4(0, 0, 0, 0);
             const int nr = b1 - i0 < kLanes ? int(b1 - i0) : kLanes;
+            // the starts of the round's first kPre unchained ops, fetched together
+            const uint64_t unchained = __builtin_amdgcn_read_exec() &
+                                       __ballot(lane < nr && !((uint32_t)cur.y & kChained));
+            int64_t pre[kPre];
+            {
+                uint64_t um = unchained;
+#pragma unroll
+                for (int q = 0; q < kPre; ++q) {
+                    pre[q] = 0;
+                    if (um) {
+                        const int jq = __builtin_ctzll(um);
+                        um &= um - 1;
+                        const int64_t vq = __builtin_amdgcn_readlane(cur.x, jq);
+                        pre[q] = (sbase + vq * ns)[col];
+                    }
+                }
+                __builtin_amdgcn_s_waitcnt(kWaitVm0);
+            }
             for (int j = 0; j < nr; ++j) {
                 const int64_t v = __builtin_amdgcn_readlane(cur.x, j);
                 const int meta = __builtin_amdgcn_readlane(cur.y, j);
@@ -703,8 +722,15 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 // every path, for the previous op's store as well.
                 int64_t sv = fprev;
                 if (!(meta & kChained)) {
-                    sv = (sbase + v * ns)[col];
-                    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                    const int ord = __builtin_popcountll(unchained & ((uint64_t(1) << j) - 1));
+                    if (ord < kPre) {
+#pragma unroll
+                        for (int q = 0; q < kPre; ++q)
+                            if (q == ord) sv = pre[q];
+                    } else {
+                        sv = (sbase + v * ns)[col];
+                        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                    }
                 }
                 const int64_t D = amp != 0 ? jittered(d0, (int32_t)v, jbase, amp) : d0;
                 int64_t d = D;                   // the duration v ran with in the previous pass
