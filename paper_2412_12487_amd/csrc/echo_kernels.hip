@@ -203,6 +203,11 @@ __device__ bool wait_arrivals(const unsigned *cnt, unsigned need, unsigned *stat
 
 constexpr int kBlock = 32;   // walk items fetched (and overlap masks staged) per round
 
+// Timeline stores stream through the caches (non-temporal): each (op, tile) row
+// segment is written once per pass and read again only by the same wavefront
+// (a far predecessor) or by the next kernel.
+__device__ __forceinline__ void put(int64_t *p, int64_t v) { __builtin_nontemporal_store(v, p); }
+
 // Duration d inflated by the slowdown factor of overlap mask m (Sec. 6): the
 // largest entry of the op's class row over the collective types in m; an empty
 // mask is factor 65536, which q16 maps to d itself.  tbl: the lane's table in
@@ -354,7 +359,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); \
         f_ = (int64_t)b_ + t_;                                                                   \
         hi_or |= (uint32_t)((uint64_t)(f_) >> 32);                                               \
-        (fbase + (int64_t)(v_) * ns)[col] = f_;                                                  \
+        put(fbase + (int64_t)(v_) * ns + col, f_);                                               \
         if (DIGEST) {                                                                            \
             const int64_t s_ = (sbase + (int64_t)(v_) * ns)[col];                                \
             dig += mix64(mix64((uint64_t)(v_) ^ (uint64_t)s_) ^ (uint64_t)(f_));                 \
@@ -408,8 +413,8 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 if (REFINED && item_kind(meta) == ECHO_COMPUTE)
                     d = PRORATE ? d + fst32[j * kLanes + lane] : inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane);
                 const int64_t f = s0 + d;
-                if ((meta | keep) & kNeedS) (sbase + (int64_t)op * ns)[col] = s0;
-                if ((meta | keep) & kNeedF) (fbase + (int64_t)op * ns)[col] = f;
+                if ((meta | keep) & kNeedS) put(sbase + (int64_t)op * ns + col, s0);
+                if ((meta | keep) & kNeedF) put(fbase + (int64_t)op * ns + col, f);
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)s0) ^ (uint64_t)f);
                 s0 = f;
@@ -449,7 +454,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 const int64_t fu = (fbase + u * ns)[col];
                 ready = fu > ready ? fu : ready;
             }
-            if ((meta | keep) & kNeedS) (sbase + (int64_t)op * ns)[col] = ready;
+            if ((meta | keep) & kNeedS) put(sbase + (int64_t)op * ns + col, ready);
             if (kind == ECHO_COMM) {
                 // launch: publish this member's launch time, then count the arrival
                 if (aux & kAuxLocal) {
@@ -482,7 +487,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                     d = PRORATE ? d + fst32[j * kLanes + lane] : inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane);
                 const int64_t f = ready + d;
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
-                if ((meta | keep) & kNeedF) (fbase + (int64_t)op * ns)[col] = f;
+                if ((meta | keep) & kNeedF) put(fbase + (int64_t)op * ns + col, f);
                 if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)ready) ^ (uint64_t)f);
                 if (meta & kNoReg) {
                     xmax = f > xmax ? f : xmax;
