@@ -562,6 +562,7 @@ __device__ __forceinline__ uint32_t factor_of(uint32_t m, const uint32_t *slow, 
 // walk stops at a leaf; paths are at most ECHO_TREE_DEPTH splits long).
 constexpr int kForestLanes = 8;
 constexpr int kPre = 8;          // unchained starts prefetched per round of overlap detection
+constexpr int kIdStage = 2048;   // comm ops of a rank whose ids overlap detection keeps in LDS
 
 // feat: this wavefront's LDS feature rows, feature k of lane l at feat[k * 64 + l].
 __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_t *smax, const int32_t *nmax,
@@ -627,6 +628,8 @@ template <bool PRORATE, bool DETECT, bool FOREST>
 __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     constexpr bool EXT = PRORATE || FOREST;      // output: extra time per op instead of a mask
     __shared__ int64_t feat[FOREST ? 12 * kLanes : 1];   // the ensemble's feature vectors, one per lane
+    __shared__ int32_t sid[kIdStage];            // the rank's comm op ids and collective types, staged
+    __shared__ uint8_t stype[kIdStage];
     if (a.stable && __builtin_amdgcn_readfirstlane(__hip_atomic_load(a.stable, __ATOMIC_RELAXED,
                                                                       __HIP_MEMORY_SCOPE_AGENT)))
         return;                                  // every scenario is at its fixed point
@@ -649,6 +652,28 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     const int64_t *cp_off = a.cp_off + (int64_t)r * kStreams;
     bool changed = false;                        // some duration differs from the previous pass's
     bool ext_over = false;                       // a prorated extra time does not fit 32 bits
+
+    // Stage the rank's comm lists in LDS: a cursor move then costs one memory round trip
+    // (the comm op's interval) instead of two (its id, then the interval).
+    const int64_t cbase = cl_off[0];
+    const int64_t nstage = cl_off[kStreams] - cbase < kIdStage ? cl_off[kStreams] - cbase : kIdStage;
+    for (int64_t i = lane; i < nstage; i += kLanes) {
+        sid[i] = a.cl[cbase + i];
+        stype[i] = a.cl_type[cbase + i];
+    }
+    __syncthreads();
+    // comm op at position x of the rank's lists and its collective type
+    auto comm_id = [&](int64_t x) -> int64_t {
+        const int64_t o = x - cbase;
+        if (o < nstage) return sid[o];
+        return __hip_atomic_load(a.cl + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
+    auto comm_type = [&](int64_t x) -> uint32_t {
+        const int64_t o = x - cbase;
+        if (o < nstage) return stype[o];
+        // an atomic load keeps this read and the LDS one from merging into a flat load
+        return __hip_atomic_load(a.cl_type + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
 
     // comm streams of this rank that carry comm ops, packed to the front
     int64_t kb[kStreams];
@@ -785,7 +810,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                         while (cf[k] <= sv) {              // ends before v starts: never again
                             ++p[k];
                             if (p[k] < nk[k]) {
-                                const int64_t c = a.cl[kb[k] + p[k]];
+                                const int64_t c = comm_id(kb[k] + p[k]);
                                 cs[k] = (sbase + c * ns)[col];
                                 cf[k] = (fbase + c * ns)[col];
                             } else {
@@ -799,13 +824,13 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                         while (qs < fv) {
                             const int64_t lo = sv > qs ? sv : qs, hi = fv < qf ? fv : qf;
                             if (lo < hi) {
-                                const uint32_t ty = a.cl_type[kb[k] + q];
+                                const uint32_t ty = comm_type(kb[k] + q);
                                 m |= 1u << ty;
                                 NOTE_FOREST(kb[k] + q, ty)
                             }
                             if (qf >= fv) break;           // the next one starts after v ends
                             if (++q >= nk[k]) break;
-                            const int64_t c = a.cl[kb[k] + q];
+                            const int64_t c = comm_id(kb[k] + q);
                             qs = (sbase + c * ns)[col];
                             qf = (fbase + c * ns)[col];
                         }
@@ -837,7 +862,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                                 if (k != bk) continue;
                                 const int64_t lo = sv > qs[k] ? sv : qs[k], hi = fv < qf[k] ? fv : qf[k];
                                 if (lo < hi) {
-                                    const uint32_t ty = a.cl_type[kb[k] + q[k]];
+                                    const uint32_t ty = comm_type(kb[k] + q[k]);
                                     m |= 1u << ty;
                                     NOTE_FOREST(kb[k] + q[k], ty)
                                     const int64_t from = lo > t ? lo : t;
@@ -847,7 +872,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                                     }
                                 }
                                 if (++q[k] < nk[k]) {
-                                    const int64_t c = a.cl[kb[k] + q[k]];
+                                    const int64_t c = comm_id(kb[k] + q[k]);
                                     qs[k] = (sbase + c * ns)[col];
                                     qf[k] = (fbase + c * ns)[col];
                                     __builtin_amdgcn_s_waitcnt(kWaitVm0);
