@@ -302,6 +302,9 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     const echo_scenario *sc = a.scen + sigma;
     const uint64_t jbase = jitter_base(sc->jitter_seed, sc->jitter_stream);
     const int32_t amp = sc->jitter_amp_q16;
+    // one branch for the whole wavefront: a lane without jitter draws the identity factor
+    // (amplitude 0 gives f = 65536 and q16(d, 65536) = d)
+    const bool any_jitter = __builtin_amdgcn_readfirstlane(__ballot(amp != 0) != 0);
     int64_t *const sbase = a.start + (int64_t)tile * kLanes;    // row v of tile: sbase + v * ns
     int64_t *const fbase = a.finish + (int64_t)tile * kLanes;
     const unsigned *tile_count = a.count + tile;
@@ -403,23 +406,33 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
         int j = 0;
         while (j < nb) {
             // a run of fast items: compute/memcpy ops right after the previous op of slot 0
+            // (fast bits exist only below nb, so the run ends there at the latest)
+            const int run_end = j + (int)__builtin_ctzll(~(fast_bits >> j));
             int64_t s0 = lf[0];
-            while (j < nb && ((fast_bits >> j) & 1)) {
-                const int32_t op = __builtin_amdgcn_readlane(cur.x, j);
-                const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);
-                const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) |
-                                              (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32));
-                int64_t d = amp != 0 ? jittered(dur, op, jbase, amp) : dur;
-                if (REFINED && item_kind(meta) == ECHO_COMPUTE)
-                    d = PRORATE ? d + fst32[j * kLanes + lane] : inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane);
-                const int64_t f = s0 + d;
-                if ((meta | keep) & kNeedS) put(sbase + (int64_t)op * ns + col, s0);
-                if ((meta | keep) & kNeedF) put(fbase + (int64_t)op * ns + col, f);
-                hi_or |= (uint32_t)((uint64_t)f >> 32);
-                if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)s0) ^ (uint64_t)f);
-                s0 = f;
-                ++j;
+// ALL: the pass stores every start and finish, so the items' own needs are not consulted
+#define FAST_RUN(ALL)                                                                            \
+            for (; j < run_end; ++j) {                                                           \
+                const int32_t op = __builtin_amdgcn_readlane(cur.x, j);                          \
+                const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);             \
+                const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) | \
+                                              (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32)); \
+                int64_t d = any_jitter ? jittered(dur, op, jbase, amp) : dur;                    \
+                if (REFINED && item_kind(meta) == ECHO_COMPUTE)                                  \
+                    d = PRORATE ? d + fst32[j * kLanes + lane]                                   \
+                                : inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane); \
+                const int64_t f = s0 + d;                                                        \
+                if ((ALL) || (meta & kNeedS)) put(sbase + (int64_t)op * ns + col, s0);           \
+                if ((ALL) || (meta & kNeedF)) put(fbase + (int64_t)op * ns + col, f);            \
+                hi_or |= (uint32_t)((uint64_t)f >> 32);                                          \
+                if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)s0) ^ (uint64_t)f);     \
+                s0 = f;                                                                          \
             }
+            if (keep) {
+                FAST_RUN(true)
+            } else {
+                FAST_RUN(false)
+            }
+#undef FAST_RUN
             lf[0] = s0;
             if (j >= nb) break;
             const int32_t op = __builtin_amdgcn_readlane(cur.x, j);
@@ -482,7 +495,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                     pending |= 1u << st;
                 }
             } else {
-                int64_t d = amp != 0 ? jittered(dur, op, jbase, amp) : dur;
+                int64_t d = any_jitter ? jittered(dur, op, jbase, amp) : dur;
                 if (REFINED && kind == ECHO_COMPUTE)
                     d = PRORATE ? d + fst32[j * kLanes + lane] : inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane);
                 const int64_t f = ready + d;
