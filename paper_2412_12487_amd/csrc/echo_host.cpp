@@ -97,6 +97,7 @@ hipError_t upload(T **dst, const std::vector<T> &src) {
 struct echo_graph_s {
     int device = 0;
     int64_t n_ops = 0, n_colls = 0, n_levels = 0;
+    int64_t n_items = 0;               // entries of the walk lists
     int32_t n_ranks = 0, n_walkers = 0;
     int64_t capacity[kWalkVariants] = {};   // co-resident walk workgroups per kernel variant
     bool need_coll_cost = false;       // some comm op reads its cost per collective
@@ -657,7 +658,13 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     std::vector<int32_t> cl(cl_off.back()), cl_coll(cl_off.back());
     std::vector<uint8_t> cl_type(cl_off.back());
     std::vector<ComputeRec> cp(cp_off.back());
+    std::vector<int32_t> cp_pos(cp_off.back());
     {
+        // overlap detection writes its per-op outputs where the walk reads them: at the
+        // row of the op's item (resolve items aside, every op has exactly one)
+        std::vector<int32_t> item_pos(n, -1);
+        for (size_t i = 0; i < items.size(); ++i)
+            if (item_kind(items[i].meta) != kResolve) item_pos[items[i].op] = (int32_t)i;
         std::vector<int64_t> fl(cl_off.begin(), cl_off.end() - 1), fp(cp_off.begin(), cp_off.end() - 1);
         std::vector<int32_t> prev_on_stream(R * kStreams, -1);
         for (int64_t v = 0; v < n; ++v) {
@@ -672,6 +679,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
                 // chained: the only predecessor is the previous op of the stream, a compute op
                 const bool chained = prev >= 0 && d->op_kind[prev] == ECHO_COMPUTE && poff[v + 1] - poff[v] == 1 &&
                                      preds[poff[v]] == prev;
+                cp_pos[fp[k]] = item_pos[v];
                 cp[fp[k]++] = ComputeRec{(int32_t)v, (uint32_t)d->op_class[v] | (chained ? kChained : 0u),
                                          d->op_dur_ns[v]};
             }
@@ -690,6 +698,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     if (!g) return fail(ECHO_ERR_NOMEM, "host allocation");
     g->device = device;
     g->n_ops = n;
+    g->n_items = (int64_t)items.size();
     g->n_colls = nc;
     g->n_levels = n_levels;
     g->n_ranks = (int32_t)R;
@@ -736,6 +745,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     UP(dg.cl_coll, cl_coll);
     UP(dg.cp_off, cp_off);
     UP(dg.cp, cp);
+    UP(dg.cp_pos, cp_pos);
     UP(dg.status, std::vector<unsigned>(1, 0u));
 #undef UP
     *out = g;
@@ -762,9 +772,12 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
     if ((rc = ensure(&g->class_cost, &g->class_cost_n, (size_t)(g->dg.classes.n * ns), "class cost"))) return rc;
     if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->n_colls * ns), "arrivals"))) return rc;
     if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * n_tiles), "arrival counts"))) return rc;
-    if (n_refine > 0 && !ext && (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(g->n_ops * ns), "overlap masks")))
+    // per-item outputs of overlap detection: whole tiles of columns, and one round of
+    // rows past the last item (the walk fetches a round's rows at once)
+    const int64_t mstride = (int64_t)n_tiles * kLanes, mrows = g->n_items + kBlock;
+    if (n_refine > 0 && !ext && (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(mrows * mstride), "overlap masks")))
         return rc;
-    if (ext && (rc = ensure(&g->ext, &g->ext_n, (size_t)(g->n_ops * ns), "extra times"))) return rc;
+    if (ext && (rc = ensure(&g->ext, &g->ext_n, (size_t)(mrows * mstride), "extra times"))) return rc;
     if (until_stable && (rc = ensure(&g->chg, &g->chg_n, (size_t)(ns + 1), "change flags"))) return rc;
     unsigned *stable = until_stable ? g->chg + ns : nullptr;
     if (!d_start && (rc = ensure(&g->tmp_start, &g->tmp_start_n, (size_t)(g->n_ops * ns), "start"))) return rc;
@@ -812,6 +825,8 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
             o.finish = finish;
             o.tmask = ext ? nullptr : g->tmask;
             o.ext = ext ? g->ext : nullptr;
+            o.cp_pos = g->dg.cp_pos;
+            o.mstride = mstride;
             o.chg = until_stable ? g->chg : nullptr;
             o.stable = stable;
             if (forest) {
@@ -846,6 +861,7 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
             a.class_cost = g->class_cost;
             a.tmask = p > 0 && !ext ? g->tmask : nullptr;
             a.ext = p > 0 && ext ? g->ext : nullptr;
+            a.mstride = mstride;
             a.stable = p < n_refine ? stable : nullptr;     // the final pass always runs
             a.start = start;
             a.finish = finish;

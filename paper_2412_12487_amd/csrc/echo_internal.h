@@ -74,6 +74,7 @@ constexpr int kResolve = 3;
 // looked up per cost class -- the (type, S, N, M, K) tuple that fixes T(c, s)
 // for a scenario -- and a block stages its most used classes in LDS.
 constexpr int kBlockWalkers = 8;
+constexpr int kBlock = 32;          // walk items fetched (and overlap masks staged) per round
 constexpr int kChannels = 8;          // LDS barrier channels per block
 constexpr int kClassSlots = 8;        // LDS cost classes per block
 constexpr uint32_t kNoSlot = 15;
@@ -134,6 +135,7 @@ struct DeviceGraph {
     uint8_t *cl_type = nullptr;      // collective type of each listed comm op
     int64_t *cp_off = nullptr;       // [n_ranks * 8 + 1]
     ComputeRec *cp = nullptr;
+    int32_t *cp_pos = nullptr;       // [compute record] position of the op's item in the walk lists
     unsigned *status = nullptr;      // device status word
     echo_cc_table *cc_tables = nullptr;   // CC parameter tables (echo_set_cc_tables)
     int32_t n_cc_tables = 0;
@@ -156,8 +158,11 @@ struct WalkArgs {
     const echo_scenario *scen;
     const int64_t *cost;             // [coll][scen]
     const int64_t *class_cost;       // [class][scen]
-    const uint8_t *tmask;            // [op][scen] overlap type masks of compute ops, or null (pass 1)
-    const uint32_t *ext;             // [op][scen] prorated extra time of compute ops (prorating), or null
+    // Per-item outputs of overlap detection, one row per walk item (rows of items that are
+    // not compute ops unused), mstride columns (the tiles' scenarios, padded to whole tiles):
+    const uint8_t *tmask;            // overlap type masks, or null (pass 1)
+    const uint32_t *ext;             // extra times (prorating, ensemble factors), or null
+    int64_t mstride;
     const unsigned *stable;          // non-null: skip the pass when *stable (every scenario at its fixed point)
     int64_t *start, *finish;         // [op][scen]
     unsigned long long *arrive;      // [coll][scen] latest member launch
@@ -181,8 +186,11 @@ struct OverlapArgs {
     const ComputeRec *cp;
     const echo_scenario *scen;
     const int64_t *start, *finish;
+    // rows of the walk items (cp_pos), mstride columns, as the walk reads them
     uint8_t *tmask;                  // in: masks of the previous pass (if it was refined), out: new ones
     uint32_t *ext;                   // prorating: in/out like tmask, the extra time q16(o, F) - o
+    const int32_t *cp_pos;
+    int64_t mstride;
     unsigned *chg;                   // non-null: [scen] set when some duration changes
     const unsigned *stable;          // non-null: skip when *stable
     // ensemble factors (forest_nodes non-null): features of the overlapping comm ops

@@ -201,8 +201,6 @@ __device__ bool wait_arrivals(const unsigned *cnt, unsigned need, unsigned *stat
     }
 }
 
-constexpr int kBlock = 32;   // walk items fetched (and overlap masks staged) per round
-
 // Timeline stores stream through the caches (non-temporal): each (op, tile) row
 // segment is written once per pass and read again only by the same wavefront
 // (a far predecessor) or by the next kernel.
@@ -256,7 +254,7 @@ __device__ bool wait_local(const unsigned *cnt, unsigned need, unsigned *status,
 template <bool REFINED, bool FINAL, bool DIGEST, bool PRORATE>
 __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     // staged per item and lane: overlap masks (one byte) or, prorating, extra times (32 bits)
-    __shared__ uint32_t fstage[REFINED ? kBlockWalkers * kBlock * kLanes / (PRORATE ? 1 : 4) : 1];
+    __shared__ __align__(16) uint32_t fstage[REFINED ? kBlockWalkers * kBlock * kLanes / (PRORATE ? 1 : 4) : 1];
     __shared__ unsigned long long lbar[kChannels][2][kLanes];   // per channel and slot: latest launch per lane
     __shared__ unsigned lcnt[kChannels][2];                      // per channel and slot: members arrived
     __shared__ int64_t ccost[kClassSlots][kLanes];               // staged class costs of this tile
@@ -331,8 +329,20 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     // lane j < 32 holds the first half of item j of the round, lane 32 + j its second half
     const int4 *items4 = reinterpret_cast<const int4 *>(a.items);
     const int half = lane >> 5, slotl = lane & 31;
-    // lanes past the end of the list hold op 0, so staged factor loads stay in bounds
+    // lanes past the end of the list hold op 0
     int4 nxt = beg + slotl < end ? items4[2 * (beg + slotl) + half] : make_int4(0, 0, 0, 0);
+    // Overlap masks of a round: its kBlock rows of the mask array (row = item), 64 bytes of
+    // this tile each.  Lane l fetches 16 bytes, row l / 4 (+16 in the second half), quarter
+    // l % 4 -- laid down in LDS as they come, that is the [item][lane] staging order.  The
+    // next round's masks are fetched while this round runs.  (The array has kBlock rows
+    // past the last item, for the last round's fetch.)
+    const uint4 *const mrow = reinterpret_cast<const uint4 *>(a.tmask + (int64_t)tile * kLanes) + (lane & 3);
+    const int64_t mst4 = a.mstride / 16;
+    uint4 mnx0 = make_uint4(0, 0, 0, 0), mnx1 = mnx0;
+    if (REFINED && !PRORATE) {
+        mnx0 = mrow[(beg + (lane >> 2)) * mst4];
+        mnx1 = mrow[(beg + 16 + (lane >> 2)) * mst4];
+    }
 
 // Finish f_ of comm op v_ (collective c_, aux word x_): its barrier -- the
 // latest member launch -- plus the collective's cost; written to the finish array.
@@ -382,23 +392,30 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     for (int64_t blk0 = beg; blk0 < end; blk0 += kBlock) {
         const int4 cur = nxt;
         const int nb = end - blk0 < kBlock ? int(end - blk0) : kBlock;
-        nxt = blk0 + kBlock + slotl < end ? items4[2 * (blk0 + kBlock + slotl) + half] : make_int4(0, 0, 0, 0);
-        if (REFINED) {
-            // stage this round's overlap masks (or extra times), half a round per memory round trip
+        // This round's items and masks (fetched during the last round) are settled first: a
+        // wait at their first use would also wait for the fetches issued below.
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        if (REFINED && !PRORATE) {
+            uint4 *const f4 = reinterpret_cast<uint4 *>(fst);
+            f4[lane] = mnx0;
+            f4[kLanes + lane] = mnx1;
+        }
+        if (REFINED && PRORATE) {
+            // stage this round's extra times, half a round per memory round trip
+            const uint32_t *const erow = a.ext + (int64_t)tile * kLanes + col;
 #pragma unroll
             for (int h = 0; h < kBlock; h += kBlock / 2) {
                 uint32_t mv[kBlock / 2];
 #pragma unroll
-                for (int j = 0; j < kBlock / 2; ++j) {
-                    const int32_t opj = __builtin_amdgcn_readlane(cur.x, h + j);
-                    mv[j] = PRORATE ? a.ext[(int64_t)opj * ns + sigma] : a.tmask[(int64_t)opj * ns + sigma];
-                }
+                for (int j = 0; j < kBlock / 2; ++j) mv[j] = erow[(blk0 + h + j) * a.mstride];
 #pragma unroll
-                for (int j = 0; j < kBlock / 2; ++j) {
-                    if (PRORATE) fst32[(h + j) * kLanes + lane] = mv[j];
-                    else fst[(h + j) * kLanes + lane] = (uint8_t)mv[j];
-                }
+                for (int j = 0; j < kBlock / 2; ++j) fst32[(h + j) * kLanes + lane] = mv[j];
             }
+        }
+        nxt = blk0 + kBlock + slotl < end ? items4[2 * (blk0 + kBlock + slotl) + half] : make_int4(0, 0, 0, 0);
+        if (REFINED && !PRORATE && blk0 + kBlock < end) {
+            mnx0 = mrow[(blk0 + kBlock + (lane >> 2)) * mst4];
+            mnx1 = mrow[(blk0 + kBlock + 16 + (lane >> 2)) * mst4];
         }
         // fast flags of the round, one bit per item
         const uint64_t fast_bits = __builtin_amdgcn_read_exec() &
@@ -419,7 +436,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 int64_t d = any_jitter ? jittered(dur, op, jbase, amp) : dur;                    \
                 if (REFINED && item_kind(meta) == ECHO_COMPUTE)                                  \
                     d = PRORATE ? d + fst32[j * kLanes + lane]                                   \
-                                : inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane); \
+                                : inflate(d, fst[j * kLanes + col], slow, item_class(meta), lane); \
                 const int64_t f = s0 + d;                                                        \
                 if ((ALL) || (meta & kNeedS)) put(sbase + (int64_t)op * ns + col, s0);           \
                 if ((ALL) || (meta & kNeedF)) put(fbase + (int64_t)op * ns + col, f);            \
@@ -497,7 +514,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             } else {
                 int64_t d = any_jitter ? jittered(dur, op, jbase, amp) : dur;
                 if (REFINED && kind == ECHO_COMPUTE)
-                    d = PRORATE ? d + fst32[j * kLanes + lane] : inflate(d, fst[j * kLanes + lane], slow, item_class(meta), lane);
+                    d = PRORATE ? d + fst32[j * kLanes + lane] : inflate(d, fst[j * kLanes + col], slow, item_class(meta), lane);
                 const int64_t f = ready + d;
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 if ((meta | keep) & kNeedF) put(fbase + (int64_t)op * ns + col, f);
@@ -725,16 +742,23 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 cf[k] = (fbase + c * ns)[col];
             }
         }
+        // earliest start among the cursors: an op ending by then overlaps nothing
+        int64_t cmin = kInf;
+#pragma unroll
+        for (int k = 0; k < kStreams; ++k) cmin = cs[k] < cmin ? cs[k] : cmin;
         int64_t fprev = 0;
         // lane j holds compute record i0 + j of the current round of 64
         const int4 *recs = reinterpret_cast<const int4 *>(a.cp);
         int4 nxt = b0 + lane < b1 ? recs[b0 + lane] : make_int4(0, 0, 0, 0);
+        int32_t nxt_pos = b0 + lane < b1 ? a.cp_pos[b0 + lane] : 0;
         for (int64_t i0 = b0; i0 < b1; i0 += kLanes) {
             const int4 cur = nxt;
+            const int32_t cur_pos = nxt_pos;
             // settle the round's records here, once, so the per-op loop below carries
             // no memory wait (a wait there would also wait for the previous op's store)
             __builtin_amdgcn_s_waitcnt(kWaitVm0);
             nxt = i0 + kLanes + lane < b1 ? recs[i0 + kLanes + lane] : make_int4(0, 0, 0, 0);
+            nxt_pos = i0 + kLanes + lane < b1 ? a.cp_pos[i0 + kLanes + lane] : 0;
             const int nr = b1 - i0 < kLanes ? int(b1 - i0) : kLanes;
             // the starts of the round's first kPre unchained ops, fetched together
             const uint64_t unchained = __builtin_amdgcn_read_exec() &
@@ -756,6 +780,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
             }
             for (int j = 0; j < nr; ++j) {
                 const int64_t v = __builtin_amdgcn_readlane(cur.x, j);
+                const int64_t row = (int64_t)__builtin_amdgcn_readlane(cur_pos, j) * a.mstride;   // v's item
                 const int meta = __builtin_amdgcn_readlane(cur.y, j);
                 const int cls = meta & 7;
                 const int64_t d0 = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.w, j) << 32) |
@@ -780,21 +805,18 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 uint32_t m_old = 0, e_old = 0;
                 if (a.prev_refined) {
                     if (EXT) {
-                        e_old = (ebase + v * ns)[col];
+                        e_old = (ebase + row)[col];
                         __builtin_amdgcn_s_waitcnt(kWaitVm0);
                         d = D + e_old;
                     } else {
-                        m_old = (obase + v * ns)[col];
+                        m_old = (obase + row)[col];
                         __builtin_amdgcn_s_waitcnt(kWaitVm0);
                         if (m_old != 0) d = q16(D, factor_of(m_old, slow, cls));
                     }
                 }
                 const int64_t fv = sv + d;
                 fprev = fv;
-                bool busy = false;
-    #pragma unroll
-                for (int k = 0; k < kStreams; ++k)
-                    if (k < ncs) busy |= cs[k] < fv;
+                const bool busy = cmin < fv;
                 uint32_t m = 0;                            // types of the comm ops overlapping v
                 int64_t o = 0;                             // covered length (PRORATE)
                 int64_t smax[kTypes];                      // FOREST: largest S per overlapping type
@@ -896,6 +918,9 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                         }
                     }
                     __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                    cmin = kInf;
+#pragma unroll
+                    for (int k = 0; k < kStreams; ++k) cmin = cs[k] < cmin ? cs[k] : cmin;
                 }
 #undef NOTE_FOREST
                 if (EXT) {
@@ -909,11 +934,11 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                         e = x >= (int64_t)kExtLimit ? kExtLimit : (uint32_t)x;
                     }
                     if (DETECT) changed |= e != e_old;
-                    (ebase + v * ns)[col] = e;
+                    (ebase + row)[col] = e;
                 } else {
                     if (DETECT && m != m_old)
                         changed |= (m == 0 ? D : q16(D, factor_of(m, slow, cls))) != d;
-                    (obase + v * ns)[col] = (uint8_t)m;
+                    (obase + row)[col] = (uint8_t)m;
                 }
             }
         }
