@@ -73,7 +73,8 @@ def cpu_baseline(g, sc, n_refine, n_sample):
     import oracle
     from workloads import scenarios
     sub = scenarios.take(sc, slice(0, n_sample))
-    threads = max(1, min(n_sample, os.cpu_count() or 1))
+    # at most 16 threads: the host cores one GPU's share of the machine comes with
+    threads = max(1, min(n_sample, 16, len(os.sched_getaffinity(0))))
     t = time.perf_counter()
     oracle.run(g, sub, n_refine, threads=threads, timelines=False)
     dt = time.perf_counter() - t
@@ -104,7 +105,7 @@ def main():
                     help="validator variant: refine until no duration changes (at most --refine times)")
     ap.add_argument("--prorate", action="store_true",
                     help="validator variant: inflate only the overlapped part of a compute op")
-    ap.add_argument("--cpu-sample", type=int, default=8, help="scenarios the CPU oracle composes (0 = skip)")
+    ap.add_argument("--cpu-sample", type=int, default=48, help="scenarios the CPU oracle composes (0 = skip)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device once (calibrates HBM byte counters) and exit")
     args = ap.parse_args()

@@ -426,30 +426,32 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             // (fast bits exist only below nb, so the run ends there at the latest)
             const int run_end = j + (int)__builtin_ctzll(~(fast_bits >> j));
             int64_t s0 = lf[0];
-// ALL: the pass stores every start and finish, so the items' own needs are not consulted
-#define FAST_RUN(ALL)                                                                            \
+// ALL: the pass stores every start and finish, so the items' own needs are not consulted;
+// JIT: some lane draws jitter (the branch stays out of the loop)
+#define FAST_RUN(ALL, JIT)                                                                       \
             for (; j < run_end; ++j) {                                                           \
                 const int32_t op = __builtin_amdgcn_readlane(cur.x, j);                          \
                 const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);             \
                 const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) | \
                                               (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32)); \
-                int64_t d = any_jitter ? jittered(dur, op, jbase, amp) : dur;                    \
+                int64_t d = (JIT) ? jittered(dur, op, jbase, amp) : dur;                         \
                 if (REFINED && item_kind(meta) == ECHO_COMPUTE)                                  \
                     d = PRORATE ? d + fst32[j * kLanes + lane]                                   \
                                 : inflate(d, fst[j * kLanes + col], slow, item_class(meta), lane); \
                 const int64_t f = s0 + d;                                                        \
                 if ((ALL) || (meta & kNeedS)) put(sbase + (int64_t)op * ns + col, s0);           \
                 if ((ALL) || (meta & kNeedF)) put(fbase + (int64_t)op * ns + col, f);            \
-                hi_or |= (uint32_t)((uint64_t)f >> 32);                                          \
                 if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)s0) ^ (uint64_t)f);     \
                 s0 = f;                                                                          \
             }
             if (keep) {
-                FAST_RUN(true)
+                if (any_jitter) FAST_RUN(true, true) else FAST_RUN(true, false)
             } else {
-                FAST_RUN(false)
+                if (any_jitter) FAST_RUN(false, true) else FAST_RUN(false, false)
             }
 #undef FAST_RUN
+            // durations are never negative: the run's last finish is its latest time
+            hi_or |= (uint32_t)((uint64_t)s0 >> 32);
             lf[0] = s0;
             if (j >= nb) break;
             const int32_t op = __builtin_amdgcn_readlane(cur.x, j);
