@@ -518,15 +518,16 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
         std::vector<int32_t> latest(kStreams);
         std::vector<int64_t> busy(npair), total(npair);
         std::vector<int> slot(npair);
-        std::vector<uint8_t> noreg(n, 0);
-        std::vector<int32_t> first_succ;                // walk position of the first successor
-        std::vector<int32_t> due;                       // kNoReg comm ops, by first successor
-        std::vector<std::pair<int32_t, int32_t>> sched;
+        std::vector<int32_t> first_succ(n, -1);         // walk position of a comm op's first successor
+        std::vector<std::pair<int32_t, int32_t>> sched; // (position, comm op) of the resolve items
         auto pair_of = [&](int64_t v, int64_t r0) { return (int)((d->op_rank[v] - r0) * kStreams + d->op_stream[v]); };
-        auto emit_resolve = [&](int32_t v) {
+        // resolve item of comm op v: its barrier wait and finish; sv = its register slot
+        // (-1: none), fold: also raise slot 0 to that finish for the compute op that follows
+        auto emit_resolve = [&](int32_t v, int sv, bool fold) {
             WalkItem it{};
             it.op = v;
-            it.meta = (uint32_t)kResolve | kNoReg;
+            it.meta = (uint32_t)kResolve | ((uint32_t)(sv >= 0 ? sv : 0) << 2) | (sv < 0 ? kNoReg : 0u) |
+                      (fold ? kFold : 0u);
             it.far_off = (int32_t)far.size();
             it.coll = (int32_t)d->op_coll[v];
             it.dur = 0;
@@ -556,53 +557,59 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
                 slot[top] = 0;
                 for (int k = 0; k < (int)rest.size(); ++k) slot[rest[k]] = k + 1 < kStreams ? k + 1 : -1;
             }
-            for (int64_t i = lo; i < hi; ++i) noreg[i] = slot[pair_of(i, r0)] < 0;
-            // comm ops without a slot are finished by a resolve item placed before
-            // their first successor in the walk (or at its end)
+            // Every comm op is finished by a resolve item placed right before its first
+            // successor in the walk (or at the walk's end): its barrier is waited for as
+            // late as the walk allows, and every reader of its slot comes after.
             sched.clear();
-            if (rpw > 1) {
-                if (first_succ.empty()) first_succ.assign(n, -1);
-                for (int64_t i = lo; i < hi; ++i) {
-                    const int32_t v = order[i];
-                    for (int32_t j = poff[v]; j < poff[v + 1]; ++j) {
-                        const int32_t u = preds[j];
-                        if (d->op_kind[u] == ECHO_COMM && noreg[u] && first_succ[u] < 0) {
-                            first_succ[u] = (int32_t)(i - lo);
-                            sched.emplace_back((int32_t)(i - lo), u);
-                        }
+            for (int64_t i = lo; i < hi; ++i) {
+                const int32_t v = order[i];
+                for (int32_t j = poff[v]; j < poff[v + 1]; ++j) {
+                    const int32_t u = preds[j];
+                    if (d->op_kind[u] == ECHO_COMM && first_succ[u] < 0) {
+                        first_succ[u] = (int32_t)(i - lo);
+                        sched.emplace_back((int32_t)(i - lo), u);
                     }
                 }
-                for (int64_t i = lo; i < hi; ++i) {
-                    const int32_t v = order[i];
-                    if (d->op_kind[v] == ECHO_COMM && noreg[v] && first_succ[v] < 0)
-                        sched.emplace_back((int32_t)(hi - lo), v);
-                }
-                std::stable_sort(sched.begin(), sched.end(),
-                                 [](const std::pair<int32_t, int32_t> &x, const std::pair<int32_t, int32_t> &y) {
-                                     return x.first < y.first;
-                                 });
             }
+            for (int64_t i = lo; i < hi; ++i) {
+                const int32_t v = order[i];
+                if (d->op_kind[v] == ECHO_COMM && first_succ[v] < 0) sched.emplace_back((int32_t)(hi - lo), v);
+            }
+            std::stable_sort(sched.begin(), sched.end(),
+                             [](const std::pair<int32_t, int32_t> &x, const std::pair<int32_t, int32_t> &y) {
+                                 return x.first < y.first;
+                             });
             size_t next_due = 0;
             std::fill(latest.begin(), latest.end(), -1);
             for (int64_t i = lo; i < hi; ++i) {
-                while (next_due < sched.size() && sched[next_due].first == i - lo) emit_resolve(sched[next_due++].second);
                 const int32_t v = order[i];
+                const int sv = slot[pair_of(v, r0)];
+                size_t due_end = next_due;
+                while (due_end < sched.size() && sched[due_end].first == i - lo) ++due_end;
+                // a compute/memcpy op of slot 0 whose other predecessors are exactly the comm ops
+                // resolved right before it: the resolve items raise slot 0 to their finishes and
+                // the op becomes a fast one (start = slot 0)
+                bool fold = due_end > next_due && d->op_kind[v] != ECHO_COMM && sv == 0;
+                for (int32_t j = poff[v]; fold && j < poff[v + 1]; ++j) {
+                    const int32_t u = preds[j];
+                    fold = u == latest[0] || (d->op_kind[u] == ECHO_COMM && first_succ[u] == i - lo);
+                }
+                for (; next_due < due_end; ++next_due) {
+                    const int32_t u = sched[next_due].second;
+                    emit_resolve(u, slot[pair_of(u, r0)], fold);
+                }
                 unsigned mask = 0;
                 const int64_t f0 = (int64_t)far.size();
                 for (int32_t j = poff[v]; j < poff[v + 1]; ++j) {
                     const int32_t u = preds[j];
+                    if (fold && u != latest[0]) continue;          // folded into slot 0
                     const int su = slot[pair_of(u, r0)];
                     if (su >= 0 && latest[su] == u) mask |= 1u << su;
                     else far.push_back(u);
                 }
-                const int sv = slot[pair_of(v, r0)];
-                int32_t prev = -1;
-                if (sv >= 0) {
-                    prev = latest[sv];
-                    latest[sv] = v;
-                }
+                if (sv >= 0) latest[sv] = v;
                 const bool fast = d->op_kind[v] != ECHO_COMM && sv == 0 && (mask & ~1u) == 0 &&
-                                  (int64_t)far.size() == f0 && (prev < 0 || d->op_kind[prev] != ECHO_COMM);
+                                  (int64_t)far.size() == f0;
                 WalkItem it{};
                 it.op = v;
                 it.meta = (uint32_t)d->op_kind[v] | ((uint32_t)(sv >= 0 ? sv : 0) << 2) |
@@ -617,7 +624,10 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
                 it.dur = d->op_kind[v] == ECHO_COMM ? 0 : d->op_dur_ns[v];
                 items.push_back(it);
             }
-            while (next_due < sched.size()) emit_resolve(sched[next_due++].second);
+            while (next_due < sched.size()) {
+                const int32_t u = sched[next_due++].second;
+                emit_resolve(u, slot[pair_of(u, r0)], false);
+            }
             walk_off[w + 1] = (int64_t)items.size();
         }
     }

@@ -36,13 +36,14 @@ constexpr unsigned kStatusAbort = 8u;            // stop all waits (set with tim
 // stream) pairs of a walker are mapped to eight register "slots": slot 0 is
 // its busiest compute/memcpy stream, so most items only touch slot 0.  Pairs
 // left without a slot (a walker of several ranks) keep nothing in registers:
-// their ops carry kNoReg, their successors read them back from memory, and a
-// comm op among them is finished by a resolve item placed before its first
-// successor.
+// their ops carry kNoReg and their successors read them back from memory.
+// A comm op's launch item publishes its arrival; a resolve item placed right
+// before its first successor waits for the barrier and writes its finish (to its
+// slot, or only to memory without one).
 struct WalkItem {
     int32_t op;         // op id: row of the [op][scenario] outputs
     uint32_t meta;      // kind | slot << 2 | class << 5 | regmask << 8 | fast << 16 | noreg << 17
-                        // | need start << 18 | need finish << 19
+                        // | need start << 18 | need finish << 19 | fold << 20
     int32_t far_off;    // predecessors read back from memory: far[far_off .. +nfar)
     int32_t coll;       // collective of a comm op, -1 otherwise
     int64_t dur;        // base duration of compute / memcpy ops
@@ -51,8 +52,9 @@ struct WalkItem {
 };
 static_assert(sizeof(WalkItem) == 32, "walk item must stay 32 bytes");
 
-// A "fast" item is a compute/memcpy op on slot 0 whose only predecessor is
-// the previous op of slot 0, itself not a comm op: its start is that op's finish.
+// A "fast" item is a compute/memcpy op on slot 0 whose start is slot 0's value:
+// its only predecessors are the previous op of slot 0 and comm ops whose resolve
+// items, right before it, folded their finishes into slot 0 (kFold).
 constexpr uint32_t kFast = 1u << 16;
 // The op's (rank, stream) pair has no register slot.
 constexpr uint32_t kNoReg = 1u << 17;
@@ -63,6 +65,8 @@ constexpr uint32_t kNoReg = 1u << 17;
 // far predecessors.
 constexpr uint32_t kNeedS = 1u << 18;
 constexpr uint32_t kNeedF = 1u << 19;
+// Resolve item: after writing the comm op's finish, raise slot 0 to it.
+constexpr uint32_t kFold = 1u << 20;
 // Item kind (besides compute/comm/memcpy) that finishes a kNoReg comm op:
 // wait for its barrier, then write its finish.
 constexpr int kResolve = 3;

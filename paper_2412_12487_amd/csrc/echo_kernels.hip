@@ -258,7 +258,6 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     __shared__ unsigned long long lbar[kChannels][2][kLanes];   // per channel and slot: latest launch per lane
     __shared__ unsigned lcnt[kChannels][2];                      // per channel and slot: members arrived
     __shared__ int64_t ccost[kClassSlots][kLanes];               // staged class costs of this tile
-    __shared__ int32_t pinfo[kBlockWalkers][kStreams][3];          // per wave and slot: pending collective, op, aux
     __shared__ uint32_t slow[REFINED && !PRORATE ? kClasses * kTypes * kLanes : 1];   // lanes' slowdown tables
     static_assert(kBlockWalkers * 4 == kClasses * kTypes, "one 16-byte table slice per wavefront");
 
@@ -309,13 +308,11 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     uint8_t *const fst = reinterpret_cast<uint8_t *>(fstage) + (REFINED && !PRORATE ? wave * kBlock * kLanes : 0);
     uint32_t *const fst32 = fstage + (REFINED && PRORATE ? wave * kBlock * kLanes : 0);
 
-    // Per slot: finish of the latest op, or (bit j of `pending`) a comm op still
-    // waiting for its barrier, described in this wave's row of pinfo.
+    // Per slot: finish of the latest op (of a comm op: once its resolve item ran;
+    // no item reads the slot in between).
     int64_t lf[kStreams];
 #pragma unroll
     for (int j = 0; j < kStreams; ++j) lf[j] = 0;
-    uint32_t pending = 0;
-    int32_t (*const pend)[3] = pinfo[wave];
     // A wait that gave up (timeout or abort) marks the wave dead: it finishes its
     // list without waiting again; the times it writes are meaningless and the
     // status word already reports the failure.
@@ -377,16 +374,6 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             const int64_t s_ = (sbase + (int64_t)(v_) * ns)[col];                                \
             dig += mix64(mix64((uint64_t)(v_) ^ (uint64_t)s_) ^ (uint64_t)(f_));                 \
         }                                                                                        \
-    }
-
-// Finish of the comm op pending on slot j.
-#define RESOLVE(j)                                                                               \
-    if (pending & (1u << j)) {                                                                   \
-        const int32_t pc_ = __builtin_amdgcn_readfirstlane(pend[j][0]);                          \
-        const int32_t pv_ = __builtin_amdgcn_readfirstlane(pend[j][1]);                          \
-        const uint32_t px_ = (uint32_t)__builtin_amdgcn_readfirstlane(pend[j][2]);               \
-        MEET(pc_, pv_, px_, lf[j])                                                               \
-        pending &= ~(1u << j);                                                                   \
     }
 
     for (int64_t blk0 = beg; blk0 < end; blk0 += kBlock) {
@@ -463,24 +450,27 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             const int32_t coll = __builtin_amdgcn_readlane(cur.w, j);
             const int32_t nfar = __builtin_amdgcn_readlane(cur.z, j + 32);
             const uint32_t aux = (uint32_t)__builtin_amdgcn_readlane(cur.w, j + 32);
+            const int st = item_stream(meta);
             if (kind == kResolve) {
-                // a comm op without a register slot: its barrier is due before its first successor
+                // a comm op's barrier, due right before its first successor
                 int64_t f;
                 MEET(coll, op, aux, f)
-                xmax = f > xmax ? f : xmax;
+                if (meta & kNoReg) {
+                    xmax = f > xmax ? f : xmax;
+                } else {
+#pragma unroll
+                    for (int q = 0; q < kStreams; ++q)
+                        if (q == st) lf[q] = f;
+                }
+                if (meta & kFold) lf[0] = f > lf[0] ? f : lf[0];
                 ++j;
                 continue;
             }
-            const int st = item_stream(meta);
             const unsigned mask = item_regmask(meta);
             int64_t ready = 0;
 #pragma unroll
-            for (int q = 0; q < kStreams; ++q) {
-                if (mask & (1u << q)) {
-                    RESOLVE(q)
-                    ready = lf[q] > ready ? lf[q] : ready;
-                }
-            }
+            for (int q = 0; q < kStreams; ++q)
+                if (mask & (1u << q)) ready = lf[q] > ready ? lf[q] : ready;
             for (int32_t q = 0; q < nfar; ++q) {
                 const int64_t u = a.far[far_off + q];
                 const int64_t fu = (fbase + u * ns)[col];
@@ -505,14 +495,6 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                         __hip_atomic_fetch_add(a.count + (int64_t)coll * a.n_tiles + tile, 1u, __ATOMIC_RELAXED,
                                                __HIP_MEMORY_SCOPE_AGENT);
                 }
-                if (!(meta & kNoReg)) {
-                    if (lane == 0) {
-                        pend[st][0] = coll;
-                        pend[st][1] = op;
-                        pend[st][2] = (int32_t)aux;
-                    }
-                    pending |= 1u << st;
-                }
             } else {
                 int64_t d = any_jitter ? jittered(dur, op, jbase, amp) : dur;
                 if (REFINED && kind == ECHO_COMPUTE)
@@ -532,9 +514,6 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             ++j;
         }
     }
-#pragma unroll
-    for (int q = 0; q < kStreams; ++q) { RESOLVE(q) }
-#undef RESOLVE
 #undef MEET
     if (hi_or >> 30) err |= kStatusOverflow;
     if (active && err) __hip_atomic_fetch_or(a.status, err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
