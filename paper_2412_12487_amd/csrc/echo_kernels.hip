@@ -310,9 +310,10 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
 
     // Per slot: finish of the latest op (of a comm op: once its resolve item ran;
     // no item reads the slot in between).
-    int64_t lf[kStreams];
+    // (entry kStreams: where ops without a slot put their finish; never read as a slot)
+    int64_t lf[kStreams + 1];
 #pragma unroll
-    for (int j = 0; j < kStreams; ++j) lf[j] = 0;
+    for (int j = 0; j <= kStreams; ++j) lf[j] = 0;
     // A wait that gave up (timeout or abort) marks the wave dead: it finishes its
     // list without waiting again; the times it writes are meaningless and the
     // status word already reports the failure.
@@ -455,22 +456,18 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 // a comm op's barrier, due right before its first successor
                 int64_t f;
                 MEET(coll, op, aux, f)
-                if (meta & kNoReg) {
-                    xmax = f > xmax ? f : xmax;
-                } else {
-#pragma unroll
-                    for (int q = 0; q < kStreams; ++q)
-                        if (q == st) lf[q] = f;
-                }
+                xmax = f > xmax ? f : xmax;
+                lf[__builtin_amdgcn_readfirstlane((meta & kNoReg) ? kStreams : st)] = f;
                 if (meta & kFold) lf[0] = f > lf[0] ? f : lf[0];
                 ++j;
                 continue;
             }
             const unsigned mask = item_regmask(meta);
             int64_t ready = 0;
-#pragma unroll
-            for (int q = 0; q < kStreams; ++q)
-                if (mask & (1u << q)) ready = lf[q] > ready ? lf[q] : ready;
+            for (unsigned m = mask; m; m &= m - 1) {
+                const int q = __builtin_amdgcn_readfirstlane(__builtin_ctz(m));
+                ready = lf[q] > ready ? lf[q] : ready;
+            }
             for (int32_t q = 0; q < nfar; ++q) {
                 const int64_t u = a.far[far_off + q];
                 const int64_t fu = (fbase + u * ns)[col];
@@ -503,13 +500,8 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 if ((meta | keep) & kNeedF) put(fbase + (int64_t)op * ns + col, f);
                 if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)ready) ^ (uint64_t)f);
-                if (meta & kNoReg) {
-                    xmax = f > xmax ? f : xmax;
-                } else {
-#pragma unroll
-                    for (int q = 0; q < kStreams; ++q)
-                        if (q == st) lf[q] = f;
-                }
+                xmax = f > xmax ? f : xmax;
+                lf[__builtin_amdgcn_readfirstlane((meta & kNoReg) ? kStreams : st)] = f;
             }
             ++j;
         }
