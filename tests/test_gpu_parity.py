@@ -218,6 +218,26 @@ def test_config3_gpt175b_1024ranks_sampled(E):
     assert (gpu["step"] > 0).all()
 
 
+def test_config3_every_pass_is_one_launch(E):
+    """All 256 scenarios (four tiles) of the 1024-rank graph fit the device at once in
+    every walk variant of a plain and a digest compose: a kernel that outgrew its register
+    or LDS budget would split a pass into several launches and double its time."""
+    import torch
+    g = configs.graph(3)
+    d, n = E.scenarios_to_device(configs.scenario_batch(3))
+    G = E.Graph(g, 0)
+    try:
+        G.set_timing(True)
+        for digest in (False, True):
+            out = G.compose(d, n, 1, timelines=True, digest=digest)
+            torch.cuda.synchronize()
+            kinds = [k for k, _ in G.kernel_times()]
+            assert kinds.count("walk") == 2, kinds
+            del out
+    finally:
+        G.close()
+
+
 # graph 6 has 8192 ranks: more than the device holds wavefronts, so it is walked
 # with several ranks per wavefront
 @pytest.mark.parametrize("index", [0, 3, 6] if not os.environ.get("ECHO_FULL") else list(range(16)))
