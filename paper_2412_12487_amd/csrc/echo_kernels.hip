@@ -651,6 +651,8 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     const uint32_t *slow = &sc->slowdown_q16[0][0];
     const uint64_t jbase = jitter_base(sc->jitter_seed, sc->jitter_stream);
     const int32_t amp = sc->jitter_amp_q16;
+    // one branch for the wavefront: a lane without jitter draws the identity factor
+    const bool any_jitter = __builtin_amdgcn_readfirstlane(__ballot(amp != 0) != 0);
     const int64_t *cl_off = a.cl_off + (int64_t)r * kStreams;
     const int64_t *cp_off = a.cp_off + (int64_t)r * kStreams;
     bool changed = false;                        // some duration differs from the previous pass's
@@ -762,7 +764,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 // left pending, they would make the compiler wait at the next join, on
                 // every path, for the previous op's store as well.
                 int64_t sv = fprev;
-                if (!(meta & kChained)) {
+                if (__builtin_expect(!(meta & kChained), 0)) {
                     const int ord = __builtin_popcountll(unchained & ((uint64_t(1) << j) - 1));
                     if (ord < kPre) {
 #pragma unroll
@@ -773,7 +775,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                         __builtin_amdgcn_s_waitcnt(kWaitVm0);
                     }
                 }
-                const int64_t D = amp != 0 ? jittered(d0, (int32_t)v, jbase, amp) : d0;
+                const int64_t D = any_jitter ? jittered(d0, (int32_t)v, jbase, amp) : d0;
                 int64_t d = D;                   // the duration v ran with in the previous pass
                 uint32_t m_old = 0, e_old = 0;
                 if (a.prev_refined) {
