@@ -13,7 +13,10 @@ LIB = os.path.join(HERE, "libecho.so")
 ARCH = "gfx950"
 
 # -packed-fp32-ops: keep the compiler from emitting packed FP32 VALU forms.
-DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# atomic optimizer off: the kernels' same-address atomics already come from one lane
+# (arrival counts), and the optimizer's lane-count prologue only lengthens the barrier path.
+DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", INCLUDE, "-I", CSRC]
 
 
