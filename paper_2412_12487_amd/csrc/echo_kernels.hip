@@ -258,6 +258,10 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     __shared__ unsigned long long lbar[kChannels][2][kLanes];   // per channel and slot: latest launch per lane
     __shared__ unsigned lcnt[kChannels][2];                      // per channel and slot: members arrived
     __shared__ int64_t ccost[kClassSlots][kLanes];               // staged class costs of this tile
+    // slots 1..7 of every wave (slot 0 stays in a register); the prorating refined
+    // pass has no LDS left for them and keeps them in registers
+    constexpr bool kLdsSlots = !(REFINED && PRORATE);
+    __shared__ int64_t slotmem[kLdsSlots ? kBlockWalkers * kStreams * kLanes : 1];
     __shared__ uint32_t slow[REFINED && !PRORATE ? kClasses * kTypes * kLanes : 1];   // lanes' slowdown tables
     static_assert(kBlockWalkers * 4 == kClasses * kTypes, "one 16-byte table slice per wavefront");
 
@@ -311,9 +315,25 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     // Per slot: finish of the latest op (of a comm op: once its resolve item ran;
     // no item reads the slot in between).
     // (entry kStreams: where ops without a slot put their finish; never read as a slot)
-    int64_t lf[kStreams + 1];
+    int64_t lf0 = 0;
+    int64_t lf[kLdsSlots ? 1 : kStreams + 1];
+    int64_t *const smem = slotmem + (kLdsSlots ? wave * kStreams * kLanes + lane : 0);
+    if (kLdsSlots) {
 #pragma unroll
-    for (int j = 0; j <= kStreams; ++j) lf[j] = 0;
+        for (int j = 1; j < kStreams; ++j) smem[j * kLanes] = 0;
+    } else {
+#pragma unroll
+        for (int j = 0; j <= kStreams; ++j) lf[j] = 0;
+    }
+    // slot q (q >= 1, wave-uniform); q == kStreams: the entry of ops without a slot
+    auto slot_get = [&](int q) -> int64_t { return kLdsSlots ? smem[q * kLanes] : lf[q]; };
+    auto slot_set = [&](int q, int64_t f) {
+        if (kLdsSlots) {
+            if (q < kStreams) smem[q * kLanes] = f;
+        } else {
+            lf[q] = f;
+        }
+    };
     // A wait that gave up (timeout or abort) marks the wave dead: it finishes its
     // list without waiting again; the times it writes are meaningless and the
     // status word already reports the failure.
@@ -413,7 +433,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             // a run of fast items: compute/memcpy ops right after the previous op of slot 0
             // (fast bits exist only below nb, so the run ends there at the latest)
             const int run_end = j + (int)__builtin_ctzll(~(fast_bits >> j));
-            int64_t s0 = lf[0];
+            int64_t s0 = lf0;
 // ALL: the pass stores every start and finish, so the items' own needs are not consulted;
 // JIT: some lane draws jitter (the branch stays out of the loop)
 #define FAST_RUN(ALL, JIT)                                                                       \
@@ -440,7 +460,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
 #undef FAST_RUN
             // durations are never negative: the run's last finish is its latest time
             hi_or |= (uint32_t)((uint64_t)s0 >> 32);
-            lf[0] = s0;
+            lf0 = s0;
             if (j >= nb) break;
             const int32_t op = __builtin_amdgcn_readlane(cur.x, j);
             const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);
@@ -457,16 +477,19 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 int64_t f;
                 MEET(coll, op, aux, f)
                 xmax = f > xmax ? f : xmax;
-                lf[__builtin_amdgcn_readfirstlane((meta & kNoReg) ? kStreams : st)] = f;
-                if (meta & kFold) lf[0] = f > lf[0] ? f : lf[0];
+                const int sq = __builtin_amdgcn_readfirstlane((meta & kNoReg) ? kStreams : st);
+                if (sq == 0) lf0 = f;
+                else slot_set(sq, f);
+                if (meta & kFold) lf0 = f > lf0 ? f : lf0;
                 ++j;
                 continue;
             }
             const unsigned mask = item_regmask(meta);
             int64_t ready = 0;
-            for (unsigned m = mask; m; m &= m - 1) {
-                const int q = __builtin_amdgcn_readfirstlane(__builtin_ctz(m));
-                ready = lf[q] > ready ? lf[q] : ready;
+            if (mask & 1u) ready = lf0;
+            for (unsigned m = mask & ~1u; m; m &= m - 1) {
+                const int64_t x = slot_get(__builtin_amdgcn_readfirstlane(__builtin_ctz(m)));
+                ready = x > ready ? x : ready;
             }
             for (int32_t q = 0; q < nfar; ++q) {
                 const int64_t u = a.far[far_off + q];
@@ -501,7 +524,9 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 if ((meta | keep) & kNeedF) put(fbase + (int64_t)op * ns + col, f);
                 if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)ready) ^ (uint64_t)f);
                 xmax = f > xmax ? f : xmax;
-                lf[__builtin_amdgcn_readfirstlane((meta & kNoReg) ? kStreams : st)] = f;
+                const int sq = __builtin_amdgcn_readfirstlane((meta & kNoReg) ? kStreams : st);
+                if (sq == 0) lf0 = f;
+                else slot_set(sq, f);
             }
             ++j;
         }
@@ -512,9 +537,9 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     if (FINAL && active && !dead) {
         // finishes along a FIFO stream never decrease: the last op of each slot holds its
         // maximum; ops without a slot went into xmax
-        int64_t smax = xmax;
+        int64_t smax = lf0 > xmax ? lf0 : xmax;
 #pragma unroll
-        for (int q = 0; q < kStreams; ++q) smax = lf[q] > smax ? lf[q] : smax;
+        for (int q = 1; q < kStreams; ++q) smax = slot_get(q) > smax ? slot_get(q) : smax;
         __hip_atomic_fetch_max(reinterpret_cast<unsigned long long *>(a.step) + sigma, (unsigned long long)smax,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (DIGEST)
