@@ -590,7 +590,7 @@ __device__ __forceinline__ uint32_t factor_of(uint32_t m, const uint32_t *slow, 
 // walk stops at a leaf; paths are at most ECHO_TREE_DEPTH splits long).
 constexpr int kForestLanes = 8;
 constexpr int kPre = 8;          // unchained starts prefetched per round of overlap detection
-constexpr int kIdStage = 2048;   // comm ops of a rank whose ids overlap detection keeps in LDS
+constexpr int kIdStage = 1024;   // comm ops of a rank whose ids overlap detection keeps in LDS
 
 // feat: this wavefront's LDS feature rows, feature k of lane l at feat[k * 64 + l].
 __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_t *smax, const int32_t *nmax,
@@ -658,6 +658,8 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     __shared__ int64_t feat[FOREST ? 12 * kLanes : 1];   // the ensemble's feature vectors, one per lane
     __shared__ int32_t sid[kIdStage];            // the rank's comm op ids and collective types, staged
     __shared__ uint8_t stype[kIdStage];
+    // masks of the round's ops, [op][lane]: written out row by row once per round
+    __shared__ __align__(16) uint8_t mstage[EXT ? 16 : kLanes * kLanes];
     if (a.stable && __builtin_amdgcn_readfirstlane(__hip_atomic_load(a.stable, __ATOMIC_RELAXED,
                                                                       __HIP_MEMORY_SCOPE_AGENT)))
         return;                                  // every scenario is at its fixed point
@@ -938,8 +940,15 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 } else {
                     if (DETECT && m != m_old)
                         changed |= (m == 0 ? D : q16(D, factor_of(m, slow, cls))) != d;
-                    (obase + row)[col] = (uint8_t)m;
+                    mstage[j * kLanes + lane] = (uint8_t)m;
                 }
+            }
+            if (!EXT && lane < nr) {
+                // lane L writes the 64 masks of the round's op L to that op's row
+                const uint4 *const src = reinterpret_cast<const uint4 *>(mstage + lane * kLanes);
+                uint4 *const dst = reinterpret_cast<uint4 *>(obase + (int64_t)cur_pos * a.mstride);
+#pragma unroll
+                for (int q = 0; q < kLanes / 16; ++q) dst[q] = src[q];
             }
         }
     }
