@@ -106,7 +106,7 @@ __global__ __launch_bounds__(64) void k_cc_cost(CollTable t, const echo_cc_table
     const int64_t S = t.bytes[c];
     const int64_t N = t.N[c], M = t.M[c], K = t.K[c];
     const unsigned __int128 n1 = (unsigned __int128)(N - 1);
-    for (int32_t s = threadIdx.x; s < n_scen; s += blockDim.x) {
+    for (int64_t s = (int64_t)blockIdx.y * blockDim.x + threadIdx.x; s < n_scen; s += (int64_t)gridDim.y * blockDim.x) {
         const echo_scenario &sc = scen[s];
         // invalid knobs are reported by k_init; keep the divisions defined
         const int64_t bwa = sc.bw_intra_MBps >= 1 ? sc.bw_intra_MBps : 1;
@@ -1008,7 +1008,10 @@ hipError_t launch_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *
 hipError_t launch_cc_cost(const CollTable &t, const echo_cc_table *tables, const echo_scenario *scen,
                           int32_t n_scen, int64_t *cost, unsigned *status, hipStream_t stream) {
     if (t.n == 0 || n_scen == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_cc_cost, dim3((unsigned)t.n), dim3(64), 0, stream, t, tables, scen, n_scen, cost, status);
+    // one lane per (collective, scenario): collectives along x, 64-scenario tiles along y
+    const unsigned tiles = (unsigned)std::min<int64_t>((n_scen + 63) / 64, 65535);
+    hipLaunchKernelGGL(k_cc_cost, dim3((unsigned)t.n, tiles), dim3(64), 0, stream, t, tables, scen, n_scen, cost,
+                       status);
     return hipGetLastError();
 }
 
