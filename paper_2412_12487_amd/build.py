@@ -34,7 +34,7 @@ def build(verbose: bool = False) -> str:
     _run(["hipcc", "-c", *DEVICE_FLAGS, *COMMON, os.path.join(CSRC, "echo_kernels.hip"), "-o", kobj], verbose)
     _run(["hipcc", "-c", *COMMON, os.path.join(CSRC, "echo_host.cpp"), "-o", hobj], verbose)
     tmp = LIB + ".tmp"
-    _run(["hipcc", "-shared", "-fPIC", *DEVICE_FLAGS, kobj, hobj, "-o", tmp], verbose)
+    _run(["hipcc", "-shared", "-fPIC", "--offload-arch=" + ARCH, kobj, hobj, "-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 
