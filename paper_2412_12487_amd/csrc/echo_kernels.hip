@@ -782,7 +782,8 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
             }
             for (int j = 0; j < nr; ++j) {
                 const int64_t v = __builtin_amdgcn_readlane(cur.x, j);
-                const int64_t row = (int64_t)__builtin_amdgcn_readlane(cur_pos, j) * a.mstride;   // v's item
+                // v's row of the per-item outputs (computed where used: the common path needs none)
+                auto row = [&]() { return (int64_t)__builtin_amdgcn_readlane(cur_pos, j) * a.mstride; };
                 const int meta = __builtin_amdgcn_readlane(cur.y, j);
                 const int cls = meta & 7;
                 const int64_t d0 = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.w, j) << 32) |
@@ -807,11 +808,11 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 uint32_t m_old = 0, e_old = 0;
                 if (a.prev_refined) {
                     if (EXT) {
-                        e_old = (ebase + row)[col];
+                        e_old = (ebase + row())[col];
                         __builtin_amdgcn_s_waitcnt(kWaitVm0);
                         d = D + e_old;
                     } else {
-                        m_old = (obase + row)[col];
+                        m_old = (obase + row())[col];
                         __builtin_amdgcn_s_waitcnt(kWaitVm0);
                         if (m_old != 0) d = q16(D, factor_of(m_old, slow, cls));
                     }
@@ -936,7 +937,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                         e = x >= (int64_t)kExtLimit ? kExtLimit : (uint32_t)x;
                     }
                     if (DETECT) changed |= e != e_old;
-                    (ebase + row)[col] = e;
+                    (ebase + row())[col] = e;
                 } else {
                     if (DETECT && m != m_old)
                         changed |= (m == 0 ? D : q16(D, factor_of(m, slow, cls))) != d;
