@@ -637,6 +637,16 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
         // what a pass without caller-visible timelines must still store
         std::vector<uint32_t> need(n, 0);
         for (int32_t u : far) need[u] |= kNeedF;
+        // the last op of every overlap-detection block of a (rank, stream) compute list
+        std::vector<int32_t> n_compute(R * kStreams, 0), i_compute(R * kStreams, 0);
+        for (int64_t v = 0; v < n; ++v)
+            if (d->op_kind[v] == ECHO_COMPUTE) ++n_compute[(int64_t)d->op_rank[v] * kStreams + d->op_stream[v]];
+        for (int64_t v = 0; v < n; ++v)
+            if (d->op_kind[v] == ECHO_COMPUTE) {
+                const int64_t k = (int64_t)d->op_rank[v] * kStreams + d->op_stream[v];
+                const int32_t i = i_compute[k]++;
+                if (i % kOverlapBlock == kOverlapBlock - 1 || i == n_compute[k] - 1) need[v] |= kNeedF;
+            }
         std::vector<int32_t> prev_on_stream(R * kStreams, -1);
         for (int64_t v = 0; v < n; ++v) {
             const int64_t k = (int64_t)d->op_rank[v] * kStreams + d->op_stream[v];

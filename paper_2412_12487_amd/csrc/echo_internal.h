@@ -110,6 +110,10 @@ static_assert(sizeof(ComputeRec) == 16, "compute record must stay 16 bytes");
 // Compute op whose only predecessor is the previous compute op of its stream:
 // it starts exactly when that op finishes.
 constexpr uint32_t kChained = 0x80;
+// Overlap detection checks compute ops in blocks of kOverlapBlock (per (rank, stream)
+// list, from its start): the walk stores the finish of every block's last op, and a
+// block that ends before every comm cursor starts overlaps nothing.
+constexpr int kOverlapBlock = 8;
 
 // Inputs of the CC model for a table of collectives (or of cost classes).
 struct CollTable {

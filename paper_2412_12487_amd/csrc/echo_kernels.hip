@@ -655,6 +655,8 @@ __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_
 template <bool PRORATE, bool DETECT, bool FOREST>
 __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     constexpr bool EXT = PRORATE || FOREST;      // output: extra time per op instead of a mask
+    constexpr bool SKIP = !EXT && !DETECT;       // whole blocks of ops may be skipped
+    constexpr int NPRE = SKIP ? kPre / 2 : kPre; // (the block checks take the other registers)
     __shared__ int64_t feat[FOREST ? 12 * kLanes : 1];   // the ensemble's feature vectors, one per lane
     __shared__ int32_t sid[kIdStage];            // the rank's comm op ids and collective types, staged
     __shared__ uint8_t stype[kIdStage];
@@ -762,14 +764,29 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
             nxt = i0 + kLanes + lane < b1 ? recs[i0 + kLanes + lane] : make_int4(0, 0, 0, 0);
             nxt_pos = i0 + kLanes + lane < b1 ? a.cp_pos[i0 + kLanes + lane] : 0;
             const int nr = b1 - i0 < kLanes ? int(b1 - i0) : kLanes;
-            // the starts of the round's first kPre unchained ops, fetched together
+            // the starts of the round's first NPRE unchained ops, fetched together
             const uint64_t unchained = __builtin_amdgcn_read_exec() &
                                        __ballot(lane < nr && !((uint32_t)cur.y & kChained));
-            int64_t pre[kPre];
+            int64_t pre[NPRE];
+            // finishes of the round's blocks' last ops (stored by the walk): a block ending
+            // before every cursor starts is skipped whole
+            constexpr int kBlocks = kLanes / kOverlapBlock;
+            int64_t ck[SKIP ? kBlocks : 1];
+            if (SKIP) {
+#pragma unroll
+                for (int b = 0; b < kBlocks; ++b) {
+                    ck[b] = kInf;
+                    if (b * kOverlapBlock < nr) {
+                        const int jl = (b + 1) * kOverlapBlock - 1 < nr ? (b + 1) * kOverlapBlock - 1 : nr - 1;
+                        const int64_t vl = __builtin_amdgcn_readlane(cur.x, jl);
+                        ck[b] = (fbase + vl * ns)[col];
+                    }
+                }
+            }
             {
                 uint64_t um = unchained;
 #pragma unroll
-                for (int q = 0; q < kPre; ++q) {
+                for (int q = 0; q < NPRE; ++q) {
                     pre[q] = 0;
                     if (um) {
                         const int jq = __builtin_ctzll(um);
@@ -781,6 +798,20 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 __builtin_amdgcn_s_waitcnt(kWaitVm0);
             }
             for (int j = 0; j < nr; ++j) {
+                if (SKIP && (j & (kOverlapBlock - 1)) == 0) {
+                    int64_t c = kInf;
+#pragma unroll
+                    for (int b = 0; b < kBlocks; ++b)
+                        if (b == (j >> 3)) c = ck[b];
+                    if (!__builtin_amdgcn_readfirstlane(__ballot(c > cmin) != 0)) {
+                        // every op of the block ends by cmin: no overlaps, no cursor moves
+                        const int je = j + kOverlapBlock < nr ? j + kOverlapBlock : nr;
+                        for (int jj = j; jj < je; ++jj) mstage[jj * kLanes + lane] = 0;
+                        fprev = c;
+                        j = je - 1;
+                        continue;
+                    }
+                }
                 const int64_t v = __builtin_amdgcn_readlane(cur.x, j);
                 // v's row of the per-item outputs (computed where used: the common path needs none)
                 auto row = [&]() { return (int64_t)__builtin_amdgcn_readlane(cur_pos, j) * a.mstride; };
@@ -794,9 +825,9 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 int64_t sv = fprev;
                 if (__builtin_expect(!(meta & kChained), 0)) {
                     const int ord = __builtin_popcountll(unchained & ((uint64_t(1) << j) - 1));
-                    if (ord < kPre) {
+                    if (ord < NPRE) {
 #pragma unroll
-                        for (int q = 0; q < kPre; ++q)
+                        for (int q = 0; q < NPRE; ++q)
                             if (q == ord) sv = pre[q];
                     } else {
                         sv = (sbase + v * ns)[col];
