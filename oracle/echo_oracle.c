@@ -916,7 +916,7 @@ int oracle_run(int64_t n_ops, int32_t n_ranks, int32_t gpus_per_node, const int3
     /* the ensemble, if any: every tree at most TREE_DEPTH splits deep, indices in range */
     forest_t fo = {(const tree_node_t *)forest_nodes, n_nodes, forest_roots, n_trees, forest_base, class_metrics};
     if (n_trees > 0) {
-        if (!forest_nodes || !forest_roots || !class_metrics || n_nodes < 1 || forest_base < Q16_ONE
+        if (!forest_nodes || !forest_roots || !class_metrics || n_nodes < 1 || forest_base < (int32_t)Q16_ONE
             || forest_base >= (1 << 20)) {
             set_err(err, errlen, "bad forest (%lld trees, %lld nodes)", n_trees, n_nodes);
             return E_ARG;
