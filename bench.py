@@ -237,15 +237,19 @@ def time_compose(E, g, sc, args):
     wall = time.perf_counter() - t0
     G.sync_status()
     ms_per_step = wall * 1000.0 / args.steps
-    # walk launches that ran (a pass past every scenario's fixed point returns at once)
-    lw = [ms for k, ms in G.kernel_times() if k == "walk"]
-    ran = [ms for ms in lw if ms > 0.02 * max(lw, default=0.0)]
-    n_walk = len(ran)
+    # walk passes that ran (a pass past every scenario's fixed point returns at once);
+    # a pass whose tiles do not all fit one cooperative launch runs as several launches
+    passes = walk_passes(G.kernel_times())
+    top = max((ms for p in passes for ms in p), default=0.0)
+    ran = [p for p in passes if p and max(p) > 0.02 * top]
+    lw = [ms for p in passes for ms in p]
+    n_launch = sum(len(p) for p in ran)
+    ran_ms = sum(sum(p) for p in ran)
     res = {"n_ops": G.n_ops, "n_scen": n_scen, "levels": G.n_levels, "load_s": load_s,
            "ms_per_step": ms_per_step, "gpu_ms": float(np.median(step_ms)),
            "value": G.n_ops * n_scen / (ms_per_step / 1000.0),
-           "walk_avg_ms": float(np.mean(walk_ms)) * (sum(ran) / max(sum(lw), 1e-9)) / max(n_walk, 1),
-           "n_walk": n_walk,
+           "walk_avg_ms": float(np.mean(walk_ms)) * (ran_ms / max(sum(lw), 1e-9)) / max(n_launch, 1),
+           "n_pass": len(ran), "n_launch": n_launch,
            "kernels_ms": {k: round(float(np.mean(v)), 4) for k, v in kernels.items()}}
     if args.steps and "refinements" in last:
         rf = last["refinements"].cpu().numpy()
@@ -265,9 +269,21 @@ def time_compose(E, g, sc, args):
     return res
 
 
+def walk_passes(kernel_times):
+    """One compose call's walk launch times grouped by pass: every pass after the
+    first begins with its overlap detection launch."""
+    passes = [[]]
+    for kind, ms in kernel_times:
+        if kind == "overlap":
+            passes.append([])
+        elif kind == "walk":
+            passes[-1].append(ms)
+    return passes
+
+
 def roofline(g, r, args, traffic_config):
-    passes = walk_bytes(g, r["n_scen"], max(r["n_walk"] - 1, 0))
-    bytes_per_launch = sum(passes) / max(r["n_walk"], 1)
+    passes = walk_bytes(g, r["n_scen"], max(r["n_pass"] - 1, 0))
+    bytes_per_launch = sum(passes) / max(r["n_launch"], 1)
     achieved = bytes_per_launch / (r["walk_avg_ms"] / 1000.0) / 1e9
     traffic = None
     if traffic_config is not None and os.path.exists(TRAFFIC_FILE):

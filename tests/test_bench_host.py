@@ -1,0 +1,63 @@
+"""Host-side accounting of bench.py (no GPU): predecessor counts of the
+algorithmic byte model and the grouping of walk launches into passes."""
+from __future__ import annotations
+
+import numpy as np
+
+import bench
+from tests.tinygraph import AR, Builder
+
+
+def _graph():
+    b = Builder(2)
+    c = b.collective(AR, 1 << 20)
+    a0 = b.compute(0, 10)
+    x0 = b.comm(0, c, preds=[a0])
+    b.compute(0, 20, preds=[x0, a0])           # a0 is also the stream predecessor
+    b.compute(0, 5, stream=5, preds=[a0])
+    a1 = b.compute(1, 7)
+    x1 = b.comm(1, c, preds=[a1, a1])          # a repeated explicit dependency
+    b.compute(1, 3, preds=[x1])
+    return b.graph()
+
+
+def test_merged_pred_counts_by_enumeration():
+    g = _graph()
+    n = len(g["op_rank"])
+    want = []
+    for v in range(n):
+        preds = {int(u) for u in g["pred_idx"][g["pred_off"][v]:g["pred_off"][v + 1]]}
+        same = [u for u in range(v) if g["op_rank"][u] == g["op_rank"][v] and g["op_stream"][u] == g["op_stream"][v]]
+        if same:
+            preds.add(same[-1])
+        want.append(len(preds))
+    assert bench.merged_pred_counts(g).tolist() == want
+
+
+def test_walk_bytes_per_pass():
+    g = _graph()
+    preds = int(bench.merged_pred_counts(g).sum())
+    n, n_colls, n_compute = len(g["op_rank"]), len(g["coll_type"]), int((g["op_kind"] == 0).sum())
+    p = bench.walk_bytes(g, 3, 2)
+    first = (16 * n + 8 * preds + 8 * n_colls) * 3
+    assert p == [first, first + n_compute * 3, first + n_compute * 3]
+
+
+def test_walk_passes_split_launches():
+    kt = [("init", 0.1), ("cc_cost", 0.2), ("walk", 5.0), ("walk", 4.0),
+          ("overlap", 1.0), ("clear", 0.1), ("walk", 6.0), ("walk", 6.5),
+          ("overlap", 1.0), ("clear", 0.1), ("walk", 0.01), ("walk", 0.01)]
+    assert bench.walk_passes(kt) == [[5.0, 4.0], [6.0, 6.5], [0.01, 0.01]]
+    assert bench.walk_passes([("init", 0.1)]) == [[]]
+
+
+def test_roofline_counts_each_pass_once():
+    """Two passes of two launches each (half the tiles per launch): one
+    launch moves half a pass's bytes on average."""
+    g = _graph()
+    r = {"n_scen": 128, "n_pass": 2, "n_launch": 4, "walk_avg_ms": 2.0}
+    rf = bench.roofline(g, r, None, None)
+    total = sum(bench.walk_bytes(g, 128, 1))
+    assert rf["algorithmic_bytes_per_launch"] == int(total / 4)
+    assert np.isclose(rf["achieved"], round(total / 4 / 2e-3 / 1e9, 1))
+    assert rf["traffic"] is None
