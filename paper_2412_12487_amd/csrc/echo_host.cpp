@@ -157,6 +157,8 @@ void free_graph(echo_graph g) {
 template <class T>
 int ensure(T **p, size_t *have, size_t need, const char *what) {
     if (*have >= need && *p) return ECHO_OK;
+    if (need > (size_t(1) << 56) / sizeof(T))        // far beyond any device; keeps the byte count exact
+        return fail(ECHO_ERR_NOMEM, "workspace (%s): %zu elements", what, need);
     (void)hipFree(*p);
     *p = nullptr;
     *have = 0;
@@ -259,6 +261,8 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
             std::sort(tmp.begin(), tmp.end());
             tmp.erase(std::unique(tmp.begin(), tmp.end()), tmp.end());
             preds.insert(preds.end(), tmp.begin(), tmp.end());
+            if ((int64_t)preds.size() > kI32Max)
+                return fail(ECHO_ERR_RANGE, "more than 2^31 merged dependencies");
             poff[v + 1] = (int32_t)preds.size();
         }
     }

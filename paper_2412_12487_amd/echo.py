@@ -134,6 +134,23 @@ def scenarios_to_device(sc, device="cuda"):
     return t, int(rec.shape[0])
 
 
+def _device_buffer(t, name, device, nbytes, dtype=None):
+    """Check that tensor t can take nbytes at its data pointer on `device`: a
+    contiguous tensor of that device (and dtype), large enough."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise EchoError(ECHO_ERR_ARG, f"{name} must be a torch tensor")
+    if t.device != device:
+        raise EchoError(ECHO_ERR_ARG, f"{name} is on {t.device}, the graph on {device}")
+    if not t.is_contiguous():
+        raise EchoError(ECHO_ERR_ARG, f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise EchoError(ECHO_ERR_ARG, f"{name} must be {dtype} (got {t.dtype})")
+    if t.numel() * t.element_size() < nbytes:
+        raise EchoError(ECHO_ERR_ARG, f"{name} holds {t.numel() * t.element_size()} bytes, needs {nbytes}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
 def _stream_ptr(device):
     import torch
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
@@ -204,9 +221,12 @@ class Graph:
         """Collective costs [n_colls, n_scen] int64 (torch, on the graph's device)."""
         import torch
         dev = torch.device("cuda", self.device)
+        if int(n_scen) < 1:
+            raise EchoError(ECHO_ERR_ARG, "n_scen must be >= 1")
+        scen = _device_buffer(d_scen, "scenarios", dev, int(n_scen) * SCENARIO_DTYPE.itemsize)
         out = torch.empty((self.n_colls, n_scen), dtype=torch.int64, device=dev)
         L = lib()
-        _check(L.echo_cc_cost(self.handle, ctypes.c_void_p(d_scen.data_ptr()), int(n_scen),
+        _check(L.echo_cc_cost(self.handle, scen, int(n_scen),
                               ctypes.c_void_p(out.data_ptr()), _stream_ptr(dev)))
         if check:
             self.sync_status()
@@ -233,17 +253,25 @@ class Graph:
             res["digest"] = torch.empty(n_scen, dtype=torch.int64, device=dev)
         if refinements and "refinements" not in res:
             res["refinements"] = torch.empty(n_scen, dtype=torch.int32, device=dev)
-        p = lambda k: ctypes.c_void_p(res[k].data_ptr()) if k in res else ctypes.c_void_p(None)
+        if int(n_scen) < 1:
+            raise EchoError(ECHO_ERR_ARG, "n_scen must be >= 1")
+        scen = _device_buffer(d_scen, "scenarios", dev, int(n_scen) * SCENARIO_DTYPE.itemsize)
+        rows = {"start": self.n_ops, "finish": self.n_ops, "step": 1, "digest": 1, "refinements": 1}
+        types = {"start": torch.int64, "finish": torch.int64, "step": torch.int64, "digest": torch.int64,
+                 "refinements": torch.int32}
+        ptrs = {k: _device_buffer(res[k], k, dev, rows[k] * int(n_scen) * (4 if k == "refinements" else 8),
+                                  types[k]) for k in res if k in rows}
+        p = lambda k: ptrs.get(k, ctypes.c_void_p(None))
         none = ctypes.c_void_p(None)
         start, finish = (p("start"), p("finish")) if timelines else (none, none)
         dig = p("digest") if digest else none
         if until_stable or prorate or forest or refinements:
             opts = _Validator(int(n_refine), int(bool(until_stable)), int(bool(prorate)), int(bool(forest)))
-            _check(lib().echo_compose_validated(self.handle, ctypes.c_void_p(d_scen.data_ptr()), int(n_scen),
+            _check(lib().echo_compose_validated(self.handle, scen, int(n_scen),
                                                 ctypes.byref(opts), start, finish, p("step"), dig,
                                                 p("refinements") if refinements else none, _stream_ptr(dev)))
         else:
-            _check(lib().echo_compose_batch(self.handle, ctypes.c_void_p(d_scen.data_ptr()), int(n_scen),
+            _check(lib().echo_compose_batch(self.handle, scen, int(n_scen),
                                             int(n_refine), start, finish, p("step"), dig, _stream_ptr(dev)))
         if check:
             self.sync_status()

@@ -183,3 +183,24 @@ def test_inconsistent_group_membership_is_an_argument_error(E, what):
         q = int(np.flatnonzero(g["coll_type"] == P2P)[0])
         g["coll_N"][q], g["coll_M"][q], g["coll_K"][q] = 4, 2, 2
     assert _load_code(E, g) == E.ECHO_ERR_ARG
+
+
+def test_binding_rejects_unfit_buffers(E):
+    """Output and scenario tensors are checked on the host before their pointers
+    reach the library: device, contiguity, dtype and size."""
+    import torch
+    from paper_2412_12487_amd import echo as B
+    cpu = torch.device("cpu")
+    ok = torch.zeros((4, 8), dtype=torch.int64)
+    assert B._device_buffer(ok, "start", cpu, 4 * 8 * 8, torch.int64).value == ok.data_ptr()
+    bad = [
+        (ok.t(), "contiguous"),
+        (ok.to(torch.int32), "must be torch.int64"),
+        (ok[:3], "needs 256"),
+        ([0] * 32, "torch tensor"),
+    ]
+    for t, msg in bad:
+        with pytest.raises(B.EchoError, match=msg):
+            B._device_buffer(t, "start", cpu, 4 * 8 * 8, torch.int64)
+    with pytest.raises(B.EchoError, match="the graph on"):
+        B._device_buffer(ok, "start", torch.device("meta"), 8)
