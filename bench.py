@@ -69,19 +69,44 @@ def source_hash():
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def cpu_baseline(g, sc, n_refine, n_sample):
+def cpu_baseline(g, sc, n_refine, n_sample, variant, ops_counted=None):
+    """The oracle on the first n_sample scenarios, with the same validator, CC tables
+    and ensemble as the GPU run; op-evals counted as the GPU line counts them."""
     import oracle
     from workloads import scenarios
     sub = scenarios.take(sc, slice(0, n_sample))
     # at most 16 threads: the host cores one GPU's share of the machine comes with
     threads = max(1, min(n_sample, 16, len(os.sched_getaffinity(0))))
     t = time.perf_counter()
-    oracle.run(g, sub, n_refine, threads=threads, timelines=False)
+    oracle.run(g, sub, n_refine, threads=threads, timelines=False, **variant)
     dt = time.perf_counter() - t
-    return {"value": len(g["op_rank"]) * n_sample / dt, "unit": "op-evals/s", "cores": threads,
+    ops = len(g["op_rank"]) if ops_counted is None else ops_counted
+    return {"value": ops * n_sample / dt, "unit": "op-evals/s", "cores": threads,
             "kind": "oracle", "wall_s": round(dt, 3),
             "sample": f"scenarios 0..{n_sample - 1} of the same graph, {n_refine} refinement(s), "
                       f"{threads} thread(s)"}
+
+
+def oracle_variant(args, extras):
+    """oracle.run keyword arguments matching the GPU run's options."""
+    v = {"until_stable": args.until_stable, "prorate": args.prorate}
+    if extras.get("forest") is not None:
+        v["forest"] = extras["forest"]
+    if extras.get("cc_tables") is not None:
+        v["cc_tables"] = extras["cc_tables"]
+    return v
+
+
+def extras_for(args):
+    """The CC tables and the slowdown ensemble the options ask for."""
+    from workloads import scenarios
+    ex = {}
+    if args.cc == "tables":
+        ex["cc_tables"] = scenarios.draw_cc_tables(CC_TABLES, np.random.default_rng(99))
+    if args.forest:
+        from workloads import slowdown_forest
+        ex["forest"] = slowdown_forest.synthetic_forest(0)
+    return ex
 
 
 def main():
@@ -139,7 +164,8 @@ def main():
     sc = cc_variant(configs.scenario_batch(args.config, args.index, args.scenarios or None), args)
     log(f"graph: config {args.config} {configs.NAMES[args.config]}: {len(g['op_rank'])} ops, "
         f"{len(g['coll_type'])} collectives, {g['n_ranks']} ranks ({time.perf_counter() - t:.1f} s)")
-    r = time_compose(E, g, sc, args)
+    extras = extras_for(args)
+    r = time_compose(E, g, sc, args, extras)
     line = {
         "metric": "op-evaluations/sec (ops x scenarios composed), 1 GPU",
         "value": round(r["value"], 1),
@@ -167,7 +193,7 @@ def main():
         line["config"]["refinements"] = r["refinements"]
     if args.cpu_sample > 0:
         log(f"cpu baseline: oracle on {args.cpu_sample} scenario(s) ...")
-        line["cpu_baseline"] = cpu_baseline(g, sc, args.refine, args.cpu_sample)
+        line["cpu_baseline"] = cpu_baseline(g, sc, args.refine, args.cpu_sample, oracle_variant(args, extras))
     print(json.dumps(line), flush=True)
 
 
@@ -194,17 +220,15 @@ def cc_variant(sc, args):
     return sc
 
 
-def time_compose(E, g, sc, args):
+def time_compose(E, g, sc, args, extras):
     """Load g, compose the batch warmup + steps times; wall and per-kernel timings."""
     import torch
-    from workloads import scenarios
     t = time.perf_counter()
     G = E.Graph(g, 0)
-    if args.cc == "tables":
-        G.set_cc_tables(scenarios.draw_cc_tables(CC_TABLES, np.random.default_rng(99)))
-    if args.forest:
-        from workloads import slowdown_forest
-        G.set_forest(slowdown_forest.synthetic_forest(0))
+    if extras.get("cc_tables") is not None:
+        G.set_cc_tables(extras["cc_tables"])
+    if extras.get("forest") is not None:
+        G.set_forest(extras["forest"])
     load_s = time.perf_counter() - t
     log(f"loaded: {G.n_levels} levels in {load_s:.1f} s")
     d_scen, n_scen = E.scenarios_to_device(sc, "cuda:0")
@@ -311,8 +335,9 @@ def replica_mode(args, E, configs, gpt1f1b):
     n_scen = len(sc["alpha_ns"])
     # the sweep over every replica needs start + finish + masks for all of the job's ops
     full_fits = len(g["op_rank"]) * n_scen * 17 < 200 * 10**9
-    full = time_compose(E, g, sc, args) if full_fits else None
-    red = time_compose(E, rg, sc, args)
+    extras = extras_for(args)
+    full = time_compose(E, g, sc, args, extras) if full_fits else None
+    red = time_compose(E, rg, sc, args, extras)
     line = {
         "metric": "op-evaluations/sec (ops x scenarios of the whole job, composed through one DP replica), 1 GPU",
         "value": round(len(g["op_rank"]) * red["n_scen"] / (red["ms_per_step"] / 1000.0), 1),
@@ -338,7 +363,8 @@ def replica_mode(args, E, configs, gpt1f1b):
     }
     if args.cpu_sample > 0:
         log(f"cpu baseline: oracle on {args.cpu_sample} scenario(s) of the replica ...")
-        line["cpu_baseline"] = cpu_baseline(rg, sc, args.refine, args.cpu_sample)
+        line["cpu_baseline"] = cpu_baseline(rg, sc, args.refine, args.cpu_sample, oracle_variant(args, extras),
+                                            ops_counted=len(g["op_rank"]))
     print(json.dumps(line), flush=True)
 
 

@@ -61,3 +61,29 @@ def test_roofline_counts_each_pass_once():
     assert rf["algorithmic_bytes_per_launch"] == int(total / 4)
     assert np.isclose(rf["achieved"], round(total / 4 / 2e-3 / 1e9, 1))
     assert rf["traffic"] is None
+
+
+def test_cpu_baseline_runs_the_gpu_run_options():
+    """The oracle leg gets the same validator, CC tables and ensemble as the GPU
+    run (a scenario naming a CC table the oracle lacks would be an error)."""
+    import argparse
+
+    import oracle
+    from workloads import configs, scenarios
+
+    g = configs.graph(1)
+    for opts in ({"cc": "tables"}, {"forest": True}, {"until_stable": True, "prorate": True}):
+        args = argparse.Namespace(**{"cc": "echo", "forest": False, "until_stable": False, "prorate": False,
+                                     **opts})
+        sc = bench.cc_variant(configs.scenario_batch(4, 0, 8), args)
+        extras = bench.extras_for(args)
+        variant = bench.oracle_variant(args, extras)
+        cb = bench.cpu_baseline(g, sc, 2, 4, variant)
+        assert cb["value"] > 0 and cb["kind"] == "oracle"
+        # the options reach the oracle: the ensemble and prorating change its result
+        ref = oracle.run(g, scenarios.take(sc, slice(0, 4)), 2, timelines=False, **variant)
+        plain = oracle.run(g, scenarios.take(sc, slice(0, 4)), 2, timelines=False,
+                           **({"cc_tables": extras["cc_tables"]} if "cc_tables" in extras else {}))
+        if opts.get("forest") or opts.get("prorate"):
+            assert not np.array_equal(ref["digest"], plain["digest"])
+    assert bench.cpu_baseline(g, configs.scenario_batch(1), 1, 1, {}, ops_counted=10)["value"] > 0
