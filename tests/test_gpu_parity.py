@@ -189,33 +189,69 @@ def test_config2_gpt175b_96ranks(E):
     assert_same(gpu_run(E, g, sc, 1), ref)
 
 
-def _sampled(E, g, sc, R, cols):
+def _sampled(E, g, sc, R, cols, *, digest=True):
     """Compose every scenario on the GPU; compare the sampled columns in full."""
     import torch
     G = E.Graph(g, 0)
     d, n = E.scenarios_to_device(sc)
-    out = G.compose(d, n, R, timelines=True, digest=True)
+    out = G.compose(d, n, R, timelines=True, digest=digest)
     idx = torch.tensor(cols, device=out["start"].device)
-    gpu = {"step": out["step"].cpu().numpy(), "digest": out["digest"].cpu().numpy().view(np.uint64),
+    gpu = {"step": out["step"].cpu().numpy(),
            "start": out["start"].index_select(1, idx).cpu().numpy(),
            "finish": out["finish"].index_select(1, idx).cpu().numpy()}
+    if digest:
+        gpu["digest"] = out["digest"].cpu().numpy().view(np.uint64)
     del out
     G.close()
     ref = oracle.run(g, scenarios.take(sc, cols), R, threads=min(THREADS, len(cols)))
     np.testing.assert_array_equal(gpu["step"][cols], ref["step"])
-    np.testing.assert_array_equal(gpu["digest"][cols], ref["digest"])
+    if digest:
+        np.testing.assert_array_equal(gpu["digest"][cols], ref["digest"])
     for j, c in enumerate(cols):
         np.testing.assert_array_equal(gpu["start"][:, j], ref["start"][j], err_msg=f"start, scenario {c}")
         np.testing.assert_array_equal(gpu["finish"][:, j], ref["finish"][j], err_msg=f"finish, scenario {c}")
     return gpu
 
 
+def _stored(config, index, g, sc):
+    """The oracle's step times and digests of every scenario (tests/golden), after
+    checking that they were made from these very inputs."""
+    from tests.golden import make_full_digests as fd
+    h, step, dig = fd.load(config)[index]
+    assert h == fd.input_hash(g, sc), \
+        f"stored digests of config {config} graph {index} were made from other inputs: rerun {fd.__file__}"
+    return step, dig
+
+
+def _all_digests(E, g, sc, R):
+    """Step time and digest of every scenario (digest variant, no timelines)."""
+    G = E.Graph(g, 0)
+    d, n = E.scenarios_to_device(sc)
+    out = G.compose(d, n, R, timelines=False, digest=True)
+    res = out["step"].cpu().numpy(), out["digest"].cpu().numpy().view(np.uint64)
+    G.close()
+    return res
+
+
 def test_config3_gpt175b_1024ranks_sampled(E):
+    """The benchmark's launch configuration (timelines out, no digest): every
+    scenario's step time against the oracle's stored values, four scenarios'
+    timelines in full against the oracle run here."""
     g, sc = configs.graph(3), configs.scenario_batch(3)
     n = scenarios.count(sc)
+    step, _ = _stored(3, 0, g, sc)
     cols = sorted({0, n - 1, *np.random.default_rng(3).choice(n, 2, replace=False).tolist()})
-    gpu = _sampled(E, g, sc, 1, cols)
+    gpu = _sampled(E, g, sc, 1, cols, digest=False)
+    np.testing.assert_array_equal(gpu["step"], step)
     assert (gpu["step"] > 0).all()
+
+
+def test_config3_gpt175b_1024ranks_all_digests(E):
+    g, sc = configs.graph(3), configs.scenario_batch(3)
+    step, dig = _stored(3, 0, g, sc)
+    gs, gd = _all_digests(E, g, sc, 1)
+    np.testing.assert_array_equal(gs, step)
+    np.testing.assert_array_equal(gd, dig)
 
 
 def test_config3_every_pass_is_one_launch(E):
@@ -243,7 +279,12 @@ def test_config3_every_pass_is_one_launch(E):
 @pytest.mark.parametrize("index", [0, 3, 6] if not os.environ.get("ECHO_FULL") else list(range(16)))
 def test_config5_extrapolation_sampled(E, index):
     g, sc = configs.graph(5, index), configs.scenario_batch(5, index)
-    _sampled(E, g, sc, 1, [0, scenarios.count(sc) - 1])
+    step, dig = _stored(5, index, g, sc)
+    gpu = _sampled(E, g, sc, 1, [0, scenarios.count(sc) - 1], digest=False)
+    np.testing.assert_array_equal(gpu["step"], step)
+    gs, gd = _all_digests(E, g, sc, 1)
+    np.testing.assert_array_equal(gs, step)
+    np.testing.assert_array_equal(gd, dig)
 
 
 # ---------------------------------------------------------------- properties and edge cases
