@@ -2,8 +2,10 @@
 
 All calls go through the C ABI (libecho.so via the ctypes binding).  Small
 configurations compare every start/finish/step/digest; the full-size GPT-175B
-graphs compare sampled scenarios in full plus every step time the sample
-covers, in the same launch configuration the benchmark times.
+graphs compare sampled scenarios' timelines in full against the oracle run in
+the test, in the launch configuration the benchmark times (timelines out, no
+digest), and every scenario's step time and digest against the oracle's values
+stored by tests/golden/make_full_digests.py.
 """
 from __future__ import annotations
 

@@ -853,3 +853,14 @@ def test_malformed_forests_rejected():
     with pytest.raises(oracle.OracleError) as e:
         oracle.run(g, sc, 1, forest=bad)
     assert e.value.code == -1
+
+
+def test_stored_full_digests_are_whole():
+    """The stored oracle digests of the two largest workloads (full-size parity
+    tests) parse into every graph and scenario they cover."""
+    from tests.golden import make_full_digests as fd
+    c3, c5 = fd.load(3), fd.load(5)
+    assert sorted(c3) == [0] and len(c3[0][1]) == 256
+    assert sorted(c5) == list(range(16)) and all(len(s) == 32 and len(d) == 32 for _, s, d in c5.values())
+    for h, step, dig in list(c3.values()) + list(c5.values()):
+        assert len(h) == 16 and (step > 0).all() and dig.dtype == np.uint64
