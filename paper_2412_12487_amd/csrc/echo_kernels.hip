@@ -655,8 +655,10 @@ __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_
 template <bool PRORATE, bool DETECT, bool FOREST>
 __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     constexpr bool EXT = PRORATE || FOREST;      // output: extra time per op instead of a mask
-    constexpr bool SKIP = !EXT && !DETECT;       // whole blocks of ops may be skipped
-    constexpr int NPRE = SKIP ? kPre / 2 : kPre; // (the block checks take the other registers)
+    // whole blocks of ops may be skipped; the mask variants prefetch fewer unchained
+    // starts to keep four wavefronts per SIMD (the block checks take those registers)
+    constexpr bool SKIP = true;
+    constexpr int NPRE = EXT ? kPre : DETECT ? kPre / 4 : kPre / 2;
     __shared__ int64_t feat[FOREST ? 12 * kLanes : 1];   // the ensemble's feature vectors, one per lane
     __shared__ int32_t sid[kIdStage];            // the rank's comm op ids and collective types, staged
     __shared__ uint8_t stype[kIdStage];
@@ -806,7 +808,42 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                     if (!__builtin_amdgcn_readfirstlane(__ballot(c > cmin) != 0)) {
                         // every op of the block ends by cmin: no overlaps, no cursor moves
                         const int je = j + kOverlapBlock < nr ? j + kOverlapBlock : nr;
-                        for (int jj = j; jj < je; ++jj) mstage[jj * kLanes + lane] = 0;
+                        if (EXT) {
+                            // no extra times; DETECT: a duration changes where the previous
+                            // pass added one
+                            if (DETECT && a.prev_refined) {
+                                uint32_t eo = 0;
+                                for (int jj = j; jj < je; ++jj)
+                                    eo |= (ebase + (int64_t)__builtin_amdgcn_readlane(cur_pos, jj) * a.mstride)[col];
+                                __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                                changed |= eo != 0;
+                            }
+                            for (int jj = j; jj < je; ++jj)
+                                (ebase + (int64_t)__builtin_amdgcn_readlane(cur_pos, jj) * a.mstride)[col] = 0;
+                        } else {
+                            for (int jj = j; jj < je; ++jj) mstage[jj * kLanes + lane] = 0;
+                            if (DETECT && a.prev_refined) {
+                                // an op inflated in the previous pass runs with D now: a change
+                                // unless its factor left D as it was
+                                uint32_t mo[kOverlapBlock];
+#pragma unroll
+                                for (int q = 0; q < kOverlapBlock; ++q)
+                                    mo[q] = j + q < je ? (obase + (int64_t)__builtin_amdgcn_readlane(cur_pos, j + q) *
+                                                                      a.mstride)[col]
+                                                       : 0u;
+                                __builtin_amdgcn_s_waitcnt(kWaitVm0);
+#pragma unroll
+                                for (int q = 0; q < kOverlapBlock; ++q) {
+                                    if (!__builtin_amdgcn_readfirstlane(__ballot(mo[q] != 0) != 0)) continue;
+                                    const int64_t vq = __builtin_amdgcn_readlane(cur.x, j + q);
+                                    const int mq = __builtin_amdgcn_readlane(cur.y, j + q);
+                                    const int64_t dq = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.w, j + q) << 32) |
+                                                                 (uint32_t)__builtin_amdgcn_readlane(cur.z, j + q));
+                                    const int64_t Dq = any_jitter ? jittered(dq, (int32_t)vq, jbase, amp) : dq;
+                                    if (mo[q] != 0) changed |= q16(Dq, factor_of(mo[q], slow, mq & 7)) != Dq;
+                                }
+                            }
+                        }
                         fprev = c;
                         j = je - 1;
                         continue;

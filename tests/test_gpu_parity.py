@@ -74,7 +74,7 @@ def test_tiny_graphs(E, name, R):
     assert_same(gpu_run(E, g, sc, R), oracle.run(g, sc, R))
 
 
-def _random_graph(rng, n_ranks, ops_per_rank, n_coll):
+def _random_graph(rng, n_ranks, ops_per_rank, n_coll, p_comm=0.3):
     b = Builder(n_ranks, gpus_per_node=int(rng.integers(1, 5)))
     colls = []
     for _ in range(n_coll):
@@ -90,7 +90,7 @@ def _random_graph(rng, n_ranks, ops_per_rank, n_coll):
         mine = [(c, s) for c, m, s in colls if r in m]
         for k in range(ops_per_rank):
             preds = [int(u) for u in ids[-6:] if rng.random() < 0.25]
-            if mine and rng.random() < 0.3:
+            if mine and rng.random() < p_comm:
                 c, s = mine.pop(0)
                 ids.append(b.comm(r, c, stream=s, preds=preds))
             elif rng.random() < 0.1:
@@ -490,6 +490,25 @@ def test_validator_variants_tiny(E, until_stable, prorate):
         gpu = _variant_run(E, g, sc, 4, until_stable, prorate)
         assert_same(gpu, ref)
         np.testing.assert_array_equal(gpu["refinements"], ref["refinements"])
+
+
+@pytest.mark.parametrize("prorate", [False, True])
+@pytest.mark.parametrize("seed", range(4))
+def test_fixed_point_with_strong_slowdowns(E, seed, prorate):
+    """Long compute runs between sparse collectives and slowdowns up to 3x: ops move in
+    and out of overlap from one refinement to the next (2 to 16 refinements), so blocks
+    of ops that overlapped on the previous timeline are skipped whole by overlap
+    detection on the next one, where returning to the plain duration is a change."""
+    rng = np.random.default_rng(5000 + seed)
+    g = _random_graph(rng, int(rng.integers(2, 9)), int(rng.integers(100, 200)), int(rng.integers(8, 24)),
+                      p_comm=0.08)
+    sc = scenarios.draw(130, rng, bw_inter=(20000, 400000), alpha=(0, 40000), slowdown=(65536, 196608),
+                        jitter=(4000, seed) if seed % 2 else None)
+    ref = oracle.run(g, sc, 16, threads=THREADS, until_stable=True, prorate=prorate)
+    gpu = _variant_run(E, g, sc, 16, True, prorate)
+    assert_same(gpu, ref)
+    np.testing.assert_array_equal(gpu["refinements"], ref["refinements"])
+    assert ref["refinements"].max() >= 3
 
 
 @pytest.mark.parametrize("until_stable,prorate", VARIANTS)
