@@ -679,6 +679,12 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
         cl_off[k + 1] += cl_off[k];
         cp_off[k + 1] += cp_off[k];
     }
+    int32_t max_comm_streams = 0;
+    for (int64_t r = 0; r < R; ++r) {
+        int32_t k = 0;
+        for (int st = 0; st < kStreams; ++st) k += cl_off[r * kStreams + st + 1] > cl_off[r * kStreams + st];
+        max_comm_streams = std::max(max_comm_streams, k);
+    }
     std::vector<int32_t> cl(cl_off.back()), cl_coll(cl_off.back());
     std::vector<uint8_t> cl_type(cl_off.back());
     std::vector<ComputeRec> cp(cp_off.back());
@@ -734,6 +740,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     dg.n_ranks = (int32_t)R;
     dg.n_walkers = (int32_t)W;
     dg.n_blocks = (int32_t)nblk;
+    dg.max_comm_streams = max_comm_streams;
     g->need_coll_cost = need_coll_cost;
 #define UP(dst, src)                                                        \
     do {                                                                    \
@@ -867,6 +874,7 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
             o.n_scen = n_scen;
             o.n_tiles = n_tiles;
             o.prev_refined = p > 1;
+            o.max_comm_streams = g->dg.max_comm_streams;
             o.status = g->dg.status;
             TIMED(ECHO_K_OVERLAP, launch_overlap(o, g->n_ranks, stream), "overlap kernel");
             if (until_stable && (e = launch_settle(g->chg, n_scen, d_refinements, stable, stream)))

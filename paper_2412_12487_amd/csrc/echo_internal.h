@@ -153,6 +153,7 @@ struct DeviceGraph {
     int32_t *forest_roots = nullptr;
     int64_t *class_metrics = nullptr;  // [8][4]
     int32_t n_trees = 0, forest_base = 65536;
+    int32_t max_comm_streams = 0;    // the most streams with comm ops on one rank
 };
 
 constexpr int kClassMetrics = 4;
@@ -212,6 +213,7 @@ struct OverlapArgs {
     int32_t prorate;                 // inflate only the overlapped part (extra times in ext)
     int32_t n_scen, n_tiles;
     int32_t prev_refined;            // the previous pass inflated its compute ops
+    int32_t max_comm_streams;        // the most streams with comm ops on one rank (kernel variant)
     unsigned *status;
 };
 

@@ -652,13 +652,15 @@ __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_
 // order), and record the extra time q16(min(o, D), F) - min(o, D) instead of a mask.
 // DETECT: flag the scenarios whose durations change (fixed-point iteration).
 // FOREST: the factor is the tree ensemble's prediction (recorded as an extra time).
-template <bool PRORATE, bool DETECT, bool FOREST>
+// NC: room for this many comm streams per rank (the cursor and merge state scale with it).
+template <bool PRORATE, bool DETECT, bool FOREST, int NC>
 __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     constexpr bool EXT = PRORATE || FOREST;      // output: extra time per op instead of a mask
-    // whole blocks of ops may be skipped; the mask variants prefetch fewer unchained
-    // starts to keep four wavefronts per SIMD (the block checks take those registers)
+    // whole blocks of ops may be skipped; all but the ensemble variants prefetch fewer
+    // unchained starts for the registers the block checks take (four wavefronts per SIMD
+    // for the mask and prorating variants with four comm streams)
     constexpr bool SKIP = true;
-    constexpr int NPRE = EXT ? kPre : DETECT ? kPre / 4 : kPre / 2;
+    constexpr int NPRE = FOREST ? kPre : (DETECT || PRORATE) ? kPre / 4 : kPre / 2;
     __shared__ int64_t feat[FOREST ? 12 * kLanes : 1];   // the ensemble's feature vectors, one per lane
     __shared__ int32_t sid[kIdStage];            // the rank's comm op ids and collective types, staged
     __shared__ uint8_t stype[kIdStage];
@@ -712,11 +714,11 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     };
 
     // comm streams of this rank that carry comm ops, packed to the front
-    int64_t kb[kStreams];
-    int32_t nk[kStreams];
+    int64_t kb[NC];
+    int32_t nk[NC];
     int ncs = 0;
 #pragma unroll
-    for (int k = 0; k < kStreams; ++k) {
+    for (int k = 0; k < NC; ++k) {
         kb[k] = 0;
         nk[k] = 0;
     }
@@ -724,21 +726,26 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
         const int64_t b = cl_off[k], n = cl_off[k + 1] - b;
         if (n == 0) continue;
 #pragma unroll
-        for (int q = 0; q < kStreams; ++q)
+        for (int q = 0; q < NC; ++q)
             if (q == ncs) {
                 kb[q] = b;
                 nk[q] = (int32_t)n;
             }
         ++ncs;
     }
+    if (ncs > NC) {
+        // more comm streams than this variant holds: the loader counts them, so never
+        if (lane == 0) __hip_atomic_fetch_or(a.status, kStatusRange, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
 
     for (int s = 0; s < kStreams; ++s) {
         const int64_t b0 = cp_off[s], b1 = cp_off[s + 1];
         if (b0 == b1) continue;
-        int32_t p[kStreams];
-        int64_t cs[kStreams], cf[kStreams];
+        int32_t p[NC];
+        int64_t cs[NC], cf[NC];
 #pragma unroll
-        for (int k = 0; k < kStreams; ++k) {
+        for (int k = 0; k < NC; ++k) {
             p[k] = 0;
             cs[k] = kInf;
             cf[k] = kInf;
@@ -751,7 +758,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
         // earliest start among the cursors: an op ending by then overlaps nothing
         int64_t cmin = kInf;
 #pragma unroll
-        for (int k = 0; k < kStreams; ++k) cmin = cs[k] < cmin ? cs[k] : cmin;
+        for (int k = 0; k < NC; ++k) cmin = cs[k] < cmin ? cs[k] : cmin;
         int64_t fprev = 0;
         // lane j holds compute record i0 + j of the current round of 64
         const int4 *recs = reinterpret_cast<const int4 *>(a.cp);
@@ -774,6 +781,9 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
             // before every cursor starts is skipped whole
             constexpr int kBlocks = kLanes / kOverlapBlock;
             int64_t ck[SKIP ? kBlocks : 1];
+            // the fixed-point variants (every pass after the first reads the previous pass's
+            // values): the current block's previous masks or extra times
+            uint32_t old8[DETECT ? kOverlapBlock : 1];
             if (SKIP) {
 #pragma unroll
                 for (int b = 0; b < kBlocks; ++b) {
@@ -801,6 +811,19 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
             }
             for (int j = 0; j < nr; ++j) {
                 if (SKIP && (j & (kOverlapBlock - 1)) == 0) {
+                    if (DETECT && a.prev_refined) {
+                        // the previous pass's masks (extra times) of the block's ops, fetched
+                        // together: one memory round trip per block instead of one per op
+#pragma unroll
+                        for (int q = 0; q < kOverlapBlock; ++q) {
+                            old8[q] = 0;
+                            if (j + q < nr) {
+                                const int64_t rq = (int64_t)__builtin_amdgcn_readlane(cur_pos, j + q) * a.mstride;
+                                old8[q] = EXT ? (ebase + rq)[col] : (uint32_t)(obase + rq)[col];
+                            }
+                        }
+                        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                    }
                     int64_t c = kInf;
 #pragma unroll
                     for (int b = 0; b < kBlocks; ++b)
@@ -813,9 +836,8 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                             // pass added one
                             if (DETECT && a.prev_refined) {
                                 uint32_t eo = 0;
-                                for (int jj = j; jj < je; ++jj)
-                                    eo |= (ebase + (int64_t)__builtin_amdgcn_readlane(cur_pos, jj) * a.mstride)[col];
-                                __builtin_amdgcn_s_waitcnt(kWaitVm0);
+#pragma unroll
+                                for (int q = 0; q < kOverlapBlock; ++q) eo |= old8[q];
                                 changed |= eo != 0;
                             }
                             for (int jj = j; jj < je; ++jj)
@@ -825,13 +847,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                             if (DETECT && a.prev_refined) {
                                 // an op inflated in the previous pass runs with D now: a change
                                 // unless its factor left D as it was
-                                uint32_t mo[kOverlapBlock];
-#pragma unroll
-                                for (int q = 0; q < kOverlapBlock; ++q)
-                                    mo[q] = j + q < je ? (obase + (int64_t)__builtin_amdgcn_readlane(cur_pos, j + q) *
-                                                                      a.mstride)[col]
-                                                       : 0u;
-                                __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                                const uint32_t *const mo = old8;
 #pragma unroll
                                 for (int q = 0; q < kOverlapBlock; ++q) {
                                     if (!__builtin_amdgcn_readfirstlane(__ballot(mo[q] != 0) != 0)) continue;
@@ -875,13 +891,20 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 int64_t d = D;                   // the duration v ran with in the previous pass
                 uint32_t m_old = 0, e_old = 0;
                 if (a.prev_refined) {
-                    if (EXT) {
-                        e_old = (ebase + row())[col];
+                    uint32_t ov = 0;
+                    if (DETECT) {
+#pragma unroll
+                        for (int q = 0; q < kOverlapBlock; ++q)
+                            if (q == (j & (kOverlapBlock - 1))) ov = old8[q];
+                    } else {
+                        ov = EXT ? (ebase + row())[col] : (uint32_t)(obase + row())[col];
                         __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                    }
+                    if (EXT) {
+                        e_old = ov;
                         d = D + e_old;
                     } else {
-                        m_old = (obase + row())[col];
-                        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                        m_old = ov;
                         if (m_old != 0) d = q16(D, factor_of(m_old, slow, cls));
                     }
                 }
@@ -910,7 +933,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     }
                 if (busy) {
     #pragma unroll
-                    for (int k = 0; k < kStreams; ++k) {
+                    for (int k = 0; k < NC; ++k) {
                         if (k >= ncs) break;
                         if (!(cs[k] < fv)) continue;
                         while (cf[k] <= sv) {              // ends before v starts: never again
@@ -944,10 +967,10 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                     if (PRORATE) {
                         // merge the streams' overlapping intervals in start order; every one of
                         // them ends after sv (each stream's intervals are disjoint and sorted)
-                        int32_t q[kStreams];
-                        int64_t qs[kStreams], qf[kStreams];
+                        int32_t q[NC];
+                        int64_t qs[NC], qf[NC];
     #pragma unroll
-                        for (int k = 0; k < kStreams; ++k) {
+                        for (int k = 0; k < NC; ++k) {
                             q[k] = p[k];
                             qs[k] = k < ncs ? cs[k] : kInf;
                             qf[k] = k < ncs ? cf[k] : kInf;
@@ -957,14 +980,14 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                             int bk = -1;
                             int64_t bs = fv;
     #pragma unroll
-                            for (int k = 0; k < kStreams; ++k)
+                            for (int k = 0; k < NC; ++k)
                                 if (qs[k] < bs) {
                                     bs = qs[k];
                                     bk = k;
                                 }
                             if (bk < 0) break;
     #pragma unroll
-                            for (int k = 0; k < kStreams; ++k) {
+                            for (int k = 0; k < NC; ++k) {
                                 if (k != bk) continue;
                                 const int64_t lo = sv > qs[k] ? sv : qs[k], hi = fv < qf[k] ? fv : qf[k];
                                 if (lo < hi) {
@@ -991,7 +1014,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                     __builtin_amdgcn_s_waitcnt(kWaitVm0);
                     cmin = kInf;
 #pragma unroll
-                    for (int k = 0; k < kStreams; ++k) cmin = cs[k] < cmin ? cs[k] : cmin;
+                    for (int k = 0; k < NC; ++k) cmin = cs[k] < cmin ? cs[k] : cmin;
                 }
 #undef NOTE_FOREST
                 if (EXT) {
@@ -1093,20 +1116,26 @@ hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream) 
                                       dim3(kBlockWalkers * kLanes), params, 0, stream);
 }
 
-hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
+template <int NC>
+hipError_t launch_overlap_nc(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
     const dim3 grid((unsigned)(n_ranks * a.n_tiles)), block(kLanes);
     // a.ext: extra-time output (prorating and/or ensemble factors); a.forest_nodes: ensemble
     const bool forest = a.forest_nodes != nullptr, prorate = a.prorate != 0;
     if (forest) {
-        if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, true>), grid, block, 0, stream, a);
-        else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, true>), grid, block, 0, stream, a);
-        else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, true>), grid, block, 0, stream, a);
-        else hipLaunchKernelGGL((k_overlap<false, false, true>), grid, block, 0, stream, a);
-    } else if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, false>), grid, block, 0, stream, a);
-    else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, false>), grid, block, 0, stream, a);
-    else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, false>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((k_overlap<false, false, false>), grid, block, 0, stream, a);
+        if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, true, NC>), grid, block, 0, stream, a);
+        else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, true, NC>), grid, block, 0, stream, a);
+        else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, true, NC>), grid, block, 0, stream, a);
+        else hipLaunchKernelGGL((k_overlap<false, false, true, NC>), grid, block, 0, stream, a);
+    } else if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, false, NC>), grid, block, 0, stream, a);
+    else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, false, NC>), grid, block, 0, stream, a);
+    else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, false, NC>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((k_overlap<false, false, false, NC>), grid, block, 0, stream, a);
     return hipGetLastError();
+}
+
+hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
+    if (a.max_comm_streams > 4) return launch_overlap_nc<kStreams>(a, n_ranks, stream);
+    return launch_overlap_nc<4>(a, n_ranks, stream);
 }
 
 hipError_t launch_settle(unsigned *chg, int32_t n_scen, int32_t *refinements, unsigned *stable,

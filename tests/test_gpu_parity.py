@@ -74,7 +74,7 @@ def test_tiny_graphs(E, name, R):
     assert_same(gpu_run(E, g, sc, R), oracle.run(g, sc, R))
 
 
-def _random_graph(rng, n_ranks, ops_per_rank, n_coll, p_comm=0.3):
+def _random_graph(rng, n_ranks, ops_per_rank, n_coll, p_comm=0.3, comm_streams=4):
     b = Builder(n_ranks, gpus_per_node=int(rng.integers(1, 5)))
     colls = []
     for _ in range(n_coll):
@@ -83,7 +83,8 @@ def _random_graph(rng, n_ranks, ops_per_rank, n_coll, p_comm=0.3):
         members = sorted(rng.choice(n_ranks, size=min(k, n_ranks), replace=False).tolist())
         if t == P2P and len(members) < 2:
             continue
-        colls.append((b.collective(t, int(rng.integers(0, 64 << 20))), members, int(rng.integers(1, 5))))
+        colls.append((b.collective(t, int(rng.integers(0, 64 << 20))), members,
+                      int(rng.integers(1, 1 + comm_streams))))
     # every rank issues its collectives in collective-id order on a per-collective stream
     for r in range(n_ranks):
         ids = []
@@ -488,6 +489,32 @@ def test_validator_variants_tiny(E, until_stable, prorate):
         g = TINY[name]
         ref = oracle.run(g, sc, 4, until_stable=until_stable, prorate=prorate)
         gpu = _variant_run(E, g, sc, 4, until_stable, prorate)
+        assert_same(gpu, ref)
+        np.testing.assert_array_equal(gpu["refinements"], ref["refinements"])
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_more_than_four_comm_streams(E, seed):
+    """Ranks with up to seven comm streams (overlap detection's wide variant) under
+    every validator."""
+    rng = np.random.default_rng(7000 + seed)
+    g = _random_graph(rng, int(rng.integers(2, 9)), int(rng.integers(60, 160)), int(rng.integers(12, 30)),
+                      p_comm=0.15, comm_streams=7)
+    per_rank = [len({int(s) for s, k, r in zip(g["op_stream"], g["op_kind"], g["op_rank"]) if k == 1 and r == q})
+                for q in range(g["n_ranks"])]
+    assert max(per_rank) > 4
+    sc = scenarios.draw(70, rng, bw_inter=(20000, 400000), alpha=(0, 40000), slowdown=(65536, 196608),
+                        jitter=(4000, seed) if seed % 2 else None)
+    try:
+        oracle.run(g, scenarios.take(sc, [0]), 0)
+    except oracle.OracleError as e:
+        assert e.code == -4
+        return
+    for R in (0, 2):
+        assert_same(gpu_run(E, g, sc, R), oracle.run(g, sc, R, threads=THREADS))
+    for until_stable, prorate in VARIANTS:
+        ref = oracle.run(g, sc, 8, threads=THREADS, until_stable=until_stable, prorate=prorate)
+        gpu = _variant_run(E, g, sc, 8, until_stable, prorate)
         assert_same(gpu, ref)
         np.testing.assert_array_equal(gpu["refinements"], ref["refinements"])
 
