@@ -296,7 +296,9 @@ typedef struct {
  * roots of n_trees trees, the base score (65536 <= base < 2^20) and
  * class_metrics[8][4].  Every root-to-leaf path has at most ECHO_TREE_DEPTH
  * splits.  n_trees = 0 removes the ensemble.  Errors: ARG (malformed trees or
- * arrays), NOMEM, HIP.
+ * arrays), RANGE (more than 2^26 nodes once every tree is laid out on its own,
+ * nodes shared between paths copied), NOMEM, HIP; on ARG and RANGE the graph
+ * keeps its previous ensemble.
  */
 int echo_set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes, const int32_t *roots,
                     int32_t n_trees, int32_t base_q16, const int64_t *class_metrics);

@@ -49,6 +49,7 @@ constexpr int64_t kI32Max = INT32_MAX;
 constexpr int kMaxRanksPerWalker = 16;
 constexpr int64_t kKnobLimitHost = int64_t(1) << 40;
 constexpr int64_t kDefaultSpinNs = 20LL * 1000 * 1000 * 1000;   // 20 s
+constexpr int64_t kMaxDevTreeNodes = int64_t(1) << 26;          // device ensemble: 1 GiB
 
 // Table 6 (all-reduce breakdown): NCCL chunk size by tensor size.  The size
 // row is read as MiB upper bounds, the chunk row in units of 1000 bytes.
@@ -1026,9 +1027,8 @@ int echo_set_cc_tables(echo_graph g, const echo_cc_table *tables, int32_t n_tabl
     return ECHO_OK;
 }
 
-int echo_set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes, const int32_t *roots,
-                    int32_t n_trees, int32_t base_q16, const int64_t *class_metrics) {
-    g_last_error.clear();
+static int set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes, const int32_t *roots,
+                      int32_t n_trees, int32_t base_q16, const int64_t *class_metrics) {
     if (!g) return fail(ECHO_ERR_ARG, "null graph");
     if (n_trees < 0) return fail(ECHO_ERR_ARG, "n_trees %d < 0", n_trees);
     if (n_trees > 0) {
@@ -1053,6 +1053,33 @@ int echo_set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes, 
             }
         }
     }
+    // device layout: each tree laid out breadth first from its root, a split's two
+    // children side by side (a node reached along two paths is copied)
+    std::vector<DevTreeNode> hn;
+    std::vector<int32_t> hr(n_trees);
+    std::vector<std::pair<int32_t, int64_t>> todo;    // (source node, device slot)
+    for (int32_t t = 0; t < n_trees; ++t) {
+        hr[t] = (int32_t)hn.size();
+        hn.push_back(DevTreeNode{});
+        todo.assign(1, {roots[t], (int64_t)hr[t]});
+        for (size_t h = 0; h < todo.size(); ++h) {
+            const echo_tree_node &nd = nodes[todo[h].first];
+            const int64_t slot = todo[h].second;
+            if (nd.feature < 0) {
+                hn[slot] = DevTreeNode{(int64_t)nd.value, -1, 0};
+                continue;
+            }
+            if ((int64_t)hn.size() + 2 > kMaxDevTreeNodes)
+                return fail(ECHO_ERR_RANGE, "ensemble too large: more than %lld nodes once laid out",
+                            (long long)kMaxDevTreeNodes);
+            const int32_t l = (int32_t)hn.size();
+            hn.push_back(DevTreeNode{});
+            hn.push_back(DevTreeNode{});
+            hn[slot] = DevTreeNode{nd.threshold, nd.feature, l};
+            todo.push_back({nd.left, (int64_t)l});
+            todo.push_back({nd.right, (int64_t)l + 1});
+        }
+    }
     hipError_t e = hipSetDevice(g->device);
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     (void)hipDeviceSynchronize();                  // composes already enqueued may read the old ensemble
@@ -1064,8 +1091,6 @@ int echo_set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes, 
     g->dg.class_metrics = nullptr;
     g->dg.n_trees = 0;
     if (n_trees == 0) return ECHO_OK;
-    std::vector<echo_tree_node> hn(nodes, nodes + n_nodes);
-    std::vector<int32_t> hr(roots, roots + n_trees);
     std::vector<int64_t> hm(class_metrics, class_metrics + kClasses * kClassMetrics);
     if ((e = upload(&g->dg.forest_nodes, hn)) || (e = upload(&g->dg.forest_roots, hr)) ||
         (e = upload(&g->dg.class_metrics, hm)))
@@ -1073,6 +1098,18 @@ int echo_set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes, 
     g->dg.n_trees = n_trees;
     g->dg.forest_base = base_q16;
     return ECHO_OK;
+}
+
+int echo_set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes, const int32_t *roots,
+                    int32_t n_trees, int32_t base_q16, const int64_t *class_metrics) {
+    g_last_error.clear();
+    try {
+        return set_forest(g, nodes, n_nodes, roots, n_trees, base_q16, class_metrics);
+    } catch (const std::bad_alloc &) {
+        return fail(ECHO_ERR_NOMEM, "host allocation failed while laying out the ensemble");
+    } catch (...) {
+        return fail(ECHO_ERR_ARG, "unexpected exception while setting the ensemble");
+    }
 }
 
 int echo_sync_status(echo_graph g, void *hip_stream) {

@@ -127,6 +127,16 @@ struct CollTable {
 };
 
 // Device copy of a loaded graph (all pointers are device memory).
+// Device form of a tree node, one 16-byte load: the two children of a split sit side
+// by side (right = left + 1); a split keeps its threshold in tv, a leaf (feature < 0)
+// its value.
+struct DevTreeNode {
+    int64_t tv;
+    int32_t feature;
+    int32_t left;
+};
+static_assert(sizeof(DevTreeNode) == 16, "one 16-byte load per node");
+
 struct DeviceGraph {
     int64_t n_ops = 0, n_colls = 0;
     int32_t n_ranks = 0, n_walkers = 0, n_blocks = 0;
@@ -149,7 +159,7 @@ struct DeviceGraph {
     int32_t n_cc_tables = 0;
     int32_t *cl_coll = nullptr;      // collective of each listed comm op (parallel to cl)
     // slowdown ensemble (echo_set_forest)
-    echo_tree_node *forest_nodes = nullptr;
+    DevTreeNode *forest_nodes = nullptr;
     int32_t *forest_roots = nullptr;
     int64_t *class_metrics = nullptr;  // [8][4]
     int32_t n_trees = 0, forest_base = 65536;
@@ -206,7 +216,7 @@ struct OverlapArgs {
     const int32_t *cl_coll;
     const int64_t *coll_bytes;       // S of each collective
     const int32_t *coll_N;           // N its cost uses
-    const echo_tree_node *forest_nodes;
+    const DevTreeNode *forest_nodes;
     const int32_t *forest_roots;
     const int64_t *class_metrics;
     int32_t n_trees, forest_base;

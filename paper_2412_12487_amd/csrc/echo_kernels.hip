@@ -621,21 +621,23 @@ __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_
                 idx[q] = live[q] ? a.forest_roots[tr0 + q] : 0;
             }
             for (int step = 0; step <= ECHO_TREE_DEPTH; ++step) {
-                echo_tree_node nd[kForestLanes];
+                int4 nd[kForestLanes];          // tv low, tv high, feature, left
 #pragma unroll
-                for (int q = 0; q < kForestLanes; ++q) nd[q] = a.forest_nodes[idx[q]];
+                for (int q = 0; q < kForestLanes; ++q)
+                    nd[q] = reinterpret_cast<const int4 *>(a.forest_nodes)[idx[q]];
                 bool more = false;
 #pragma unroll
                 for (int q = 0; q < kForestLanes; ++q) {
-                    if (!live[q] || nd[q].feature < 0) continue;
-                    const int64_t x = feat[nd[q].feature * kLanes + lane];
-                    idx[q] = x < nd[q].threshold ? nd[q].left : nd[q].right;
+                    if (!live[q] || nd[q].z < 0) continue;
+                    const int64_t x = feat[nd[q].z * kLanes + lane];
+                    const int64_t thr = (int64_t)(((uint64_t)(uint32_t)nd[q].y << 32) | (uint32_t)nd[q].x);
+                    idx[q] = nd[q].w + (x < thr ? 0 : 1);
                     more = true;
                 }
                 if (!more) {
 #pragma unroll
                     for (int q = 0; q < kForestLanes; ++q)
-                        if (live[q]) sum += nd[q].value;
+                        if (live[q]) sum += (int64_t)(((uint64_t)(uint32_t)nd[q].y << 32) | (uint32_t)nd[q].x);
                     break;
                 }
             }
