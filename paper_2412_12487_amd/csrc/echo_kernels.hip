@@ -588,7 +588,7 @@ __device__ __forceinline__ uint32_t factor_of(uint32_t m, const uint32_t *slow, 
 // type, the base score plus one leaf per tree, kept inside [65536, 2^20); the
 // largest over the types.  Trees are walked per lane from global memory (the
 // walk stops at a leaf; paths are at most ECHO_TREE_DEPTH splits long).
-constexpr int kForestLanes = 8;
+constexpr int kForestLanes = 16;
 constexpr int kPre = 8;          // unchained starts prefetched per round of overlap detection
 constexpr int kIdStage = 1024;   // comm ops of a rank whose ids overlap detection keeps in LDS
 
