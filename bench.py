@@ -314,10 +314,14 @@ def roofline(g, r, args, traffic_config):
         tr = json.load(open(TRAFFIC_FILE))
         if tr.get("kernel_source_sha") == source_hash() and tr.get("config") == traffic_config:
             traffic = tr.get("bytes_per_launch")
-    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-            "kernel": "k_walk", "avg_launch_ms": round(r["walk_avg_ms"], 4),
-            "algorithmic_bytes_per_launch": int(bytes_per_launch)}
+    out = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+           "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+           "kernel": "k_walk", "avg_launch_ms": round(r["walk_avg_ms"], 4),
+           "algorithmic_bytes_per_launch": int(bytes_per_launch)}
+    if traffic is not None:
+        # the same launches by the bytes the counters saw (stream predecessors stay in registers)
+        out["traffic_frac"] = round(traffic / (r["walk_avg_ms"] / 1000.0) / 1e9 / HBM_PEAK_GBS, 4)
+    return out
 
 
 def replica_mode(args, E, configs, gpt1f1b):

@@ -87,3 +87,19 @@ def test_cpu_baseline_runs_the_gpu_run_options():
         if opts.get("forest") or opts.get("prorate"):
             assert not np.array_equal(ref["digest"], plain["digest"])
     assert bench.cpu_baseline(g, configs.scenario_batch(1), 1, 1, {}, ops_counted=10)["value"] > 0
+
+
+def test_roofline_reports_measured_traffic_fraction(tmp_path, monkeypatch):
+    """With a byte-counter record for the built kernels, the line carries the measured
+    bytes per launch and their fraction of the peak beside the algorithmic one."""
+    import json
+    g = _graph()
+    rec = {"config": 3, "kernel_source_sha": bench.source_hash(), "bytes_per_launch": 4_000_000_000}
+    f = tmp_path / "walk_traffic.json"
+    f.write_text(json.dumps(rec))
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
+    rf = bench.roofline(g, {"n_scen": 64, "n_pass": 2, "n_launch": 2, "walk_avg_ms": 1.0}, None, 3)
+    assert rf["traffic"] == 4_000_000_000
+    assert rf["traffic_frac"] == round(4e9 / 1e-3 / 1e9 / bench.HBM_PEAK_GBS, 4)
+    rf = bench.roofline(g, {"n_scen": 64, "n_pass": 2, "n_launch": 2, "walk_avg_ms": 1.0}, None, 2)
+    assert rf["traffic"] is None and "traffic_frac" not in rf
