@@ -136,9 +136,9 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py runs on one GPU: this build composes every scenario on a single MI355X "
-              f"(asked for {max(args.gpus, world)}).  Sharding scenarios across GPUs is described "
-              f"in DESIGN.md but not built.", file=sys.stderr)
+        print(f"bench.py runs on one GPU: the composer evaluates every scenario on a single MI355X "
+              f"(asked for {max(args.gpus, world)}); sharding the scenarios across GPUs is not built.",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -21,7 +21,7 @@
  *      running time with overlap to running time without), and the timeline
  *      is composed again.
  *
- * Readings taken where the paper is silent (each documented in the design doc):
+ * Readings taken where the paper is silent:
  *   - stream timelines are FIFO in program order; the k-th op of a stream
  *     waits for the (k-1)-th to finish;
  *   - a comm op starts at its own launch and finishes at barrier + T(c);
