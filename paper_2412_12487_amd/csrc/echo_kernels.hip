@@ -187,7 +187,13 @@ __global__ __launch_bounds__(64) void k_cc_cost(CollTable t, const echo_cc_table
 // their launch times.  Bounded: gives up (and tells every other waiter to give
 // up) after spin_limit ticks of the 100 MHz wall clock.
 __device__ bool wait_arrivals(const unsigned *cnt, unsigned need, unsigned *status, int64_t limit) {
-    if (__builtin_amdgcn_readfirstlane(ld_relaxed(cnt)) >= need) return true;
+    // Issue priority on the SIMD follows lateness: the last member to arrive is what the
+    // others wait for, so it runs at raised priority until it next arrives early.
+    if (__builtin_amdgcn_readfirstlane(ld_relaxed(cnt)) >= need) {
+        __builtin_amdgcn_s_setprio(2);
+        return true;
+    }
+    __builtin_amdgcn_s_setprio(0);
     const uint64_t t0 = wall_clock64();
     for (;;) {
         __builtin_amdgcn_s_sleep(2);
@@ -230,7 +236,11 @@ __device__ __forceinline__ unsigned ld_local(const unsigned *p) {
 }
 
 __device__ bool wait_local(const unsigned *cnt, unsigned need, unsigned *status, int64_t limit) {
-    if (ld_local(cnt) >= need) return true;
+    if (ld_local(cnt) >= need) {
+        __builtin_amdgcn_s_setprio(2);             // last to arrive: see wait_arrivals
+        return true;
+    }
+    __builtin_amdgcn_s_setprio(0);
     const uint64_t t0 = wall_clock64();
     for (unsigned it = 1;; ++it) {
         __builtin_amdgcn_s_sleep(1);
