@@ -332,6 +332,33 @@ def test_cc_costs_match_oracle(E):
         np.testing.assert_array_equal(cost.T, ref["cost"])
 
 
+def test_unfit_buffers_rejected_before_launch(E):
+    """Output and scenario tensors that do not fit the call are refused on the host
+    (no kernel sees them); the graph stays usable."""
+    import torch
+    g = configs.graph(1)
+    sc = scenarios.take(configs.scenario_batch(4), slice(0, 70))
+    G = E.Graph(g, 0)
+    try:
+        d, n = E.scenarios_to_device(sc)
+        dev = d.device
+        small = torch.empty((G.n_ops, n - 1), dtype=torch.int64, device=dev)
+        with pytest.raises(E.EchoError, match="start holds"):
+            G.compose(d, n, 1, out={"start": small})
+        with pytest.raises(E.EchoError, match="contiguous"):
+            G.compose(d, n, 1, out={"finish": torch.empty((n, G.n_ops), dtype=torch.int64, device=dev).t()})
+        with pytest.raises(E.EchoError, match="int64"):
+            G.compose(d, n, 1, out={"step": torch.empty(n, dtype=torch.int32, device=dev)})
+        with pytest.raises(E.EchoError, match="scenarios holds"):
+            G.compose(d[: 192 * (n - 1)], n, 1)
+        with pytest.raises(E.EchoError, match="scenarios is on"):
+            G.compose(d.cpu(), n, 1)
+        ref = oracle.run(g, sc, 1, threads=THREADS)
+        assert_same(gpu_run(E, g, sc, 1, graph=G), ref)
+    finally:
+        G.close()
+
+
 def test_graph_without_ops(E):
     g = Builder(4).graph()
     res = gpu_run(E, g, scenarios.default_scenarios(3), 1)
