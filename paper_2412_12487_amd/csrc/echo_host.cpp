@@ -101,13 +101,10 @@ struct echo_graph_s {
     int64_t n_items = 0;               // entries of the walk lists
     int32_t n_ranks = 0, n_walkers = 0;
     int64_t capacity[kWalkVariants] = {};   // co-resident walk workgroups per kernel variant
-    bool need_coll_cost = false;       // some comm op reads its cost per collective
     int64_t spin_limit = kDefaultSpinNs / 10;   // 100 MHz ticks
     DeviceGraph dg;
     std::vector<void *> owned;         // device allocations of the graph
     // workspace, grown on demand
-    int64_t *cost = nullptr;
-    size_t cost_n = 0;
     int64_t *class_cost = nullptr;
     size_t class_cost_n = 0;
     unsigned long long *arrive = nullptr;
@@ -137,7 +134,6 @@ void free_graph(echo_graph g) {
     (void)hipSetDevice(g->device);
     (void)hipDeviceSynchronize();
     for (void *p : g->owned) (void)hipFree(p);
-    (void)hipFree(g->cost);
     (void)hipFree(g->class_cost);
     (void)hipFree(g->arrive);
     (void)hipFree(g->count);
@@ -535,7 +531,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
                       (fold ? kFold : 0u);
             it.far_off = (int32_t)far.size();
             it.coll = (int32_t)d->op_coll[v];
-            it.dur = 0;
+            it.dur = ccls[d->op_coll[v]];    // the cost class its finish reads
             it.nfar = 0;
             it.aux = coll_aux[d->op_coll[v]] | ((uint32_t)op_slot[v] << 5);
             items.push_back(it);
@@ -721,8 +717,6 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     for (size_t k = 0; k < classes.size(); ++k)
         cls.set((int64_t)k, (int)classes[k][0], classes[k][1], (int32_t)classes[k][2], (int32_t)classes[k][3],
                 (int32_t)classes[k][4]);
-    bool need_coll_cost = false;
-    for (int64_t v = 0; v < n; ++v) need_coll_cost = need_coll_cost || (d->op_kind[v] == ECHO_COMM && op_slot[v] == kNoSlot);
 
     // upload
     echo_graph g = new (std::nothrow) echo_graph_s();
@@ -742,7 +736,6 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     dg.n_walkers = (int32_t)W;
     dg.n_blocks = (int32_t)nblk;
     dg.max_comm_streams = max_comm_streams;
-    g->need_coll_cost = need_coll_cost;
 #define UP(dst, src)                                                        \
     do {                                                                    \
         e = upload(&dst, src);                                              \
@@ -800,7 +793,6 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
     const int64_t ns = n_scen;
     const int32_t n_tiles = (int32_t)((ns + kLanes - 1) / kLanes);
     int rc;
-    if ((rc = ensure(&g->cost, &g->cost_n, (size_t)(g->n_colls * ns), "cost"))) return rc;
     if ((rc = ensure(&g->class_cost, &g->class_cost_n, (size_t)(g->dg.classes.n * ns), "class cost"))) return rc;
     if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->n_colls * ns), "arrivals"))) return rc;
     if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * n_tiles), "arrival counts"))) return rc;
@@ -833,9 +825,6 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
                                    stream), "init kernel");
     TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.classes, g->dg.cc_tables, d_scen, n_scen, g->class_cost, g->dg.status, stream),
           "cc_cost kernel");
-    if (g->need_coll_cost)
-        TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.colls, g->dg.cc_tables, d_scen, n_scen, g->cost, g->dg.status, stream),
-              "cc_cost kernel");
     if (until_stable && (e = launch_fill_i32(reinterpret_cast<int32_t *>(g->chg), ns + 1, 0, stream)))
         return hip_fail(e, "fill kernel");
     if (d_refinements && (e = launch_fill_i32(d_refinements, ns, until_stable ? 0 : n_refine, stream)))
@@ -890,7 +879,6 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
             a.c_N = g->dg.members;
             a.block_class = g->dg.block_class;
             a.scen = d_scen;
-            a.cost = g->cost;
             a.class_cost = g->class_cost;
             a.tmask = p > 0 && !ext ? g->tmask : nullptr;
             a.ext = p > 0 && ext ? g->ext : nullptr;

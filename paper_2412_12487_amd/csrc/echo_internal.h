@@ -46,7 +46,7 @@ struct WalkItem {
                         // | need start << 18 | need finish << 19 | fold << 20
     int32_t far_off;    // predecessors read back from memory: far[far_off .. +nfar)
     int32_t coll;       // collective of a comm op, -1 otherwise
-    int64_t dur;        // base duration of compute / memcpy ops
+    int64_t dur;        // base duration of compute / memcpy ops; resolve item: cost class
     int32_t nfar;
     int32_t aux;
 };
@@ -83,7 +83,7 @@ constexpr int kChannels = 8;          // LDS barrier channels per block
 constexpr int kClassSlots = 8;        // LDS cost classes per block
 constexpr uint32_t kNoSlot = 15;
 // Comm item aux word: bit 0 local barrier | channel << 1 | slot parity << 4 |
-// class slot << 5 (kNoSlot: read the cost from global memory) | expected count << 9.
+// class slot << 5 (kNoSlot: read the class's cost from global memory) | expected count << 9.
 constexpr uint32_t kAuxLocal = 1u;
 constexpr int kExpectedBits = 23;
 __host__ __device__ inline int aux_channel(uint32_t x) { return int((x >> 1) & 7u); }
@@ -175,7 +175,6 @@ struct WalkArgs {
     const int32_t *c_N;              // [coll] member ops present (arrivals that complete the barrier)
     const int32_t *block_class;
     const echo_scenario *scen;
-    const int64_t *cost;             // [coll][scen]
     const int64_t *class_cost;       // [class][scen]
     // Per-item outputs of overlap detection, one row per walk item (rows of items that are
     // not compute ops unused), mstride columns (the tiles' scenarios, padded to whole tiles):

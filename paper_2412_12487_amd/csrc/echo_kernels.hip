@@ -374,7 +374,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
 
 // Finish f_ of comm op v_ (collective c_, aux word x_): its barrier -- the
 // latest member launch -- plus the collective's cost; written to the finish array.
-#define MEET(c_, v_, x_, f_)                                                                     \
+#define MEET(c_, v_, x_, k_, f_)                                                                 \
     {                                                                                            \
         uint64_t b_ = 0;                                                                         \
         if ((x_) & kAuxLocal) {                                                                  \
@@ -396,7 +396,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
         const int sl_ = aux_slot(x_);                                                            \
         /* distinct load kinds keep the two reads from merging into one flat load */            \
         const int64_t t_ = sl_ < kClassSlots ? ccost[sl_][lane]                                  \
-                                             : __hip_atomic_load(a.cost + (int64_t)(c_) * ns + sigma, \
+                                             : __hip_atomic_load(a.class_cost + (int64_t)(k_) * ns + sigma, \
                                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); \
         f_ = (int64_t)b_ + t_;                                                                   \
         hi_or |= (uint32_t)((uint64_t)(f_) >> 32);                                               \
@@ -485,7 +485,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             if (kind == kResolve) {
                 // a comm op's barrier, due right before its first successor
                 int64_t f;
-                MEET(coll, op, aux, f)
+                MEET(coll, op, aux, (int32_t)dur, f)
                 xmax = f > xmax ? f : xmax;
                 const int sq = __builtin_amdgcn_readfirstlane((meta & kNoReg) ? kStreams : st);
                 if (sq == 0) lf0 = f;
