@@ -190,7 +190,7 @@ __device__ bool wait_arrivals(const unsigned *cnt, unsigned need, unsigned *stat
     // Issue priority on the SIMD follows lateness: the last member to arrive is what the
     // others wait for, so it runs at raised priority until it next arrives early.
     if (__builtin_amdgcn_readfirstlane(ld_relaxed(cnt)) >= need) {
-        __builtin_amdgcn_s_setprio(2);
+        __builtin_amdgcn_s_setprio(3);
         return true;
     }
     __builtin_amdgcn_s_setprio(0);
@@ -237,7 +237,7 @@ __device__ __forceinline__ unsigned ld_local(const unsigned *p) {
 
 __device__ bool wait_local(const unsigned *cnt, unsigned need, unsigned *status, int64_t limit) {
     if (ld_local(cnt) >= need) {
-        __builtin_amdgcn_s_setprio(2);             // last to arrive: see wait_arrivals
+        __builtin_amdgcn_s_setprio(3);             // last to arrive: see wait_arrivals
         return true;
     }
     __builtin_amdgcn_s_setprio(0);
