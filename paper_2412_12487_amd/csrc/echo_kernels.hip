@@ -46,7 +46,14 @@ __device__ __forceinline__ uint64_t jitter_base(uint64_t seed, uint32_t jstream)
     return seed + ((uint64_t)jstream << 36) * kGolden;
 }
 __device__ __forceinline__ int64_t jittered(int64_t d0, int32_t v, uint64_t jbase, int32_t amp) {
-    const uint64_t u = mix64(jbase + ((uint64_t)(uint32_t)v + 1ull) * kGolden);
+    // (v + 1) * golden is the same for every lane: two scalar multiplies (kept opaque so the
+    // compiler does not fold them into a vector multiply-add with the lane's jbase)
+    const uint32_t k = (uint32_t)v + 1u;
+    uint32_t lo, hi;
+    asm("s_mul_i32 %0, %1, %2" : "=s"(lo) : "s"(k), "s"((uint32_t)kGolden));
+    asm("s_mul_hi_u32 %0, %1, %2" : "=s"(hi) : "s"(k), "s"((uint32_t)kGolden));
+    hi += k * (uint32_t)(kGolden >> 32);
+    const uint64_t u = mix64(jbase + (((uint64_t)hi << 32) | lo));
     const uint32_t f = (uint32_t)(65536 - amp) + __umulhi((uint32_t)(u >> 32), (uint32_t)(2 * amp + 1));
     return q16(d0, f);
 }
