@@ -771,4 +771,22 @@ def test_forest_errors(E):
     with pytest.raises(E.EchoError) as x:
         G.set_forest(deep)
     assert x.value.code == E.ECHO_ERR_ARG
+    # nodes shared along every path: 13 nodes describe a full tree of depth 12 (8191 nodes
+    # once laid out), and 8200 such trees pass the 2^26-node limit; the previous ensemble stays
+    good = slowdown_forest.synthetic_forest(3, n_trees=8)
+    G.set_forest(good)
+    shared = {"nodes": np.zeros(13, slowdown_forest.TREE_NODE_DTYPE), "roots": np.zeros(8200, np.int32),
+              "base": 65536, "class_metrics": np.zeros((8, 4), np.int64)}
+    for i in range(12):
+        shared["nodes"][i] = (i % 4, i + 1, i + 1, 0, 1000)
+    shared["nodes"][12] = (-1, 0, 0, 7, 0)
+    with pytest.raises(E.EchoError) as x:
+        G.set_forest(shared)
+    assert x.value.code == E.ECHO_ERR_RANGE
+    sc = scenarios.take(configs.scenario_batch(4), slice(0, 70))
+    d, n = E.scenarios_to_device(sc)
+    out = G.compose(d, n, 1, timelines=True, digest=True, forest=True)
+    ref = oracle.run(g, sc, 1, threads=THREADS, forest=good)
+    assert_same({"step": out["step"].cpu().numpy(), "digest": out["digest"].cpu().numpy().view(np.uint64),
+                 "start": out["start"].cpu().numpy(), "finish": out["finish"].cpu().numpy()}, ref)
     G.close()
