@@ -675,10 +675,9 @@ __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_
 template <bool PRORATE, bool DETECT, bool FOREST, int NC>
 __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     constexpr bool EXT = PRORATE || FOREST;      // output: extra time per op instead of a mask
-    // whole blocks of ops may be skipped; all but the ensemble variants prefetch fewer
-    // unchained starts for the registers the block checks take (four wavefronts per SIMD
-    // for the mask and prorating variants with four comm streams)
-    constexpr bool SKIP = true;
+    // unchained starts prefetched per round: all but the ensemble variants prefetch fewer,
+    // for the registers the block checks take (four wavefronts per SIMD for the mask and
+    // prorating variants with four comm streams)
     constexpr int NPRE = FOREST ? kPre : (DETECT || PRORATE) ? kPre / 4 : kPre / 2;
     __shared__ int64_t feat[FOREST ? 12 * kLanes : 1];   // the ensemble's feature vectors, one per lane
     __shared__ int32_t sid[kIdStage];            // the rank's comm op ids and collective types, staged
@@ -799,19 +798,17 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
             // finishes of the round's blocks' last ops (stored by the walk): a block ending
             // before every cursor starts is skipped whole
             constexpr int kBlocks = kLanes / kOverlapBlock;
-            int64_t ck[SKIP ? kBlocks : 1];
+            int64_t ck[kBlocks];
             // the fixed-point variants (every pass after the first reads the previous pass's
             // values): the current block's previous masks or extra times
             uint32_t old8[DETECT ? kOverlapBlock : 1];
-            if (SKIP) {
 #pragma unroll
-                for (int b = 0; b < kBlocks; ++b) {
-                    ck[b] = kInf;
-                    if (b * kOverlapBlock < nr) {
-                        const int jl = (b + 1) * kOverlapBlock - 1 < nr ? (b + 1) * kOverlapBlock - 1 : nr - 1;
-                        const int64_t vl = __builtin_amdgcn_readlane(cur.x, jl);
-                        ck[b] = (fbase + vl * ns)[col];
-                    }
+            for (int b = 0; b < kBlocks; ++b) {
+                ck[b] = kInf;
+                if (b * kOverlapBlock < nr) {
+                    const int jl = (b + 1) * kOverlapBlock - 1 < nr ? (b + 1) * kOverlapBlock - 1 : nr - 1;
+                    const int64_t vl = __builtin_amdgcn_readlane(cur.x, jl);
+                    ck[b] = (fbase + vl * ns)[col];
                 }
             }
             {
@@ -829,7 +826,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 __builtin_amdgcn_s_waitcnt(kWaitVm0);
             }
             for (int j = 0; j < nr; ++j) {
-                if (SKIP && (j & (kOverlapBlock - 1)) == 0) {
+                if ((j & (kOverlapBlock - 1)) == 0) {
                     if (DETECT && a.prev_refined) {
                         // the previous pass's masks (extra times) of the block's ops, fetched
                         // together: one memory round trip per block instead of one per op
