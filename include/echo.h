@@ -241,7 +241,10 @@ int echo_cc_cost(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int6
  * Works on the device only; range violations found there are reported by
  * echo_sync_status.  Calls on one graph must not overlap (they share its
  * workspace); the workspace grows on demand (hipMalloc) and is freed with
- * the graph.
+ * the graph.  The call enqueues kernels only (no memset, no host
+ * synchronisation), so once an eager call with at least as many scenarios
+ * and the same options has sized the workspace, it can be recorded by HIP
+ * stream capture and replayed as a graph (kernel timing must be off).
  */
 int echo_compose_batch(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n_refine,
                        int64_t *d_start, int64_t *d_finish, int64_t *d_step, uint64_t *d_digest,

@@ -359,6 +359,50 @@ def test_unfit_buffers_rejected_before_launch(E):
         G.close()
 
 
+@pytest.mark.parametrize("until_stable", [False, True])
+def test_compose_captured_in_a_hip_graph(E, until_stable):
+    """After one eager call has sized the workspace, a compose call can be captured in a
+    HIP graph: every replay (with eager work between replays) reproduces the eager
+    outputs bit for bit."""
+    import torch
+    g = configs.graph(1)
+    sc = scenarios.take(configs.scenario_batch(4), slice(0, 130))
+    G = E.Graph(g, 0)
+    try:
+        d, n = E.scenarios_to_device(sc)
+        dev = d.device
+        out = {"step": torch.empty(n, dtype=torch.int64, device=dev),
+               "start": torch.empty((G.n_ops, n), dtype=torch.int64, device=dev),
+               "finish": torch.empty((G.n_ops, n), dtype=torch.int64, device=dev),
+               "digest": torch.empty(n, dtype=torch.int64, device=dev)}
+        kw = dict(out=out, digest=True, check=False, until_stable=until_stable)
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            G.compose(d, n, 4, **kw)
+        torch.cuda.synchronize()
+        G.sync_status()
+        ref = {k: v.clone() for k, v in out.items()}
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=s):
+            G.compose(d, n, 4, **kw)
+        for _ in range(3):
+            for v in out.values():
+                v.fill_(-1)
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            for k in out:
+                assert torch.equal(out[k], ref[k]), k
+            assert out["start"].sum().item() == ref["start"].sum().item()     # eager work between
+        G.sync_status()
+        want = oracle.run(g, sc, 4, threads=THREADS, until_stable=until_stable)
+        np.testing.assert_array_equal(ref["step"].cpu().numpy(), want["step"])
+        np.testing.assert_array_equal(ref["digest"].cpu().numpy().view(np.uint64), want["digest"])
+        del graph
+    finally:
+        G.close()
+
+
 def test_graph_without_ops(E):
     g = Builder(4).graph()
     res = gpu_run(E, g, scenarios.default_scenarios(3), 1)
