@@ -82,7 +82,8 @@ def cpu_baseline(g, sc, n_refine, n_sample, variant, ops_counted=None):
     dt = time.perf_counter() - t
     ops = len(g["op_rank"]) if ops_counted is None else ops_counted
     return {"value": ops * n_sample / dt, "unit": "op-evals/s", "cores": threads,
-            "kind": "oracle", "wall_s": round(dt, 3),
+            "kind": "oracle", "wall_s": round(dt, 3), "nproc": os.cpu_count(),
+            "per_core": ops * n_sample / dt / threads,
             "sample": f"scenarios 0..{n_sample - 1} of the same graph, {n_refine} refinement(s), "
                       f"{threads} thread(s)"}
 
