@@ -187,6 +187,7 @@ def main():
                    "ranks": int(g["n_ranks"]), "levels": r["levels"], "load_s": round(r["load_s"], 2),
                    "cc_model": args.cc, "cc_cost_all_collectives_ms": r["cc_cost_all_ms"]},
         "kernels_ms": r["kernels_ms"],
+        "walk_pass_ms": r["walk_pass_ms"],
         "roofline": roofline(g, r, args, args.config if not (args.until_stable or args.prorate or args.forest
                                                              or args.cc != "echo") else None),
     }
@@ -275,7 +276,9 @@ def time_compose(E, g, sc, args, extras):
            "value": G.n_ops * n_scen / (ms_per_step / 1000.0),
            "walk_avg_ms": float(np.mean(walk_ms)) * (ran_ms / max(sum(lw), 1e-9)) / max(n_launch, 1),
            "n_pass": len(ran), "n_launch": n_launch,
-           "kernels_ms": {k: round(float(np.mean(v)), 4) for k, v in kernels.items()}}
+           "kernels_ms": {k: round(float(np.mean(v)), 4) for k, v in kernels.items()},
+           # the last step's walk launches, pass by pass (a split pass lists each launch)
+           "walk_pass_ms": [[round(ms, 4) for ms in p] for p in passes if p]}
     if args.steps and "refinements" in last:
         rf = last["refinements"].cpu().numpy()
         res["refinements"] = {"min": int(rf.min()), "mean": round(float(rf.mean()), 3), "max": int(rf.max())}
@@ -364,6 +367,7 @@ def replica_mode(args, E, configs, gpt1f1b):
                    "full_sweep_ms_per_step": round(full["ms_per_step"], 4) if full else None,
                    "speedup_vs_full_sweep": round(full["ms_per_step"] / red["ms_per_step"], 2) if full else None},
         "kernels_ms": red["kernels_ms"],
+        "walk_pass_ms": red["walk_pass_ms"],
         "roofline": roofline(rg, red, args, None),
     }
     if args.cpu_sample > 0:
