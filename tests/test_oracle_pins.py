@@ -864,3 +864,17 @@ def test_stored_full_digests_are_whole():
     assert sorted(c5) == list(range(16)) and all(len(s) == 32 and len(d) == 32 for _, s, d in c5.values())
     for h, step, dig in list(c3.values()) + list(c5.values()):
         assert len(h) == 16 and (step > 0).all() and dig.dtype == np.uint64
+
+
+def test_stored_full_digests_match_their_inputs():
+    """The smallest extrapolation graph: the stored block was made from exactly these
+    inputs, and the oracle reproduces its first and last scenarios."""
+    from tests.golden import make_full_digests as fd
+    from workloads import configs, scenarios
+    g, sc = configs.graph(5, 0), configs.scenario_batch(5, 0)
+    h, step, dig = fd.load(5)[0]
+    assert h == fd.input_hash(g, sc)
+    n = scenarios.count(sc)
+    ref = oracle.run(g, scenarios.take(sc, [0, n - 1]), 1, threads=2, timelines=False, jitter_stream=[0, n - 1])
+    np.testing.assert_array_equal(ref["step"], step[[0, n - 1]])
+    np.testing.assert_array_equal(ref["digest"], dig[[0, n - 1]])
