@@ -10,6 +10,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdint>
 #include <array>
 #include <cstdarg>
 #include <cstdio>
@@ -140,6 +141,7 @@ void free_graph(echo_graph g) {
     (void)hipFree(g->tmask);
     (void)hipFree(g->dg.cc_tables);
     (void)hipFree(g->dg.forest_nodes);
+    (void)hipFree(g->dg.forest_leaf);
     (void)hipFree(g->dg.forest_roots);
     (void)hipFree(g->dg.class_metrics);
     (void)hipFree(g->ext);
@@ -855,6 +857,7 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
                 o.coll_bytes = g->dg.colls.bytes;
                 o.coll_N = g->dg.colls.N;
                 o.forest_nodes = g->dg.forest_nodes;
+                o.forest_leaf = g->dg.forest_leaf;
                 o.forest_roots = g->dg.forest_roots;
                 o.class_metrics = g->dg.class_metrics;
                 o.n_trees = g->dg.n_trees;
@@ -1044,6 +1047,7 @@ static int set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes
     // device layout: each tree laid out breadth first from its root, a split's two
     // children side by side (a node reached along two paths is copied)
     std::vector<DevTreeNode> hn;
+    std::vector<int32_t> hleaf;
     std::vector<int32_t> hr(n_trees);
     std::vector<std::pair<int32_t, int64_t>> todo;    // (source node, device slot)
     for (int32_t t = 0; t < n_trees; ++t) {
@@ -1054,7 +1058,9 @@ static int set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes
             const echo_tree_node &nd = nodes[todo[h].first];
             const int64_t slot = todo[h].second;
             if (nd.feature < 0) {
-                hn[slot] = DevTreeNode{(int64_t)nd.value, -1, 0};
+                hn[slot] = DevTreeNode{INT64_MIN, 0, (int32_t)slot - 1};   // loops to itself
+                hleaf.resize(hn.size());
+                hleaf[slot] = nd.value;
                 continue;
             }
             if ((int64_t)hn.size() + 2 > kMaxDevTreeNodes)
@@ -1072,15 +1078,19 @@ static int set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     (void)hipDeviceSynchronize();                  // composes already enqueued may read the old ensemble
     (void)hipFree(g->dg.forest_nodes);
+    (void)hipFree(g->dg.forest_leaf);
     (void)hipFree(g->dg.forest_roots);
     (void)hipFree(g->dg.class_metrics);
     g->dg.forest_nodes = nullptr;
+    g->dg.forest_leaf = nullptr;
     g->dg.forest_roots = nullptr;
     g->dg.class_metrics = nullptr;
     g->dg.n_trees = 0;
     if (n_trees == 0) return ECHO_OK;
     std::vector<int64_t> hm(class_metrics, class_metrics + kClasses * kClassMetrics);
-    if ((e = upload(&g->dg.forest_nodes, hn)) || (e = upload(&g->dg.forest_roots, hr)) ||
+    hleaf.resize(hn.size());
+    if ((e = upload(&g->dg.forest_nodes, hn)) || (e = upload(&g->dg.forest_leaf, hleaf)) ||
+        (e = upload(&g->dg.forest_roots, hr)) ||
         (e = upload(&g->dg.class_metrics, hm)))
         return fail(e == hipErrorOutOfMemory ? ECHO_ERR_NOMEM : ECHO_ERR_HIP, "ensemble upload: %s", hipGetErrorString(e));
     g->dg.n_trees = n_trees;

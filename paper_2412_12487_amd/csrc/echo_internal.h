@@ -128,10 +128,11 @@ struct CollTable {
 
 // Device copy of a loaded graph (all pointers are device memory).
 // Device form of a tree node, one 16-byte load: the two children of a split sit side
-// by side (right = left + 1); a split keeps its threshold in tv, a leaf (feature < 0)
-// its value.
+// by side, and the walk goes to left + (x >= threshold).  A leaf loops to itself
+// (threshold INT64_MIN, left = its own index - 1), so every tree is walked exactly
+// ECHO_TREE_DEPTH steps without a branch; leaf values live in a separate array.
 struct DevTreeNode {
-    int64_t tv;
+    int64_t threshold;
     int32_t feature;
     int32_t left;
 };
@@ -160,6 +161,7 @@ struct DeviceGraph {
     int32_t *cl_coll = nullptr;      // collective of each listed comm op (parallel to cl)
     // slowdown ensemble (echo_set_forest)
     DevTreeNode *forest_nodes = nullptr;
+    int32_t *forest_leaf = nullptr;  // [node] value of a leaf (0 for a split)
     int32_t *forest_roots = nullptr;
     int64_t *class_metrics = nullptr;  // [8][4]
     int32_t n_trees = 0, forest_base = 65536;
@@ -216,6 +218,7 @@ struct OverlapArgs {
     const int64_t *coll_bytes;       // S of each collective
     const int32_t *coll_N;           // N its cost uses
     const DevTreeNode *forest_nodes;
+    const int32_t *forest_leaf;
     const int32_t *forest_roots;
     const int64_t *class_metrics;
     int32_t n_trees, forest_base;

@@ -637,27 +637,23 @@ __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_
                 live[q] = tr0 + q < a.n_trees;
                 idx[q] = live[q] ? a.forest_roots[tr0 + q] : 0;
             }
-            for (int step = 0; step <= ECHO_TREE_DEPTH; ++step) {
-                int4 nd[kForestLanes];          // tv low, tv high, feature, left
+            // every path has at most ECHO_TREE_DEPTH splits and a leaf loops to itself, so
+            // after that many steps each walk rests on its leaf: no per-lane exit
+            for (int step = 0; step < ECHO_TREE_DEPTH; ++step) {
+                int4 nd[kForestLanes];          // threshold low, threshold high, feature, left
 #pragma unroll
                 for (int q = 0; q < kForestLanes; ++q)
                     nd[q] = reinterpret_cast<const int4 *>(a.forest_nodes)[idx[q]];
-                bool more = false;
 #pragma unroll
                 for (int q = 0; q < kForestLanes; ++q) {
-                    if (!live[q] || nd[q].z < 0) continue;
                     const int64_t x = feat[nd[q].z * kLanes + lane];
                     const int64_t thr = (int64_t)(((uint64_t)(uint32_t)nd[q].y << 32) | (uint32_t)nd[q].x);
                     idx[q] = nd[q].w + (x < thr ? 0 : 1);
-                    more = true;
-                }
-                if (!more) {
-#pragma unroll
-                    for (int q = 0; q < kForestLanes; ++q)
-                        if (live[q]) sum += (int64_t)(((uint64_t)(uint32_t)nd[q].y << 32) | (uint32_t)nd[q].x);
-                    break;
                 }
             }
+#pragma unroll
+            for (int q = 0; q < kForestLanes; ++q)
+                if (live[q]) sum += a.forest_leaf[idx[q]];
         }
         sum = sum < 65536 ? 65536 : sum;
         sum = sum >= (int64_t(1) << 20) ? (int64_t(1) << 20) - 1 : sum;
