@@ -140,6 +140,58 @@ def test_jitter_amplitude_zero_is_identity_and_bounds_hold():
     assert not np.array_equal(d[0], d[1])          # each scenario has its own stream
 
 
+def _jitter_rows():
+    """Rows of jitter_worked.txt grouped by scenario and base duration: {(seed, stream, A, d0): {v: D}}."""
+    groups = {}
+    for r in _rows("jitter_worked.txt"):
+        seed, stream, v, A, d0 = int(r[0], 16), int(r[1]), int(r[2]), int(r[3]), int(r[4])
+        groups.setdefault((seed, stream, A, d0), {})[v] = int(r[11])
+    return groups
+
+
+@pytest.mark.parametrize("key", sorted(_jitter_rows()), ids=lambda k: "s%d-A%d-d%d" % (k[1], k[2], k[3]))
+def test_jittered_durations_hand_worked(key):
+    """D(v) of a three-op chain (ops v = 0, 1, 2, each of base duration d0) under a
+    jittered scenario equals the values worked by hand from published SplitMix64
+    outputs (the draw's sub-stream offset 2^36, k = v + 1, the high half of u and
+    the 2A + 1 levels each change some of them)."""
+    seed, stream, A, d0 = key
+    want = _jitter_rows()[key]
+    g = _chain_graph([d0] * 3)
+    sc = _scen(1, jitter_amp_q16=A)
+    sc["jitter_seed"] = np.array([seed], np.uint64)
+    sc["jitter_stream"] = np.array([stream], np.uint32)
+    r = oracle.run(g, sc, 0)
+    got = (r["finish"][0] - r["start"][0]).tolist()
+    assert got == [want[v] for v in range(3)]
+    assert r["step"][0] == sum(want.values())
+
+
+def test_jitter_table_refutes_plausible_slips():
+    """Each plausible slip in the draw changes at least one hand-worked D: k = v
+    instead of v + 1, the low instead of the high half of u, 2A instead of 2A + 1
+    levels, a 2^32 instead of a 2^36 sub-stream offset (u computed here from the
+    published generator definition; the table's u column is the published list)."""
+    M = (1 << 64) - 1
+    golden = 0x9E3779B97F4A7C15
+
+    def mix(z):
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & M
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & M
+        return z ^ (z >> 31)
+
+    def draw(seed, stream, v, A, d0, k_off=1, low=False, levels=1, shift=36):
+        u = mix((seed + ((stream << shift) + v + k_off) * golden) & M)
+        x = (u & 0xFFFFFFFF) if low else (u >> 32)
+        J = ((x * (2 * A + levels)) >> 32) - A
+        return (d0 * (65536 + J) + 32768) >> 16
+
+    rows = [(k, v, D) for k, vs in _jitter_rows().items() for v, D in vs.items()]
+    assert all(draw(*k[:2], v, *k[2:]) == D for k, v, D in rows)     # the table is self-consistent
+    for slip in (dict(k_off=0), dict(low=True), dict(levels=0), dict(shift=32)):
+        assert any(draw(*k[:2], v, *k[2:], **slip) != D for k, v, D in rows), slip
+
+
 # ---------------------------------------------------------------- composer vs brute force
 def _dur_cost(g, sc, si=0):
     r = oracle.run(g, scenarios.take(sc, [si]), 0, costs=True, jitter_stream=[si])
@@ -683,6 +735,16 @@ def test_random_small_dags_validator_variants():
 _AB = dict(alpha=10000, bw_intra=400000, bw_inter=50000, reduce=160000)
 
 
+def _table_from_bandwidths(alpha_ns, bw_intra_MBps, bw_inter_MBps, reduce_MBps):
+    """The CC parameter table holding what a table-less scenario with these knobs
+    uses (reading 11): Table 6 bands and chunks, per-chunk times
+    ceil(chunk * 1000 / bandwidth), alpha and the reduce throughput as given."""
+    cdiv = lambda a, b: -(-a // b)
+    chunk = scenarios.TABLE6_CHUNK
+    return scenarios.cc_table(chunk=chunk, alpha=alpha_ns, beta=cdiv(chunk * 1000, bw_intra_MBps),
+                              gamma=cdiv(chunk * 1000, bw_inter_MBps), reduce=reduce_MBps)
+
+
 @pytest.mark.parametrize("row", _rows("cc_alpha_beta.txt"), ids=lambda r: "-".join(r[:5]))
 def test_alpha_beta_hand_values(row):
     t, algo, S, N, M, K, want = (int(x) for x in row)
@@ -701,7 +763,7 @@ def test_cc_table_equal_to_bandwidth_parameters_reproduces_every_cost():
     for _ in range(200):
         kn = dict(alpha=int(rng.integers(0, 30000)), bw_intra=int(rng.integers(1000, 500000)),
                   bw_inter=int(rng.integers(1000, 500000)), reduce=int(rng.integers(1000, 500000)))
-        table = scenarios.cc_table_from_bandwidths(kn["alpha"], kn["bw_intra"], kn["bw_inter"], kn["reduce"])
+        table = _table_from_bandwidths(kn["alpha"], kn["bw_intra"], kn["bw_inter"], kn["reduce"])
         S = int(rng.choice([0, 1, 4 << 20, (4 << 20) + 1, 16 << 20, (128 << 20) + 7, 1 << 30,
                             int(rng.integers(0, 1 << 31))]))
         N = int(rng.integers(1, 300))
@@ -734,7 +796,7 @@ def test_compose_with_cc_tables_and_models():
     g = configs.graph(1)
     sc = scenarios.draw(4, np.random.default_rng(31), bw_inter=(20000, 90000), bw_intra=(50000, 400000),
                         alpha=(0, 9000), ar_algo_random=True)
-    tables = np.stack([scenarios.cc_table_from_bandwidths(int(sc["alpha_ns"][i]), int(sc["bw_intra_MBps"][i]),
+    tables = np.stack([_table_from_bandwidths(int(sc["alpha_ns"][i]), int(sc["bw_intra_MBps"][i]),
                                                           int(sc["bw_inter_MBps"][i]), int(sc["reduce_MBps"][i]))
                        for i in range(4)])
     plain = oracle.run(g, sc, 1)

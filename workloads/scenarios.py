@@ -19,8 +19,7 @@ a dict of numpy arrays, one entry per field (structure of arrays):
     slowdown_q16   uint32 [n, 8, 4]  slowdown factor per (kernel class, collective type), Q16
 
 CC parameter tables (int64 [6, 7]: per row max_bytes, chunk, alpha_ns,
-beta_ns, gamma_ns, reduce_MBps) are inputs too; `cc_table_from_bandwidths`
-writes the table equal to a scenario's bandwidth-derived parameters.
+beta_ns, gamma_ns, reduce_MBps) are inputs too.
 
 Only input values live here; no formula of the method is evaluated.
 """
@@ -121,14 +120,6 @@ def cc_table(*, chunk, alpha, beta, gamma, reduce, max_bytes=TABLE6_MAX_BYTES) -
     """One CC parameter table, int64 [6, 7]; each argument a scalar or 7 values."""
     rows = [np.broadcast_to(np.asarray(x, np.int64), (7,)) for x in (max_bytes, chunk, alpha, beta, gamma, reduce)]
     return np.stack(rows).astype(np.int64)
-
-
-def cc_table_from_bandwidths(alpha_ns, bw_intra_MBps, bw_inter_MBps, reduce_MBps) -> np.ndarray:
-    """The table holding exactly what a table-less scenario with these knobs uses:
-    Table 6 chunks, per-chunk times ceil(chunk * 1000 / bandwidth)."""
-    cdiv = lambda a, b: -(-a // b)
-    return cc_table(chunk=TABLE6_CHUNK, alpha=alpha_ns, beta=cdiv(TABLE6_CHUNK * 1000, bw_intra_MBps),
-                    gamma=cdiv(TABLE6_CHUNK * 1000, bw_inter_MBps), reduce=reduce_MBps)
 
 
 def draw_cc_tables(n: int, rng: np.random.Generator) -> np.ndarray:
