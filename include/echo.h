@@ -340,6 +340,41 @@ enum { ECHO_K_INIT = 0, ECHO_K_CC_COST = 1, ECHO_K_WALK = 2, ECHO_K_OVERLAP = 3,
 int echo_set_timing(echo_graph g, int enable);
 int echo_kernel_times(echo_graph g, int32_t max, int32_t *kinds, float *ms, int32_t *n);
 
+/*
+ * Bounded waits.  A composer wavefront that waits for the members of a
+ * collective gives up after limit_ns nanoseconds of wall clock (default 20 s):
+ * it sets the graph's timeout status, every other wait of the launch gives
+ * up too, and every kernel runs to its end (the timelines it writes are then
+ * meaningless) -- echo_sync_status reports ECHO_ERR_DEVICE.  The limit applies
+ * to each wait, not to a whole call; it is read when a compose is enqueued.
+ * 10 <= limit_ns <= 2^40 (the device clock ticks every 10 ns).  Errors: ARG.
+ */
+int echo_set_spin_limit(echo_graph g, int64_t limit_ns);
+
+/*
+ * Scenario tiles per walk launch.  The composer walks all scenario tiles of a
+ * pass in as few cooperative launches as the device holds co-resident (every
+ * walker of a tile must run at once); max_tiles > 0 caps the tiles of one
+ * launch (a pass then takes more launches), 0 restores the default.  Results
+ * do not depend on it.  Errors: ARG for max_tiles < 0.
+ */
+int echo_set_launch_tiles(echo_graph g, int32_t max_tiles);
+
+/*
+ * Latency floor of the composer's walk (analysis; reads host-side copies of
+ * the walk lists, no device work).  Each scenario tile is walked by one
+ * wavefront per walker, which visits its walk list in order; a comm op's
+ * finish is taken at its resolve item, which waits until every member's
+ * launch item has run.  With weight_ps[0] picoseconds per item, plus
+ * weight_ps[1] for a resolve item whose barrier is met in LDS (all members in
+ * one workgroup) or weight_ps[2] for one met in device memory, out receives
+ * the longest chain through those dependencies:
+ *   out[0] its length in picoseconds, out[1] its items, out[2] its
+ *   LDS-barrier and out[3] its device-memory-barrier resolve items.
+ * Weights in [0, 2^40).  Errors: ARG.
+ */
+int echo_walk_chain(echo_graph g, const int64_t weight_ps[3], int64_t out[4]);
+
 /* Message of the calling thread's last error ("" if none). */
 const char *echo_last_error(void);
 

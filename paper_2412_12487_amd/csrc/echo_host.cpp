@@ -103,6 +103,7 @@ struct echo_graph_s {
     int32_t n_ranks = 0, n_walkers = 0;
     int64_t capacity[kWalkVariants] = {};   // co-resident walk workgroups per kernel variant
     int64_t spin_limit = kDefaultSpinNs / 10;   // 100 MHz ticks
+    int64_t max_launch_tiles = 0;      // > 0: at most this many scenario tiles per walk launch
     DeviceGraph dg;
     std::vector<void *> owned;         // device allocations of the graph
     // workspace, grown on demand
@@ -779,55 +780,100 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     return ECHO_OK;
 }
 
-int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const echo_validator &val, int64_t *d_start,
-            int64_t *d_finish, int64_t *d_step, uint64_t *d_digest, int32_t *d_refinements, hipStream_t stream) {
+// Device workspace of one compose call (see ensure_workspace for the sizes).
+struct Workspace {
+    int64_t *class_cost = nullptr;         // [class][scen] collective cost of each cost class
+    unsigned long long *arrive = nullptr;  // [coll][scen] latest member launch
+    unsigned *count = nullptr;             // [coll][tile] members arrived
+    uint8_t *tmask = nullptr;              // [item + kBlock][mstride] overlap masks (refined passes)
+    uint32_t *ext = nullptr;               // same rows: prorated / ensemble extra times
+    unsigned *chg = nullptr;               // [scen] change flags + 1 stability word (until_stable)
+    int64_t *start = nullptr, *finish = nullptr, *step = nullptr;   // timelines (caller's or workspace)
+};
+
+struct ComposeShape {
+    int64_t ns = 0;
+    int32_t n_tiles = 0;
+    int64_t mstride = 0, mrows = 0;
+    bool until_stable = false, prorate = false, forest = false, ext = false;
+};
+
+int check_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const echo_validator &val,
+                  ComposeShape *sh) {
     if (!g || !d_scen) return fail(ECHO_ERR_ARG, "null graph or scenario array");
     const int32_t n_refine = val.max_refine;
-    const bool until_stable = val.until_stable != 0 && n_refine > 0;
-    const bool prorate = val.prorate != 0 && n_refine > 0;
-    const bool forest = val.forest != 0 && n_refine > 0;
-    const bool ext = prorate || forest;             // refined passes add per-op extra times
-    if (forest && g->dg.n_trees == 0) return fail(ECHO_ERR_ARG, "forest factors requested, but the graph has no ensemble");
+    sh->until_stable = val.until_stable != 0 && n_refine > 0;
+    sh->prorate = val.prorate != 0 && n_refine > 0;
+    sh->forest = val.forest != 0 && n_refine > 0;
+    sh->ext = sh->prorate || sh->forest;           // refined passes add per-op extra times
+    if (sh->forest && g->dg.n_trees == 0)
+        return fail(ECHO_ERR_ARG, "forest factors requested, but the graph has no ensemble");
     if (n_scen < 1 || n_refine < 0 || n_refine > 64)
         return fail(ECHO_ERR_ARG, "n_scen must be >= 1 and 0 <= n_refine <= 64 (got %d, %d)", n_scen, n_refine);
-    hipError_t e = hipSetDevice(g->device);
-    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
-    const int64_t ns = n_scen;
-    const int32_t n_tiles = (int32_t)((ns + kLanes - 1) / kLanes);
+    sh->ns = n_scen;
+    sh->n_tiles = (int32_t)((sh->ns + kLanes - 1) / kLanes);
+    // per-item outputs of overlap detection: whole tiles of columns, and one round of
+    // rows past the last item (the walk fetches a round's rows at once)
+    sh->mstride = (int64_t)sh->n_tiles * kLanes;
+    sh->mrows = g->n_items + kBlock;
+    return ECHO_OK;
+}
+
+// Workspace grown on demand in the graph's own device allocations.
+int ensure_workspace(echo_graph g, const ComposeShape &sh, int32_t n_refine, int64_t *d_start, int64_t *d_finish,
+                     int64_t *d_step, Workspace *ws) {
+    const int64_t ns = sh.ns;
     int rc;
     if ((rc = ensure(&g->class_cost, &g->class_cost_n, (size_t)(g->dg.classes.n * ns), "class cost"))) return rc;
     if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->n_colls * ns), "arrivals"))) return rc;
-    if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * n_tiles), "arrival counts"))) return rc;
-    // per-item outputs of overlap detection: whole tiles of columns, and one round of
-    // rows past the last item (the walk fetches a round's rows at once)
-    const int64_t mstride = (int64_t)n_tiles * kLanes, mrows = g->n_items + kBlock;
-    if (n_refine > 0 && !ext && (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(mrows * mstride), "overlap masks")))
+    if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * sh.n_tiles), "arrival counts"))) return rc;
+    if (n_refine > 0 && !sh.ext &&
+        (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(sh.mrows * sh.mstride), "overlap masks")))
         return rc;
-    if (ext && (rc = ensure(&g->ext, &g->ext_n, (size_t)(mrows * mstride), "extra times"))) return rc;
-    if (until_stable && (rc = ensure(&g->chg, &g->chg_n, (size_t)(ns + 1), "change flags"))) return rc;
-    unsigned *stable = until_stable ? g->chg + ns : nullptr;
+    if (sh.ext && (rc = ensure(&g->ext, &g->ext_n, (size_t)(sh.mrows * sh.mstride), "extra times"))) return rc;
+    if (sh.until_stable && (rc = ensure(&g->chg, &g->chg_n, (size_t)(ns + 1), "change flags"))) return rc;
     if (!d_start && (rc = ensure(&g->tmp_start, &g->tmp_start_n, (size_t)(g->n_ops * ns), "start"))) return rc;
     if (!d_finish && (rc = ensure(&g->tmp_finish, &g->tmp_finish_n, (size_t)(g->n_ops * ns), "finish")))
         return rc;
     if (!d_step && (rc = ensure(&g->tmp_step, &g->tmp_step_n, (size_t)ns, "step"))) return rc;
-    int64_t *start = d_start ? d_start : g->tmp_start;
-    int64_t *finish = d_finish ? d_finish : g->tmp_finish;
-    int64_t *step = d_step ? d_step : g->tmp_step;
+    ws->class_cost = g->class_cost;
+    ws->arrive = g->arrive;
+    ws->count = g->count;
+    ws->tmask = n_refine > 0 && !sh.ext ? g->tmask : nullptr;
+    ws->ext = sh.ext ? g->ext : nullptr;
+    ws->chg = sh.until_stable ? g->chg : nullptr;
+    ws->start = d_start ? d_start : g->tmp_start;
+    ws->finish = d_finish ? d_finish : g->tmp_finish;
+    ws->step = d_step ? d_step : g->tmp_step;
+    return ECHO_OK;
+}
 
+// Enqueue one compose: init, class costs, pass 1, then per refinement overlap
+// detection (+ settle) and the refined pass.  `timed`: record kernel events.
+int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const echo_validator &val,
+                    const ComposeShape &sh, const Workspace &ws, bool store_all, uint64_t *d_digest,
+                    int32_t *d_refinements, hipStream_t stream, bool timed) {
+    const int32_t n_refine = val.max_refine;
+    const int64_t ns = sh.ns;
+    const int32_t n_tiles = sh.n_tiles;
+    const bool until_stable = sh.until_stable, prorate = sh.prorate, forest = sh.forest, ext = sh.ext;
+    unsigned *stable = until_stable ? ws.chg + ns : nullptr;
+    hipError_t e;
     const int64_t n_arrive = g->n_colls * ns, n_count = g->n_colls * n_tiles;
     g->timed_kinds.clear();
+    const bool timing = timed && g->timing;
     Timed tm{g, stream};
-#define TIMED(kind, call, what)                                   \
-    do {                                                          \
-        if ((e = tm.begin(kind))) return hip_fail(e, "event");    \
-        if ((e = (call))) return hip_fail(e, what);               \
-        if ((e = tm.end())) return hip_fail(e, "event");          \
+#define TIMED(kind, call, what)                                                \
+    do {                                                                       \
+        if (timing && (e = tm.begin(kind))) return hip_fail(e, "event");       \
+        if ((e = (call))) return hip_fail(e, what);                            \
+        if (timing && (e = tm.end())) return hip_fail(e, "event");             \
     } while (0)
-    TIMED(ECHO_K_INIT, launch_init(g->dg, d_scen, n_scen, g->arrive, n_arrive, g->count, n_count, step, d_digest,
-                                   stream), "init kernel");
-    TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.classes, g->dg.cc_tables, d_scen, n_scen, g->class_cost, g->dg.status, stream),
-          "cc_cost kernel");
-    if (until_stable && (e = launch_fill_i32(reinterpret_cast<int32_t *>(g->chg), ns + 1, 0, stream)))
+    TIMED(ECHO_K_INIT, launch_init(g->dg, d_scen, n_scen, ws.arrive, n_arrive, ws.count, n_count, ws.step,
+                                   d_digest, stream), "init kernel");
+    TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.classes, g->dg.cc_tables, d_scen, n_scen, ws.class_cost,
+                                         g->dg.status, stream), "cc_cost kernel");
+    if (until_stable && (e = launch_fill_i32(reinterpret_cast<int32_t *>(ws.chg), ns + 1, 0, stream)))
         return hip_fail(e, "fill kernel");
     if (d_refinements && (e = launch_fill_i32(d_refinements, ns, until_stable ? 0 : n_refine, stream)))
         return hip_fail(e, "fill kernel");
@@ -835,7 +881,8 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
     for (int32_t p = 0; p <= n_refine; ++p) {
         // tiles per walk launch: every rank block of a tile must be co-resident
         const int64_t cap = g->capacity[walk_variant(p > 0, p == n_refine, d_digest != nullptr, ext)];
-        const int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, cap / g->dg.n_blocks));
+        int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, cap / g->dg.n_blocks));
+        if (g->max_launch_tiles > 0) per_launch = std::min<int64_t>(per_launch, g->max_launch_tiles);
         if (p > 0) {
             OverlapArgs o{};
             o.cl_off = g->dg.cl_off;
@@ -844,13 +891,13 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
             o.cl_type = g->dg.cl_type;
             o.cp = g->dg.cp;
             o.scen = d_scen;
-            o.start = start;
-            o.finish = finish;
-            o.tmask = ext ? nullptr : g->tmask;
-            o.ext = ext ? g->ext : nullptr;
+            o.start = ws.start;
+            o.finish = ws.finish;
+            o.tmask = ext ? nullptr : ws.tmask;
+            o.ext = ext ? ws.ext : nullptr;
             o.cp_pos = g->dg.cp_pos;
-            o.mstride = mstride;
-            o.chg = until_stable ? g->chg : nullptr;
+            o.mstride = sh.mstride;
+            o.chg = until_stable ? ws.chg : nullptr;
             o.stable = stable;
             if (forest) {
                 o.cl_coll = g->dg.cl_coll;
@@ -870,9 +917,9 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
             o.max_comm_streams = g->dg.max_comm_streams;
             o.status = g->dg.status;
             TIMED(ECHO_K_OVERLAP, launch_overlap(o, g->n_ranks, stream), "overlap kernel");
-            if (until_stable && (e = launch_settle(g->chg, n_scen, d_refinements, stable, stream)))
+            if (until_stable && (e = launch_settle(ws.chg, n_scen, d_refinements, stable, stream)))
                 return hip_fail(e, "settle kernel");
-            TIMED(ECHO_K_CLEAR, launch_clear(g->arrive, n_arrive, g->count, n_count, stream), "clear kernel");
+            TIMED(ECHO_K_CLEAR, launch_clear(ws.arrive, n_arrive, ws.count, n_count, stream), "clear kernel");
         }
         for (int64_t t0 = 0; t0 < n_tiles; t0 += per_launch) {
             WalkArgs a;
@@ -882,16 +929,16 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
             a.c_N = g->dg.members;
             a.block_class = g->dg.block_class;
             a.scen = d_scen;
-            a.class_cost = g->class_cost;
-            a.tmask = p > 0 && !ext ? g->tmask : nullptr;
-            a.ext = p > 0 && ext ? g->ext : nullptr;
-            a.mstride = mstride;
+            a.class_cost = ws.class_cost;
+            a.tmask = p > 0 && !ext ? ws.tmask : nullptr;
+            a.ext = p > 0 && ext ? ws.ext : nullptr;
+            a.mstride = sh.mstride;
             a.stable = p < n_refine ? stable : nullptr;     // the final pass always runs
-            a.start = start;
-            a.finish = finish;
-            a.arrive = g->arrive;
-            a.count = g->count;
-            a.step = step;
+            a.start = ws.start;
+            a.finish = ws.finish;
+            a.arrive = ws.arrive;
+            a.count = ws.count;
+            a.step = ws.step;
             a.digest = d_digest;
             a.status = g->dg.status;
             a.spin_limit = g->spin_limit;
@@ -901,12 +948,93 @@ int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const ech
             a.tiles = (int32_t)std::min<int64_t>(per_launch, n_tiles - t0);
             a.n_walkers = g->n_walkers;
             a.final_pass = p == n_refine;
-            a.store_all = p == n_refine && (d_start || d_finish);
+            a.store_all = p == n_refine && store_all;
             if (g->n_ranks == 0 || g->n_ops == 0) continue;
             TIMED(ECHO_K_WALK, launch_walk(a, g->dg.n_blocks, stream), "walk kernel");
         }
     }
 #undef TIMED
+    return ECHO_OK;
+}
+
+int compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, const echo_validator &val, int64_t *d_start,
+            int64_t *d_finish, int64_t *d_step, uint64_t *d_digest, int32_t *d_refinements, hipStream_t stream) {
+    ComposeShape sh;
+    int rc = check_compose(g, d_scen, n_scen, val, &sh);
+    if (rc) return rc;
+    hipError_t e = hipSetDevice(g->device);
+    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+    Workspace ws;
+    if ((rc = ensure_workspace(g, sh, val.max_refine, d_start, d_finish, d_step, &ws))) return rc;
+    return enqueue_compose(g, d_scen, n_scen, val, sh, ws, d_start || d_finish, d_digest, d_refinements, stream,
+                           true);
+}
+
+// Longest chain of the walk (echo_walk_chain): every walker's items run in list
+// order; a resolve item also waits for the launch items of every member of its
+// collective.  The walk lists drain in this order by construction (the loader's
+// key order), so a walker only ever waits for launches that are still to come.
+int walk_chain(echo_graph g, const int64_t w[3], int64_t out[4]) {
+    struct Pt {
+        int64_t len = 0, items = 0, loc = 0, glob = 0;
+    };
+    auto later = [](const Pt &a, const Pt &b) { return a.len > b.len ? a : b; };
+    const int64_t W = g->n_walkers, nc = g->n_colls, n_items = g->n_items;
+    std::vector<WalkItem> items(n_items);
+    std::vector<int64_t> off(W + 1, 0);
+    std::vector<int32_t> members(nc);
+    hipError_t e = hipSetDevice(g->device);
+    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+    if (n_items > 0 && (e = hipMemcpy(items.data(), g->dg.items, n_items * sizeof(WalkItem), hipMemcpyDeviceToHost)))
+        return hip_fail(e, "walk list download");
+    if (W > 0 && (e = hipMemcpy(off.data(), g->dg.walk_off, (W + 1) * sizeof(int64_t), hipMemcpyDeviceToHost)))
+        return hip_fail(e, "walk offsets download");
+    if (nc > 0 && (e = hipMemcpy(members.data(), g->dg.members, nc * sizeof(int32_t), hipMemcpyDeviceToHost)))
+        return hip_fail(e, "member counts download");
+    std::vector<Pt> cur(W), cmax(nc);
+    std::vector<int32_t> arrived(nc, 0), wait_head(nc, -1), wait_next(W, -1);
+    std::vector<int64_t> pos(off.begin(), off.end() - (W > 0 ? 1 : 0));
+    std::vector<int32_t> runnable;
+    for (int64_t x = W - 1; x >= 0; --x) runnable.push_back((int32_t)x);
+    int64_t done = 0;
+    while (!runnable.empty()) {
+        const int32_t x = runnable.back();
+        runnable.pop_back();
+        for (; pos[x] < off[x + 1]; ++pos[x]) {
+            const WalkItem &it = items[pos[x]];
+            const int kind = item_kind(it.meta);
+            Pt p = cur[x];
+            if (kind == kResolve) {
+                if (arrived[it.coll] < members[it.coll]) {     // some member has not launched yet
+                    wait_next[x] = wait_head[it.coll];
+                    wait_head[it.coll] = x;
+                    break;
+                }
+                p = later(p, cmax[it.coll]);
+                const bool local = ((uint32_t)it.aux & kAuxLocal) != 0;
+                p.len += w[0] + (local ? w[1] : w[2]);
+                (local ? p.loc : p.glob) += 1;
+            } else {
+                p.len += w[0];
+            }
+            p.items += 1;
+            cur[x] = p;
+            ++done;
+            if (kind == ECHO_COMM) {
+                cmax[it.coll] = later(cmax[it.coll], p);
+                if (++arrived[it.coll] == members[it.coll])
+                    for (int32_t y = wait_head[it.coll]; y >= 0; y = wait_next[y]) runnable.push_back(y);
+            }
+        }
+    }
+    if (done != n_items) return fail(ECHO_ERR_ARG, "walk lists do not drain (%lld of %lld items)", (long long)done,
+                                     (long long)n_items);
+    Pt best;
+    for (const Pt &p : cur) best = later(best, p);
+    out[0] = best.len;
+    out[1] = best.items;
+    out[2] = best.loc;
+    out[3] = best.glob;
     return ECHO_OK;
 }
 
@@ -1147,6 +1275,36 @@ int echo_kernel_times(echo_graph g, int32_t max, int32_t *kinds, float *ms, int3
             return hip_fail(e, "hipEventElapsedTime");
     }
     return ECHO_OK;
+}
+
+int echo_set_spin_limit(echo_graph g, int64_t limit_ns) {
+    g_last_error.clear();
+    if (!g) return fail(ECHO_ERR_ARG, "null graph");
+    if (limit_ns < 10 || limit_ns > (int64_t(1) << 40))
+        return fail(ECHO_ERR_ARG, "spin limit %lld ns outside [10, 2^40]", (long long)limit_ns);
+    g->spin_limit = limit_ns / 10;
+    return ECHO_OK;
+}
+
+int echo_set_launch_tiles(echo_graph g, int32_t max_tiles) {
+    g_last_error.clear();
+    if (!g) return fail(ECHO_ERR_ARG, "null graph");
+    if (max_tiles < 0) return fail(ECHO_ERR_ARG, "max_tiles %d < 0", max_tiles);
+    g->max_launch_tiles = max_tiles;
+    return ECHO_OK;
+}
+
+int echo_walk_chain(echo_graph g, const int64_t weight_ps[3], int64_t out[4]) {
+    g_last_error.clear();
+    if (!g || !weight_ps || !out) return fail(ECHO_ERR_ARG, "null argument");
+    for (int i = 0; i < 3; ++i)
+        if (weight_ps[i] < 0 || weight_ps[i] >= (int64_t(1) << 40))
+            return fail(ECHO_ERR_ARG, "weight %d = %lld outside [0, 2^40)", i, (long long)weight_ps[i]);
+    try {
+        return walk_chain(g, weight_ps, out);
+    } catch (const std::bad_alloc &) {
+        return fail(ECHO_ERR_NOMEM, "host allocation failed while following the walk lists");
+    }
 }
 
 const char *echo_last_error(void) { return g_last_error.c_str(); }

@@ -8,8 +8,11 @@ There is no fallback: if libecho.so is missing, importing the library fails.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import sys
+import weakref
 
 import numpy as np
 
@@ -21,8 +24,9 @@ ECHO_ERR_CYCLE, ECHO_ERR_NOMEM, ECHO_ERR_HIP, ECHO_ERR_DEVICE = -4, -5, -6, -7
 ERROR_NAMES = {0: "OK", -1: "ARG", -2: "RANGE", -3: "MATCH", -4: "CYCLE", -5: "NOMEM", -6: "HIP",
                -7: "DEVICE"}
 EXPORTS = ("echo_load_graph", "echo_load_graph_ex", "echo_graph_info", "echo_free_graph", "echo_cc_cost",
-           "echo_compose_batch", "echo_compose_validated", "echo_set_cc_tables", "echo_set_forest", "echo_sync_status", "echo_set_timing", "echo_kernel_times",
-           "echo_last_error")
+           "echo_compose_batch", "echo_compose_validated", "echo_set_cc_tables", "echo_set_forest",
+           "echo_sync_status", "echo_set_timing", "echo_kernel_times", "echo_set_spin_limit",
+           "echo_set_launch_tiles", "echo_walk_chain", "echo_last_error")
 KERNEL_KINDS = {0: "init", 1: "cc_cost", 2: "walk", 3: "overlap", 4: "clear"}
 
 # echo_scenario (include/echo.h): 192 bytes.
@@ -100,6 +104,12 @@ def lib():
     L.echo_set_timing.restype = ctypes.c_int
     L.echo_kernel_times.argtypes = [P, i32, P, P, ctypes.POINTER(i32)]
     L.echo_kernel_times.restype = ctypes.c_int
+    L.echo_set_spin_limit.argtypes = [P, i64]
+    L.echo_set_spin_limit.restype = ctypes.c_int
+    L.echo_set_launch_tiles.argtypes = [P, i32]
+    L.echo_set_launch_tiles.restype = ctypes.c_int
+    L.echo_walk_chain.argtypes = [P, P, P]
+    L.echo_walk_chain.restype = ctypes.c_int
     L.echo_last_error.argtypes = []
     L.echo_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -156,6 +166,18 @@ def _stream_ptr(device):
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
+# Graphs still open are freed at interpreter exit, before modules are torn down and
+# while the HIP runtime (and any profiler attached to it) is still up; a graph
+# collected later than that is left to the process's exit.
+_open_graphs = weakref.WeakSet()
+
+
+@atexit.register
+def _close_open_graphs():
+    for g in list(_open_graphs):
+        g.close()
+
+
 class Graph:
     """A loaded graph: validated, matched, levelled and resident on one GPU."""
 
@@ -198,13 +220,19 @@ class Graph:
         a, b, c = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
         _check(L.echo_graph_info(h, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
         self.n_ops, self.n_colls, self.n_levels = a.value, b.value, c.value
+        _open_graphs.add(self)
 
     def close(self):
+        """Free the graph's host and device memory (waits for the device to be idle)."""
         if getattr(self, "handle", None):
             lib().echo_free_graph(self.handle)
             self.handle = None
+        _open_graphs.discard(self)
 
     def __del__(self):
+        # no HIP calls while the interpreter shuts down: the runtime may be gone
+        if sys.is_finalizing():
+            return
         try:
             self.close()
         except Exception:
@@ -311,6 +339,24 @@ class Graph:
         _check(lib().echo_kernel_times(self.handle, n.value, kinds.ctypes.data_as(ctypes.c_void_p),
                                        ms.ctypes.data_as(ctypes.c_void_p), ctypes.byref(n)))
         return [(KERNEL_KINDS[int(k)], float(t)) for k, t in zip(kinds[:n.value], ms[:n.value])]
+
+    def set_spin_limit(self, limit_ns):
+        """Give up a wait for a collective's members after limit_ns of wall clock."""
+        _check(lib().echo_set_spin_limit(self.handle, int(limit_ns)))
+
+    def set_launch_tiles(self, max_tiles):
+        """At most max_tiles scenario tiles per walk launch (0: as many as fit)."""
+        _check(lib().echo_set_launch_tiles(self.handle, int(max_tiles)))
+
+    def walk_chain(self, item_ps, lds_barrier_ps, global_barrier_ps):
+        """Longest chain of the walk with these per-item weights (picoseconds):
+        {'ps': length, 'items': n, 'lds_barriers': n, 'global_barriers': n}."""
+        w = np.array([item_ps, lds_barrier_ps, global_barrier_ps], np.int64)
+        out = np.zeros(4, np.int64)
+        _check(lib().echo_walk_chain(self.handle, w.ctypes.data_as(ctypes.c_void_p),
+                                     out.ctypes.data_as(ctypes.c_void_p)))
+        return {"ps": int(out[0]), "items": int(out[1]), "lds_barriers": int(out[2]),
+                "global_barriers": int(out[3])}
 
     def sync_status(self):
         import torch

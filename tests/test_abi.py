@@ -65,6 +65,9 @@ def test_scenario_record_layout_matches_header(E):
 
 
 def _valid_code(E):
+    # the sanitizer run links the loader against a host-memory stand-in of the HIP runtime
+    if os.environ.get("ECHO_HOST_STUB"):
+        return E.ECHO_OK
     return E.ECHO_OK if _gpu_present() else E.ECHO_ERR_HIP
 
 

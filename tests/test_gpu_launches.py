@@ -1,0 +1,159 @@
+"""GPU tests of the composer's launch layout and bounded waits, through the C ABI.
+
+- A pass whose scenario tiles do not all fit one cooperative launch runs as
+  several walk launches (each launch takes a range of tiles, every walker of
+  a tile resident): results stay bit-identical to the oracle, both when the
+  device's own capacity splits the pass and when the caller caps the tiles
+  per launch.
+- A tiny spin limit makes the bounded barrier waits give up: every kernel
+  still runs to its end, the call reports ECHO_ERR_DEVICE, and the same graph
+  composes bit-exactly again at the default limit.
+- The walk-chain analysis runs on a graph resident on the GPU.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+from tests.test_gpu_parity import THREADS, assert_same, gpu_run
+from workloads import configs, gpt1f1b, scenarios
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def E():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2412_12487_amd as E
+    E.lib()
+    return E
+
+
+def _gpt64():
+    """A small GPT graph of 64 ranks (TP2 x PP4 x DP8, 4 layers, 4 microbatches): eight
+    walk workgroups per scenario tile, P2P and data-parallel barriers across them."""
+    return gpt1f1b.gpt_graph(n_layers=4, hidden=1024, seq=512, tp=2, pp=4, dp=8, microbatches=4, seed=11)
+
+
+def _walk_launches_per_pass(G):
+    passes = [[]]
+    for kind, _ in G.kernel_times():
+        if kind == "overlap":
+            passes.append([])
+        elif kind == "walk":
+            passes[-1].append(kind)
+    return [len(p) for p in passes]
+
+
+def test_pass_split_by_device_capacity(E):
+    """65 scenario tiles x 8 workgroups = 520 workgroups, more than the 512 an MI355X
+    holds co-resident of the final (timeline-producing) walk variant, two
+    eight-wavefront workgroups per compute unit: that pass runs as two launches (the
+    lighter first pass may fit more workgroups per compute unit).  All step times
+    and digests, and six scenarios' timelines (both launches' tiles and the ragged
+    last one) against the oracle."""
+    import torch
+    g = _gpt64()
+    n = 65 * 64 - 7
+    sc = scenarios.draw(n, np.random.default_rng(21), bw_inter=(50_000, 400_000), alpha=(2_000, 20_000),
+                        slowdown=(65536, 91750), ar_algo_random=True)
+    G = E.Graph(g, 0)
+    try:
+        G.set_timing(True)
+        d, n = E.scenarios_to_device(sc)
+        out = G.compose(d, n, 1, timelines=True, digest=True)
+        torch.cuda.synchronize()
+        per_pass = _walk_launches_per_pass(G)
+        assert len(per_pass) == 2 and per_pass[-1] == 2, per_pass
+        cols = [0, 63, 64 * 64 - 1, 64 * 64, 64 * 64 + 5, n - 1]
+        idx = torch.tensor(cols, device=out["start"].device)
+        gpu = {"step": out["step"].cpu().numpy(), "digest": out["digest"].cpu().numpy().view(np.uint64),
+               "start": out["start"].index_select(1, idx).cpu().numpy(),
+               "finish": out["finish"].index_select(1, idx).cpu().numpy()}
+        del out
+    finally:
+        G.close()
+    ref = oracle.run(g, sc, 1, threads=THREADS, timelines=False)
+    np.testing.assert_array_equal(gpu["step"], ref["step"])
+    np.testing.assert_array_equal(gpu["digest"], ref["digest"])
+    full = oracle.run(g, scenarios.take(sc, cols), 1, threads=len(cols), jitter_stream=cols)
+    for j, c in enumerate(cols):
+        np.testing.assert_array_equal(gpu["start"][:, j], full["start"][j], err_msg=f"start, scenario {c}")
+        np.testing.assert_array_equal(gpu["finish"][:, j], full["finish"][j], err_msg=f"finish, scenario {c}")
+
+
+@pytest.mark.parametrize("max_tiles", [1, 2])
+@pytest.mark.parametrize("R", [0, 1, 2])
+def test_pass_split_by_tile_cap(E, max_tiles, R):
+    """Config 1 with 130 scenarios (three tiles, the last ragged) and at most one or
+    two tiles per walk launch: every start, finish, step and digest."""
+    import torch
+    g = configs.graph(1)
+    sc = scenarios.draw(130, np.random.default_rng(22), bw_inter=(50_000, 400_000), bw_intra=(50_000, 400_000),
+                        alpha=(2_000, 20_000), slowdown=(65536, 91750), jitter=(6554, 7), ar_algo_random=True)
+    G = E.Graph(g, 0)
+    try:
+        G.set_launch_tiles(max_tiles)
+        G.set_timing(True)
+        gpu = gpu_run(E, g, sc, R, graph=G)
+        torch.cuda.synchronize()
+        per_pass = _walk_launches_per_pass(G)
+        assert per_pass == [-(-3 // max_tiles)] * (R + 1), per_pass
+        assert_same(gpu, oracle.run(g, sc, R, threads=THREADS))
+        G.set_launch_tiles(0)
+        gpu_run(E, g, sc, R, graph=G)
+        assert _walk_launches_per_pass(G) == [1] * (R + 1)
+    finally:
+        G.close()
+
+
+def test_launch_tile_cap_rejects_negative(E):
+    G = E.Graph(configs.graph(1), 0)
+    try:
+        with pytest.raises(E.EchoError) as x:
+            G.set_launch_tiles(-1)
+        assert x.value.code == E.ECHO_ERR_ARG
+    finally:
+        G.close()
+
+
+def test_tiny_spin_limit_gives_up_every_wait_and_the_graph_recovers(E):
+    """A 10 ns limit: the waits for collective members give up at once, every kernel
+    runs to its end and the call reports ECHO_ERR_DEVICE; at the default limit the
+    same graph composes bit-exactly again."""
+    g = _gpt64()
+    sc = scenarios.draw(130, np.random.default_rng(23), bw_inter=(50_000, 400_000), alpha=(2_000, 20_000),
+                        slowdown=(65536, 91750), jitter=(6554, 9))
+    G = E.Graph(g, 0)
+    try:
+        d, n = E.scenarios_to_device(sc)
+        G.set_spin_limit(10)
+        G.compose(d, n, 1, timelines=True, digest=True, check=False)
+        with pytest.raises(E.EchoError) as x:
+            G.sync_status()
+        assert x.value.code == E.ECHO_ERR_DEVICE
+        G.set_spin_limit(20 * 10**9)
+        assert_same(gpu_run(E, g, sc, 1, graph=G), oracle.run(g, sc, 1, threads=THREADS))
+        for bad in (0, 9, (1 << 40) + 1):
+            with pytest.raises(E.EchoError) as y:
+                G.set_spin_limit(bad)
+            assert y.value.code == E.ECHO_ERR_ARG
+    finally:
+        G.close()
+
+
+def test_walk_chain_of_a_resident_graph(E):
+    g = configs.graph(1)
+    G = E.Graph(g, 0)
+    try:
+        ch = G.walk_chain(1, 0, 0)
+        per_rank = np.bincount(g["op_rank"], minlength=g["n_ranks"])
+        comm_per_rank = np.bincount(g["op_rank"][g["op_kind"] == 1], minlength=g["n_ranks"])
+        assert ch["items"] >= int((per_rank + comm_per_rank).max())
+        assert ch["ps"] == ch["items"]
+        ch2 = G.walk_chain(1000, 5000, 9000)
+        assert ch2["ps"] == 1000 * ch2["items"] + 5000 * ch2["lds_barriers"] + 9000 * ch2["global_barriers"]
+    finally:
+        G.close()
