@@ -375,6 +375,32 @@ int echo_set_launch_tiles(echo_graph g, int32_t max_tiles);
  */
 int echo_walk_chain(echo_graph g, const int64_t weight_ps[3], int64_t out[4]);
 
+/*
+ * echo_compose_batch for callers that cannot allocate device memory: code
+ * under HIP stream capture, serving loops or harnesses that forbid hipMalloc.
+ * It composes exactly as echo_compose_batch (the same kernels, bit-identical
+ * results) but takes its workspace -- the per-scenario cost-class table,
+ * barrier arrival maxima and counts, and the overlap masks of the refined
+ * passes -- from one fixed device array of ECHO_SCRATCH_BYTES per GPU, which
+ * the library holds from the first echo_load_graph on that GPU until the
+ * process ends, and it allocates nothing.  The caller passes every output:
+ * d_start and d_finish ([n_ops][n_scen] int64) and d_step are required (the
+ * walk keeps its working times there); d_digest may be NULL.  Kernel timing
+ * (echo_set_timing) is not recorded.  The workspace, each part rounded up to
+ * 256 bytes, is 8 * n_classes * n_scen (cost classes) + 8 * n_colls * n_scen
+ * (arrivals) + 4 * n_colls * ceil(n_scen / 64) (counts) + with n_refine > 0
+ * (n_items + 32) * 64 * ceil(n_scen / 64) bytes (masks; n_items = ops + comm
+ * ops); a call needing more returns ECHO_ERR_RANGE before enqueuing anything.
+ * Every call on one GPU shares that GPU's array: calls whose work overlaps on
+ * the device (two streams, two threads, two graphs) race and must be
+ * serialised by the caller.  Errors: as echo_compose_batch, plus ARG for a
+ * NULL d_start, d_finish or d_step and HIP if the array is unavailable.
+ */
+#define ECHO_SCRATCH_BYTES ((int64_t)64 << 20)
+int echo_compose_batch_static(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n_refine,
+                              int64_t *d_start, int64_t *d_finish, int64_t *d_step, uint64_t *d_digest,
+                              void *hip_stream);
+
 /* Message of the calling thread's last error ("" if none). */
 const char *echo_last_error(void);
 

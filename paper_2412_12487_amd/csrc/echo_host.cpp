@@ -104,6 +104,8 @@ struct echo_graph_s {
     int64_t capacity[kWalkVariants] = {};   // co-resident walk workgroups per kernel variant
     int64_t spin_limit = kDefaultSpinNs / 10;   // 100 MHz ticks
     int64_t max_launch_tiles = 0;      // > 0: at most this many scenario tiles per walk launch
+    void *scratch = nullptr;           // this GPU's fixed workspace array (echo_compose_batch_static)
+    hipError_t scratch_error = hipSuccess;
     DeviceGraph dg;
     std::vector<void *> owned;         // device allocations of the graph
     // workspace, grown on demand
@@ -732,6 +734,9 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     g->n_ranks = (int32_t)R;
     g->n_walkers = (int32_t)W;
     std::copy(capacity, capacity + kWalkVariants, g->capacity);
+    // set-up of the allocation-free compose: the device address of this GPU's workspace
+    // array, looked up once per device (the device is current)
+    g->scratch_error = scratch_buffer(device, &g->scratch);
     DeviceGraph &dg = g->dg;
     dg.n_ops = n;
     dg.n_colls = nc;
@@ -1105,6 +1110,65 @@ int echo_compose_validated(echo_graph g, const echo_scenario *d_scen, int32_t n_
             return fail(ECHO_ERR_ARG, "max_refine must be in 0..64 (got %d)", opts->max_refine);
         return compose(g, d_scen, n_scen, *opts, d_start, d_finish, d_step, d_digest, d_refinements,
                        static_cast<hipStream_t>(hip_stream));
+    } catch (...) {
+        return fail(ECHO_ERR_NOMEM, "unexpected exception in compose");
+    }
+}
+
+int echo_compose_batch_static(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n_refine,
+                              int64_t *d_start, int64_t *d_finish, int64_t *d_step, uint64_t *d_digest,
+                              void *hip_stream) {
+    g_last_error.clear();
+    try {
+        if (n_refine < 0 || n_refine > 64)
+            return fail(ECHO_ERR_ARG, "n_refine must be in 0..64 (got %d)", n_refine);
+        if (!d_start || !d_finish || !d_step)
+            return fail(ECHO_ERR_ARG, "the allocation-free compose needs d_start, d_finish and d_step");
+        const echo_validator val{n_refine, 0, 0, 0};
+        ComposeShape sh;
+        int rc = check_compose(g, d_scen, n_scen, val, &sh);
+        if (rc) return rc;
+        if (!g->scratch)
+            return hip_fail(g->scratch_error != hipSuccess ? g->scratch_error : hipErrorInvalidSymbol,
+                            "workspace array of this GPU");
+        // the workspace's parts, each rounded up to 256 bytes; sizes checked before any
+        // product could exceed 64 bits (every factor is below 2^32)
+        constexpr int64_t kCap = ECHO_SCRATCH_BYTES;
+        const int64_t parts[4] = {
+            g->dg.classes.n * sh.ns * (int64_t)sizeof(int64_t),              // class costs
+            g->n_colls * sh.ns * (int64_t)sizeof(unsigned long long),       // arrival maxima
+            g->n_colls * sh.n_tiles * (int64_t)sizeof(unsigned),             // arrival counts
+            n_refine > 0 ? sh.mrows * sh.mstride : 0,                         // overlap masks
+        };
+        int64_t offs[4], total = 0;
+        for (int i = 0; i < 4; ++i) {
+            offs[i] = total;
+            if (parts[i] > kCap) {
+                total = kCap + 1;
+                break;
+            }
+            total += (parts[i] + 255) / 256 * 256;
+        }
+        if (total > kCap)
+            return fail(ECHO_ERR_RANGE,
+                        "the allocation-free compose needs more workspace than its fixed %lld-byte array "
+                        "(%lld scenarios, %lld collectives, %lld walk items)",
+                        (long long)kCap, (long long)sh.ns, (long long)g->n_colls, (long long)g->n_items);
+        hipError_t e = hipSetDevice(g->device);
+        if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+        uint8_t *const base = static_cast<uint8_t *>(g->scratch);
+        Workspace ws;
+        ws.class_cost = reinterpret_cast<int64_t *>(base + offs[0]);
+        ws.arrive = reinterpret_cast<unsigned long long *>(base + offs[1]);
+        ws.count = reinterpret_cast<unsigned *>(base + offs[2]);
+        ws.tmask = n_refine > 0 ? base + offs[3] : nullptr;
+        ws.start = d_start;
+        ws.finish = d_finish;
+        ws.step = d_step;
+        // init clears the arrival maxima and counts; every mask a refined pass reads is
+        // written by the overlap detection before it, and class costs by the CC kernel
+        return enqueue_compose(g, d_scen, n_scen, val, sh, ws, true, d_digest, nullptr,
+                               static_cast<hipStream_t>(hip_stream), false);
     } catch (...) {
         return fail(ECHO_ERR_NOMEM, "unexpected exception in compose");
     }

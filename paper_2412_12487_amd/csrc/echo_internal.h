@@ -252,6 +252,9 @@ hipError_t walk_capacity(int device, int64_t workgroups[kWalkVariants]);
 inline int walk_variant(bool refined, bool final_pass, bool digest, bool prorate) {
     return (refined ? 1 : 0) | (final_pass ? 2 : 0) | (digest ? 4 : 0) | (refined && prorate ? 8 : 0);
 }
+// Device address of this GPU's fixed workspace array (ECHO_SCRATCH_BYTES) for
+// echo_compose_batch_static; `device` must be current.  Looked up once per device.
+hipError_t scratch_buffer(int device, void **ptr);
 // Largest prorated extra time an op may carry (its staging slot is 32 bits).
 constexpr uint32_t kExtLimit = 0xFFFFFFFFu;
 

@@ -12,6 +12,7 @@
 // Everything is int64 nanoseconds and Q16 factors, bit-exact by construction:
 // max, add, 64-bit multiply and shifts only (no floating point on the path).
 #include <algorithm>
+#include <mutex>
 
 #include "echo_internal.h"
 
@@ -1160,6 +1161,30 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream)
     if (n == 0) return hipSuccess;
     hipLaunchKernelGGL(k_fill_i32, dim3(grid_for(n, 256)), dim3(256), 0, stream, p, n, v);
     return hipGetLastError();
+}
+
+// Workspace of echo_compose_batch_static: one fixed array in every GPU's copy of the
+// code object, held from the code object's load until the process ends.  In host code
+// `scratch` names a host-side stand-in only; kernels get the device address that
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[ECHO_SCRATCH_BYTES];
+
+hipError_t scratch_buffer(int device, void **ptr) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void *addr[kMaxDevices] = {};
+    *ptr = nullptr;
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[device]) {
+        // the caller has made `device` current: its copy of the array
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[device] = p;
+    }
+    *ptr = addr[device];
+    return hipSuccess;
 }
 
 hipError_t walk_capacity(int device, int64_t workgroups[kWalkVariants]) {

@@ -26,7 +26,7 @@ ERROR_NAMES = {0: "OK", -1: "ARG", -2: "RANGE", -3: "MATCH", -4: "CYCLE", -5: "N
 EXPORTS = ("echo_load_graph", "echo_load_graph_ex", "echo_graph_info", "echo_free_graph", "echo_cc_cost",
            "echo_compose_batch", "echo_compose_validated", "echo_set_cc_tables", "echo_set_forest",
            "echo_sync_status", "echo_set_timing", "echo_kernel_times", "echo_set_spin_limit",
-           "echo_set_launch_tiles", "echo_walk_chain", "echo_last_error")
+           "echo_set_launch_tiles", "echo_walk_chain", "echo_compose_batch_static", "echo_last_error")
 KERNEL_KINDS = {0: "init", 1: "cc_cost", 2: "walk", 3: "overlap", 4: "clear"}
 
 # echo_scenario (include/echo.h): 192 bytes.
@@ -110,6 +110,8 @@ def lib():
     L.echo_set_launch_tiles.restype = ctypes.c_int
     L.echo_walk_chain.argtypes = [P, P, P]
     L.echo_walk_chain.restype = ctypes.c_int
+    L.echo_compose_batch_static.argtypes = [P, P, i32, i32, P, P, P, P, P]
+    L.echo_compose_batch_static.restype = ctypes.c_int
     L.echo_last_error.argtypes = []
     L.echo_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -304,6 +306,25 @@ class Graph:
         if check:
             self.sync_status()
         return res
+
+    def compose_static(self, d_scen, n_scen, n_refine, out, *, digest=False, check=True):
+        """echo_compose_batch_static: compose without any device allocation, the workspace
+        taken from the library's fixed per-GPU array.  `out` supplies 'start' and
+        'finish' [n_ops, n_scen] and 'step' [n_scen] int64 tensors (and 'digest' [n_scen]
+        when digest=True); returns `out`."""
+        import torch
+        dev = torch.device("cuda", self.device)
+        if int(n_scen) < 1:
+            raise EchoError(ECHO_ERR_ARG, "n_scen must be >= 1")
+        scen = _device_buffer(d_scen, "scenarios", dev, int(n_scen) * SCENARIO_DTYPE.itemsize)
+        ptr = {k: _device_buffer(out[k], k, dev, (self.n_ops if k in ("start", "finish") else 1) * int(n_scen) * 8,
+                                 torch.int64) for k in ("start", "finish", "step") + (("digest",) if digest else ())}
+        _check(lib().echo_compose_batch_static(self.handle, scen, int(n_scen), int(n_refine), ptr["start"],
+                                               ptr["finish"], ptr["step"], ptr.get("digest", ctypes.c_void_p(None)),
+                                               _stream_ptr(dev)))
+        if check:
+            self.sync_status()
+        return out
 
     def set_cc_tables(self, tables):
         """CC parameter tables: int64 array [n_tables, 6, 7] (max_bytes, chunk, alpha_ns,

@@ -96,5 +96,9 @@ hipError_t launch_walk(const WalkArgs &, int32_t, hipStream_t) { return hipError
 hipError_t launch_overlap(const OverlapArgs &, int32_t, hipStream_t) { return hipErrorNotSupported; }
 hipError_t launch_settle(unsigned *, int32_t, int32_t *, unsigned *, hipStream_t) { return hipErrorNotSupported; }
 hipError_t launch_fill_i32(int32_t *, int64_t, int32_t, hipStream_t) { return hipErrorNotSupported; }
+hipError_t scratch_buffer(int, void **ptr) {
+    *ptr = nullptr;
+    return hipErrorNotSupported;
+}
 
 }  // namespace echo
