@@ -131,6 +131,10 @@ def main():
                     help="validator variant: refine until no duration changes (at most --refine times)")
     ap.add_argument("--prorate", action="store_true",
                     help="validator variant: inflate only the overlapped part of a compute op")
+    ap.add_argument("--all", action="store_true",
+                    help="config 5 as one batch: its 16 graphs composed back to back in every step")
+    ap.add_argument("--no-floor", dest="floor", action="store_false",
+                    help="skip the walk latency microbenchmarks (no latency floor per pass)")
     ap.add_argument("--cpu-sample", type=int, default=48, help="scenarios the CPU oracle composes (0 = skip)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device once (calibrates HBM byte counters) and exit")
@@ -160,13 +164,19 @@ def main():
     E.lib()
     if args.replica:
         return replica_mode(args, E, configs, gpt1f1b)
+    if args.all:
+        return batch_mode(args, E, configs)
     t = time.perf_counter()
     g = configs.graph(args.config, args.index)
     sc = cc_variant(configs.scenario_batch(args.config, args.index, args.scenarios or None), args)
     log(f"graph: config {args.config} {configs.NAMES[args.config]}: {len(g['op_rank'])} ops, "
         f"{len(g['coll_type'])} collectives, {g['n_ranks']} ranks ({time.perf_counter() - t:.1f} s)")
     extras = extras_for(args)
-    r = time_compose(E, g, sc, args, extras)
+    latency = None
+    if args.floor:
+        latency = latency_model(E, int(np.max(sc["jitter_amp_q16"])))
+        log(f"walk latencies: {latency}")
+    r = time_compose(E, g, sc, args, extras, latency)
     line = {
         "metric": "op-evaluations/sec (ops x scenarios composed), 1 GPU",
         "value": round(r["value"], 1),
@@ -191,6 +201,8 @@ def main():
         "roofline": roofline(g, r, args, args.config if not (args.until_stable or args.prorate or args.forest
                                                              or args.cc != "echo") else None),
     }
+    if latency is not None:
+        line["latency_model"] = latency
     if "refinements" in r:
         line["config"]["refinements"] = r["refinements"]
     if args.cpu_sample > 0:
@@ -222,16 +234,29 @@ def cc_variant(sc, args):
     return sc
 
 
-def time_compose(E, g, sc, args, extras):
-    """Load g, compose the batch warmup + steps times; wall and per-kernel timings."""
-    import torch
+def walk_kernel_name(refined, final, digest, prorate):
+    b = lambda x: "true" if x else "false"
+    return f"k_walk<{b(refined)}, {b(final)}, {b(digest)}, {b(refined and prorate)}>"
+
+
+def time_compose(E, g, sc, args, extras, latency=None):
+    """Load g, compose the batch warmup + steps times; wall and per-kernel timings.
+    latency: the walk's measured per-item and per-barrier latencies (latency_model),
+    turned into a latency floor per pass with the graph's longest walk chain."""
     t = time.perf_counter()
     G = E.Graph(g, 0)
+    try:
+        return _time_compose(E, G, sc, args, extras, latency, time.perf_counter() - t)
+    finally:
+        G.close()
+
+
+def _time_compose(E, G, sc, args, extras, latency, load_s):
+    import torch
     if extras.get("cc_tables") is not None:
         G.set_cc_tables(extras["cc_tables"])
     if extras.get("forest") is not None:
         G.set_forest(extras["forest"])
-    load_s = time.perf_counter() - t
     log(f"loaded: {G.n_levels} levels in {load_s:.1f} s")
     d_scen, n_scen = E.scenarios_to_device(sc, "cuda:0")
     dev = torch.device("cuda:0")
@@ -246,7 +271,8 @@ def time_compose(E, g, sc, args, extras):
         log(f"warmup {i}: {G.kernel_times()}")
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream(dev)
-    step_ms, walk_ms, kernels = [], [], {}
+    step_ms, kernels, pass_runs = [], {}, []
+    last = {}
     t0 = time.perf_counter()
     for i in range(args.steps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -256,30 +282,24 @@ def time_compose(E, g, sc, args, extras):
         torch.cuda.synchronize()
         step_ms.append(e0.elapsed_time(e1))
         kt = G.kernel_times()
-        walk_ms.append(sum(ms for k, ms in kt if k == "walk"))
+        pass_runs.append(walk_passes(kt))
         for k, ms in kt:
             kernels.setdefault(k, []).append(ms)
-        log(f"step {i}: {step_ms[-1]:.3f} ms  walk {walk_ms[-1]:.3f} ms")
+        log(f"step {i}: {step_ms[-1]:.3f} ms  walk passes {[round(sum(p), 3) for p in pass_runs[-1]]} ms")
     wall = time.perf_counter() - t0
     G.sync_status()
-    ms_per_step = wall * 1000.0 / args.steps
-    # walk passes that ran (a pass past every scenario's fixed point returns at once);
-    # a pass whose tiles do not all fit one cooperative launch runs as several launches
-    passes = walk_passes(G.kernel_times())
-    top = max((ms for p in passes for ms in p), default=0.0)
-    ran = [p for p in passes if p and max(p) > 0.02 * top]
-    lw = [ms for p in passes for ms in p]
-    n_launch = sum(len(p) for p in ran)
-    ran_ms = sum(sum(p) for p in ran)
+    ms_per_step = wall * 1000.0 / max(args.steps, 1)
     res = {"n_ops": G.n_ops, "n_scen": n_scen, "levels": G.n_levels, "load_s": load_s,
-           "ms_per_step": ms_per_step, "gpu_ms": float(np.median(step_ms)),
+           "ms_per_step": ms_per_step, "gpu_ms": float(np.median(step_ms)) if step_ms else 0.0,
            "value": G.n_ops * n_scen / (ms_per_step / 1000.0),
-           "walk_avg_ms": float(np.mean(walk_ms)) * (ran_ms / max(sum(lw), 1e-9)) / max(n_launch, 1),
-           "n_pass": len(ran), "n_launch": n_launch,
            "kernels_ms": {k: round(float(np.mean(v)), 4) for k, v in kernels.items()},
            # the last step's walk launches, pass by pass (a split pass lists each launch)
-           "walk_pass_ms": [[round(ms, 4) for ms in p] for p in passes if p]}
-    if args.steps and "refinements" in last:
+           "walk_pass_ms": [[round(ms, 4) for ms in p] for p in pass_runs[-1] if p] if pass_runs else []}
+    res.update(pass_summary(pass_runs, args.prorate or args.forest))
+    if latency is not None:
+        n_pass = max(res["pass_index"]) + 1 if res["pass_index"] else 1
+        res["floors"] = [walk_floor(G, latency, k, n_pass) for k in res["pass_index"]]
+    if "refinements" in last:
         rf = last["refinements"].cpu().numpy()
         res["refinements"] = {"min": int(rf.min()), "mean": round(float(rf.mean()), 3), "max": int(rf.max())}
     # the CC estimator alone over every collective (echo_cc_cost), per call
@@ -293,8 +313,21 @@ def time_compose(E, g, sc, args, extras):
     res["cc_cost_all_ms"] = round(e0.elapsed_time(e1) / 3, 4)
     del costs
     del out
-    G.close()
     return res
+
+
+def pass_summary(pass_runs, ext):
+    """Walk passes of the timed steps: mean time per pass (a pass split over several
+    launches counts all of them), launches per pass and the kernel variant; passes that
+    returned at once (every scenario already at its fixed point) are left out."""
+    n_pass = max((len(p) for p in pass_runs), default=0)
+    pass_ms = [float(np.mean([sum(p[k]) for p in pass_runs if k < len(p)])) for k in range(n_pass)]
+    launches = [max(len(p[k]) for p in pass_runs if k < len(p)) for k in range(n_pass)]
+    top = max(pass_ms, default=0.0)
+    ran = [k for k in range(n_pass) if pass_ms[k] > 0.02 * top]
+    names = [walk_kernel_name(k > 0, k == n_pass - 1, False, ext) for k in range(n_pass)]
+    return {"pass_ms": [pass_ms[k] for k in ran], "pass_launches": [launches[k] for k in ran],
+            "pass_kernels": [names[k] for k in ran], "pass_index": ran}
 
 
 def walk_passes(kernel_times):
@@ -309,23 +342,214 @@ def walk_passes(kernel_times):
     return passes
 
 
+# ---------------------------------------------------------------- latency floor of the walk
+def latency_model(E, jitter_amp, n_scen=64):
+    """The walk's latencies measured on the device with small graphs whose longest
+    chain is known (workloads.microbench): ns per walk item (a chain of 40,000
+    compute ops on one rank), and per barrier met in LDS (eight ranks joining an
+    all-reduce after every eight ops) or in device memory (send/recv between ranks
+    of two workgroups), for the first pass (stores only what later kernels read)
+    and the final, refined pass (stores every start and finish).  Each graph
+    composes one 64-scenario tile with the workload's jitter amplitude and one
+    refinement; median of three calls after a warm-up.  A barrier's latency is
+    what its chain takes beyond its items."""
+    import torch
+    from workloads import microbench, scenarios
+    sc = scenarios.default_scenarios(n_scen)
+    if jitter_amp:
+        sc["jitter_amp_q16"][:] = jitter_amp
+        sc["jitter_seed"][:] = 1
+    d, n = E.scenarios_to_device(sc, "cuda:0")
+    graphs = {"chain": microbench.chain(40_000), "lds": microbench.allreduce_rounds(8, 2_000, 8),
+              "global": microbench.p2p_pingpong(1_000, 8)}
+    meas = {}
+    for name, g in graphs.items():
+        G = E.Graph(g, 0)
+        try:
+            G.set_timing(True)
+            chain = G.walk_chain(1, 0, 0)
+            runs = []
+            for _ in range(4):
+                G.compose(d, n, 1, timelines=True)
+                torch.cuda.synchronize()
+                runs.append([sum(p) for p in walk_passes(G.kernel_times())])
+        finally:
+            G.close()
+        meas[name] = ([float(np.median([r[k] for r in runs[1:]])) for k in (0, 1)], chain)
+    return latency_from(meas, jitter_amp)
+
+
+def latency_from(meas, jitter_amp):
+    """Per-item and per-barrier latencies (ns) from the microbenchmark walk times
+    {name: ([first-pass ms, final-pass ms], its walk chain with unit item weights)}."""
+    out = {}
+    (mc, cc), (ml, cl), (mg, cg) = meas["chain"], meas["lds"], meas["global"]
+    for k, key in ((0, "first"), (1, "final")):
+        item = mc[k] * 1e6 / cc["items"]
+        lds = max(0.0, (ml[k] * 1e6 - cl["items"] * item) / max(cl["lds_barriers"], 1))
+        glob = max(0.0, (mg[k] * 1e6 - cg["items"] * item - cg["lds_barriers"] * lds) /
+                   max(cg["global_barriers"], 1))
+        out[key] = {"item_ns": round(item, 2), "lds_barrier_ns": round(lds, 1), "global_barrier_ns": round(glob, 1)}
+    out["jitter_amp_q16"] = int(jitter_amp)
+    out["walk_ms"] = {name: [round(x, 4) for x in m[0]] for name, m in meas.items()}
+    return out
+
+
+def walk_floor(G, latency, k, n_pass):
+    """Latency floor of walk pass k: the graph's longest walk chain with the measured
+    per-item and per-barrier latencies of that kind of pass (a refined pass that is
+    not the last takes the smaller of the two kinds' latencies, so it stays a floor)."""
+    first, final = latency["first"], latency["final"]
+    if k == 0:
+        w = first
+    elif k == n_pass - 1:
+        w = final
+    else:
+        w = {key: min(first[key], final[key]) for key in first}
+    ps = [int(w["item_ns"] * 1000), int(w["lds_barrier_ns"] * 1000), int(w["global_barrier_ns"] * 1000)]
+    ch = G.walk_chain(*ps)
+    return {"floor_ms": round(ch["ps"] / 1e9, 4), "chain_items": ch["items"], "lds_barriers": ch["lds_barriers"],
+            "global_barriers": ch["global_barriers"]}
+
+
 def roofline(g, r, args, traffic_config):
-    passes = walk_bytes(g, r["n_scen"], max(r["n_pass"] - 1, 0))
-    bytes_per_launch = sum(passes) / max(r["n_launch"], 1)
-    achieved = bytes_per_launch / (r["walk_avg_ms"] / 1000.0) / 1e9
-    traffic = None
+    """Per walk pass: algorithmic bytes (edge-relaxation model) and their fraction of
+    the HBM peak at the pass's measured time, the byte counters' bytes when recorded
+    for these very kernels, and the latency floor; the headline is the final,
+    timeline-producing pass."""
+    n_pass = max(r["pass_index"]) + 1 if r["pass_index"] else 1
+    alg = walk_bytes(g, r["n_scen"], n_pass - 1)
+    traffic = {}
     if traffic_config is not None and os.path.exists(TRAFFIC_FILE):
         tr = json.load(open(TRAFFIC_FILE))
         if tr.get("kernel_source_sha") == source_hash() and tr.get("config") == traffic_config:
-            traffic = tr.get("bytes_per_launch")
+            traffic = tr.get("pass_bytes", {})
+    passes = []
+    for j, k in enumerate(r["pass_index"]):
+        ms = r["pass_ms"][j]
+        e = {"pass": k + 1, "kernel": r["pass_kernels"][j], "launches": r["pass_launches"][j], "ms": round(ms, 4),
+             "alg_bytes": int(alg[k]), "alg_frac": round(alg[k] / (ms / 1000.0) / 1e9 / HBM_PEAK_GBS, 4)}
+        cb = traffic.get(r["pass_kernels"][j])
+        e["counter_bytes"] = int(cb) if cb is not None else None
+        e["counter_frac"] = round(cb / (ms / 1000.0) / 1e9 / HBM_PEAK_GBS, 4) if cb is not None else None
+        if r.get("floors"):
+            f = r["floors"][j]
+            e.update(f)
+            e["over_floor"] = round(ms / f["floor_ms"], 3) if f["floor_ms"] > 0 else None
+        passes.append(e)
+    head = passes[-1] if passes else {"kernel": "k_walk", "launches": 1, "ms": 0.0, "alg_bytes": 0,
+                                      "counter_bytes": None, "counter_frac": None}
+    per_launch = head["alg_bytes"] / max(head["launches"], 1)
+    launch_ms = head["ms"] / max(head["launches"], 1)
+    achieved = per_launch / (launch_ms / 1000.0) / 1e9 if launch_ms > 0 else 0.0
     out = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-           "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-           "kernel": "k_walk", "avg_launch_ms": round(r["walk_avg_ms"], 4),
-           "algorithmic_bytes_per_launch": int(bytes_per_launch)}
-    if traffic is not None:
-        # the same launches by the bytes the counters saw (stream predecessors stay in registers)
-        out["traffic_frac"] = round(traffic / (r["walk_avg_ms"] / 1000.0) / 1e9 / HBM_PEAK_GBS, 4)
+           "frac": round(achieved / HBM_PEAK_GBS, 4),
+           "traffic": int(head["counter_bytes"] / max(head["launches"], 1))
+           if head["counter_bytes"] is not None else None,
+           "kernel": head["kernel"], "role": "final walk pass, the one that writes the caller's timelines",
+           "avg_launch_ms": round(launch_ms, 4), "algorithmic_bytes_per_launch": int(per_launch)}
+    if out["traffic"] is not None:
+        out["traffic_frac"] = head["counter_frac"]
+    out["passes"] = passes
     return out
+
+
+def batch_mode(args, E, configs):
+    """Config 5 as the batch it is: all 16 extrapolation graphs resident at once, every
+    step composing each of them (its own 32 scenarios, one refinement, timelines out)
+    back to back on one stream.  One pair of timeline buffers, sized for the largest
+    graph, serves every call (the calls run one after the other)."""
+    import torch
+    if args.config != 5:
+        raise SystemExit("--all is for config 5 (the 16-graph extrapolation batch)")
+    n_graphs = len(configs.EXTRAP_GRAPHS)
+    graphs, alg, pred_counts = [], [], []
+    t = time.perf_counter()
+    for i in range(n_graphs):
+        g = configs.graph(5, i)
+        sc = cc_variant(configs.scenario_batch(5, i, args.scenarios or None), args)
+        G = E.Graph(g, 0)
+        G.set_timing(True)
+        d, n = E.scenarios_to_device(sc, "cuda:0")
+        graphs.append({"G": G, "d": d, "n": n, "ops": G.n_ops, "ranks": int(g["n_ranks"]), "levels": G.n_levels})
+        alg.append(walk_bytes(g, n, args.refine))
+        log(f"graph {i + 1}/{n_graphs}: {G.n_ops} ops, {g['n_ranks']} ranks, loaded "
+            f"({time.perf_counter() - t:.1f} s so far)")
+        del g
+    try:
+        dev = torch.device("cuda:0")
+        rows = max(x["ops"] * x["n"] for x in graphs)
+        out = {"step": torch.empty(max(x["n"] for x in graphs), dtype=torch.int64, device=dev),
+               "start": torch.empty(rows, dtype=torch.int64, device=dev),
+               "finish": torch.empty(rows, dtype=torch.int64, device=dev)}
+
+        def one_step():
+            for x in graphs:
+                x["G"].compose(x["d"], x["n"], args.refine, out=out, check=False)
+
+        for i in range(args.warmup):
+            one_step()
+            torch.cuda.synchronize()
+            log(f"warmup {i} done")
+        stream = torch.cuda.current_stream(dev)
+        step_ms, per_graph = [], [[] for _ in graphs]
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for x in graphs:
+                x["G"].compose(x["d"], x["n"], args.refine, out=out, check=False)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            step_ms.append(e0.elapsed_time(e1))
+            for j, x in enumerate(graphs):       # each graph records its own kernels' events
+                per_graph[j].append(x["G"].kernel_times())
+            log(f"step {i}: {step_ms[-1]:.3f} ms")
+        wall = time.perf_counter() - t0
+        for x in graphs:
+            x["G"].sync_status()
+    finally:
+        for x in graphs:
+            x["G"].close()
+    ms_per_step = wall * 1000.0 / max(args.steps, 1)
+    total = sum(x["ops"] * x["n"] for x in graphs)
+    rows = []
+    for j, x in enumerate(graphs):
+        runs = [walk_passes(kt) for kt in per_graph[j]]
+        ps = pass_summary(runs, False)
+        compose_ms = float(np.mean([sum(ms for _, ms in kt) for kt in per_graph[j]]))
+        final = ps["pass_index"][-1] if ps["pass_index"] else 0
+        fms = ps["pass_ms"][-1] if ps["pass_ms"] else 0.0
+        model, tp, pp, dp, m, distopt = configs.EXTRAP_GRAPHS[j]
+        rows.append({"graph": j + 1, "model": model, "tp": tp, "pp": pp, "dp": dp, "microbatches": m,
+                     "distributed_optimizer": distopt, "ops": x["ops"], "ranks": x["ranks"], "levels": x["levels"],
+                     "kernels_ms": round(compose_ms, 4), "walk_pass_ms": [round(v, 4) for v in ps["pass_ms"]],
+                     "final_pass_alg_frac": round(alg[j][final] / (fms / 1000.0) / 1e9 / HBM_PEAK_GBS, 4)
+                     if fms > 0 else None})
+    line = {
+        "metric": "op-evaluations/sec (ops x scenarios composed), 1 GPU",
+        "value": round(total / (ms_per_step / 1000.0), 1),
+        "unit": "op-evals/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "gpu_ms_per_step": round(float(np.median(step_ms)), 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": f"config 5: {configs.NAMES[5]}, all {n_graphs} graphs composed back to back, "
+                               f"{sum(x['ops'] for x in graphs)} ops, {graphs[0]['n']} scenarios each, "
+                               f"{args.refine} refinement(s)",
+                   "n_ops": sum(x["ops"] for x in graphs), "n_scenarios_each": graphs[0]["n"],
+                   "n_refine": args.refine, "load_s": round(time.perf_counter() - t - wall, 1)},
+        "note": "32 scenarios fill half of each 64-lane wavefront: every walk item costs a whole "
+                "wavefront for half its lanes",
+        "graphs": rows,
+    }
+    print(json.dumps(line), flush=True)
 
 
 def replica_mode(args, E, configs, gpt1f1b):

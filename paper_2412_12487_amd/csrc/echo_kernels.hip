@@ -399,13 +399,21 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             if (active)                                                                          \
                 b_ = __hip_atomic_fetch_max(a.arrive + (int64_t)(c_) * ns + sigma, 0ull,         \
                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);         \
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);    /* settled on this path, not at the join */ \
             b_ = mirror ? (uint64_t)__shfl((long long)b_, col) : b_;                             \
         }                                                                                        \
         const int sl_ = aux_slot(x_);                                                            \
-        /* distinct load kinds keep the two reads from merging into one flat load */            \
-        const int64_t t_ = sl_ < kClassSlots ? ccost[sl_][lane]                                  \
-                                             : __hip_atomic_load(a.class_cost + (int64_t)(k_) * ns + sigma, \
-                                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); \
+        /* The cost: from the workgroup's LDS slot, read first on every path; a class without  \
+           a slot then reads device memory and waits for that load inside its own branch, so   \
+           the common path carries no wait on vector memory (which on this target would also  \
+           wait for every timeline store still in flight).  Distinct load kinds keep the two  \
+           reads from merging into one flat load. */                                            \
+        int64_t t_ = ccost[sl_ & (kClassSlots - 1)][lane];                                       \
+        if (sl_ >= kClassSlots) {                                                                \
+            t_ = __hip_atomic_load(a.class_cost + (int64_t)(k_) * ns + sigma, __ATOMIC_RELAXED,  \
+                                   __HIP_MEMORY_SCOPE_AGENT);                                    \
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);                                                \
+        }                                                                                        \
         f_ = (int64_t)b_ + t_;                                                                   \
         hi_or |= (uint32_t)((uint64_t)(f_) >> 32);                                               \
         put(fbase + (int64_t)(v_) * ns + col, f_);                                               \

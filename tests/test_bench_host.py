@@ -51,16 +51,44 @@ def test_walk_passes_split_launches():
     assert bench.walk_passes([("init", 0.1)]) == [[]]
 
 
-def test_roofline_counts_each_pass_once():
-    """Two passes of two launches each (half the tiles per launch): one
-    launch moves half a pass's bytes on average."""
+def _timed(pass_ms, launches):
+    return {"n_scen": 128, "pass_ms": pass_ms, "pass_launches": launches,
+            "pass_kernels": [bench.walk_kernel_name(k > 0, k == len(pass_ms) - 1, False, False)
+                             for k in range(len(pass_ms))],
+            "pass_index": list(range(len(pass_ms)))}
+
+
+def test_roofline_headline_is_the_final_pass():
+    """Two passes of two launches each: the headline is the final (timeline-writing)
+    pass, per launch; every pass is listed with its own algorithmic fraction."""
     g = _graph()
-    r = {"n_scen": 128, "n_pass": 2, "n_launch": 4, "walk_avg_ms": 2.0}
-    rf = bench.roofline(g, r, None, None)
-    total = sum(bench.walk_bytes(g, 128, 1))
-    assert rf["algorithmic_bytes_per_launch"] == int(total / 4)
-    assert np.isclose(rf["achieved"], round(total / 4 / 2e-3 / 1e9, 1))
-    assert rf["traffic"] is None
+    rf = bench.roofline(g, _timed([4.0, 6.0], [2, 2]), None, None)
+    alg = bench.walk_bytes(g, 128, 1)
+    assert rf["algorithmic_bytes_per_launch"] == int(alg[1] / 2)
+    assert np.isclose(rf["achieved"], round(alg[1] / 2 / 3e-3 / 1e9, 1))
+    assert rf["kernel"] == "k_walk<true, true, false, false>" and rf["traffic"] is None
+    assert [p["kernel"] for p in rf["passes"]] == ["k_walk<false, false, false, false>",
+                                                   "k_walk<true, true, false, false>"]
+    assert rf["passes"][0]["alg_frac"] == round(alg[0] / 4e-3 / 1e9 / bench.HBM_PEAK_GBS, 4)
+
+
+def test_pass_summary_groups_and_drops_skipped_passes():
+    runs = [[[5.0, 4.0], [6.0, 6.5], [0.01]], [[5.2, 4.0], [6.2, 6.5], [0.01]]]
+    ps = bench.pass_summary(runs, False)
+    assert ps["pass_index"] == [0, 1] and ps["pass_launches"] == [2, 2]
+    assert np.allclose(ps["pass_ms"], [9.1, 12.6])
+    assert ps["pass_kernels"] == ["k_walk<false, false, false, false>", "k_walk<true, false, false, false>"]
+
+
+def test_latency_model_arithmetic():
+    """Item latency from the chain; a barrier's latency is what its chain takes
+    beyond its items."""
+    meas = {"chain": ([4.0, 8.0], {"items": 40_000, "lds_barriers": 0, "global_barriers": 0}),
+            "lds": ([3.0, 5.0], {"items": 20_000, "lds_barriers": 2_000, "global_barriers": 0}),
+            "global": ([6.0, 9.0], {"items": 24_000, "lds_barriers": 0, "global_barriers": 2_000})}
+    lat = bench.latency_from(meas, 6554)
+    assert lat["first"] == {"item_ns": 100.0, "lds_barrier_ns": 500.0, "global_barrier_ns": 1800.0}
+    assert lat["final"] == {"item_ns": 200.0, "lds_barrier_ns": 500.0, "global_barrier_ns": 2100.0}
 
 
 def test_cpu_baseline_runs_the_gpu_run_options():
@@ -90,16 +118,20 @@ def test_cpu_baseline_runs_the_gpu_run_options():
 
 
 def test_roofline_reports_measured_traffic_fraction(tmp_path, monkeypatch):
-    """With a byte-counter record for the built kernels, the line carries the measured
-    bytes per launch and their fraction of the peak beside the algorithmic one."""
+    """With a byte-counter record for the built kernels, each pass carries its measured
+    bytes and their fraction of the peak beside the algorithmic ones."""
     import json
     g = _graph()
-    rec = {"config": 3, "kernel_source_sha": bench.source_hash(), "bytes_per_launch": 4_000_000_000}
+    rec = {"config": 3, "kernel_source_sha": bench.source_hash(),
+           "pass_bytes": {"k_walk<false, false, false, false>": 1_000_000_000,
+                          "k_walk<true, true, false, false>": 4_000_000_000}}
     f = tmp_path / "walk_traffic.json"
     f.write_text(json.dumps(rec))
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
-    rf = bench.roofline(g, {"n_scen": 64, "n_pass": 2, "n_launch": 2, "walk_avg_ms": 1.0}, None, 3)
+    rf = bench.roofline(g, _timed([0.5, 1.0], [1, 1]), None, 3)
     assert rf["traffic"] == 4_000_000_000
     assert rf["traffic_frac"] == round(4e9 / 1e-3 / 1e9 / bench.HBM_PEAK_GBS, 4)
-    rf = bench.roofline(g, {"n_scen": 64, "n_pass": 2, "n_launch": 2, "walk_avg_ms": 1.0}, None, 2)
+    assert rf["passes"][0]["counter_bytes"] == 1_000_000_000
+    assert rf["passes"][0]["counter_frac"] == round(1e9 / 0.5e-3 / 1e9 / bench.HBM_PEAK_GBS, 4)
+    rf = bench.roofline(g, _timed([0.5, 1.0], [1, 1]), None, 2)
     assert rf["traffic"] is None and "traffic_frac" not in rf
