@@ -380,7 +380,7 @@ int echo_walk_chain(echo_graph g, const int64_t weight_ps[3], int64_t out[4]);
  * under HIP stream capture, serving loops or harnesses that forbid hipMalloc.
  * It composes exactly as echo_compose_batch (the same kernels, bit-identical
  * results) but takes its workspace -- the per-scenario cost-class table,
- * barrier arrival maxima and counts, and the overlap masks of the refined
+ * barrier arrival maxima, counts and member slots, and the overlap masks of the refined
  * passes -- from one fixed device array of ECHO_SCRATCH_BYTES per GPU, which
  * the library holds from the first echo_load_graph on that GPU until the
  * process ends, and it allocates nothing.  The caller passes every output:
@@ -388,7 +388,9 @@ int echo_walk_chain(echo_graph g, const int64_t weight_ps[3], int64_t out[4]);
  * walk keeps its working times there); d_digest may be NULL.  Kernel timing
  * (echo_set_timing) is not recorded.  The workspace, each part rounded up to
  * 256 bytes, is 8 * n_classes * n_scen (cost classes) + 8 * n_colls * n_scen
- * (arrivals) + 4 * n_colls * ceil(n_scen / 64) (counts) + with n_refine > 0
+ * (arrivals) + 4 * n_colls * ceil(n_scen / 64) (counts) + 8 * n_slots * n_scen
+ * (n_slots: the member ops of collectives of at most eight members that are
+ * met in device memory, not in one workgroup) + with n_refine > 0
  * (n_items + 32) * 64 * ceil(n_scen / 64) bytes (masks; n_items = ops + comm
  * ops); a call needing more returns ECHO_ERR_RANGE before enqueuing anything.
  * Every call on one GPU shares that GPU's array: calls whose work overlaps on

@@ -115,6 +115,8 @@ struct echo_graph_s {
     size_t arrive_n = 0;
     unsigned *count = nullptr;
     size_t count_n = 0;
+    int64_t *slots = nullptr;
+    size_t slots_n = 0;
     uint8_t *tmask = nullptr;
     size_t tmask_n = 0;
     uint32_t *ext = nullptr;           // prorated extra times
@@ -141,6 +143,7 @@ void free_graph(echo_graph g) {
     (void)hipFree(g->class_cost);
     (void)hipFree(g->arrive);
     (void)hipFree(g->count);
+    (void)hipFree(g->slots);
     (void)hipFree(g->tmask);
     (void)hipFree(g->dg.cc_tables);
     (void)hipFree(g->dg.forest_nodes);
@@ -494,6 +497,17 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
             if (it != ok.end() && !it->second) coll_aux[c] = 0;
         }
     }
+    // collectives met in device memory with few members meet through per-member slots
+    std::vector<int64_t> slot_base(nc, -1);
+    std::vector<int32_t> op_member(n, -1);        // position of a comm op among its collective's members
+    int64_t n_slots = 0;
+    for (int64_t c = 0; c < nc; ++c) {
+        for (int64_t j = moff[c]; j < moff[c + 1]; ++j) op_member[mem[j]] = (int32_t)(j - moff[c]);
+        if ((coll_aux[c] & kAuxLocal) || cN[c] > kSlotMembers || n_slots + cN[c] > kI32Max) continue;
+        coll_aux[c] = kAuxSlots | ((uint32_t)cN[c] << 9);
+        slot_base[c] = n_slots;
+        n_slots += cN[c];
+    }
 
     // walk lists: each walker's ops by (key, rank, program order), key = level
     // for compute/memcpy, the launch level for a comm op
@@ -534,9 +548,11 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
             it.op = v;
             it.meta = (uint32_t)kResolve | ((uint32_t)(sv >= 0 ? sv : 0) << 2) | (sv < 0 ? kNoReg : 0u) |
                       (fold ? kFold : 0u);
-            it.far_off = (int32_t)far.size();
-            it.coll = (int32_t)d->op_coll[v];
-            it.dur = ccls[d->op_coll[v]];    // the cost class its finish reads
+            const int64_t c = d->op_coll[v];
+            // the collective's first member slot (slot mode), else unused
+            it.far_off = slot_base[c] >= 0 ? (int32_t)slot_base[c] : (int32_t)far.size();
+            it.coll = (int32_t)c;
+            it.dur = ccls[c];    // the cost class its finish reads
             it.nfar = 0;
             it.aux = coll_aux[d->op_coll[v]] | ((uint32_t)op_slot[v] << 5);
             items.push_back(it);
@@ -627,7 +643,12 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
                 it.aux = d->op_kind[v] == ECHO_COMM
                              ? coll_aux[d->op_coll[v]] | ((uint32_t)op_slot[v] << 5)
                              : 0u;
-                it.dur = d->op_kind[v] == ECHO_COMM ? 0 : d->op_dur_ns[v];
+                if (d->op_kind[v] == ECHO_COMM) {
+                    const int64_t c = d->op_coll[v];
+                    it.dur = slot_base[c] >= 0 ? slot_base[c] + op_member[v] : 0;   // this member's slot
+                } else {
+                    it.dur = d->op_dur_ns[v];
+                }
                 items.push_back(it);
             }
             while (next_due < sched.size()) {
@@ -639,6 +660,26 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     }
     if ((int64_t)far.size() > kI32Max || (int64_t)items.size() > kI32Max)
         return fail(ECHO_ERR_RANGE, "walk lists exceed 2^31 entries");
+    {
+        // member slots: every slot is written by exactly one launch item, and every
+        // resolve item reads its collective's slots only (the kernels index with them)
+        std::vector<uint8_t> written(n_slots, 0);
+        for (const WalkItem &it : items) {
+            const uint32_t x = (uint32_t)it.aux;
+            if ((x & kAuxLocal) || !(x & kAuxSlots)) continue;
+            const int64_t c = it.coll, base = slot_base[c], N = aux_expected(x);
+            if (base < 0 || N != cN[c])
+                return fail(ECHO_ERR_ARG, "internal: collective %lld has an inconsistent slot layout", (long long)c);
+            if (item_kind(it.meta) == kResolve) {
+                if (it.far_off != base || base + N > n_slots)
+                    return fail(ECHO_ERR_ARG, "internal: resolve item of op %d reads slots out of range", it.op);
+            } else if (it.dur < base || it.dur >= base + N || written[it.dur]++) {
+                return fail(ECHO_ERR_ARG, "internal: launch item of op %d writes a wrong slot", it.op);
+            }
+        }
+        for (int64_t k = 0; k < n_slots; ++k)
+            if (!written[k]) return fail(ECHO_ERR_ARG, "internal: member slot %lld is never written", (long long)k);
+    }
     {
         // what a pass without caller-visible timelines must still store
         std::vector<uint32_t> need(n, 0);
@@ -744,6 +785,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     dg.n_walkers = (int32_t)W;
     dg.n_blocks = (int32_t)nblk;
     dg.max_comm_streams = max_comm_streams;
+    dg.n_slots = n_slots;
 #define UP(dst, src)                                                        \
     do {                                                                    \
         e = upload(&dst, src);                                              \
@@ -790,6 +832,7 @@ struct Workspace {
     int64_t *class_cost = nullptr;         // [class][scen] collective cost of each cost class
     unsigned long long *arrive = nullptr;  // [coll][scen] latest member launch
     unsigned *count = nullptr;             // [coll][tile] members arrived
+    int64_t *slots = nullptr;              // [slot][scen] member launch times (slot collectives)
     uint8_t *tmask = nullptr;              // [item + kBlock][mstride] overlap masks (refined passes)
     uint32_t *ext = nullptr;               // same rows: prorated / ensemble extra times
     unsigned *chg = nullptr;               // [scen] change flags + 1 stability word (until_stable)
@@ -832,6 +875,7 @@ int ensure_workspace(echo_graph g, const ComposeShape &sh, int32_t n_refine, int
     if ((rc = ensure(&g->class_cost, &g->class_cost_n, (size_t)(g->dg.classes.n * ns), "class cost"))) return rc;
     if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->n_colls * ns), "arrivals"))) return rc;
     if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * sh.n_tiles), "arrival counts"))) return rc;
+    if ((rc = ensure(&g->slots, &g->slots_n, (size_t)(g->dg.n_slots * ns), "member slots"))) return rc;
     if (n_refine > 0 && !sh.ext &&
         (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(sh.mrows * sh.mstride), "overlap masks")))
         return rc;
@@ -844,6 +888,7 @@ int ensure_workspace(echo_graph g, const ComposeShape &sh, int32_t n_refine, int
     ws->class_cost = g->class_cost;
     ws->arrive = g->arrive;
     ws->count = g->count;
+    ws->slots = g->slots;
     ws->tmask = n_refine > 0 && !sh.ext ? g->tmask : nullptr;
     ws->ext = sh.ext ? g->ext : nullptr;
     ws->chg = sh.until_stable ? g->chg : nullptr;
@@ -864,7 +909,7 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
     const bool until_stable = sh.until_stable, prorate = sh.prorate, forest = sh.forest, ext = sh.ext;
     unsigned *stable = until_stable ? ws.chg + ns : nullptr;
     hipError_t e;
-    const int64_t n_arrive = g->n_colls * ns, n_count = g->n_colls * n_tiles;
+    const int64_t n_arrive = g->n_colls * ns, n_count = g->n_colls * n_tiles, n_slot_values = g->dg.n_slots * ns;
     g->timed_kinds.clear();
     const bool timing = timed && g->timing;
     Timed tm{g, stream};
@@ -874,8 +919,8 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
         if ((e = (call))) return hip_fail(e, what);                            \
         if (timing && (e = tm.end())) return hip_fail(e, "event");             \
     } while (0)
-    TIMED(ECHO_K_INIT, launch_init(g->dg, d_scen, n_scen, ws.arrive, n_arrive, ws.count, n_count, ws.step,
-                                   d_digest, stream), "init kernel");
+    TIMED(ECHO_K_INIT, launch_init(g->dg, d_scen, n_scen, ws.arrive, n_arrive, ws.count, n_count, ws.slots,
+                                   n_slot_values, ws.step, d_digest, stream), "init kernel");
     TIMED(ECHO_K_CC_COST, launch_cc_cost(g->dg.classes, g->dg.cc_tables, d_scen, n_scen, ws.class_cost,
                                          g->dg.status, stream), "cc_cost kernel");
     if (until_stable && (e = launch_fill_i32(reinterpret_cast<int32_t *>(ws.chg), ns + 1, 0, stream)))
@@ -924,7 +969,8 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
             TIMED(ECHO_K_OVERLAP, launch_overlap(o, g->n_ranks, stream), "overlap kernel");
             if (until_stable && (e = launch_settle(ws.chg, n_scen, d_refinements, stable, stream)))
                 return hip_fail(e, "settle kernel");
-            TIMED(ECHO_K_CLEAR, launch_clear(ws.arrive, n_arrive, ws.count, n_count, stream), "clear kernel");
+            TIMED(ECHO_K_CLEAR, launch_clear(ws.arrive, n_arrive, ws.count, n_count, ws.slots, n_slot_values, stream),
+                  "clear kernel");
         }
         for (int64_t t0 = 0; t0 < n_tiles; t0 += per_launch) {
             WalkArgs a;
@@ -943,6 +989,7 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
             a.finish = ws.finish;
             a.arrive = ws.arrive;
             a.count = ws.count;
+            a.slots = ws.slots;
             a.step = ws.step;
             a.digest = d_digest;
             a.status = g->dg.status;
@@ -1078,7 +1125,7 @@ int echo_cc_cost(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int6
     hipError_t e = hipSetDevice(g->device);
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
-    if ((e = launch_init(g->dg, d_scen, n_scen, nullptr, 0, nullptr, 0, nullptr, nullptr, s)))
+    if ((e = launch_init(g->dg, d_scen, n_scen, nullptr, 0, nullptr, 0, nullptr, 0, nullptr, nullptr, s)))
         return hip_fail(e, "init kernel");
     if ((e = launch_cc_cost(g->dg.colls, g->dg.cc_tables, d_scen, n_scen, d_cost, g->dg.status, s)))
         return hip_fail(e, "cc_cost kernel");
@@ -1134,14 +1181,15 @@ int echo_compose_batch_static(echo_graph g, const echo_scenario *d_scen, int32_t
         // the workspace's parts, each rounded up to 256 bytes; sizes checked before any
         // product could exceed 64 bits (every factor is below 2^32)
         constexpr int64_t kCap = ECHO_SCRATCH_BYTES;
-        const int64_t parts[4] = {
+        const int64_t parts[5] = {
             g->dg.classes.n * sh.ns * (int64_t)sizeof(int64_t),              // class costs
             g->n_colls * sh.ns * (int64_t)sizeof(unsigned long long),       // arrival maxima
             g->n_colls * sh.n_tiles * (int64_t)sizeof(unsigned),             // arrival counts
             n_refine > 0 ? sh.mrows * sh.mstride : 0,                         // overlap masks
+            g->dg.n_slots * sh.ns * (int64_t)sizeof(int64_t),               // member slots
         };
-        int64_t offs[4], total = 0;
-        for (int i = 0; i < 4; ++i) {
+        int64_t offs[5], total = 0;
+        for (int i = 0; i < 5; ++i) {
             offs[i] = total;
             if (parts[i] > kCap) {
                 total = kCap + 1;
@@ -1162,10 +1210,11 @@ int echo_compose_batch_static(echo_graph g, const echo_scenario *d_scen, int32_t
         ws.arrive = reinterpret_cast<unsigned long long *>(base + offs[1]);
         ws.count = reinterpret_cast<unsigned *>(base + offs[2]);
         ws.tmask = n_refine > 0 ? base + offs[3] : nullptr;
+        ws.slots = reinterpret_cast<int64_t *>(base + offs[4]);
         ws.start = d_start;
         ws.finish = d_finish;
         ws.step = d_step;
-        // init clears the arrival maxima and counts; every mask a refined pass reads is
+        // init clears the arrival maxima, counts and member slots; every mask a refined pass reads is
         // written by the overlap detection before it, and class costs by the CC kernel
         return enqueue_compose(g, d_scen, n_scen, val, sh, ws, true, d_digest, nullptr,
                                static_cast<hipStream_t>(hip_stream), false);

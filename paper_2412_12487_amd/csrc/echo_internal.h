@@ -86,6 +86,15 @@ constexpr uint32_t kNoSlot = 15;
 // class slot << 5 (kNoSlot: read the class's cost from global memory) | expected count << 9.
 constexpr uint32_t kAuxLocal = 1u;
 constexpr int kExpectedBits = 23;
+// A collective met in device memory whose members are few (at most kSlotMembers)
+// meets through per-member slots: each member's launch item stores its launch time
+// into its own slot (cleared to -1 before every pass), and a resolve item reads all
+// its collective's slots -- a value of -1 means "not yet launched".  The launch item
+// carries its slot in `dur`, the resolve item the collective's first slot in
+// `far_off`; aux bit 1 marks the mode and the expected-count field holds the member
+// count.  Larger collectives count their arrivals and keep a per-scenario maximum.
+constexpr uint32_t kAuxSlots = 2u;
+constexpr int kSlotMembers = 8;
 __host__ __device__ inline int aux_channel(uint32_t x) { return int((x >> 1) & 7u); }
 __host__ __device__ inline int aux_parity(uint32_t x) { return int((x >> 4) & 1u); }
 __host__ __device__ inline int aux_slot(uint32_t x) { return int((x >> 5) & 15u); }
@@ -166,6 +175,7 @@ struct DeviceGraph {
     int64_t *class_metrics = nullptr;  // [8][4]
     int32_t n_trees = 0, forest_base = 65536;
     int32_t max_comm_streams = 0;    // the most streams with comm ops on one rank
+    int64_t n_slots = 0;             // member slots of the collectives met through slots
 };
 
 constexpr int kClassMetrics = 4;
@@ -187,6 +197,7 @@ struct WalkArgs {
     int64_t *start, *finish;         // [op][scen]
     unsigned long long *arrive;      // [coll][scen] latest member launch
     unsigned *count;                 // [coll][tile] members arrived
+    int64_t *slots;                  // [slot][scen] launch time of a slot collective's member, -1 before it
     int64_t *step;                   // [scen]
     uint64_t *digest;                // [scen] or null
     unsigned *status;
@@ -232,9 +243,10 @@ struct OverlapArgs {
 // Kernel launchers (echo_kernels.hip).  All enqueue on `stream`.
 hipError_t launch_init(const DeviceGraph &g, const echo_scenario *scen, int32_t n_scen,
                        unsigned long long *arrive, int64_t n_arrive, unsigned *count,
-                       int64_t n_count, int64_t *step, uint64_t *digest, hipStream_t stream);
+                       int64_t n_count, int64_t *slots, int64_t n_slot_values, int64_t *step,
+                       uint64_t *digest, hipStream_t stream);
 hipError_t launch_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *count,
-                        int64_t n_count, hipStream_t stream);
+                        int64_t n_count, int64_t *slots, int64_t n_slot_values, hipStream_t stream);
 hipError_t launch_cc_cost(const CollTable &t, const echo_cc_table *tables, const echo_scenario *scen,
                           int32_t n_scen, int64_t *cost, unsigned *status, hipStream_t stream);
 hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream);

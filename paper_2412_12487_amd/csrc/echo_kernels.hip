@@ -73,12 +73,13 @@ __device__ __forceinline__ unsigned ld_relaxed(const unsigned *p) {
 
 // ------------------------------------------------------------------ set-up
 __global__ void k_init(const echo_scenario *scen, int32_t n_scen, unsigned long long *arrive,
-                       int64_t n_arrive, unsigned *count, int64_t n_count, int64_t *step,
-                       uint64_t *digest, int32_t n_tables, unsigned *status) {
+                       int64_t n_arrive, unsigned *count, int64_t n_count, int64_t *slots, int64_t n_slots,
+                       int64_t *step, uint64_t *digest, int32_t n_tables, unsigned *status) {
     const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t nth = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = tid; i < n_arrive; i += nth) arrive[i] = 0;
     for (int64_t i = tid; i < n_count; i += nth) count[i] = 0;
+    for (int64_t i = tid; i < n_slots; i += nth) slots[i] = -1;
     for (int64_t i = tid; i < n_scen; i += nth) {
         if (step) step[i] = 0;
         if (digest) digest[i] = 0;
@@ -98,11 +99,13 @@ __global__ void k_init(const echo_scenario *scen, int32_t n_scen, unsigned long 
     }
 }
 
-__global__ void k_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *count, int64_t n_count) {
+__global__ void k_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *count, int64_t n_count,
+                        int64_t *slots, int64_t n_slots) {
     const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t nth = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = tid; i < n_arrive; i += nth) arrive[i] = 0;
     for (int64_t i = tid; i < n_count; i += nth) count[i] = 0;
+    for (int64_t i = tid; i < n_slots; i += nth) slots[i] = -1;
 }
 
 // ------------------------------------------------------------------ CC estimator
@@ -213,6 +216,46 @@ __device__ bool wait_arrivals(const unsigned *cnt, unsigned need, unsigned *stat
             return false;
         }
     }
+}
+
+// Barrier of a collective met through member slots: the latest launch time over
+// its n members' slots p[m * ns] (m < n <= kSlotMembers), once every member of every
+// lane's scenario has stored its launch (a slot reads -1 until then).  All slots are
+// read in one memory round trip per poll.  Bounded like wait_arrivals; on giving up
+// it returns 0 and clears *ok.
+__device__ int64_t wait_slots(const int64_t *p, unsigned n, int64_t ns, unsigned *status, int64_t limit, bool *ok) {
+    uint64_t t0 = 0;
+    for (int poll = 0;; ++poll) {
+        int64_t v[kSlotMembers];
+#pragma unroll
+        for (int m = 0; m < kSlotMembers; ++m)
+            v[m] = m < (int)n ? __hip_atomic_load(p + m * ns, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+        int64_t mx = 0;
+        bool all = true;
+#pragma unroll
+        for (int m = 0; m < kSlotMembers; ++m) {
+            all = all && v[m] >= 0;
+            mx = v[m] > mx ? v[m] : mx;
+        }
+        if (!__builtin_amdgcn_readfirstlane(__ballot(!all) != 0)) {
+            // every member had launched at the first look: this wave was the last to arrive
+            // and the others wait for it (issue priority as in wait_arrivals)
+            if (poll == 0) __builtin_amdgcn_s_setprio(3);
+            return mx;
+        }
+        if (poll == 0) {
+            __builtin_amdgcn_s_setprio(0);
+            t0 = wall_clock64();
+        }
+        __builtin_amdgcn_s_sleep(2);
+        if (__builtin_amdgcn_readfirstlane(ld_relaxed(status)) & kStatusAbort) break;
+        if ((int64_t)(wall_clock64() - t0) > limit) {
+            __hip_atomic_fetch_or(status, kStatusTimeout | kStatusAbort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+        }
+    }
+    *ok = false;
+    return 0;
 }
 
 // Timeline stores stream through the caches (non-temporal): each (op, tile) row
@@ -382,7 +425,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
 
 // Finish f_ of comm op v_ (collective c_, aux word x_): its barrier -- the
 // latest member launch -- plus the collective's cost; written to the finish array.
-#define MEET(c_, v_, x_, k_, f_)                                                                 \
+#define MEET(c_, v_, x_, k_, f_, s_base_)                                                        \
     {                                                                                            \
         uint64_t b_ = 0;                                                                         \
         if ((x_) & kAuxLocal) {                                                                  \
@@ -391,6 +434,13 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                              wait_local(&lcnt[ch_][par_], aux_expected(x_), a.status, a.spin_limit))) \
                 dead = true;                                                                     \
             b_ = lbar[ch_][par_][lane];                                                          \
+        } else if ((x_) & kAuxSlots) {                                                           \
+            bool ok_ = true;                                                                     \
+            if (!dead)                                                                           \
+                b_ = (uint64_t)wait_slots(a.slots + (int64_t)(s_base_) * ns + sigma, aux_expected(x_), ns, \
+                                          a.status, a.spin_limit, &ok_);                         \
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);    /* settled on this path, not at the join */ \
+            if (!__builtin_amdgcn_readfirstlane(ok_)) dead = true;                               \
         } else {                                                                                 \
             if (!dead && !__builtin_amdgcn_readfirstlane(wait_arrivals(tile_count + (int64_t)(c_) * a.n_tiles, \
                                                                        (unsigned)a.c_N[c_], a.status, \
@@ -501,7 +551,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             if (kind == kResolve) {
                 // a comm op's barrier, due right before its first successor
                 int64_t f;
-                MEET(coll, op, aux, (int32_t)dur, f)
+                MEET(coll, op, aux, (int32_t)dur, f, far_off)
                 xmax = f > xmax ? f : xmax;
                 const int sq = __builtin_amdgcn_readfirstlane((meta & kNoReg) ? kStreams : st);
                 if (sq == 0) lf0 = f;
@@ -532,6 +582,12 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
                     if (lane == 0)
                         __hip_atomic_fetch_add(&lcnt[ch][par], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                } else if (aux & kAuxSlots) {
+                    // this member's slot (its index is in the item's duration field): one store,
+                    // no wait -- the value is its own arrival flag
+                    if (active)
+                        __hip_atomic_store(a.slots + dur * ns + sigma, ready, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
                 } else {
                     if (active)
                         __hip_atomic_fetch_max(a.arrive + (int64_t)coll * ns + sigma, (unsigned long long)ready,
@@ -1101,20 +1157,20 @@ int grid_for(int64_t n, int block) {
 
 hipError_t launch_init(const DeviceGraph &g, const echo_scenario *scen, int32_t n_scen,
                        unsigned long long *arrive, int64_t n_arrive, unsigned *count, int64_t n_count,
-                       int64_t *step, uint64_t *digest, hipStream_t stream) {
-    int64_t n = n_arrive > n_count ? n_arrive : n_count;
+                       int64_t *slots, int64_t n_slot_values, int64_t *step, uint64_t *digest, hipStream_t stream) {
+    int64_t n = std::max<int64_t>(std::max(n_arrive, n_count), n_slot_values);
     if (n_scen > n) n = n_scen;
     hipLaunchKernelGGL(k_init, dim3(grid_for(n, 256)), dim3(256), 0, stream, scen, n_scen, arrive,
-                       n_arrive, count, n_count, step, digest, g.n_cc_tables, g.status);
+                       n_arrive, count, n_count, slots, n_slot_values, step, digest, g.n_cc_tables, g.status);
     return hipGetLastError();
 }
 
 hipError_t launch_clear(unsigned long long *arrive, int64_t n_arrive, unsigned *count, int64_t n_count,
-                        hipStream_t stream) {
-    const int64_t n = n_arrive > n_count ? n_arrive : n_count;
+                        int64_t *slots, int64_t n_slot_values, hipStream_t stream) {
+    const int64_t n = std::max<int64_t>(std::max(n_arrive, n_count), n_slot_values);
     if (n == 0) return hipSuccess;
     hipLaunchKernelGGL(k_clear, dim3(grid_for(n, 256)), dim3(256), 0, stream, arrive, n_arrive, count,
-                       n_count);
+                       n_count, slots, n_slot_values);
     return hipGetLastError();
 }
 

@@ -84,10 +84,12 @@ hipError_t walk_capacity(int, int64_t workgroups[kWalkVariants]) {
 }
 
 hipError_t launch_init(const DeviceGraph &, const echo_scenario *, int32_t, unsigned long long *, int64_t, unsigned *,
-                       int64_t, int64_t *, uint64_t *, hipStream_t) {
+                       int64_t, int64_t *, int64_t, int64_t *, uint64_t *, hipStream_t) {
     return hipErrorNotSupported;
 }
-hipError_t launch_clear(unsigned long long *, int64_t, unsigned *, int64_t, hipStream_t) { return hipErrorNotSupported; }
+hipError_t launch_clear(unsigned long long *, int64_t, unsigned *, int64_t, int64_t *, int64_t, hipStream_t) {
+    return hipErrorNotSupported;
+}
 hipError_t launch_cc_cost(const CollTable &, const echo_cc_table *, const echo_scenario *, int32_t, int64_t *,
                           unsigned *, hipStream_t) {
     return hipErrorNotSupported;
