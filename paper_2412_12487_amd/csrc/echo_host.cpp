@@ -100,6 +100,7 @@ struct echo_graph_s {
     int device = 0;
     int64_t n_ops = 0, n_colls = 0, n_levels = 0;
     int64_t n_items = 0;               // entries of the walk lists
+    int64_t n_compute = 0;             // compute ops (overlap detection's compute records)
     int32_t n_ranks = 0, n_walkers = 0;
     int64_t capacity[kWalkVariants] = {};   // co-resident walk workgroups per kernel variant
     int64_t spin_limit = kDefaultSpinNs / 10;   // 100 MHz ticks
@@ -135,6 +136,15 @@ struct echo_graph_s {
 
 namespace {
 
+void free_compact(CompactForest &fx) {
+    (void)hipFree(fx.words);
+    (void)hipFree(fx.thr);
+    (void)hipFree(fx.cbin);
+    (void)hipFree(fx.coll_bin);
+    (void)hipFree(fx.cp_bin);
+    fx = CompactForest{};
+}
+
 void free_graph(echo_graph g) {
     if (!g) return;
     (void)hipSetDevice(g->device);
@@ -150,6 +160,7 @@ void free_graph(echo_graph g) {
     (void)hipFree(g->dg.forest_leaf);
     (void)hipFree(g->dg.forest_roots);
     (void)hipFree(g->dg.class_metrics);
+    free_compact(g->dg.fx);
     (void)hipFree(g->ext);
     (void)hipFree(g->chg);
     (void)hipFree(g->tmp_start);
@@ -770,6 +781,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     g->device = device;
     g->n_ops = n;
     g->n_items = (int64_t)items.size();
+    g->n_compute = (int64_t)cp.size();
     g->n_colls = nc;
     g->n_levels = n_levels;
     g->n_ranks = (int32_t)R;
@@ -959,10 +971,12 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
                 o.class_metrics = g->dg.class_metrics;
                 o.n_trees = g->dg.n_trees;
                 o.forest_base = g->dg.forest_base;
+                o.fx = g->dg.fx;
             }
             o.prorate = prorate;
             o.n_scen = n_scen;
             o.n_tiles = n_tiles;
+            o.n_ranks = g->n_ranks;
             o.prev_refined = p > 1;
             o.max_comm_streams = g->dg.max_comm_streams;
             o.status = g->dg.status;
@@ -1289,6 +1303,7 @@ static int set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes
     // children side by side (a node reached along two paths is copied)
     std::vector<DevTreeNode> hn;
     std::vector<int32_t> hleaf;
+    std::vector<uint8_t> is_leaf;
     std::vector<int32_t> hr(n_trees);
     std::vector<std::pair<int32_t, int64_t>> todo;    // (source node, device slot)
     for (int32_t t = 0; t < n_trees; ++t) {
@@ -1302,6 +1317,8 @@ static int set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes
                 hn[slot] = DevTreeNode{INT64_MIN, 0, (int32_t)slot - 1};   // loops to itself
                 hleaf.resize(hn.size());
                 hleaf[slot] = nd.value;
+                is_leaf.resize(hn.size());
+                is_leaf[slot] = 1;
                 continue;
             }
             if ((int64_t)hn.size() + 2 > kMaxDevTreeNodes)
@@ -1315,6 +1332,57 @@ static int set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes
             todo.push_back({nd.right, (int64_t)l + 1});
         }
     }
+    hleaf.resize(hn.size());
+    is_leaf.resize(hn.size());
+    // compact form (overlap detection keeps it in LDS): thresholds ranked per feature,
+    // one 32-bit word per node; left out when a limit of the word layout or of the LDS
+    // budget is exceeded (the ensemble is then walked from device memory)
+    std::vector<uint32_t> words;
+    std::vector<int64_t> thr;
+    int32_t thr_off[kFxFeatures + 1] = {};
+    std::vector<int32_t> cbin;
+    int32_t tbin[4] = {};
+    if (n_trees > 0 && (int64_t)hn.size() + n_trees <= kFxMaxWords) {
+        std::vector<std::vector<int64_t>> tf(kFxFeatures);
+        for (size_t i = 0; i < hn.size(); ++i)
+            if (!is_leaf[i]) tf[hn[i].feature].push_back(hn[i].threshold);
+        bool fits = true;
+        for (int f = 0; f < kFxFeatures; ++f) {
+            std::sort(tf[f].begin(), tf[f].end());
+            tf[f].erase(std::unique(tf[f].begin(), tf[f].end()), tf[f].end());
+            fits = fits && (int64_t)tf[f].size() < (int64_t(1) << kFxRankBits);
+            thr_off[f + 1] = thr_off[f] + (int32_t)tf[f].size();
+            thr.insert(thr.end(), tf[f].begin(), tf[f].end());
+        }
+        // bin of x for feature f: thresholds <= x
+        auto bin = [&](int f, int64_t x) {
+            return (int32_t)(std::upper_bound(tf[f].begin(), tf[f].end(), x) - tf[f].begin());
+        };
+        for (size_t i = 0; fits && i < hn.size(); ++i) {
+            if (is_leaf[i]) {
+                const int64_t v = hleaf[i];
+                fits = v >= -(int64_t(1) << 27) && v < (int64_t(1) << 27);
+                words.push_back((uint32_t)(int32_t)(v * 16) | kFxLeaf);
+            } else {
+                const int f = hn[i].feature;
+                const int64_t r = std::lower_bound(tf[f].begin(), tf[f].end(), hn[i].threshold) - tf[f].begin();
+                const int64_t off = (int64_t)hn[i].left - (int64_t)i;
+                fits = off >= 1 && off < (int64_t(1) << (32 - 4 - kFxRankBits));
+                words.push_back((uint32_t)f | ((uint32_t)r << 4) | ((uint32_t)off << (4 + kFxRankBits)));
+            }
+        }
+        if (fits) {
+            cbin.assign(kClasses * kFxFeatures, 0);
+            for (int k = 0; k < kClasses; ++k) {
+                cbin[k * kFxFeatures + 0] = bin(0, k);
+                for (int j = 0; j < kClassMetrics; ++j)
+                    cbin[k * kFxFeatures + 8 + j] = bin(8 + j, class_metrics[k * kClassMetrics + j]);
+            }
+            for (int t = 0; t < 4; ++t) tbin[t] = bin(2, t);
+        } else {
+            words.clear();
+        }
+    }
     hipError_t e = hipSetDevice(g->device);
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     (void)hipDeviceSynchronize();                  // composes already enqueued may read the old ensemble
@@ -1322,6 +1390,7 @@ static int set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes
     (void)hipFree(g->dg.forest_leaf);
     (void)hipFree(g->dg.forest_roots);
     (void)hipFree(g->dg.class_metrics);
+    free_compact(g->dg.fx);
     g->dg.forest_nodes = nullptr;
     g->dg.forest_leaf = nullptr;
     g->dg.forest_roots = nullptr;
@@ -1329,11 +1398,33 @@ static int set_forest(echo_graph g, const echo_tree_node *nodes, int64_t n_nodes
     g->dg.n_trees = 0;
     if (n_trees == 0) return ECHO_OK;
     std::vector<int64_t> hm(class_metrics, class_metrics + kClasses * kClassMetrics);
-    hleaf.resize(hn.size());
+    auto nomem = [&](hipError_t err) {
+        return fail(err == hipErrorOutOfMemory ? ECHO_ERR_NOMEM : ECHO_ERR_HIP, "ensemble upload: %s",
+                    hipGetErrorString(err));
+    };
     if ((e = upload(&g->dg.forest_nodes, hn)) || (e = upload(&g->dg.forest_leaf, hleaf)) ||
         (e = upload(&g->dg.forest_roots, hr)) ||
         (e = upload(&g->dg.class_metrics, hm)))
-        return fail(e == hipErrorOutOfMemory ? ECHO_ERR_NOMEM : ECHO_ERR_HIP, "ensemble upload: %s", hipGetErrorString(e));
+        return nomem(e);
+    if (!words.empty()) {
+        CompactForest &fx = g->dg.fx;
+        std::copy(thr_off, thr_off + kFxFeatures + 1, fx.thr_off);
+        std::copy(tbin, tbin + 4, fx.tbin);
+        if ((e = upload(&fx.words, words)) || (e = upload(&fx.thr, thr)) || (e = upload(&fx.cbin, cbin)) ||
+            (e = hipMalloc(reinterpret_cast<void **>(&fx.coll_bin), sizeof(int32_t) * 2 * std::max<int64_t>(g->n_colls, 1))) ||
+            (e = hipMalloc(reinterpret_cast<void **>(&fx.cp_bin),
+                           sizeof(int32_t) * std::max<int64_t>(g->n_compute, 1)))) {
+            free_compact(fx);
+            return nomem(e);
+        }
+        // per-collective and per-compute-record bins, computed on the device where the
+        // graph's sizes and durations live
+        if ((e = launch_forest_bins(g->dg, g->n_compute, fx, nullptr)) || (e = hipDeviceSynchronize())) {
+            free_compact(fx);
+            return hip_fail(e, "ensemble bins");
+        }
+        fx.n_words = (int32_t)words.size();
+    }
     g->dg.n_trees = n_trees;
     g->dg.forest_base = base_q16;
     return ECHO_OK;

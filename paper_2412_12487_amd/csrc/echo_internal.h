@@ -147,6 +147,30 @@ struct DevTreeNode {
 };
 static_assert(sizeof(DevTreeNode) == 16, "one 16-byte load per node");
 
+// Compact form of the ensemble, held in LDS while overlap detection runs.  Features are
+// compared by bin: for feature f the ensemble's split thresholds, sorted and without
+// repeats, are T_f[0 .. K_f); the bin of a value x is the number of them <= x, so
+// "x < T_f[r]" holds exactly when bin(x) <= r.  A node is one 32-bit word laid out like
+// DevTreeNode (breadth first per tree, a split's children side by side): feature
+// (bits 0-3), the rank r of its threshold in T_f (bits 4-17), left child minus its own
+// index (bits 18-31; right = left + 1).  A leaf has feature kFxLeaf and its value in
+// bits 4-31 (signed); its feature's bin is always 0, so it loops to itself.
+constexpr int kFxFeatures = 12;
+constexpr uint32_t kFxLeaf = 15;
+constexpr int kFxRows = 16;                  // bin rows per lane; rows 12..15 stay 0
+constexpr int kFxMaxWords = 12 * 1024;       // LDS budget of the nodes (48 KB of a 64 KB workgroup, roots aside)
+constexpr int kFxRankBits = 14;
+struct CompactForest {
+    uint32_t *words = nullptr;               // [n_words]
+    int32_t n_words = 0;                     // 0: no compact form (the ensemble does not fit)
+    int64_t *thr = nullptr;                  // every feature's thresholds, concatenated
+    int32_t thr_off[kFxFeatures + 1] = {};   // feature f: thr[thr_off[f] .. thr_off[f + 1])
+    int32_t *cbin = nullptr;                 // [class][kFxFeatures]: bins of the class's own features
+    int32_t tbin[4] = {};                    // bin of each collective type
+    int32_t *coll_bin = nullptr;             // [coll][2]: bins of S and of the N its cost uses
+    int32_t *cp_bin = nullptr;               // [compute record]: bin of the base duration
+};
+
 struct DeviceGraph {
     int64_t n_ops = 0, n_colls = 0;
     int32_t n_ranks = 0, n_walkers = 0, n_blocks = 0;
@@ -174,6 +198,7 @@ struct DeviceGraph {
     int32_t *forest_roots = nullptr;
     int64_t *class_metrics = nullptr;  // [8][4]
     int32_t n_trees = 0, forest_base = 65536;
+    CompactForest fx;                  // the ensemble in LDS form, when it fits
     int32_t max_comm_streams = 0;    // the most streams with comm ops on one rank
     int64_t n_slots = 0;             // member slots of the collectives met through slots
 };
@@ -233,8 +258,9 @@ struct OverlapArgs {
     const int32_t *forest_roots;
     const int64_t *class_metrics;
     int32_t n_trees, forest_base;
+    CompactForest fx;                // n_words > 0: the compact ensemble (LDS variant)
     int32_t prorate;                 // inflate only the overlapped part (extra times in ext)
-    int32_t n_scen, n_tiles;
+    int32_t n_scen, n_tiles, n_ranks;
     int32_t prev_refined;            // the previous pass inflated its compute ops
     int32_t max_comm_streams;        // the most streams with comm ops on one rank (kernel variant)
     unsigned *status;
@@ -251,6 +277,10 @@ hipError_t launch_cc_cost(const CollTable &t, const echo_cc_table *tables, const
                           int32_t n_scen, int64_t *cost, unsigned *status, hipStream_t stream);
 hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream);
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream);
+// Bins of the compact ensemble's per-collective (S, N) and per-compute-record (base
+// duration) features.
+hipError_t launch_forest_bins(const DeviceGraph &g, int64_t n_compute, const CompactForest &fx,
+                              hipStream_t stream);
 // After an overlap pass: count the refinement of every scenario whose durations changed,
 // clear the change flags, and set *stable when none changed.
 hipError_t launch_settle(unsigned *chg, int32_t n_scen, int32_t *refinements, unsigned *stable,

@@ -668,15 +668,18 @@ __device__ __forceinline__ uint32_t factor_of(uint32_t m, const uint32_t *slow, 
 // Factor predicted by the tree ensemble for a compute op (class cls, base
 // duration d0) overlapped by the collective types in mask m (Sec. 6): for each
 // type, the base score plus one leaf per tree, kept inside [65536, 2^20); the
-// largest over the types.  Trees are walked per lane from global memory (the
-// walk stops at a leaf; paths are at most ECHO_TREE_DEPTH splits long).
+// largest over the types.  Trees are walked from device memory (the walk stops at
+// a leaf; paths are at most ECHO_TREE_DEPTH splits long): when every lane that
+// needs a type shares one feature vector, once for the wavefront with one tree
+// per lane, else per lane.
 constexpr int kForestLanes = 16;
 constexpr int kPre = 8;          // unchained starts prefetched per round of overlap detection
 constexpr int kIdStage = 1024;   // comm ops of a rank whose ids overlap detection keeps in LDS
 
 // feat: this wavefront's LDS feature rows, feature k of lane l at feat[k * 64 + l].
 __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_t *smax, const int32_t *nmax,
-                                  int cls, int64_t d0, const echo_scenario *sc, int64_t *feat, int lane) {
+                                  int cls, int64_t d0, const echo_scenario *sc, int64_t *feat, bool knobs_uniform,
+                                  int lane) {
     const int64_t *met = a.class_metrics + cls * kClassMetrics;
     feat[0 * kLanes + lane] = cls;
     feat[1 * kLanes + lane] = d0;
@@ -688,41 +691,175 @@ __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_
     uint32_t best = 65536u;
 #pragma unroll
     for (int t = 0; t < kTypes; ++t) {
-        if (!((m >> t) & 1u)) continue;
+        const bool has = (m >> t) & 1u;
+        const uint64_t lanes_t = __ballot(has);
+        if (!lanes_t) continue;
         feat[2 * kLanes + lane] = t;
         feat[3 * kLanes + lane] = smax[t];
         feat[4 * kLanes + lane] = nmax[t];
+        const int first = __builtin_ctzll(lanes_t);
+        const int64_t s0 = __shfl(smax[t], first);
+        const int32_t n0 = __shfl(nmax[t], first);
+        const bool uniform = knobs_uniform && __ballot(has && (smax[t] != s0 || nmax[t] != n0)) == 0;
         int64_t sum = a.forest_base;
-        // kForestLanes trees walked side by side: their node loads are independent
-        for (int32_t tr0 = 0; tr0 < a.n_trees; tr0 += kForestLanes) {
-            int32_t idx[kForestLanes];
-            bool live[kForestLanes];
+        if (uniform) {
+            // every lane that needs type t has lane `first`'s feature vector: the trees are
+            // walked side by side, one per lane, and their leaves summed across the wavefront
+            for (int32_t tr0 = 0; tr0 < a.n_trees; tr0 += kLanes) {
+                const bool live = tr0 + lane < a.n_trees;
+                int32_t idx = a.forest_roots[live ? tr0 + lane : 0];
+                for (int step = 0; step < ECHO_TREE_DEPTH; ++step) {
+                    const int4 nd = reinterpret_cast<const int4 *>(a.forest_nodes)[idx];
+                    const int64_t x = feat[nd.z * kLanes + first];
+                    const int64_t thr = (int64_t)(((uint64_t)(uint32_t)nd.y << 32) | (uint32_t)nd.x);
+                    idx = nd.w + (x < thr ? 0 : 1);
+                }
+                int64_t leaf = live ? (int64_t)a.forest_leaf[idx] : 0;
 #pragma unroll
-            for (int q = 0; q < kForestLanes; ++q) {
-                live[q] = tr0 + q < a.n_trees;
-                idx[q] = live[q] ? a.forest_roots[tr0 + q] : 0;
+                for (int o = kLanes / 2; o > 0; o >>= 1) leaf += __shfl_xor(leaf, o);
+                sum += leaf;
             }
-            // every path has at most ECHO_TREE_DEPTH splits and a leaf loops to itself, so
-            // after that many steps each walk rests on its leaf: no per-lane exit
-            for (int step = 0; step < ECHO_TREE_DEPTH; ++step) {
-                int4 nd[kForestLanes];          // threshold low, threshold high, feature, left
-#pragma unroll
-                for (int q = 0; q < kForestLanes; ++q)
-                    nd[q] = reinterpret_cast<const int4 *>(a.forest_nodes)[idx[q]];
+        } else {
+            // kForestLanes trees walked side by side: their node loads are independent
+            for (int32_t tr0 = 0; tr0 < a.n_trees; tr0 += kForestLanes) {
+                int32_t idx[kForestLanes];
+                bool live[kForestLanes];
 #pragma unroll
                 for (int q = 0; q < kForestLanes; ++q) {
-                    const int64_t x = feat[nd[q].z * kLanes + lane];
-                    const int64_t thr = (int64_t)(((uint64_t)(uint32_t)nd[q].y << 32) | (uint32_t)nd[q].x);
-                    idx[q] = nd[q].w + (x < thr ? 0 : 1);
+                    live[q] = tr0 + q < a.n_trees;
+                    idx[q] = live[q] ? a.forest_roots[tr0 + q] : 0;
                 }
-            }
+                // every path has at most ECHO_TREE_DEPTH splits and a leaf loops to itself, so
+                // after that many steps each walk rests on its leaf: no per-lane exit
+                for (int step = 0; step < ECHO_TREE_DEPTH; ++step) {
+                    int4 nd[kForestLanes];          // threshold low, threshold high, feature, left
 #pragma unroll
-            for (int q = 0; q < kForestLanes; ++q)
-                if (live[q]) sum += a.forest_leaf[idx[q]];
+                    for (int q = 0; q < kForestLanes; ++q)
+                        nd[q] = reinterpret_cast<const int4 *>(a.forest_nodes)[idx[q]];
+#pragma unroll
+                    for (int q = 0; q < kForestLanes; ++q) {
+                        const int64_t x = feat[nd[q].z * kLanes + lane];
+                        const int64_t thr = (int64_t)(((uint64_t)(uint32_t)nd[q].y << 32) | (uint32_t)nd[q].x);
+                        idx[q] = nd[q].w + (x < thr ? 0 : 1);
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < kForestLanes; ++q)
+                    if (live[q]) sum += a.forest_leaf[idx[q]];
+            }
         }
         sum = sum < 65536 ? 65536 : sum;
         sum = sum >= (int64_t(1) << 20) ? (int64_t(1) << 20) - 1 : sum;
-        best = (uint32_t)sum > best ? (uint32_t)sum : best;
+        if (has) best = (uint32_t)sum > best ? (uint32_t)sum : best;
+    }
+    return best;
+}
+
+// ---- compact ensemble (LDS): features compared by bin (see CompactForest)
+// Bin of x for a feature with sorted thresholds T[0..n): how many are <= x.
+__device__ __forceinline__ int32_t fx_bin(const int64_t *T, int32_t n, int64_t x) {
+    int32_t lo = 0, hi = n;
+    while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (T[mid] <= x) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo;
+}
+
+// Bins of every collective's S and cost N (features 3 and 4) and of every compute
+// record's base duration (feature 1).
+__global__ void k_forest_bins(CollTable colls, const ComputeRec *cp, int64_t n_cp, CompactForest fx) {
+    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t nth = (int64_t)gridDim.x * blockDim.x;
+    const int64_t *T1 = fx.thr + fx.thr_off[1], *T3 = fx.thr + fx.thr_off[3], *T4 = fx.thr + fx.thr_off[4];
+    const int32_t n1 = fx.thr_off[2] - fx.thr_off[1], n3 = fx.thr_off[4] - fx.thr_off[3],
+                  n4 = fx.thr_off[5] - fx.thr_off[4];
+    for (int64_t c = tid; c < colls.n; c += nth) {
+        fx.coll_bin[2 * c] = fx_bin(T3, n3, colls.bytes[c]);
+        fx.coll_bin[2 * c + 1] = fx_bin(T4, n4, colls.N[c]);
+    }
+    for (int64_t i = tid; i < n_cp; i += nth) fx.cp_bin[i] = fx_bin(T1, n1, cp[i].dur);
+}
+
+// Ensemble prediction from the compact LDS form, for the collective types in mask m
+// (per lane), as forest_factor computes it.  fb: this wavefront's bin rows in LDS,
+// feature f of lane l at fb[f * 64 + l] (rows 5-7: the scenario's knobs, set once;
+// rows 12-15: 0).  bS/bN: per type, the largest bins of S and N among the overlapping
+// type-t comm ops.  When every lane that has type t in its mask shares its feature
+// vector (knobs_uniform and equal S and N bins), the trees are walked once for the
+// wavefront, one tree per lane; otherwise each lane walks every tree on its own path.
+__device__ uint32_t forest_factor_compact(const OverlapArgs &a, uint32_t m, const int32_t *bS, const int32_t *bN,
+                                          int cls, int32_t bd0, const uint32_t *fw, const int32_t *froots, uint16_t *fb,
+                                          bool knobs_uniform, int lane) {
+    const int32_t *cb = a.fx.cbin + cls * kFxFeatures;
+    fb[0 * kLanes + lane] = (uint16_t)cb[0];
+    fb[1 * kLanes + lane] = (uint16_t)bd0;
+#pragma unroll
+    for (int k = 8; k < kFxFeatures; ++k) fb[k * kLanes + lane] = (uint16_t)cb[k];
+    uint32_t best = 65536u;
+#pragma unroll
+    for (int t = 0; t < kTypes; ++t) {
+        const bool has = (m >> t) & 1u;
+        const uint64_t lanes_t = __ballot(has);
+        if (!lanes_t) continue;
+        fb[2 * kLanes + lane] = (uint16_t)a.fx.tbin[t];
+        fb[3 * kLanes + lane] = (uint16_t)bS[t];
+        fb[4 * kLanes + lane] = (uint16_t)bN[t];
+        const int first = __builtin_ctzll(lanes_t);
+        const int32_t s0 = __builtin_amdgcn_readlane(bS[t], first), n0 = __builtin_amdgcn_readlane(bN[t], first);
+        const bool uniform = knobs_uniform && __ballot(has && (bS[t] != s0 || bN[t] != n0)) == 0;
+        int64_t sum = a.forest_base;
+        if (uniform) {
+            // One feature vector (lane `first`'s) for every lane that needs type t: the
+            // trees are walked side by side, one per lane, and their leaves summed across
+            // the wavefront.
+            for (int32_t tr0 = 0; tr0 < a.n_trees; tr0 += kLanes) {
+                const bool live = tr0 + lane < a.n_trees;
+                int32_t idx = froots[live ? tr0 + lane : 0];
+                for (int step = 0; step < ECHO_TREE_DEPTH; ++step) {
+                    const uint32_t w = fw[idx];
+                    const uint32_t f = w & 15u;
+                    const uint32_t r = (w >> 4) & ((1u << kFxRankBits) - 1);
+                    const int32_t off = f == kFxLeaf ? 0 : (int32_t)(w >> (4 + kFxRankBits));
+                    const uint32_t x = fb[f * kLanes + first];
+                    idx += off + (x > r ? 1 : 0);
+                }
+                int64_t leaf = live ? (int64_t)((int32_t)fw[idx] >> 4) : 0;
+#pragma unroll
+                for (int o = kLanes / 2; o > 0; o >>= 1) leaf += __shfl_xor(leaf, o);
+                sum += leaf;
+            }
+        } else {
+            for (int32_t tr0 = 0; tr0 < a.n_trees; tr0 += kForestLanes) {
+                int32_t idx[kForestLanes];
+                bool live[kForestLanes];
+#pragma unroll
+                for (int q = 0; q < kForestLanes; ++q) {
+                    live[q] = tr0 + q < a.n_trees;
+                    idx[q] = froots[live[q] ? tr0 + q : 0];
+                }
+                for (int step = 0; step < ECHO_TREE_DEPTH; ++step) {
+                    uint32_t w[kForestLanes];
+#pragma unroll
+                    for (int q = 0; q < kForestLanes; ++q) w[q] = fw[idx[q]];
+#pragma unroll
+                    for (int q = 0; q < kForestLanes; ++q) {
+                        const uint32_t f = w[q] & 15u;
+                        const uint32_t r = (w[q] >> 4) & ((1u << kFxRankBits) - 1);
+                        const int32_t off = f == kFxLeaf ? 0 : (int32_t)(w[q] >> (4 + kFxRankBits));
+                        const uint32_t x = fb[f * kLanes + lane];
+                        idx[q] += off + (x > r ? 1 : 0);
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < kForestLanes; ++q)
+                    if (live[q]) sum += (int32_t)fw[idx[q]] >> 4;
+            }
+        }
+        sum = sum < 65536 ? 65536 : sum;
+        sum = sum >= (int64_t(1) << 20) ? (int64_t(1) << 20) - 1 : sum;
+        if (has) best = (uint32_t)sum > best ? (uint32_t)sum : best;
     }
     return best;
 }
@@ -731,26 +868,43 @@ __device__ uint32_t forest_factor(const OverlapArgs &a, uint32_t m, const int64_
 // overlapping comm intervals (a merge of the per-stream interval lists in start
 // order), and record the extra time q16(min(o, D), F) - min(o, D) instead of a mask.
 // DETECT: flag the scenarios whose durations change (fixed-point iteration).
-// FOREST: the factor is the tree ensemble's prediction (recorded as an extra time).
+// FOREST: the factor is the tree ensemble's prediction (recorded as an extra time):
+// 1 walks the ensemble from device memory, 2 from its compact form in LDS (a workgroup
+// of kFxWaves wavefronts, one (rank, tile) each, shares one copy of the nodes).
 // NC: room for this many comm streams per rank (the cursor and merge state scale with it).
-template <bool PRORATE, bool DETECT, bool FOREST, int NC>
-__global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
-    constexpr bool EXT = PRORATE || FOREST;      // output: extra time per op instead of a mask
+constexpr int kFxWaves = 4;
+template <bool PRORATE, bool DETECT, int FOREST, int NC>
+__global__ __launch_bounds__(64 * (FOREST == 2 ? kFxWaves : 1)) void k_overlap(OverlapArgs a) {
+    constexpr bool EXT = PRORATE || FOREST != 0;  // output: extra time per op instead of a mask
+    constexpr int W = FOREST == 2 ? kFxWaves : 1;      // wavefronts per workgroup
+    constexpr int STAGE = FOREST == 2 ? kIdStage / 4 : kIdStage;
     // unchained starts prefetched per round: all but the ensemble variants prefetch fewer,
     // for the registers the block checks take (four wavefronts per SIMD for the mask and
     // prorating variants with four comm streams)
     constexpr int NPRE = FOREST ? kPre : (DETECT || PRORATE) ? kPre / 4 : kPre / 2;
-    __shared__ int64_t feat[FOREST ? 12 * kLanes : 1];   // the ensemble's feature vectors, one per lane
-    __shared__ int32_t sid[kIdStage];            // the rank's comm op ids and collective types, staged
-    __shared__ uint8_t stype[kIdStage];
+    __shared__ int64_t feat[FOREST == 1 ? 12 * kLanes : 1];   // the ensemble's feature vectors, one per lane
+    __shared__ uint16_t fbin[FOREST == 2 ? W * kFxRows * kLanes : 1];   // compact: bin rows per lane
+    extern __shared__ uint32_t fwords[];         // compact: the ensemble's nodes
+    __shared__ int32_t sid_all[W * STAGE];       // the rank's comm op ids and collective types, staged
+    __shared__ uint8_t stype_all[W * STAGE];
     // masks of the round's ops, [op][lane]: written out row by row once per round
     __shared__ __align__(16) uint8_t mstage[EXT ? 16 : kLanes * kLanes];
     if (a.stable && __builtin_amdgcn_readfirstlane(__hip_atomic_load(a.stable, __ATOMIC_RELAXED,
                                                                       __HIP_MEMORY_SCOPE_AGENT)))
         return;                                  // every scenario is at its fixed point
-    const int lane = threadIdx.x;
-    const int32_t r = blockIdx.x / a.n_tiles;
-    const int32_t tile = blockIdx.x % a.n_tiles;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t unit = (int64_t)blockIdx.x * W + wave;       // (rank, tile) of this wavefront
+    const bool valid = unit < (int64_t)a.n_ranks * a.n_tiles;
+    const int32_t r = valid ? (int32_t)(unit / a.n_tiles) : 0;
+    const int32_t tile = valid ? (int32_t)(unit % a.n_tiles) : 0;
+    int32_t *const sid = sid_all + wave * STAGE;
+    uint8_t *const stype = stype_all + wave * STAGE;
+    if (FOREST == 2) {
+        // the nodes, then the roots of the trees
+        for (int i = threadIdx.x; i < a.fx.n_words; i += 64 * W) fwords[i] = a.fx.words[i];
+        for (int i = threadIdx.x; i < a.n_trees; i += 64 * W) fwords[a.fx.n_words + i] = (uint32_t)a.forest_roots[i];
+    }
     const bool active = tile * kLanes + lane < a.n_scen;
     const int32_t col = active ? lane : a.n_scen - 1 - tile * kLanes;
     const int32_t sigma = tile * kLanes + col;
@@ -773,12 +927,33 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
     // Stage the rank's comm lists in LDS: a cursor move then costs one memory round trip
     // (the comm op's interval) instead of two (its id, then the interval).
     const int64_t cbase = cl_off[0];
-    const int64_t nstage = cl_off[kStreams] - cbase < kIdStage ? cl_off[kStreams] - cbase : kIdStage;
+    const int64_t nstage = !valid ? 0 : cl_off[kStreams] - cbase < STAGE ? cl_off[kStreams] - cbase : STAGE;
     for (int64_t i = lane; i < nstage; i += kLanes) {
         sid[i] = a.cl[cbase + i];
         stype[i] = a.cl_type[cbase + i];
     }
     __syncthreads();
+    if (!valid) return;                          // past the last (rank, tile); after the shared fill
+    // compact ensemble: this wavefront's bin rows; the scenario knobs' rows are fixed
+    uint16_t *const fb = fbin + (FOREST == 2 ? wave * kFxRows * kLanes : 0);
+    bool knobs_uniform = false;
+    if (FOREST == 2) {
+        const int32_t k5 = fx_bin(a.fx.thr + a.fx.thr_off[5], a.fx.thr_off[6] - a.fx.thr_off[5], sc->ar_algo);
+        const int32_t k6 = fx_bin(a.fx.thr + a.fx.thr_off[6], a.fx.thr_off[7] - a.fx.thr_off[6], sc->bw_intra_MBps);
+        const int32_t k7 = fx_bin(a.fx.thr + a.fx.thr_off[7], a.fx.thr_off[8] - a.fx.thr_off[7], sc->bw_inter_MBps);
+        fb[5 * kLanes + lane] = (uint16_t)k5;
+        fb[6 * kLanes + lane] = (uint16_t)k6;
+        fb[7 * kLanes + lane] = (uint16_t)k7;
+#pragma unroll
+        for (int k = kFxFeatures; k < kFxRows; ++k) fb[k * kLanes + lane] = 0;
+        knobs_uniform = __ballot(k5 != __builtin_amdgcn_readfirstlane(k5) || k6 != __builtin_amdgcn_readfirstlane(k6) ||
+                                 k7 != __builtin_amdgcn_readfirstlane(k7)) == 0;
+    } else if (FOREST == 1) {
+        const int64_t k6 = sc->bw_intra_MBps, k7 = sc->bw_inter_MBps;
+        const int32_t k5 = sc->ar_algo;
+        knobs_uniform = __ballot(k5 != __builtin_amdgcn_readfirstlane(k5) || k6 != __shfl(k6, 0) ||
+                                 k7 != __shfl(k7, 0)) == 0;
+    }
     // comm op at position x of the rank's lists and its collective type
     auto comm_id = [&](int64_t x) -> int64_t {
         const int64_t o = x - cbase;
@@ -991,7 +1166,7 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 uint32_t m = 0;                            // types of the comm ops overlapping v
                 int64_t o = 0;                             // covered length (PRORATE)
                 int64_t smax[kTypes];                      // FOREST: largest S per overlapping type
-                int32_t nmax[kTypes];                      //         and most members
+                int32_t nmax[kTypes];                      //         and most members (compact: their bins)
     #pragma unroll
                 for (int tt = 0; tt < kTypes; ++tt) {
                     smax[tt] = 0;
@@ -1001,8 +1176,8 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
 #define NOTE_FOREST(x_, ty_)                                                                     \
     if (FOREST) {                                                                                \
         const int32_t cc_ = a.cl_coll[x_];                                                       \
-        const int64_t S_ = a.coll_bytes[cc_];                                                    \
-        const int32_t N_ = a.coll_N[cc_];                                                        \
+        const int64_t S_ = FOREST == 2 ? a.fx.coll_bin[2 * cc_] : a.coll_bytes[cc_];            \
+        const int32_t N_ = FOREST == 2 ? a.fx.coll_bin[2 * cc_ + 1] : a.coll_N[cc_];            \
         _Pragma("unroll") for (int tt = 0; tt < kTypes; ++tt) if (tt == (int)(ty_)) {            \
             smax[tt] = S_ > smax[tt] ? S_ : smax[tt];                                            \
             nmax[tt] = N_ > nmax[tt] ? N_ : nmax[tt];                                            \
@@ -1097,8 +1272,20 @@ __global__ __launch_bounds__(64) void k_overlap(OverlapArgs a) {
                 if (EXT) {
                     uint32_t e = 0;
                     if (m != 0) {
-                        const uint32_t F = FOREST ? forest_factor(a, m, smax, nmax, cls, d0, sc, feat, lane)
-                                                  : factor_of(m, slow, cls);
+                        uint32_t F;
+                        if (FOREST == 2) {
+                            int32_t bS[kTypes];
+#pragma unroll
+                            for (int tt = 0; tt < kTypes; ++tt) bS[tt] = (int32_t)smax[tt];
+                            const int32_t bd0 = a.fx.cp_bin[i0 + j];
+                            F = forest_factor_compact(a, m, bS, nmax, cls, bd0, fwords,
+                                                      reinterpret_cast<const int32_t *>(fwords) + a.fx.n_words, fb,
+                                                      knobs_uniform, lane);
+                        } else if (FOREST == 1) {
+                            F = forest_factor(a, m, smax, nmax, cls, d0, sc, feat, knobs_uniform, lane);
+                        } else {
+                            F = factor_of(m, slow, cls);
+                        }
                         const int64_t oc = PRORATE ? (o < D ? o : D) : D;
                         const int64_t x = q16(oc, F) - oc;
                         ext_over |= x >= (int64_t)kExtLimit;
@@ -1195,24 +1382,39 @@ hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream) 
 
 template <int NC>
 hipError_t launch_overlap_nc(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
-    const dim3 grid((unsigned)(n_ranks * a.n_tiles)), block(kLanes);
+    const int64_t units = (int64_t)n_ranks * a.n_tiles;
+    const dim3 grid((unsigned)units), block(kLanes);
     // a.ext: extra-time output (prorating and/or ensemble factors); a.forest_nodes: ensemble
     const bool forest = a.forest_nodes != nullptr, prorate = a.prorate != 0;
-    if (forest) {
-        if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, true, NC>), grid, block, 0, stream, a);
-        else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, true, NC>), grid, block, 0, stream, a);
-        else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, true, NC>), grid, block, 0, stream, a);
-        else hipLaunchKernelGGL((k_overlap<false, false, true, NC>), grid, block, 0, stream, a);
-    } else if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, false, NC>), grid, block, 0, stream, a);
-    else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, false, NC>), grid, block, 0, stream, a);
-    else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, false, NC>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((k_overlap<false, false, false, NC>), grid, block, 0, stream, a);
+    if (forest && a.fx.n_words > 0) {
+        // compact ensemble in LDS: kFxWaves (rank, tile) units per workgroup share its nodes
+        const dim3 g2((unsigned)((units + kFxWaves - 1) / kFxWaves)), b2(kLanes * kFxWaves);
+        const size_t lds = sizeof(uint32_t) * ((size_t)a.fx.n_words + (size_t)a.n_trees);
+        if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, 2, NC>), g2, b2, lds, stream, a);
+        else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, 2, NC>), g2, b2, lds, stream, a);
+        else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, 2, NC>), g2, b2, lds, stream, a);
+        else hipLaunchKernelGGL((k_overlap<false, false, 2, NC>), g2, b2, lds, stream, a);
+    } else if (forest) {
+        if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, 1, NC>), grid, block, 0, stream, a);
+        else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, 1, NC>), grid, block, 0, stream, a);
+        else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, 1, NC>), grid, block, 0, stream, a);
+        else hipLaunchKernelGGL((k_overlap<false, false, 1, NC>), grid, block, 0, stream, a);
+    } else if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, 0, NC>), grid, block, 0, stream, a);
+    else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, 0, NC>), grid, block, 0, stream, a);
+    else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, 0, NC>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((k_overlap<false, false, 0, NC>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 
 hipError_t launch_overlap(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
     if (a.max_comm_streams > 4) return launch_overlap_nc<kStreams>(a, n_ranks, stream);
     return launch_overlap_nc<4>(a, n_ranks, stream);
+}
+
+hipError_t launch_forest_bins(const DeviceGraph &g, int64_t n_cp, const CompactForest &fx, hipStream_t stream) {
+    const int64_t n = std::max<int64_t>(g.colls.n, n_cp);
+    hipLaunchKernelGGL(k_forest_bins, dim3(grid_for(n, 256)), dim3(256), 0, stream, g.colls, g.cp, n_cp, fx);
+    return hipGetLastError();
 }
 
 hipError_t launch_settle(unsigned *chg, int32_t n_scen, int32_t *refinements, unsigned *stable,

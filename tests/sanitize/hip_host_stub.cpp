@@ -98,6 +98,8 @@ hipError_t launch_walk(const WalkArgs &, int32_t, hipStream_t) { return hipError
 hipError_t launch_overlap(const OverlapArgs &, int32_t, hipStream_t) { return hipErrorNotSupported; }
 hipError_t launch_settle(unsigned *, int32_t, int32_t *, unsigned *, hipStream_t) { return hipErrorNotSupported; }
 hipError_t launch_fill_i32(int32_t *, int64_t, int32_t, hipStream_t) { return hipErrorNotSupported; }
+// the bins stay unset on the CPU: no compose runs there
+hipError_t launch_forest_bins(const DeviceGraph &, int64_t, const CompactForest &, hipStream_t) { return hipSuccess; }
 hipError_t scratch_buffer(int, void **ptr) {
     *ptr = nullptr;
     return hipErrorNotSupported;

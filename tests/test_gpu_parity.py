@@ -834,3 +834,42 @@ def test_forest_errors(E):
     assert_same({"step": out["step"].cpu().numpy(), "digest": out["digest"].cpu().numpy().view(np.uint64),
                  "start": out["start"].cpu().numpy(), "finish": out["finish"].cpu().numpy()}, ref)
     G.close()
+
+
+@pytest.mark.parametrize("ensemble", ["compact", "device"])
+@pytest.mark.parametrize("knobs", ["uniform", "varied"])
+def test_forest_walk_paths(E, ensemble, knobs):
+    """Both ways the ensemble is walked, against the oracle: a 64-tree ensemble
+    (about 11k nodes) fits the compact LDS form, a 128-tree one (about 23k) is walked
+    from device memory; with the scenario knobs shared by every lane (only jitter and
+    slowdown tables vary, as in the 1024-rank workload) the compact walk follows one
+    path per wavefront wherever the lanes' features agree, with varied bandwidths and
+    algorithms every lane walks its own."""
+    fo = slowdown_forest.synthetic_forest(0, n_trees=64 if ensemble == "compact" else 128)
+    assert (len(fo["nodes"]) + len(fo["roots"]) <= 12 * 1024) == (ensemble == "compact")
+    rng = np.random.default_rng(77)
+    graphs = [configs.graph(1), _random_graph(np.random.default_rng(5), 12, 40, 20)]
+    for g in graphs:
+        if knobs == "uniform":
+            sc = scenarios.draw(130, rng, slowdown=(65536, 91750), jitter=(6554, 5))
+        else:
+            sc = scenarios.draw(130, rng, bw_inter=(20000, 400000), bw_intra=(50000, 400000), alpha=(0, 20000),
+                                ar_algo_random=True, jitter=(4000, 9))
+        for until_stable, prorate in [(False, False), (True, True)]:
+            try:
+                ref = oracle.run(g, sc, 4, threads=THREADS, until_stable=until_stable, prorate=prorate, forest=fo)
+            except oracle.OracleError as e:
+                assert e.code == -4
+                continue
+            G = E.Graph(g, 0)
+            try:
+                G.set_forest(fo)
+                d, n = E.scenarios_to_device(sc)
+                out = G.compose(d, n, 4, timelines=True, digest=True, until_stable=until_stable, prorate=prorate,
+                                forest=True, refinements=True)
+                gpu = {"step": out["step"].cpu().numpy(), "digest": out["digest"].cpu().numpy().view(np.uint64),
+                       "start": out["start"].cpu().numpy(), "finish": out["finish"].cpu().numpy()}
+                assert_same(gpu, ref)
+                np.testing.assert_array_equal(out["refinements"].cpu().numpy(), ref["refinements"])
+            finally:
+                G.close()
