@@ -56,6 +56,10 @@ __device__ __forceinline__ int64_t jittered(int64_t d0, int32_t v, uint64_t jbas
     hi += k * (uint32_t)(kGolden >> 32);
     const uint64_t u = mix64(jbase + (((uint64_t)hi << 32) | lo));
     const uint32_t f = (uint32_t)(65536 - amp) + __umulhi((uint32_t)(u >> 32), (uint32_t)(2 * amp + 1));
+    // d0 is the same for every lane: below 2^32 (durations under 4.3 s) one 32 x 32-bit
+    // multiply-add gives the whole product
+    if (__builtin_expect(((uint64_t)d0 >> 32) == 0, 1))
+        return (int64_t)(((uint64_t)(uint32_t)d0 * f + 32768ull) >> 16);
     return q16(d0, f);
 }
 

@@ -873,3 +873,24 @@ def test_forest_walk_paths(E, ensemble, knobs):
                 np.testing.assert_array_equal(out["refinements"].cpu().numpy(), ref["refinements"])
             finally:
                 G.close()
+
+
+def test_jittered_durations_beyond_32_bits(E):
+    """Base durations on both sides of 2^32 ns (the jitter draw multiplies short ones in
+    one 32-bit step) and up to the 2^43 limit, jittered with amplitudes up to 65535,
+    through every pass: timelines against the oracle."""
+    rng = np.random.default_rng(41)
+    b = Builder(2)
+    c = b.collective(AR, 1 << 20)
+    for r in range(2):
+        prev = []
+        for k in range(40):
+            d = int(rng.choice([rng.integers(1, 1 << 32), rng.integers(1 << 32, 1 << 42), (1 << 32) - 1, 1 << 32]))
+            prev = [b.compute(r, d, preds=prev, cls=k % 8)]
+        x = b.comm(r, c, preds=prev)
+        b.compute(r, 1000, preds=[x])
+    g = b.graph()
+    sc = scenarios.draw(70, rng, slowdown=(65536, 91750), jitter=(6554, 3))
+    sc["jitter_amp_q16"][::3] = 65535
+    sc["jitter_amp_q16"][1::3] = 1
+    assert_same(gpu_run(E, g, sc, 1), oracle.run(g, sc, 1))
