@@ -342,7 +342,8 @@ int echo_kernel_times(echo_graph g, int32_t max, int32_t *kinds, float *ms, int3
 
 /*
  * Bounded waits.  A composer wavefront that waits for the members of a
- * collective gives up after limit_ns nanoseconds of wall clock (default 20 s):
+ * collective gives up after limit_ns nanoseconds of wall clock (default 20 s;
+ * counted from the wait's 16th poll of device memory or 256th poll of LDS):
  * it sets the graph's timeout status, every other wait of the launch gives
  * up too, and every kernel runs to its end (the timelines it writes are then
  * meaningless) -- echo_sync_status reports ECHO_ERR_DEVICE.  The limit applies

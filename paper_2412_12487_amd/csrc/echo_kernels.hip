@@ -26,6 +26,10 @@ constexpr int64_t kKnobLimit = int64_t(1) << 40;
 constexpr int64_t kInf = INT64_MAX;
 // s_waitcnt immediate for "vmcnt(0)" on gfx9-family targets (expcnt and lgkmcnt left at their maxima)
 constexpr int kWaitVm0 = 0x0F70;
+// polls between reads of the abort bit and the clock: of a barrier in device memory (a
+// poll is a memory round trip) and of one in LDS
+constexpr unsigned kCheckPollsGlobal = 16;
+constexpr unsigned kCheckPollsLocal = 256;
 
 __device__ __forceinline__ uint64_t mix64(uint64_t z) {
     z = (z ^ (z >> 30)) * kMixA;
@@ -198,9 +202,31 @@ __global__ __launch_bounds__(64) void k_cc_cost(CollTable t, const echo_cc_table
 }
 
 // ------------------------------------------------------------------ composer
+// Bounded waits.  A wait polls; every kCheckPolls-th poll it also reads the abort bit
+// and the 100 MHz wall clock, which it first reads at that poll (a clock read on the way
+// into a wait would delay the first polls, and a wait is usually over within a few).
+// It gives up -- and tells every other waiter to give up -- once spin_limit ticks have
+// passed since then.
+struct WaitClock {
+    uint64_t t0 = 0;
+    bool started = false;
+    // false: give up (abort seen, or the limit passed: then the abort bit is set)
+    __device__ bool check(unsigned *status, int64_t limit) {
+        if (__builtin_amdgcn_readfirstlane(ld_relaxed(status)) & kStatusAbort) return false;
+        const uint64_t now = wall_clock64();
+        if (!started) {
+            started = true;
+            t0 = now;
+        } else if ((int64_t)(now - t0) > limit) {
+            __hip_atomic_fetch_or(status, kStatusTimeout | kStatusAbort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return false;
+        }
+        return true;
+    }
+};
+
 // Wait until `need` member wavefronts of one scenario tile have published
-// their launch times.  Bounded: gives up (and tells every other waiter to give
-// up) after spin_limit ticks of the 100 MHz wall clock.
+// their launch times.
 __device__ bool wait_arrivals(const unsigned *cnt, unsigned need, unsigned *status, int64_t limit) {
     // Issue priority on the SIMD follows lateness: the last member to arrive is what the
     // others wait for, so it runs at raised priority until it next arrives early.
@@ -209,16 +235,11 @@ __device__ bool wait_arrivals(const unsigned *cnt, unsigned need, unsigned *stat
         return true;
     }
     __builtin_amdgcn_s_setprio(0);
-    const uint64_t t0 = wall_clock64();
-    for (;;) {
+    WaitClock clk;
+    for (unsigned it = 1;; ++it) {
         __builtin_amdgcn_s_sleep(2);
         if (__builtin_amdgcn_readfirstlane(ld_relaxed(cnt)) >= need) return true;
-        if (__builtin_amdgcn_readfirstlane(ld_relaxed(status)) & kStatusAbort) return false;
-        if ((int64_t)(wall_clock64() - t0) > limit) {
-            __hip_atomic_fetch_or(status, kStatusTimeout | kStatusAbort, __ATOMIC_RELAXED,
-                                  __HIP_MEMORY_SCOPE_AGENT);
-            return false;
-        }
+        if ((it & (kCheckPollsGlobal - 1)) == 0 && !clk.check(status, limit)) return false;
     }
 }
 
@@ -228,8 +249,8 @@ __device__ bool wait_arrivals(const unsigned *cnt, unsigned need, unsigned *stat
 // read in one memory round trip per poll.  Bounded like wait_arrivals; on giving up
 // it returns 0 and clears *ok.
 __device__ int64_t wait_slots(const int64_t *p, unsigned n, int64_t ns, unsigned *status, int64_t limit, bool *ok) {
-    uint64_t t0 = 0;
-    for (int poll = 0;; ++poll) {
+    WaitClock clk;
+    for (unsigned poll = 0;; ++poll) {
         int64_t v[kSlotMembers];
 #pragma unroll
         for (int m = 0; m < kSlotMembers; ++m)
@@ -247,16 +268,9 @@ __device__ int64_t wait_slots(const int64_t *p, unsigned n, int64_t ns, unsigned
             if (poll == 0) __builtin_amdgcn_s_setprio(3);
             return mx;
         }
-        if (poll == 0) {
-            __builtin_amdgcn_s_setprio(0);
-            t0 = wall_clock64();
-        }
+        if (poll == 0) __builtin_amdgcn_s_setprio(0);
         __builtin_amdgcn_s_sleep(2);
-        if (__builtin_amdgcn_readfirstlane(ld_relaxed(status)) & kStatusAbort) break;
-        if ((int64_t)(wall_clock64() - t0) > limit) {
-            __hip_atomic_fetch_or(status, kStatusTimeout | kStatusAbort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            break;
-        }
+        if (((poll + 1) & (kCheckPollsGlobal - 1)) == 0 && !clk.check(status, limit)) break;
     }
     *ok = false;
     return 0;
@@ -296,18 +310,11 @@ __device__ bool wait_local(const unsigned *cnt, unsigned need, unsigned *status,
         return true;
     }
     __builtin_amdgcn_s_setprio(0);
-    const uint64_t t0 = wall_clock64();
+    WaitClock clk;
     for (unsigned it = 1;; ++it) {
         __builtin_amdgcn_s_sleep(1);
         if (ld_local(cnt) >= need) return true;
-        if ((it & 255) == 0) {
-            if (__builtin_amdgcn_readfirstlane(ld_relaxed(status)) & kStatusAbort) return false;
-            if ((int64_t)(wall_clock64() - t0) > limit) {
-                __hip_atomic_fetch_or(status, kStatusTimeout | kStatusAbort, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT);
-                return false;
-            }
-        }
+        if ((it & (kCheckPollsLocal - 1)) == 0 && !clk.check(status, limit)) return false;
     }
 }
 

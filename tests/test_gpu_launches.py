@@ -120,9 +120,11 @@ def test_launch_tile_cap_rejects_negative(E):
 
 
 def test_tiny_spin_limit_gives_up_every_wait_and_the_graph_recovers(E):
-    """A 10 ns limit: the waits for collective members give up at once, every kernel
-    runs to its end and the call reports ECHO_ERR_DEVICE; at the default limit the
-    same graph composes bit-exactly again."""
+    """A 10 ns limit: a wait for collective members that outlasts its first clock
+    check gives up at the next one (the pipeline's receives wait far longer), every
+    other wait gives up on seeing the abort bit, every kernel runs to its end and the
+    call reports ECHO_ERR_DEVICE; at the default limit the same graph composes
+    bit-exactly again."""
     g = _gpt64()
     sc = scenarios.draw(130, np.random.default_rng(23), bw_inter=(50_000, 400_000), alpha=(2_000, 20_000),
                         slowdown=(65536, 91750), jitter=(6554, 9))
