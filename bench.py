@@ -110,6 +110,33 @@ def extras_for(args):
     return ex
 
 
+def write_probe(torch, nbytes):
+    """HBM write rate of torch's own fill kernels on an int64 array of nbytes, viewed as
+    rows of 256 values (2 KB, one op's row of 256 scenarios): the whole array, and the
+    array written as four launches of one 512-byte quarter of every row (one 64-scenario
+    tile's segment, the unit the composer's timeline stores write).  Median of 3 runs."""
+    rows = nbytes // 2048
+    a = torch.empty((rows, 4, 64), dtype=torch.int64, device="cuda:0")
+    def timed(fn):
+        ts = []
+        for _ in range(4):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return sorted(ts[1:])[1]
+    whole = timed(lambda: a.fill_(1))
+    def quarters():
+        for t in range(4):
+            a[:, t, :].fill_(t)
+    quarter = timed(quarters)
+    b = rows * 2048
+    return {"write_probe_bytes": b, "whole_ms": round(whole, 3), "whole_TBps": round(b / whole / 1e9, 3),
+            "quarter_rows_ms": round(quarter, 3), "quarter_rows_TBps": round(b / quarter / 1e9, 3)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -138,6 +165,9 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=48, help="scenarios the CPU oracle composes (0 = skip)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device once (calibrates HBM byte counters) and exit")
+    ap.add_argument("--write-probe", type=int, default=0, metavar="GIB",
+                    help="only time HBM writes of a GIB GiB int64 array, whole and as 512-byte quarters of "
+                         "2 KB rows (the timeline rows' pattern), and exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -156,6 +186,9 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": n}), flush=True)
+        return
+    if args.write_probe:
+        print(json.dumps(write_probe(torch, args.write_probe << 30)), flush=True)
         return
 
     import paper_2412_12487_amd as E

@@ -353,6 +353,14 @@ def test_unfit_buffers_rejected_before_launch(E):
             G.compose(d[: 192 * (n - 1)], n, 1)
         with pytest.raises(E.EchoError, match="scenarios is on"):
             G.compose(d.cpu(), n, 1)
+        # the C ABI itself refuses the counts it cannot run (the binding checks them first)
+        step = torch.empty(n, dtype=torch.int64, device=dev)
+        for n_scen, n_refine in ((0, 1), (-1, 1), (n, -1), (n, 65)):
+            rc = E.lib().echo_compose_batch(G.handle, d.data_ptr(), n_scen, n_refine, None, None,
+                                            step.data_ptr(), None, None)
+            assert rc == E.ECHO_ERR_ARG, (n_scen, n_refine, rc)
+        rc = E.lib().echo_compose_batch(G.handle, None, n, 1, None, None, step.data_ptr(), None, None)
+        assert rc == E.ECHO_ERR_ARG
         ref = oracle.run(g, sc, 1, threads=THREADS)
         assert_same(gpu_run(E, g, sc, 1, graph=G), ref)
     finally:
