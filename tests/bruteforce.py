@@ -91,11 +91,18 @@ def compose_validated(g, base, cost, slowdown, n_refine):
 
 
 def covered(g, s, f, v):
-    """Nanoseconds of [s_v, f_v) during which some comm op of v's rank runs, counted
-    one nanosecond at a time (tiny timelines only)."""
+    """Nanoseconds of [s_v, f_v) during which some comm op of v's rank runs: the
+    endpoints of all these intervals cut the time axis into pieces on which coverage is
+    constant; each piece inside [s_v, f_v) that lies inside some comm interval counts
+    whole."""
     comm = [c for c in range(len(g["op_rank"]))
             if g["op_kind"][c] == COMM and g["op_rank"][c] == g["op_rank"][v]]
-    return sum(1 for t in range(int(s[v]), int(f[v])) if any(s[c] <= t < f[c] for c in comm))
+    cuts = sorted({int(s[v]), int(f[v])} | {int(s[c]) for c in comm} | {int(f[c]) for c in comm})
+    total = 0
+    for a, b in zip(cuts, cuts[1:]):
+        if s[v] <= a and b <= f[v] and any(s[c] <= a and b <= f[c] for c in comm):
+            total += b - a
+    return total
 
 
 def forest_predict(forest, x):

@@ -630,8 +630,6 @@ def test_validator_variants_match_brute_force(name, until_stable, prorate):
     sc = _scen(1, alpha=2500)
     sc["slowdown_q16"] = table[None].copy()
     base, cost = _dur_cost(g, sc)
-    if int(max(cost.max(initial=0), base.max(initial=0))) * len(base) > 400_000:
-        pytest.skip("timeline too long for the per-nanosecond count")
     s, f, done = bruteforce.compose_variants(g, base, cost, table, 4, until_stable=until_stable, prorate=prorate)
     r = oracle.run(g, sc, 4, until_stable=until_stable, prorate=prorate)
     np.testing.assert_array_equal(r["start"][0], s)
