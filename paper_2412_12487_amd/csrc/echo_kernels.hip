@@ -202,11 +202,11 @@ __global__ __launch_bounds__(64) void k_cc_cost(CollTable t, const echo_cc_table
 }
 
 // ------------------------------------------------------------------ composer
-// Bounded waits.  A wait polls; every kCheckPolls-th poll it also reads the abort bit
-// and the 100 MHz wall clock, which it first reads at that poll (a clock read on the way
-// into a wait would delay the first polls, and a wait is usually over within a few).
-// It gives up -- and tells every other waiter to give up -- once spin_limit ticks have
-// passed since then.
+// Bounded waits.  A wait polls; every kCheckPollsGlobal-th poll of device memory (every
+// kCheckPollsLocal-th of LDS) it also reads the abort bit and the 100 MHz wall clock, which
+// it first reads at that poll (a clock read on the way into a wait would delay the first
+// polls, and a wait is usually over within a few).  It gives up -- and tells every other
+// waiter to give up -- once spin_limit ticks have passed since then.
 struct WaitClock {
     uint64_t t0 = 0;
     bool started = false;
@@ -263,8 +263,8 @@ __device__ int64_t wait_slots(const int64_t *p, unsigned n, int64_t ns, unsigned
             mx = v[m] > mx ? v[m] : mx;
         }
         if (!__builtin_amdgcn_readfirstlane(__ballot(!all) != 0)) {
-            // every member had launched at the first look: this wave was the last to arrive
-            // and the others wait for it (issue priority as in wait_arrivals)
+            // every member had launched at the first look (poll 0): this wave was the last to
+            // arrive and the others wait for it (issue priority as in wait_arrivals)
             if (poll == 0) __builtin_amdgcn_s_setprio(3);
             return mx;
         }

@@ -104,6 +104,16 @@ def _random_graph(rng, n_ranks, ops_per_rank, n_coll, p_comm=0.3, comm_streams=4
     return b.graph()
 
 
+def test_maximum_refinement_count(E):
+    """R = 64, the largest count the ABI takes: 65 walk passes and 64 overlap detections
+    over one workspace, on a random 12-rank graph with two ragged tiles of scenarios and
+    slowdowns strong enough that the timelines keep moving for several refinements."""
+    g = _random_graph(np.random.default_rng(5), 12, 40, 20)
+    sc = scenarios.draw(70, np.random.default_rng(64), bw_inter=(20000, 90000), alpha=(0, 5000),
+                        ar_algo_random=True, slowdown=(65536, 200000), jitter=(3000, 4))
+    assert_same(gpu_run(E, g, sc, 64), oracle.run(g, sc, 64, threads=THREADS))
+
+
 @pytest.mark.parametrize("seed", range(12))
 def test_random_graphs(E, seed):
     rng = np.random.default_rng(1000 + seed)
