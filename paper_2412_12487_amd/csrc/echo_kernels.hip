@@ -45,26 +45,44 @@ __device__ __forceinline__ int64_t q16(int64_t d, uint32_t f) {
 // Base duration with uniform jitter of amplitude amp (Q16) from the k-th
 // SplitMix64 output of the scenario's seed, k = jstream * 2^36 + v + 1.  The
 // SplitMix64 state seed + k * golden is split into a per-scenario part
-// (jbase = seed + jstream * 2^36 * golden) and a per-op part ((v + 1) * golden,
-// the same for every lane).
-__device__ __forceinline__ uint64_t jitter_base(uint64_t seed, uint32_t jstream) {
-    return seed + ((uint64_t)jstream << 36) * kGolden;
+// (base = seed + jstream * 2^36 * golden) and a per-op part ((v + 1) * golden,
+// the same for every lane).  The factor is f = 65536 - amp + J with J the high word
+// of the output scaled to [0, 2 amp]; the lane's constants 65536 - amp and 2 amp + 1
+// are taken once.
+struct Jitter {
+    uint64_t base;
+    uint32_t f0;      // 65536 - amp
+    uint32_t span;    // 2 amp + 1
+};
+__device__ __forceinline__ Jitter make_jitter(uint64_t seed, uint32_t jstream, int32_t amp) {
+    return Jitter{seed + ((uint64_t)jstream << 36) * kGolden, (uint32_t)(65536 - amp), (uint32_t)(2 * amp + 1)};
 }
-__device__ __forceinline__ int64_t jittered(int64_t d0, int32_t v, uint64_t jbase, int32_t amp) {
+__device__ __forceinline__ uint32_t jitter_factor(int32_t v, const Jitter &jt) {
     // (v + 1) * golden is the same for every lane: two scalar multiplies (kept opaque so the
-    // compiler does not fold them into a vector multiply-add with the lane's jbase)
+    // compiler does not fold them into a vector multiply-add with the lane's base)
     const uint32_t k = (uint32_t)v + 1u;
     uint32_t lo, hi;
     asm("s_mul_i32 %0, %1, %2" : "=s"(lo) : "s"(k), "s"((uint32_t)kGolden));
     asm("s_mul_hi_u32 %0, %1, %2" : "=s"(hi) : "s"(k), "s"((uint32_t)kGolden));
     hi += k * (uint32_t)(kGolden >> 32);
-    const uint64_t u = mix64(jbase + (((uint64_t)hi << 32) | lo));
-    const uint32_t f = (uint32_t)(65536 - amp) + __umulhi((uint32_t)(u >> 32), (uint32_t)(2 * amp + 1));
-    // d0 is the same for every lane: below 2^32 (durations under 4.3 s) one 32 x 32-bit
-    // multiply-add gives the whole product
-    if (__builtin_expect(((uint64_t)d0 >> 32) == 0, 1))
-        return (int64_t)(((uint64_t)(uint32_t)d0 * f + 32768ull) >> 16);
-    return q16(d0, f);
+    const uint64_t u = mix64(jt.base + (((uint64_t)hi << 32) | lo));
+    return jt.f0 + __umulhi((uint32_t)(u >> 32), jt.span);
+}
+// q16(d0, f) for a wave-uniform d0: below 2^32 (durations under 4.3 s) one 32 x 32-bit
+// multiply-add gives the whole product.  The branch is explicit: left to itself the
+// compiler evaluates the general two-multiply form for every d0.
+__device__ __forceinline__ int64_t q16u(int64_t d0, uint32_t f) {
+    const uint32_t dh = (uint32_t)((uint64_t)d0 >> 32);
+    uint64_t p = (uint64_t)(uint32_t)d0 * f + 32768ull;
+    if (__builtin_expect(__builtin_amdgcn_readfirstlane(dh) != 0, 0)) {
+        uint32_t hp;
+        asm volatile("v_mul_lo_u32 %0, %1, %2" : "=v"(hp) : "s"(dh), "v"(f));
+        p += (uint64_t)hp << 32;
+    }
+    return (int64_t)(p >> 16);
+}
+__device__ __forceinline__ int64_t jittered(int64_t d0, int32_t v, const Jitter &jt) {
+    return q16u(d0, jitter_factor(v, jt));
 }
 
 __device__ __forceinline__ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -373,8 +391,8 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
         return;
 
     const echo_scenario *sc = a.scen + sigma;
-    const uint64_t jbase = jitter_base(sc->jitter_seed, sc->jitter_stream);
     const int32_t amp = sc->jitter_amp_q16;
+    const Jitter jt = make_jitter(sc->jitter_seed, sc->jitter_stream, amp);
     // one branch for the whole wavefront: a lane without jitter draws the identity factor
     // (amplitude 0 gives f = 65536 and q16(d, 65536) = d)
     const bool any_jitter = __builtin_amdgcn_readfirstlane(__ballot(amp != 0) != 0);
@@ -529,7 +547,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);             \
                 const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) | \
                                               (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32)); \
-                int64_t d = (JIT) ? jittered(dur, op, jbase, amp) : dur;                         \
+                int64_t d = (JIT) ? jittered(dur, op, jt) : dur;                         \
                 if (REFINED && item_kind(meta) == ECHO_COMPUTE)                                  \
                     d = PRORATE ? d + fst32[j * kLanes + lane]                                   \
                                 : inflate(d, fst[j * kLanes + col], slow, item_class(meta), lane); \
@@ -609,7 +627,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                                                __HIP_MEMORY_SCOPE_AGENT);
                 }
             } else {
-                int64_t d = any_jitter ? jittered(dur, op, jbase, amp) : dur;
+                int64_t d = any_jitter ? jittered(dur, op, jt) : dur;
                 if (REFINED && kind == ECHO_COMPUTE)
                     d = PRORATE ? d + fst32[j * kLanes + lane] : inflate(d, fst[j * kLanes + col], slow, item_class(meta), lane);
                 const int64_t f = ready + d;
@@ -926,8 +944,8 @@ __global__ __launch_bounds__(64 * (FOREST == 2 ? kFxWaves : 1)) void k_overlap(O
     uint32_t *const ebase = a.ext + (int64_t)tile * kLanes;
     const echo_scenario *sc = a.scen + sigma;
     const uint32_t *slow = &sc->slowdown_q16[0][0];
-    const uint64_t jbase = jitter_base(sc->jitter_seed, sc->jitter_stream);
     const int32_t amp = sc->jitter_amp_q16;
+    const Jitter jt = make_jitter(sc->jitter_seed, sc->jitter_stream, amp);
     // one branch for the wavefront: a lane without jitter draws the identity factor
     const bool any_jitter = __builtin_amdgcn_readfirstlane(__ballot(amp != 0) != 0);
     const int64_t *cl_off = a.cl_off + (int64_t)r * kStreams;
@@ -1118,7 +1136,7 @@ __global__ __launch_bounds__(64 * (FOREST == 2 ? kFxWaves : 1)) void k_overlap(O
                                     const int mq = __builtin_amdgcn_readlane(cur.y, j + q);
                                     const int64_t dq = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.w, j + q) << 32) |
                                                                  (uint32_t)__builtin_amdgcn_readlane(cur.z, j + q));
-                                    const int64_t Dq = any_jitter ? jittered(dq, (int32_t)vq, jbase, amp) : dq;
+                                    const int64_t Dq = any_jitter ? jittered(dq, (int32_t)vq, jt) : dq;
                                     if (mo[q] != 0) changed |= q16(Dq, factor_of(mo[q], slow, mq & 7)) != Dq;
                                 }
                             }
@@ -1150,7 +1168,7 @@ __global__ __launch_bounds__(64 * (FOREST == 2 ? kFxWaves : 1)) void k_overlap(O
                         __builtin_amdgcn_s_waitcnt(kWaitVm0);
                     }
                 }
-                const int64_t D = any_jitter ? jittered(d0, (int32_t)v, jbase, amp) : d0;
+                const int64_t D = any_jitter ? jittered(d0, (int32_t)v, jt) : d0;
                 int64_t d = D;                   // the duration v ran with in the previous pass
                 uint32_t m_old = 0, e_old = 0;
                 if (a.prev_refined) {
