@@ -43,6 +43,20 @@ def _load_code(E, g):
         return e.code
 
 
+def test_missing_library_fails_loudly(E, tmp_path):
+    """No fallback: without libecho.so the binding raises instead of computing anything."""
+    from paper_2412_12487_amd import echo as binding
+    saved = (binding.LIB_PATH, binding._lib)
+    try:
+        binding.LIB_PATH, binding._lib = str(tmp_path / "libecho.so"), None
+        with pytest.raises(ImportError, match="missing"):
+            binding.lib()
+        with pytest.raises(ImportError, match="missing"):
+            binding.Graph(configs.graph(1))
+    finally:
+        binding.LIB_PATH, binding._lib = saved
+
+
 def test_library_exports_every_declared_symbol(E):
     header = open(os.path.join(ROOT, "include", "echo.h")).read()
     declared = set(re.findall(r"\b(echo_[a-z_]+)\s*\(", header))
