@@ -847,6 +847,7 @@ struct Workspace {
     int64_t *slots = nullptr;              // [slot][scen] member launch times (slot collectives)
     uint8_t *tmask = nullptr;              // [item + kBlock][mstride] overlap masks (refined passes)
     uint32_t *ext = nullptr;               // same rows: prorated / ensemble extra times
+    uint8_t *xflag = nullptr;              // [row][tile]: the row has a nonzero extra time
     unsigned *chg = nullptr;               // [scen] change flags + 1 stability word (until_stable)
     int64_t *start = nullptr, *finish = nullptr, *step = nullptr;   // timelines (caller's or workspace)
 };
@@ -891,7 +892,10 @@ int ensure_workspace(echo_graph g, const ComposeShape &sh, int32_t n_refine, int
     if (n_refine > 0 && !sh.ext &&
         (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(sh.mrows * sh.mstride), "overlap masks")))
         return rc;
-    if (sh.ext && (rc = ensure(&g->ext, &g->ext_n, (size_t)(sh.mrows * sh.mstride), "extra times"))) return rc;
+    // extra times, then one flag byte per (item row, tile): whether the row has a nonzero one
+    if (sh.ext && (rc = ensure(&g->ext, &g->ext_n,
+                               (size_t)(sh.mrows * sh.mstride + (sh.mrows * sh.n_tiles + 3) / 4), "extra times")))
+        return rc;
     if (sh.until_stable && (rc = ensure(&g->chg, &g->chg_n, (size_t)(ns + 1), "change flags"))) return rc;
     if (!d_start && (rc = ensure(&g->tmp_start, &g->tmp_start_n, (size_t)(g->n_ops * ns), "start"))) return rc;
     if (!d_finish && (rc = ensure(&g->tmp_finish, &g->tmp_finish_n, (size_t)(g->n_ops * ns), "finish")))
@@ -903,6 +907,7 @@ int ensure_workspace(echo_graph g, const ComposeShape &sh, int32_t n_refine, int
     ws->slots = g->slots;
     ws->tmask = n_refine > 0 && !sh.ext ? g->tmask : nullptr;
     ws->ext = sh.ext ? g->ext : nullptr;
+    ws->xflag = sh.ext ? reinterpret_cast<uint8_t *>(g->ext + sh.mrows * sh.mstride) : nullptr;
     ws->chg = sh.until_stable ? g->chg : nullptr;
     ws->start = d_start ? d_start : g->tmp_start;
     ws->finish = d_finish ? d_finish : g->tmp_finish;
@@ -957,6 +962,7 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
             o.finish = ws.finish;
             o.tmask = ext ? nullptr : ws.tmask;
             o.ext = ext ? ws.ext : nullptr;
+            o.xflag = ext ? ws.xflag : nullptr;
             o.cp_pos = g->dg.cp_pos;
             o.mstride = sh.mstride;
             o.chg = until_stable ? ws.chg : nullptr;
@@ -997,6 +1003,7 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
             a.class_cost = ws.class_cost;
             a.tmask = p > 0 && !ext ? ws.tmask : nullptr;
             a.ext = p > 0 && ext ? ws.ext : nullptr;
+            a.xflag = p > 0 && ext ? ws.xflag : nullptr;
             a.mstride = sh.mstride;
             a.stable = p < n_refine ? stable : nullptr;     // the final pass always runs
             a.start = ws.start;

@@ -502,6 +502,38 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
         }                                                                                        \
     }
 
+    // Extra times (prorating refined pass): half a round of rows at a time, loaded straight
+    // from memory into the staging rows (no registers), one half ahead of its use -- the
+    // first half of a round during the previous round's second half, the second half during
+    // its own first half -- so that the wait for a half finds it arrived long ago.  (The
+    // array has a round of rows past the last item.)
+    // Only rows flagged by overlap detection as holding a nonzero extra time are fetched (a
+    // compute item whose row is not flagged adds nothing): `want` has bit q set for item q of
+    // the half.
+    constexpr int kHalf = kBlock / 2;
+    const uint32_t *const erow = a.ext + (int64_t)tile * kLanes + col;
+    auto stage_ext = [&](int64_t row0, int h, uint32_t want) {
+        for (uint32_t m = (want >> h) & ((1u << kHalf) - 1); m; m &= m - 1) {
+            const int q = __builtin_ctz(m);
+            __builtin_amdgcn_global_load_lds(erow + (row0 + q) * a.mstride,
+                                             fstage + (wave * kBlock + h + q) * kLanes, 4, 0, 0);
+        }
+    };
+    // a round's flags of its compute items: lane q < 32 holds item q's flag byte
+    auto round_flags = [&](uint32_t fl, int4 items, int n) -> uint32_t {
+        return (uint32_t)__ballot(lane < n && lane < 32 && fl != 0 && item_kind((uint32_t)items.y) == ECHO_COMPUTE);
+    };
+    auto load_flags = [&](int64_t row0) -> uint32_t {
+        return lane < 32 && row0 + lane < end ? (uint32_t)a.xflag[(row0 + lane) * a.n_tiles + tile] : 0u;
+    };
+    uint32_t fl_now = 0, fl_next = 0;     // this round's and the next round's flag bytes
+    uint32_t want = 0;                    // this round's flagged compute items
+    if (REFINED && PRORATE && beg < end) {
+        fl_now = load_flags(beg);
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        const int n0 = end - beg < kBlock ? int(end - beg) : kBlock;
+        stage_ext(beg, 0, round_flags(fl_now, nxt, n0));
+    }
     for (int64_t blk0 = beg; blk0 < end; blk0 += kBlock) {
         const int4 cur = nxt;
         const int nb = end - blk0 < kBlock ? int(end - blk0) : kBlock;
@@ -513,17 +545,13 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             f4[lane] = mnx0;
             f4[kLanes + lane] = mnx1;
         }
+        // (the wait above settled this round's first half of extra times; its second half
+        // is fetched now, into rows the last round's second half has finished with, and the
+        // next round's flags with it)
         if (REFINED && PRORATE) {
-            // stage this round's extra times, half a round per memory round trip
-            const uint32_t *const erow = a.ext + (int64_t)tile * kLanes + col;
-#pragma unroll
-            for (int h = 0; h < kBlock; h += kBlock / 2) {
-                uint32_t mv[kBlock / 2];
-#pragma unroll
-                for (int j = 0; j < kBlock / 2; ++j) mv[j] = erow[(blk0 + h + j) * a.mstride];
-#pragma unroll
-                for (int j = 0; j < kBlock / 2; ++j) fst32[(h + j) * kLanes + lane] = mv[j];
-            }
+            want = round_flags(fl_now, cur, nb);
+            if (nb > kHalf) stage_ext(blk0 + kHalf, kHalf, want);
+            fl_next = load_flags(blk0 + kBlock);
         }
         nxt = blk0 + kBlock + slotl < end ? items4[2 * (blk0 + kBlock + slotl) + half] : make_int4(0, 0, 0, 0);
         if (REFINED && !PRORATE && blk0 + kBlock < end) {
@@ -534,10 +562,23 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
         const uint64_t fast_bits = __builtin_amdgcn_read_exec() &
                                    __ballot((lane < nb) && (lane < 32) && (cur.y & kFast));
         int j = 0;
+        bool second_half = false;     // extra times: the second half settled
         while (j < nb) {
+            if (REFINED && PRORATE && j == kHalf && !second_half) {
+                // the second half was fetched at the round's start; the next round's first
+                // half goes into the rows the first half has finished with
+                __builtin_amdgcn_s_waitcnt(kWaitVm0);
+                if (blk0 + kBlock < end) {
+                    const int nn = end - blk0 - kBlock < kBlock ? int(end - blk0 - kBlock) : kBlock;
+                    stage_ext(blk0 + kBlock, 0, round_flags(fl_next, nxt, nn));
+                }
+                second_half = true;
+            }
             // a run of fast items: compute/memcpy ops right after the previous op of slot 0
-            // (fast bits exist only below nb, so the run ends there at the latest)
-            const int run_end = j + (int)__builtin_ctzll(~(fast_bits >> j));
+            // (fast bits exist only below nb, so the run ends there at the latest; with extra
+            // times it also stops where the second half begins)
+            int run_end = j + (int)__builtin_ctzll(~(fast_bits >> j));
+            if (REFINED && PRORATE && j < kHalf && run_end > kHalf) run_end = kHalf;
             int64_t s0 = lf0;
 // ALL: the pass stores every start and finish, so the items' own needs are not consulted;
 // JIT: some lane draws jitter (the branch stays out of the loop)
@@ -549,7 +590,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                                               (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32)); \
                 int64_t d = (JIT) ? jittered(dur, op, jt) : dur;                         \
                 if (REFINED && item_kind(meta) == ECHO_COMPUTE)                                  \
-                    d = PRORATE ? d + fst32[j * kLanes + lane]                                   \
+                    d = PRORATE ? d + ((want >> j) & 1u ? fst32[j * kLanes + lane] : 0u)         \
                                 : inflate(d, fst[j * kLanes + col], slow, item_class(meta), lane); \
                 const int64_t f = s0 + d;                                                        \
                 if ((ALL) || (meta & kNeedS)) put(sbase + (int64_t)op * ns + col, s0);           \
@@ -567,6 +608,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             hi_or |= (uint32_t)((uint64_t)s0 >> 32);
             lf0 = s0;
             if (j >= nb) break;
+            if (REFINED && PRORATE && j == kHalf && !second_half) continue;   // settle it first
             const int32_t op = __builtin_amdgcn_readlane(cur.x, j);
             const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);
             const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) |
@@ -629,7 +671,8 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             } else {
                 int64_t d = any_jitter ? jittered(dur, op, jt) : dur;
                 if (REFINED && kind == ECHO_COMPUTE)
-                    d = PRORATE ? d + fst32[j * kLanes + lane] : inflate(d, fst[j * kLanes + col], slow, item_class(meta), lane);
+                    d = PRORATE ? d + ((want >> j) & 1u ? fst32[j * kLanes + lane] : 0u)
+                                : inflate(d, fst[j * kLanes + col], slow, item_class(meta), lane);
                 const int64_t f = ready + d;
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 if ((meta | keep) & kNeedF) put(fbase + (int64_t)op * ns + col, f);
@@ -641,6 +684,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             }
             ++j;
         }
+        fl_now = fl_next;    // loaded at the round's start, settled by the wait at its second half
     }
 #undef MEET
     if (hi_or >> 30) err |= kStatusOverflow;
@@ -1121,8 +1165,11 @@ __global__ __launch_bounds__(64 * (FOREST == 2 ? kFxWaves : 1)) void k_overlap(O
                                 for (int q = 0; q < kOverlapBlock; ++q) eo |= old8[q];
                                 changed |= eo != 0;
                             }
-                            for (int jj = j; jj < je; ++jj)
-                                (ebase + (int64_t)__builtin_amdgcn_readlane(cur_pos, jj) * a.mstride)[col] = 0;
+                            for (int jj = j; jj < je; ++jj) {
+                                const int64_t pj = __builtin_amdgcn_readlane(cur_pos, jj);
+                                (ebase + pj * a.mstride)[col] = 0;
+                                if (lane == 0) a.xflag[pj * a.n_tiles + tile] = 0;
+                            }
                         } else {
                             for (int jj = j; jj < je; ++jj) mstage[jj * kLanes + lane] = 0;
                             if (DETECT && a.prev_refined) {
@@ -1322,6 +1369,12 @@ __global__ __launch_bounds__(64 * (FOREST == 2 ? kFxWaves : 1)) void k_overlap(O
                     }
                     if (DETECT) changed |= e != e_old;
                     (ebase + row())[col] = e;
+                    {
+                        // the row's flag: the walk fetches only rows that hold a nonzero time
+                        const bool any_e = __builtin_amdgcn_readfirstlane(__ballot(e != 0) != 0);
+                        if (lane == 0)
+                            a.xflag[(int64_t)__builtin_amdgcn_readlane(cur_pos, j) * a.n_tiles + tile] = any_e;
+                    }
                 } else {
                     if (DETECT && m != m_old)
                         changed |= (m == 0 ? D : q16(D, factor_of(m, slow, cls))) != d;
