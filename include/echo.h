@@ -392,8 +392,9 @@ int echo_walk_chain(echo_graph g, const int64_t weight_ps[3], int64_t out[4]);
  * (arrivals) + 4 * n_colls * ceil(n_scen / 64) (counts) + 8 * n_slots * n_scen
  * (n_slots: the member ops of collectives of at most eight members that are
  * met in device memory, not in one workgroup) + with n_refine > 0
- * (n_items + 32) * 64 * ceil(n_scen / 64) bytes (masks; n_items = ops + comm
- * ops); a call needing more returns ECHO_ERR_RANGE before enqueuing anything.
+ * (n_items + 32) * 65 * ceil(n_scen / 64) bytes (masks and a flag byte per
+ * row and tile; n_items = ops + comm ops); a call needing more returns
+ * ECHO_ERR_RANGE before enqueuing anything.
  * Every call on one GPU shares that GPU's array: calls whose work overlaps on
  * the device (two streams, two threads, two graphs) race and must be
  * serialised by the caller.  Errors: as echo_compose_batch, plus ARG for a

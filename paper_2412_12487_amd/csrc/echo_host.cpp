@@ -847,7 +847,7 @@ struct Workspace {
     int64_t *slots = nullptr;              // [slot][scen] member launch times (slot collectives)
     uint8_t *tmask = nullptr;              // [item + kBlock][mstride] overlap masks (refined passes)
     uint32_t *ext = nullptr;               // same rows: prorated / ensemble extra times
-    uint8_t *xflag = nullptr;              // [row][tile]: the row has a nonzero extra time
+    uint8_t *xflag = nullptr;              // [row][tile]: the row has a nonzero mask or extra time
     unsigned *chg = nullptr;               // [scen] change flags + 1 stability word (until_stable)
     int64_t *start = nullptr, *finish = nullptr, *step = nullptr;   // timelines (caller's or workspace)
 };
@@ -889,8 +889,9 @@ int ensure_workspace(echo_graph g, const ComposeShape &sh, int32_t n_refine, int
     if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->n_colls * ns), "arrivals"))) return rc;
     if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * sh.n_tiles), "arrival counts"))) return rc;
     if ((rc = ensure(&g->slots, &g->slots_n, (size_t)(g->dg.n_slots * ns), "member slots"))) return rc;
+    // overlap masks, then one flag byte per (item row, tile): whether the row has a nonzero one
     if (n_refine > 0 && !sh.ext &&
-        (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(sh.mrows * sh.mstride), "overlap masks")))
+        (rc = ensure(&g->tmask, &g->tmask_n, (size_t)(sh.mrows * (sh.mstride + sh.n_tiles)), "overlap masks")))
         return rc;
     // extra times, then one flag byte per (item row, tile): whether the row has a nonzero one
     if (sh.ext && (rc = ensure(&g->ext, &g->ext_n,
@@ -907,7 +908,8 @@ int ensure_workspace(echo_graph g, const ComposeShape &sh, int32_t n_refine, int
     ws->slots = g->slots;
     ws->tmask = n_refine > 0 && !sh.ext ? g->tmask : nullptr;
     ws->ext = sh.ext ? g->ext : nullptr;
-    ws->xflag = sh.ext ? reinterpret_cast<uint8_t *>(g->ext + sh.mrows * sh.mstride) : nullptr;
+    ws->xflag = sh.ext ? reinterpret_cast<uint8_t *>(g->ext + sh.mrows * sh.mstride)
+                       : (ws->tmask ? ws->tmask + sh.mrows * sh.mstride : nullptr);
     ws->chg = sh.until_stable ? g->chg : nullptr;
     ws->start = d_start ? d_start : g->tmp_start;
     ws->finish = d_finish ? d_finish : g->tmp_finish;
@@ -962,7 +964,7 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
             o.finish = ws.finish;
             o.tmask = ext ? nullptr : ws.tmask;
             o.ext = ext ? ws.ext : nullptr;
-            o.xflag = ext ? ws.xflag : nullptr;
+            o.xflag = ws.xflag;
             o.cp_pos = g->dg.cp_pos;
             o.mstride = sh.mstride;
             o.chg = until_stable ? ws.chg : nullptr;
@@ -1003,7 +1005,7 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
             a.class_cost = ws.class_cost;
             a.tmask = p > 0 && !ext ? ws.tmask : nullptr;
             a.ext = p > 0 && ext ? ws.ext : nullptr;
-            a.xflag = p > 0 && ext ? ws.xflag : nullptr;
+            a.xflag = p > 0 ? ws.xflag : nullptr;
             a.mstride = sh.mstride;
             a.stable = p < n_refine ? stable : nullptr;     // the final pass always runs
             a.start = ws.start;
@@ -1206,7 +1208,7 @@ int echo_compose_batch_static(echo_graph g, const echo_scenario *d_scen, int32_t
             g->dg.classes.n * sh.ns * (int64_t)sizeof(int64_t),              // class costs
             g->n_colls * sh.ns * (int64_t)sizeof(unsigned long long),       // arrival maxima
             g->n_colls * sh.n_tiles * (int64_t)sizeof(unsigned),             // arrival counts
-            n_refine > 0 ? sh.mrows * sh.mstride : 0,                         // overlap masks
+            n_refine > 0 ? sh.mrows * (sh.mstride + sh.n_tiles) : 0,         // overlap masks and row flags
             g->dg.n_slots * sh.ns * (int64_t)sizeof(int64_t),               // member slots
         };
         int64_t offs[5], total = 0;
@@ -1231,6 +1233,7 @@ int echo_compose_batch_static(echo_graph g, const echo_scenario *d_scen, int32_t
         ws.arrive = reinterpret_cast<unsigned long long *>(base + offs[1]);
         ws.count = reinterpret_cast<unsigned *>(base + offs[2]);
         ws.tmask = n_refine > 0 ? base + offs[3] : nullptr;
+        ws.xflag = n_refine > 0 ? base + offs[3] + sh.mrows * sh.mstride : nullptr;
         ws.slots = reinterpret_cast<int64_t *>(base + offs[4]);
         ws.start = d_start;
         ws.finish = d_finish;

@@ -217,7 +217,7 @@ struct WalkArgs {
     // not compute ops unused), mstride columns (the tiles' scenarios, padded to whole tiles):
     const uint8_t *tmask;            // overlap type masks, or null (pass 1)
     const uint32_t *ext;             // extra times (prorating, ensemble factors), or null
-    const uint8_t *xflag;            // with ext: [item row][tile] nonzero when some extra time of the row is
+    const uint8_t *xflag;            // [item row][tile]: nonzero when some mask (extra time) of the row is
     int64_t mstride;
     const unsigned *stable;          // non-null: skip the pass when *stable (every scenario at its fixed point)
     int64_t *start, *finish;         // [op][scen]
@@ -246,7 +246,7 @@ struct OverlapArgs {
     // rows of the walk items (cp_pos), mstride columns, as the walk reads them
     uint8_t *tmask;                  // in: masks of the previous pass (if it was refined), out: new ones
     uint32_t *ext;                   // prorating: in/out like tmask, the extra time q16(o, F) - o
-    uint8_t *xflag;                  // with ext: out, [item row][tile] nonzero when some extra time of the row is
+    uint8_t *xflag;                  // out, [item row][tile]: nonzero when some mask (extra time) of the row is
     const int32_t *cp_pos;
     int64_t mstride;
     unsigned *chg;                   // non-null: [scen] set when some duration changes

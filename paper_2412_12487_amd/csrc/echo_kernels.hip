@@ -439,18 +439,6 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     const int half = lane >> 5, slotl = lane & 31;
     // lanes past the end of the list hold op 0
     int4 nxt = beg + slotl < end ? items4[2 * (beg + slotl) + half] : make_int4(0, 0, 0, 0);
-    // Overlap masks of a round: its kBlock rows of the mask array (row = item), 64 bytes of
-    // this tile each.  Lane l fetches 16 bytes, row l / 4 (+16 in the second half), quarter
-    // l % 4 -- laid down in LDS as they come, that is the [item][lane] staging order.  The
-    // next round's masks are fetched while this round runs.  (The array has kBlock rows
-    // past the last item, for the last round's fetch.)
-    const uint4 *const mrow = reinterpret_cast<const uint4 *>(a.tmask + (int64_t)tile * kLanes) + (lane & 3);
-    const int64_t mst4 = a.mstride / 16;
-    uint4 mnx0 = make_uint4(0, 0, 0, 0), mnx1 = mnx0;
-    if (REFINED && !PRORATE) {
-        mnx0 = mrow[(beg + (lane >> 2)) * mst4];
-        mnx1 = mrow[(beg + 16 + (lane >> 2)) * mst4];
-    }
 
 // Finish f_ of comm op v_ (collective c_, aux word x_): its barrier -- the
 // latest member launch -- plus the collective's cost; written to the finish array.
@@ -502,21 +490,29 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
         }                                                                                        \
     }
 
-    // Extra times (prorating refined pass): half a round of rows at a time, loaded straight
-    // from memory into the staging rows (no registers), one half ahead of its use -- the
-    // first half of a round during the previous round's second half, the second half during
-    // its own first half -- so that the wait for a half finds it arrived long ago.  (The
-    // array has a round of rows past the last item.)
-    // Only rows flagged by overlap detection as holding a nonzero extra time are fetched (a
-    // compute item whose row is not flagged adds nothing): `want` has bit q set for item q of
-    // the half.
+    // The refined passes' per-item inputs (overlap masks, one byte per scenario, or extra
+    // times, four bytes), one row per walk item with this tile's 64 columns, staged in LDS
+    // in [item][lane] order: half a round of rows at a time, loaded straight from memory into
+    // LDS (no registers), one half ahead of its use -- the first half of a round during the
+    // previous round's second half, the second half during its own first half -- so that
+    // the wait for a half finds it arrived long ago.  (The arrays have a round of rows past
+    // the last item.)  Only rows that overlap detection flagged as holding a nonzero value
+    // are fetched (an unflagged compute item is not inflated): `want` has bit q set for
+    // item q of the round.
     constexpr int kHalf = kBlock / 2;
     const uint32_t *const erow = a.ext + (int64_t)tile * kLanes + col;
-    auto stage_ext = [&](int64_t row0, int h, uint32_t want) {
+    const uint32_t *const mrow = reinterpret_cast<const uint32_t *>(a.tmask + (int64_t)tile * kLanes) + lane;
+    auto stage_rows = [&](int64_t row0, int h, uint32_t want) {
         for (uint32_t m = (want >> h) & ((1u << kHalf) - 1); m; m &= m - 1) {
             const int q = __builtin_ctz(m);
-            __builtin_amdgcn_global_load_lds(erow + (row0 + q) * a.mstride,
-                                             fstage + (wave * kBlock + h + q) * kLanes, 4, 0, 0);
+            if (PRORATE) {
+                __builtin_amdgcn_global_load_lds(erow + (row0 + q) * a.mstride,
+                                                 fstage + (wave * kBlock + h + q) * kLanes, 4, 0, 0);
+            } else if (lane < kLanes / 4) {
+                // a mask row is 64 bytes: sixteen lanes load four each
+                __builtin_amdgcn_global_load_lds(mrow + (row0 + q) * (a.mstride / 4),
+                                                 fstage + (wave * kBlock + h + q) * (kLanes / 4), 4, 0, 0);
+            }
         }
     };
     // a round's flags of its compute items: lane q < 32 holds item q's flag byte
@@ -528,49 +524,40 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     };
     uint32_t fl_now = 0, fl_next = 0;     // this round's and the next round's flag bytes
     uint32_t want = 0;                    // this round's flagged compute items
-    if (REFINED && PRORATE && beg < end) {
+    if (REFINED && beg < end) {
         fl_now = load_flags(beg);
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
         const int n0 = end - beg < kBlock ? int(end - beg) : kBlock;
-        stage_ext(beg, 0, round_flags(fl_now, nxt, n0));
+        stage_rows(beg, 0, round_flags(fl_now, nxt, n0));
     }
     for (int64_t blk0 = beg; blk0 < end; blk0 += kBlock) {
         const int4 cur = nxt;
         const int nb = end - blk0 < kBlock ? int(end - blk0) : kBlock;
-        // This round's items and masks (fetched during the last round) are settled first: a
-        // wait at their first use would also wait for the fetches issued below.
+        // This round's items and its first half of staged rows (fetched during the last
+        // round) are settled first: a wait at their first use would also wait for the
+        // fetches issued below.
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
-        if (REFINED && !PRORATE) {
-            uint4 *const f4 = reinterpret_cast<uint4 *>(fst);
-            f4[lane] = mnx0;
-            f4[kLanes + lane] = mnx1;
-        }
-        // (the wait above settled this round's first half of extra times; its second half
-        // is fetched now, into rows the last round's second half has finished with, and the
-        // next round's flags with it)
-        if (REFINED && PRORATE) {
+        // the round's second half of rows is fetched now, into rows the last round's second
+        // half has finished with, and the next round's flags with it
+        if (REFINED) {
             want = round_flags(fl_now, cur, nb);
-            if (nb > kHalf) stage_ext(blk0 + kHalf, kHalf, want);
+            if (nb > kHalf) stage_rows(blk0 + kHalf, kHalf, want);
             fl_next = load_flags(blk0 + kBlock);
         }
         nxt = blk0 + kBlock + slotl < end ? items4[2 * (blk0 + kBlock + slotl) + half] : make_int4(0, 0, 0, 0);
-        if (REFINED && !PRORATE && blk0 + kBlock < end) {
-            mnx0 = mrow[(blk0 + kBlock + (lane >> 2)) * mst4];
-            mnx1 = mrow[(blk0 + kBlock + 16 + (lane >> 2)) * mst4];
-        }
         // fast flags of the round, one bit per item
         const uint64_t fast_bits = __builtin_amdgcn_read_exec() &
                                    __ballot((lane < nb) && (lane < 32) && (cur.y & kFast));
         int j = 0;
-        bool second_half = false;     // extra times: the second half settled
+        bool second_half = false;     // the round's second half of staged rows settled
         while (j < nb) {
-            if (REFINED && PRORATE && j == kHalf && !second_half) {
+            if (REFINED && j == kHalf && !second_half) {
                 // the second half was fetched at the round's start; the next round's first
                 // half goes into the rows the first half has finished with
                 __builtin_amdgcn_s_waitcnt(kWaitVm0);
                 if (blk0 + kBlock < end) {
                     const int nn = end - blk0 - kBlock < kBlock ? int(end - blk0 - kBlock) : kBlock;
-                    stage_ext(blk0 + kBlock, 0, round_flags(fl_next, nxt, nn));
+                    stage_rows(blk0 + kBlock, 0, round_flags(fl_next, nxt, nn));
                 }
                 second_half = true;
             }
@@ -578,7 +565,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             // (fast bits exist only below nb, so the run ends there at the latest; with extra
             // times it also stops where the second half begins)
             int run_end = j + (int)__builtin_ctzll(~(fast_bits >> j));
-            if (REFINED && PRORATE && j < kHalf && run_end > kHalf) run_end = kHalf;
+            if (REFINED && j < kHalf && run_end > kHalf) run_end = kHalf;
             int64_t s0 = lf0;
 // ALL: the pass stores every start and finish, so the items' own needs are not consulted;
 // JIT: some lane draws jitter (the branch stays out of the loop)
@@ -591,7 +578,8 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 int64_t d = (JIT) ? jittered(dur, op, jt) : dur;                         \
                 if (REFINED && item_kind(meta) == ECHO_COMPUTE)                                  \
                     d = PRORATE ? d + ((want >> j) & 1u ? fst32[j * kLanes + lane] : 0u)         \
-                                : inflate(d, fst[j * kLanes + col], slow, item_class(meta), lane); \
+                                : inflate(d, (want >> j) & 1u ? fst[j * kLanes + col] : 0u, slow,  \
+                                          item_class(meta), lane);                               \
                 const int64_t f = s0 + d;                                                        \
                 if ((ALL) || (meta & kNeedS)) put(sbase + (int64_t)op * ns + col, s0);           \
                 if ((ALL) || (meta & kNeedF)) put(fbase + (int64_t)op * ns + col, f);            \
@@ -608,7 +596,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             hi_or |= (uint32_t)((uint64_t)s0 >> 32);
             lf0 = s0;
             if (j >= nb) break;
-            if (REFINED && PRORATE && j == kHalf && !second_half) continue;   // settle it first
+            if (REFINED && j == kHalf && !second_half) continue;   // settle it first
             const int32_t op = __builtin_amdgcn_readlane(cur.x, j);
             const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);
             const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) |
@@ -672,7 +660,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 int64_t d = any_jitter ? jittered(dur, op, jt) : dur;
                 if (REFINED && kind == ECHO_COMPUTE)
                     d = PRORATE ? d + ((want >> j) & 1u ? fst32[j * kLanes + lane] : 0u)
-                                : inflate(d, fst[j * kLanes + col], slow, item_class(meta), lane);
+                                : inflate(d, (want >> j) & 1u ? fst[j * kLanes + col] : 0u, slow, item_class(meta), lane);
                 const int64_t f = ready + d;
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 if ((meta | keep) & kNeedF) put(fbase + (int64_t)op * ns + col, f);
@@ -1382,11 +1370,18 @@ __global__ __launch_bounds__(64 * (FOREST == 2 ? kFxWaves : 1)) void k_overlap(O
                 }
             }
             if (!EXT && lane < nr) {
-                // lane L writes the 64 masks of the round's op L to that op's row
+                // lane L writes the 64 masks of the round's op L to that op's row, and the
+                // row's flag: whether any of them is nonzero (the walk fetches only those rows)
                 const uint4 *const src = reinterpret_cast<const uint4 *>(mstage + lane * kLanes);
                 uint4 *const dst = reinterpret_cast<uint4 *>(obase + (int64_t)cur_pos * a.mstride);
+                uint32_t any = 0;
 #pragma unroll
-                for (int q = 0; q < kLanes / 16; ++q) dst[q] = src[q];
+                for (int q = 0; q < kLanes / 16; ++q) {
+                    const uint4 v = src[q];
+                    dst[q] = v;
+                    any |= v.x | v.y | v.z | v.w;
+                }
+                a.xflag[(int64_t)cur_pos * a.n_tiles + tile] = any != 0;
             }
         }
     }
