@@ -946,6 +946,10 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
         return hip_fail(e, "fill kernel");
     if (d_refinements && (e = launch_fill_i32(d_refinements, ns, until_stable ? 0 : n_refine, stream)))
         return hip_fail(e, "fill kernel");
+    // extra-time row flags start clear; overlap detection only sets them
+    if (ext && n_refine > 0 &&
+        (e = launch_fill_i32(reinterpret_cast<int32_t *>(ws.xflag), (sh.mrows * sh.n_tiles + 3) / 4, 0, stream)))
+        return hip_fail(e, "fill kernel");
 
     for (int32_t p = 0; p <= n_refine; ++p) {
         // tiles per walk launch: every rank block of a tile must be co-resident

@@ -1153,11 +1153,8 @@ __global__ __launch_bounds__(64 * (FOREST == 2 ? kFxWaves : 1)) void k_overlap(O
                                 for (int q = 0; q < kOverlapBlock; ++q) eo |= old8[q];
                                 changed |= eo != 0;
                             }
-                            for (int jj = j; jj < je; ++jj) {
-                                const int64_t pj = __builtin_amdgcn_readlane(cur_pos, jj);
-                                (ebase + pj * a.mstride)[col] = 0;
-                                if (lane == 0) a.xflag[pj * a.n_tiles + tile] = 0;
-                            }
+                            for (int jj = j; jj < je; ++jj)
+                                (ebase + (int64_t)__builtin_amdgcn_readlane(cur_pos, jj) * a.mstride)[col] = 0;
                         } else {
                             for (int jj = j; jj < je; ++jj) mstage[jj * kLanes + lane] = 0;
                             if (DETECT && a.prev_refined) {
@@ -1357,12 +1354,11 @@ __global__ __launch_bounds__(64 * (FOREST == 2 ? kFxWaves : 1)) void k_overlap(O
                     }
                     if (DETECT) changed |= e != e_old;
                     (ebase + row())[col] = e;
-                    {
-                        // the row's flag: the walk fetches only rows that hold a nonzero time
-                        const bool any_e = __builtin_amdgcn_readfirstlane(__ballot(e != 0) != 0);
-                        if (lane == 0)
-                            a.xflag[(int64_t)__builtin_amdgcn_readlane(cur_pos, j) * a.n_tiles + tile] = any_e;
-                    }
+                    // flag the row (the walk fetches only flagged rows); flags are cleared once
+                    // per compose and only ever set, so a row flagged by an earlier refinement
+                    // whose extra times are zero now is fetched and adds zero
+                    if (__builtin_amdgcn_readfirstlane(__ballot(e != 0) != 0) && lane == 0)
+                        a.xflag[(int64_t)__builtin_amdgcn_readlane(cur_pos, j) * a.n_tiles + tile] = 1;
                 } else {
                     if (DETECT && m != m_old)
                         changed |= (m == 0 ? D : q16(D, factor_of(m, slow, cls))) != d;
