@@ -499,6 +499,19 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     // the last item.)  Only rows that overlap detection flagged as holding a nonzero value
     // are fetched (an unflagged compute item is not inflated): `want` has bit q set for
     // item q of the round.
+    // The final pass is bound by its timeline stores, where the bytes of every row count; the
+    // masks of a refined pass that is not the final one are instead fetched whole, a round
+    // ahead in registers (lane l: 16 bytes, row l / 4, +16 in the second half, quarter
+    // l % 4), because that pass is bound by its chain of items, where a second wait in the
+    // middle of a round costs more than the bytes.
+    constexpr bool kFlagged = REFINED && (PRORATE || FINAL);
+    const uint4 *const mrow4 = reinterpret_cast<const uint4 *>(a.tmask + (int64_t)tile * kLanes) + (lane & 3);
+    const int64_t mst4 = a.mstride / 16;
+    uint4 mnx0 = make_uint4(0, 0, 0, 0), mnx1 = mnx0;
+    if (REFINED && !kFlagged) {
+        mnx0 = mrow4[(beg + (lane >> 2)) * mst4];
+        mnx1 = mrow4[(beg + 16 + (lane >> 2)) * mst4];
+    }
     constexpr int kHalf = kBlock / 2;
     const uint32_t *const erow = a.ext + (int64_t)tile * kLanes + col;
     const uint32_t *const mrow = reinterpret_cast<const uint32_t *>(a.tmask + (int64_t)tile * kLanes) + lane;
@@ -524,7 +537,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     };
     uint32_t fl_now = 0, fl_next = 0;     // this round's and the next round's flag bytes
     uint32_t want = 0;                    // this round's flagged compute items
-    if (REFINED && beg < end) {
+    if (kFlagged && beg < end) {
         fl_now = load_flags(beg);
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
         const int n0 = end - beg < kBlock ? int(end - beg) : kBlock;
@@ -537,21 +550,31 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
         // round) are settled first: a wait at their first use would also wait for the
         // fetches issued below.
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        if (REFINED && !kFlagged) {
+            uint4 *const f4 = reinterpret_cast<uint4 *>(fst);
+            f4[lane] = mnx0;
+            f4[kLanes + lane] = mnx1;
+        }
         // the round's second half of rows is fetched now, into rows the last round's second
         // half has finished with, and the next round's flags with it
-        if (REFINED) {
+        if (kFlagged) {
             want = round_flags(fl_now, cur, nb);
             if (nb > kHalf) stage_rows(blk0 + kHalf, kHalf, want);
             fl_next = load_flags(blk0 + kBlock);
         }
         nxt = blk0 + kBlock + slotl < end ? items4[2 * (blk0 + kBlock + slotl) + half] : make_int4(0, 0, 0, 0);
+        if (REFINED && !kFlagged && blk0 + kBlock < end) {
+            mnx0 = mrow4[(blk0 + kBlock + (lane >> 2)) * mst4];
+            mnx1 = mrow4[(blk0 + kBlock + 16 + (lane >> 2)) * mst4];
+        }
+        if (REFINED && !kFlagged) want = ~0u;     // every row staged
         // fast flags of the round, one bit per item
         const uint64_t fast_bits = __builtin_amdgcn_read_exec() &
                                    __ballot((lane < nb) && (lane < 32) && (cur.y & kFast));
         int j = 0;
         bool second_half = false;     // the round's second half of staged rows settled
         while (j < nb) {
-            if (REFINED && j == kHalf && !second_half) {
+            if (kFlagged && j == kHalf && !second_half) {
                 // the second half was fetched at the round's start; the next round's first
                 // half goes into the rows the first half has finished with
                 __builtin_amdgcn_s_waitcnt(kWaitVm0);
@@ -565,7 +588,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             // (fast bits exist only below nb, so the run ends there at the latest; with extra
             // times it also stops where the second half begins)
             int run_end = j + (int)__builtin_ctzll(~(fast_bits >> j));
-            if (REFINED && j < kHalf && run_end > kHalf) run_end = kHalf;
+            if (kFlagged && j < kHalf && run_end > kHalf) run_end = kHalf;
             int64_t s0 = lf0;
 // ALL: the pass stores every start and finish, so the items' own needs are not consulted;
 // JIT: some lane draws jitter (the branch stays out of the loop)
@@ -596,7 +619,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
             hi_or |= (uint32_t)((uint64_t)s0 >> 32);
             lf0 = s0;
             if (j >= nb) break;
-            if (REFINED && j == kHalf && !second_half) continue;   // settle it first
+            if (kFlagged && j == kHalf && !second_half) continue;   // settle it first
             const int32_t op = __builtin_amdgcn_readlane(cur.x, j);
             const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);
             const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) |
