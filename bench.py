@@ -274,9 +274,18 @@ def cc_variant(sc, args):
     return sc
 
 
-def walk_kernel_name(refined, final, digest, prorate):
+# A final mask pass over at least this many 64-scenario tiles runs the walk variant that
+# fetches only flagged mask rows (the library's kFlagRowTiles).
+FLAG_ROW_TILES = 4
+
+
+def walk_kernel_name(refined, final, digest, ext, n_tiles):
+    """The walk kernel a pass launches, as rocprofv3 names it: k_walk<input, final, digest>
+    with input 0 = none (first pass), 1 = whole mask rows, 2 = flagged mask rows (a final
+    pass over FLAG_ROW_TILES or more tiles), 3 = flagged extra-time rows."""
     b = lambda x: "true" if x else "false"
-    return f"k_walk<{b(refined)}, {b(final)}, {b(digest)}, {b(refined and prorate)}>"
+    inp = 0 if not refined else 3 if ext else 2 if final and n_tiles >= FLAG_ROW_TILES else 1
+    return f"k_walk<{inp}, {b(final)}, {b(digest)}>"
 
 
 def time_compose(E, g, sc, args, extras, latency=None):
@@ -335,7 +344,7 @@ def _time_compose(E, G, sc, args, extras, latency, load_s):
            "kernels_ms": {k: round(float(np.mean(v)), 4) for k, v in kernels.items()},
            # the last step's walk launches, pass by pass (a split pass lists each launch)
            "walk_pass_ms": [[round(ms, 4) for ms in p] for p in pass_runs[-1] if p] if pass_runs else []}
-    res.update(pass_summary(pass_runs, args.prorate or args.forest))
+    res.update(pass_summary(pass_runs, args.prorate or args.forest, (n_scen + 63) // 64))
     if latency is not None:
         n_pass = max(res["pass_index"]) + 1 if res["pass_index"] else 1
         res["floors"] = [walk_floor(G, latency, k, n_pass) for k in res["pass_index"]]
@@ -356,7 +365,7 @@ def _time_compose(E, G, sc, args, extras, latency, load_s):
     return res
 
 
-def pass_summary(pass_runs, ext):
+def pass_summary(pass_runs, ext, n_tiles):
     """Walk passes of the timed steps: mean time per pass (a pass split over several
     launches counts all of them), launches per pass and the kernel variant; passes that
     returned at once (every scenario already at its fixed point) are left out."""
@@ -365,7 +374,7 @@ def pass_summary(pass_runs, ext):
     launches = [max(len(p[k]) for p in pass_runs if k < len(p)) for k in range(n_pass)]
     top = max(pass_ms, default=0.0)
     ran = [k for k in range(n_pass) if pass_ms[k] > 0.02 * top]
-    names = [walk_kernel_name(k > 0, k == n_pass - 1, False, ext) for k in range(n_pass)]
+    names = [walk_kernel_name(k > 0, k == n_pass - 1, False, ext, n_tiles) for k in range(n_pass)]
     return {"pass_ms": [pass_ms[k] for k in ran], "pass_launches": [launches[k] for k in ran],
             "pass_kernels": [names[k] for k in ran], "pass_index": ran}
 
@@ -556,7 +565,7 @@ def batch_mode(args, E, configs):
     rows = []
     for j, x in enumerate(graphs):
         runs = [walk_passes(kt) for kt in per_graph[j]]
-        ps = pass_summary(runs, False)
+        ps = pass_summary(runs, False, (x["n"] + 63) // 64)
         compose_ms = float(np.mean([sum(ms for _, ms in kt) for kt in per_graph[j]]))
         final = ps["pass_index"][-1] if ps["pass_index"] else 0
         fms = ps["pass_ms"][-1] if ps["pass_ms"] else 0.0

@@ -953,7 +953,13 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
 
     for (int32_t p = 0; p <= n_refine; ++p) {
         // tiles per walk launch: every rank block of a tile must be co-resident
-        const int64_t cap = g->capacity[walk_variant(p > 0, p == n_refine, d_digest != nullptr, ext)];
+        // a final pass over at least kFlagRowTiles tiles writes enough timelines to be bound by
+        // HBM and fetches only the flagged mask rows; with fewer it is bound by its chain of
+        // items and fetches whole rows (measured: 256 scenarios, four tiles, on the 1024-rank
+        // graph gain 1.3 ms; one-tile 32-scenario graphs lose 0.5-2 ms)
+        const bool flag_rows = p == n_refine && n_tiles >= kFlagRowTiles;
+        const int64_t cap = g->capacity[walk_variant(walk_input(p > 0, ext, flag_rows), p == n_refine,
+                                                     d_digest != nullptr)];
         int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, cap / g->dg.n_blocks));
         if (g->max_launch_tiles > 0) per_launch = std::min<int64_t>(per_launch, g->max_launch_tiles);
         if (p > 0) {
@@ -1028,6 +1034,7 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
             a.n_walkers = g->n_walkers;
             a.final_pass = p == n_refine;
             a.store_all = p == n_refine && store_all;
+            a.flag_rows = flag_rows;
             if (g->n_ranks == 0 || g->n_ops == 0) continue;
             TIMED(ECHO_K_WALK, launch_walk(a, g->dg.n_blocks, stream), "walk kernel");
         }

@@ -78,6 +78,7 @@ constexpr int kResolve = 3;
 // looked up per cost class -- the (type, S, N, M, K) tuple that fixes T(c, s)
 // for a scenario -- and a block stages its most used classes in LDS.
 constexpr int kBlockWalkers = 8;
+constexpr int kFlagRowTiles = 4;    // final mask passes over this many tiles fetch only flagged rows
 constexpr int kBlock = 32;          // walk items fetched (and overlap masks staged) per round
 constexpr int kChannels = 8;          // LDS barrier channels per block
 constexpr int kClassSlots = 8;        // LDS cost classes per block
@@ -233,6 +234,7 @@ struct WalkArgs {
     int32_t n_walkers;
     int32_t final_pass;              // accumulate step time (and digest)
     int32_t store_all;               // store every start and finish (else only kNeedS / kNeedF)
+    int32_t flag_rows;               // final mask pass: the variant that fetches only flagged rows (kInMaskFlags)
 };
 
 
@@ -289,12 +291,20 @@ hipError_t launch_settle(unsigned *chg, int32_t n_scen, int32_t *refinements, un
                          hipStream_t stream);
 // Fill n int32 with v (a kernel, so the sequence stays capturable).
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream);
+// Per-item input of a walk pass, the walk kernel's first template argument.
+constexpr int kInNone = 0;        // first pass: base durations only
+constexpr int kInMasks = 1;       // overlap masks, every row, fetched a round ahead into registers
+constexpr int kInMaskFlags = 2;   // overlap masks, only flagged rows, staged in LDS (final passes)
+constexpr int kInExtFlags = 3;    // prorated extra times, only flagged rows, staged in LDS
+inline int walk_input(bool refined, bool prorate, bool flag_rows) {
+    return !refined ? kInNone : prorate ? kInExtFlags : flag_rows ? kInMaskFlags : kInMasks;
+}
 // Co-resident walk workgroups (kBlockWalkers wavefronts each) the device can hold,
-// for each kernel variant (bit 0 refined, bit 1 final, bit 2 digest, bit 3 prorated).
+// for each kernel variant (bits 0-1 input, bit 2 final, bit 3 digest).
 constexpr int kWalkVariants = 16;
 hipError_t walk_capacity(int device, int64_t workgroups[kWalkVariants]);
-inline int walk_variant(bool refined, bool final_pass, bool digest, bool prorate) {
-    return (refined ? 1 : 0) | (final_pass ? 2 : 0) | (digest ? 4 : 0) | (refined && prorate ? 8 : 0);
+inline int walk_variant(int in, bool final_pass, bool digest) {
+    return in | (final_pass ? 4 : 0) | (digest ? 8 : 0);
 }
 // Device address of this GPU's fixed workspace array (ECHO_SCRATCH_BYTES) for
 // echo_compose_batch_static; `device` must be current.  Looked up once per device.

@@ -340,9 +340,13 @@ __device__ bool wait_local(const unsigned *cnt, unsigned need, unsigned *status,
 // one 64-scenario tile; wavefront w walks walker block * kBlockWalkers + w.  REFINED:
 // the pass inflates compute ops by the factors of the previous pass's
 // overlaps.  FINAL: the pass produces the step time (and DIGEST: the digest).
-// PRORATE (with REFINED): compute ops take their prorated extra time instead.
-template <bool REFINED, bool FINAL, bool DIGEST, bool PRORATE>
+// IN (kIn*): the pass's per-item input -- none (the first pass), overlap masks (REFINED)
+// or prorated extra times (PRORATE), and whether only flagged rows are fetched.
+template <int IN, bool FINAL, bool DIGEST>
 __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
+    constexpr bool REFINED = IN != kInNone;
+    constexpr bool PRORATE = IN == kInExtFlags;
+    constexpr bool kFlagged = IN == kInMaskFlags || IN == kInExtFlags;
     // staged per item and lane: overlap masks (one byte) or, prorating, extra times (32 bits)
     __shared__ __align__(16) uint32_t fstage[REFINED ? kBlockWalkers * kBlock * kLanes / (PRORATE ? 1 : 4) : 1];
     __shared__ unsigned long long lbar[kChannels][2][kLanes];   // per channel and slot: latest launch per lane
@@ -499,12 +503,12 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     // the last item.)  Only rows that overlap detection flagged as holding a nonzero value
     // are fetched (an unflagged compute item is not inflated): `want` has bit q set for
     // item q of the round.
-    // The final pass is bound by its timeline stores, where the bytes of every row count; the
-    // masks of a refined pass that is not the final one are instead fetched whole, a round
-    // ahead in registers (lane l: 16 bytes, row l / 4, +16 in the second half, quarter
-    // l % 4), because that pass is bound by its chain of items, where a second wait in the
-    // middle of a round costs more than the bytes.
-    constexpr bool kFlagged = REFINED && (PRORATE || FINAL);
+    // Where the pass is bound by HBM -- a final pass over many scenario tiles, whose timeline
+    // stores fill the memory system -- the bytes of every row count; the masks of a pass bound
+    // by its chain of items (not the final one, or few tiles) are instead fetched whole, a
+    // round ahead in registers (lane l: 16 bytes, row l / 4, +16 in the second half, quarter
+    // l % 4), because there a second wait in the middle of a round costs more than the bytes.
+    // Extra times are always fetched by flag.
     const uint4 *const mrow4 = reinterpret_cast<const uint4 *>(a.tmask + (int64_t)tile * kLanes) + (lane & 3);
     const int64_t mst4 = a.mstride / 16;
     uint4 mnx0 = make_uint4(0, 0, 0, 0), mnx1 = mnx0;
@@ -715,14 +719,18 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
 }
 
 using WalkKernel = void (*)(WalkArgs);
-WalkKernel walk_kernel(bool refined, bool final_pass, bool digest, bool prorate) {
-    if (refined && prorate) {
-        if (!final_pass) return k_walk<true, false, false, true>;
-        return digest ? k_walk<true, true, true, true> : k_walk<true, true, false, true>;
+WalkKernel walk_kernel(int in, bool final_pass, bool digest) {
+    // flagged mask rows only in a final pass, a digest only in a final pass
+    if (!final_pass) {
+        if (in == kInNone) return k_walk<kInNone, false, false>;
+        return in == kInExtFlags ? k_walk<kInExtFlags, false, false> : k_walk<kInMasks, false, false>;
     }
-    if (!final_pass) return refined ? k_walk<true, false, false, false> : k_walk<false, false, false, false>;
-    if (digest) return refined ? k_walk<true, true, true, false> : k_walk<false, true, true, false>;
-    return refined ? k_walk<true, true, false, false> : k_walk<false, true, false, false>;
+    switch (in) {
+    case kInNone: return digest ? k_walk<kInNone, true, true> : k_walk<kInNone, true, false>;
+    case kInMasks: return digest ? k_walk<kInMasks, true, true> : k_walk<kInMasks, true, false>;
+    case kInMaskFlags: return digest ? k_walk<kInMaskFlags, true, true> : k_walk<kInMaskFlags, true, false>;
+    default: return digest ? k_walk<kInExtFlags, true, true> : k_walk<kInExtFlags, true, false>;
+    }
 }
 
 // ------------------------------------------------------------------ overlap detection
@@ -1470,8 +1478,9 @@ hipError_t launch_cc_cost(const CollTable &t, const echo_cc_table *tables, const
 hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream) {
     WalkArgs args = a;
     void *params[] = {&args};
-    const WalkKernel k = walk_kernel(a.tmask != nullptr || a.ext != nullptr, a.final_pass != 0,
-                                     a.digest != nullptr, a.ext != nullptr);
+    const WalkKernel k = walk_kernel(walk_input(a.tmask != nullptr || a.ext != nullptr, a.ext != nullptr,
+                                                a.flag_rows != 0),
+                                     a.final_pass != 0, a.digest != nullptr);
     return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k), dim3((unsigned)(n_blocks * a.tiles)),
                                       dim3(kBlockWalkers * kLanes), params, 0, stream);
 }
@@ -1555,7 +1564,7 @@ hipError_t walk_capacity(int device, int64_t workgroups[kWalkVariants]) {
     if (e != hipSuccess) return e;
     for (int v = 0; v < kWalkVariants; ++v) {
         int per_cu = 0;
-        const WalkKernel k = walk_kernel(v & 1, v & 2, v & 4, v & 8);
+        const WalkKernel k = walk_kernel(v & 3, v & 4, v & 8);
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(k),
                                                          kBlockWalkers * kLanes, 0);
         if (e != hipSuccess) return e;

@@ -2,10 +2,14 @@
 algorithmic byte model and the grouping of walk launches into passes."""
 from __future__ import annotations
 
+import pathlib
+
 import numpy as np
 
 import bench
 from tests.tinygraph import AR, Builder
+
+ROOT = pathlib.Path(__file__).resolve().parent.parent
 
 
 def _graph():
@@ -53,7 +57,7 @@ def test_walk_passes_split_launches():
 
 def _timed(pass_ms, launches):
     return {"n_scen": 128, "pass_ms": pass_ms, "pass_launches": launches,
-            "pass_kernels": [bench.walk_kernel_name(k > 0, k == len(pass_ms) - 1, False, False)
+            "pass_kernels": [bench.walk_kernel_name(k > 0, k == len(pass_ms) - 1, False, False, 2)
                              for k in range(len(pass_ms))],
             "pass_index": list(range(len(pass_ms)))}
 
@@ -66,18 +70,34 @@ def test_roofline_headline_is_the_final_pass():
     alg = bench.walk_bytes(g, 128, 1)
     assert rf["algorithmic_bytes_per_launch"] == int(alg[1] / 2)
     assert np.isclose(rf["achieved"], round(alg[1] / 2 / 3e-3 / 1e9, 1))
-    assert rf["kernel"] == "k_walk<true, true, false, false>" and rf["traffic"] is None
-    assert [p["kernel"] for p in rf["passes"]] == ["k_walk<false, false, false, false>",
-                                                   "k_walk<true, true, false, false>"]
+    assert rf["kernel"] == "k_walk<1, true, false>" and rf["traffic"] is None
+    assert [p["kernel"] for p in rf["passes"]] == ["k_walk<0, false, false>", "k_walk<1, true, false>"]
     assert rf["passes"][0]["alg_frac"] == round(alg[0] / 4e-3 / 1e9 / bench.HBM_PEAK_GBS, 4)
 
 
 def test_pass_summary_groups_and_drops_skipped_passes():
     runs = [[[5.0, 4.0], [6.0, 6.5], [0.01]], [[5.2, 4.0], [6.2, 6.5], [0.01]]]
-    ps = bench.pass_summary(runs, False)
+    ps = bench.pass_summary(runs, False, 4)
     assert ps["pass_index"] == [0, 1] and ps["pass_launches"] == [2, 2]
     assert np.allclose(ps["pass_ms"], [9.1, 12.6])
-    assert ps["pass_kernels"] == ["k_walk<false, false, false, false>", "k_walk<true, false, false, false>"]
+    assert ps["pass_kernels"] == ["k_walk<0, false, false>", "k_walk<1, false, false>"]
+
+
+def test_walk_kernel_names_follow_the_library_variants():
+    """Pass 1 has no per-item input; refined non-final passes fetch whole mask rows; a final
+    mask pass fetches flagged rows from the library's tile threshold on; extra-time passes
+    always fetch flagged rows.  The threshold is the one the library compiles in."""
+    import re
+    tiles = bench.FLAG_ROW_TILES
+    assert bench.walk_kernel_name(False, False, False, False, 8) == "k_walk<0, false, false>"
+    assert bench.walk_kernel_name(False, True, True, False, 8) == "k_walk<0, true, true>"
+    assert bench.walk_kernel_name(True, False, False, False, 8) == "k_walk<1, false, false>"
+    assert bench.walk_kernel_name(True, True, False, False, tiles - 1) == "k_walk<1, true, false>"
+    assert bench.walk_kernel_name(True, True, False, False, tiles) == "k_walk<2, true, false>"
+    assert bench.walk_kernel_name(True, False, False, True, 1) == "k_walk<3, false, false>"
+    assert bench.walk_kernel_name(True, True, False, True, 1) == "k_walk<3, true, false>"
+    hdr = (ROOT / "paper_2412_12487_amd" / "csrc" / "echo_internal.h").read_text()
+    assert int(re.search(r"constexpr int kFlagRowTiles = (\d+);", hdr).group(1)) == tiles
 
 
 def test_latency_model_arithmetic():
@@ -123,8 +143,8 @@ def test_roofline_reports_measured_traffic_fraction(tmp_path, monkeypatch):
     import json
     g = _graph()
     rec = {"config": 3, "kernel_source_sha": bench.source_hash(),
-           "pass_bytes": {"k_walk<false, false, false, false>": 1_000_000_000,
-                          "k_walk<true, true, false, false>": 4_000_000_000}}
+           "pass_bytes": {"k_walk<0, false, false>": 1_000_000_000,
+                          "k_walk<1, true, false>": 4_000_000_000}}
     f = tmp_path / "walk_traffic.json"
     f.write_text(json.dumps(rec))
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
