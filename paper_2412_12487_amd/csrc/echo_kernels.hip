@@ -314,6 +314,14 @@ __device__ __forceinline__ int64_t inflate(int64_t d, uint32_t m, const uint32_t
         }
     return q16(d, F);
 }
+// The same for a mask whose class row (entries t = 0..3 of the op's class) was read
+// ahead: no branch, an empty mask keeps F = 65536.
+__device__ __forceinline__ int64_t inflate_row(int64_t d, uint32_t m, const uint32_t x[kTypes]) {
+    uint32_t F = 65536u;
+#pragma unroll
+    for (int t = 0; t < kTypes; ++t) F = ((m >> t) & 1u) && x[t] > F ? x[t] : F;
+    return q16(d, F);
+}
 // s_waitcnt immediate for "lgkmcnt(0)" on gfx9-family targets (vmcnt and expcnt left at their maxima)
 constexpr int kWaitLgkm0 = 0xC07F;
 
@@ -541,6 +549,26 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     };
     uint32_t fl_now = 0, fl_next = 0;     // this round's and the next round's flag bytes
     uint32_t want = 0;                    // this round's flagged compute items
+    // A compute item's staged input (wave-uniform test: a compute op whose row was staged) is
+    // read before its jitter draw, so that the LDS latency hides behind the draw: the mask
+    // byte, with flagged rows also the class row of the lane's slowdown table (a flagged row
+    // has some nonzero mask), or the extra time.
+    uint32_t sm = 0, srow[kTypes] = {};
+    auto staged = [&](uint32_t meta, int j) -> bool {
+        return REFINED && item_kind(meta) == ECHO_COMPUTE && ((want >> j) & 1u);
+    };
+    auto read_staged = [&](int j, uint32_t meta) {
+        sm = PRORATE ? fst32[j * kLanes + lane] : fst[j * kLanes + col];
+        if (IN == kInMaskFlags) {
+#pragma unroll
+            for (int t = 0; t < kTypes; ++t) srow[t] = slow[(item_class(meta) * kTypes + t) * kLanes + lane];
+        }
+    };
+    auto apply_staged = [&](int64_t d, uint32_t meta) -> int64_t {
+        if (PRORATE) return d + sm;
+        if (IN == kInMaskFlags) return inflate_row(d, sm, srow);
+        return inflate(d, sm, slow, item_class(meta), lane);
+    };
     if (kFlagged && beg < end) {
         fl_now = load_flags(beg);
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
@@ -584,7 +612,13 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 __builtin_amdgcn_s_waitcnt(kWaitVm0);
                 if (blk0 + kBlock < end) {
                     const int nn = end - blk0 - kBlock < kBlock ? int(end - blk0 - kBlock) : kBlock;
-                    stage_rows(blk0 + kBlock, 0, round_flags(fl_next, nxt, nn));
+                    // The next round's flags and items arrived with the wait above.  The empty asm
+                    // keeps their use here: left free, the compiler computes the per-lane test
+                    // where they are fetched, at the round's start, and waits for them there.
+                    uint32_t fl = fl_next;
+                    int4 it = nxt;
+                    asm volatile("" : "+v"(fl), "+v"(it.y));
+                    stage_rows(blk0 + kBlock, 0, round_flags(fl, it, nn));
                 }
                 second_half = true;
             }
@@ -602,11 +636,10 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);             \
                 const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) | \
                                               (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32)); \
-                int64_t d = (JIT) ? jittered(dur, op, jt) : dur;                         \
-                if (REFINED && item_kind(meta) == ECHO_COMPUTE)                                  \
-                    d = PRORATE ? d + ((want >> j) & 1u ? fst32[j * kLanes + lane] : 0u)         \
-                                : inflate(d, (want >> j) & 1u ? fst[j * kLanes + col] : 0u, slow,  \
-                                          item_class(meta), lane);                               \
+                const bool stg = staged(meta, j);                                                \
+                if (stg) read_staged(j, meta);                                                   \
+                int64_t d = (JIT) ? jittered(dur, op, jt) : dur;                                 \
+                if (stg) d = apply_staged(d, meta);                                              \
                 const int64_t f = s0 + d;                                                        \
                 if ((ALL) || (meta & kNeedS)) put(sbase + (int64_t)op * ns + col, s0);           \
                 if ((ALL) || (meta & kNeedF)) put(fbase + (int64_t)op * ns + col, f);            \
@@ -684,10 +717,10 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                                                __HIP_MEMORY_SCOPE_AGENT);
                 }
             } else {
+                const bool stg = staged(meta, j);
+                if (stg) read_staged(j, meta);
                 int64_t d = any_jitter ? jittered(dur, op, jt) : dur;
-                if (REFINED && kind == ECHO_COMPUTE)
-                    d = PRORATE ? d + ((want >> j) & 1u ? fst32[j * kLanes + lane] : 0u)
-                                : inflate(d, (want >> j) & 1u ? fst[j * kLanes + col] : 0u, slow, item_class(meta), lane);
+                if (stg) d = apply_staged(d, meta);
                 const int64_t f = ready + d;
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 if ((meta | keep) & kNeedF) put(fbase + (int64_t)op * ns + col, f);
