@@ -350,8 +350,11 @@ __device__ bool wait_local(const unsigned *cnt, unsigned need, unsigned *status,
 // overlaps.  FINAL: the pass produces the step time (and DIGEST: the digest).
 // IN (kIn*): the pass's per-item input -- none (the first pass), overlap masks (REFINED)
 // or prorated extra times (PRORATE), and whether only flagged rows are fetched.
+// Every variant must fit two workgroups per CU (at most 128 registers): the loader sizes
+// walkers to the fewest co-resident workgroups of any variant, so one variant over the
+// limit would make the largest graphs walk more ranks per wavefront in every pass.
 template <int IN, bool FINAL, bool DIGEST>
-__global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
+__global__ __launch_bounds__(kBlockWalkers * 64) __attribute__((amdgpu_waves_per_eu(4))) void k_walk(WalkArgs a) {
     constexpr bool REFINED = IN != kInNone;
     constexpr bool PRORATE = IN == kInExtFlags;
     constexpr bool kFlagged = IN == kInMaskFlags || IN == kInExtFlags;
@@ -549,23 +552,26 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
     };
     uint32_t fl_now = 0, fl_next = 0;     // this round's and the next round's flag bytes
     uint32_t want = 0;                    // this round's flagged compute items
-    // A compute item's staged input (wave-uniform test: a compute op whose row was staged) is
-    // read before its jitter draw, so that the LDS latency hides behind the draw: the mask
-    // byte, with flagged rows also the class row of the lane's slowdown table (a flagged row
-    // has some nonzero mask), or the extra time.
+    // A compute item's staged mask (wave-uniform test: a compute op whose row was staged) is
+    // read before its jitter draw, so that the LDS latency hides behind the draw, and for a
+    // flagged row (some nonzero mask) the class row of the lane's slowdown table with it.  An
+    // extra time is read after the draw: held across it, it took the prorating variants past
+    // 128 registers, and the fewer co-resident workgroups made the largest graphs walk more
+    // ranks per wavefront.
     uint32_t sm = 0, srow[kTypes] = {};
     auto staged = [&](uint32_t meta, int j) -> bool {
         return REFINED && item_kind(meta) == ECHO_COMPUTE && ((want >> j) & 1u);
     };
     auto read_staged = [&](int j, uint32_t meta) {
-        sm = PRORATE ? fst32[j * kLanes + lane] : fst[j * kLanes + col];
+        if (PRORATE) return;
+        sm = fst[j * kLanes + col];
         if (IN == kInMaskFlags) {
 #pragma unroll
             for (int t = 0; t < kTypes; ++t) srow[t] = slow[(item_class(meta) * kTypes + t) * kLanes + lane];
         }
     };
-    auto apply_staged = [&](int64_t d, uint32_t meta) -> int64_t {
-        if (PRORATE) return d + sm;
+    auto apply_staged = [&](int64_t d, uint32_t meta, int j) -> int64_t {
+        if (PRORATE) return d + fst32[j * kLanes + lane];
         if (IN == kInMaskFlags) return inflate_row(d, sm, srow);
         return inflate(d, sm, slow, item_class(meta), lane);
     };
@@ -639,7 +645,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 const bool stg = staged(meta, j);                                                \
                 if (stg) read_staged(j, meta);                                                   \
                 int64_t d = (JIT) ? jittered(dur, op, jt) : dur;                                 \
-                if (stg) d = apply_staged(d, meta);                                              \
+                if (stg) d = apply_staged(d, meta, j);                                           \
                 const int64_t f = s0 + d;                                                        \
                 if ((ALL) || (meta & kNeedS)) put(sbase + (int64_t)op * ns + col, s0);           \
                 if ((ALL) || (meta & kNeedF)) put(fbase + (int64_t)op * ns + col, f);            \
@@ -720,7 +726,7 @@ __global__ __launch_bounds__(kBlockWalkers * 64) void k_walk(WalkArgs a) {
                 const bool stg = staged(meta, j);
                 if (stg) read_staged(j, meta);
                 int64_t d = any_jitter ? jittered(dur, op, jt) : dur;
-                if (stg) d = apply_staged(d, meta);
+                if (stg) d = apply_staged(d, meta, j);
                 const int64_t f = ready + d;
                 hi_or |= (uint32_t)((uint64_t)f >> 32);
                 if ((meta | keep) & kNeedF) put(fbase + (int64_t)op * ns + col, f);

@@ -17,6 +17,7 @@ import pytest
 
 import oracle
 from tests.test_gpu_parity import THREADS, assert_same, gpu_run
+from tests import tinygraph
 from workloads import configs, gpt1f1b, scenarios
 
 pytestmark = pytest.mark.gpu
@@ -159,3 +160,30 @@ def test_walk_chain_of_a_resident_graph(E):
         assert ch2["ps"] == 1000 * ch2["items"] + 5000 * ch2["lds_barriers"] + 9000 * ch2["global_barriers"]
     finally:
         G.close()
+
+
+def test_every_walk_variant_keeps_two_workgroups_per_cu(E):
+    """The loader sizes walkers to the fewest co-resident walk workgroups of any kernel
+    variant.  Every variant fits two eight-wavefront workgroups per compute unit, so a
+    graph of 2 x 8 x 2 x CUs ranks (8192 on an MI355X) walks two ranks per wavefront, as
+    when two are asked for, not three (one variant over 128 registers would make it three:
+    every pass of the largest graphs would then take half as long again).  Each rank is a
+    chain of three compute ops, so the walk's longest chain is 3 x ranks per wavefront."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    R = 2 * 8 * 2 * cus
+    b = tinygraph.Builder(R)
+    for r in range(R):
+        u = b.compute(r, 1000 + r)
+        u = b.compute(r, 2000, preds=(u,))
+        b.compute(r, 3000, preds=(u,))
+    g = b.graph()
+    chains = {}
+    for rpw in (0, 2, 3):
+        G = E.Graph(g, 0, ranks_per_walker=rpw)
+        try:
+            chains[rpw] = G.walk_chain(1, 0, 0)["items"]
+        finally:
+            G.close()
+    assert chains[2] == 6 and chains[3] == 9
+    assert chains[0] == chains[2]
