@@ -274,17 +274,18 @@ def cc_variant(sc, args):
     return sc
 
 
-# A final mask pass over at least this many 64-scenario tiles runs the walk variant that
-# fetches only flagged mask rows (the library's kFlagRowTiles).
+# A final mask pass whose launches average at least this many 64-scenario tiles runs the walk
+# variant that fetches only flagged mask rows (the library's kFlagRowTiles).
 FLAG_ROW_TILES = 4
 
 
-def walk_kernel_name(refined, final, digest, ext, n_tiles):
+def walk_kernel_name(refined, final, digest, ext, n_tiles, launches=1):
     """The walk kernel a pass launches, as rocprofv3 names it: k_walk<input, final, digest>
     with input 0 = none (first pass), 1 = whole mask rows, 2 = flagged mask rows (a final
-    pass over FLAG_ROW_TILES or more tiles), 3 = flagged extra-time rows."""
+    pass of n_tiles >= FLAG_ROW_TILES x launches), 3 = flagged extra-time rows."""
     b = lambda x: "true" if x else "false"
-    inp = 0 if not refined else 3 if ext else 2 if final and n_tiles >= FLAG_ROW_TILES else 1
+    flagged = final and n_tiles >= FLAG_ROW_TILES * launches
+    inp = 0 if not refined else 3 if ext else 2 if flagged else 1
     return f"k_walk<{inp}, {b(final)}, {b(digest)}>"
 
 
@@ -374,7 +375,7 @@ def pass_summary(pass_runs, ext, n_tiles):
     launches = [max(len(p[k]) for p in pass_runs if k < len(p)) for k in range(n_pass)]
     top = max(pass_ms, default=0.0)
     ran = [k for k in range(n_pass) if pass_ms[k] > 0.02 * top]
-    names = [walk_kernel_name(k > 0, k == n_pass - 1, False, ext, n_tiles) for k in range(n_pass)]
+    names = [walk_kernel_name(k > 0, k == n_pass - 1, False, ext, n_tiles, launches[k]) for k in range(n_pass)]
     return {"pass_ms": [pass_ms[k] for k in ran], "pass_launches": [launches[k] for k in ran],
             "pass_kernels": [names[k] for k in ran], "pass_index": ran}
 

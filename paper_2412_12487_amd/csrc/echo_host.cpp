@@ -952,16 +952,22 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
         return hip_fail(e, "fill kernel");
 
     for (int32_t p = 0; p <= n_refine; ++p) {
-        // tiles per walk launch: every rank block of a tile must be co-resident
-        // a final pass over at least kFlagRowTiles tiles writes enough timelines to be bound by
-        // HBM and fetches only the flagged mask rows; with fewer it is bound by its chain of
-        // items and fetches whole rows (measured: 256 scenarios, four tiles, on the 1024-rank
-        // graph gain 1.3 ms; one-tile 32-scenario graphs lose 0.5-2 ms)
-        const bool flag_rows = p == n_refine && n_tiles >= kFlagRowTiles;
-        const int64_t cap = g->capacity[walk_variant(walk_input(p > 0, ext, flag_rows), p == n_refine,
-                                                     d_digest != nullptr)];
+        // tiles per walk launch: every rank block of a tile must be co-resident (a final mask
+        // pass may run either mask variant, so both count)
+        const bool fin = p == n_refine, mask_pass = p > 0 && !ext;
+        int64_t cap = g->capacity[walk_variant(walk_input(p > 0, ext, false), fin, d_digest != nullptr)];
+        if (fin && mask_pass)
+            cap = std::min(cap, g->capacity[walk_variant(kInMaskFlags, true, d_digest != nullptr)]);
         int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, cap / g->dg.n_blocks));
         if (g->max_launch_tiles > 0) per_launch = std::min<int64_t>(per_launch, g->max_launch_tiles);
+        // A final mask pass whose launches average at least kFlagRowTiles tiles writes enough
+        // timelines per unit of its chain of items to be bound by HBM, and fetches only the
+        // flagged mask rows; with fewer tiles per launch it is bound by the chain and fetches
+        // whole rows (measured: the 1024-rank graph's four tiles in one launch gain 1.3 ms;
+        // one-tile 32-scenario graphs lose 0.5-2 ms, the 8192-rank graph's one tile per launch
+        // 1.1 ms per launch).
+        const int64_t n_launches = (n_tiles + per_launch - 1) / per_launch;
+        const bool flag_rows = fin && n_tiles >= kFlagRowTiles * n_launches;
         if (p > 0) {
             OverlapArgs o{};
             o.cl_off = g->dg.cl_off;

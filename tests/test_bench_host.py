@@ -85,8 +85,9 @@ def test_pass_summary_groups_and_drops_skipped_passes():
 
 def test_walk_kernel_names_follow_the_library_variants():
     """Pass 1 has no per-item input; refined non-final passes fetch whole mask rows; a final
-    mask pass fetches flagged rows from the library's tile threshold on; extra-time passes
-    always fetch flagged rows.  The threshold is the one the library compiles in."""
+    mask pass fetches flagged rows when its launches average the library's tile threshold
+    or more; extra-time passes always fetch flagged rows.  The threshold is the one the
+    library compiles in."""
     import re
     tiles = bench.FLAG_ROW_TILES
     assert bench.walk_kernel_name(False, False, False, False, 8) == "k_walk<0, false, false>"
@@ -94,6 +95,9 @@ def test_walk_kernel_names_follow_the_library_variants():
     assert bench.walk_kernel_name(True, False, False, False, 8) == "k_walk<1, false, false>"
     assert bench.walk_kernel_name(True, True, False, False, tiles - 1) == "k_walk<1, true, false>"
     assert bench.walk_kernel_name(True, True, False, False, tiles) == "k_walk<2, true, false>"
+    assert bench.walk_kernel_name(True, True, False, False, 2 * tiles, 2) == "k_walk<2, true, false>"
+    assert bench.walk_kernel_name(True, True, False, False, 2 * tiles - 1, 2) == "k_walk<1, true, false>"
+    assert bench.walk_kernel_name(True, True, False, False, tiles, tiles) == "k_walk<1, true, false>"
     assert bench.walk_kernel_name(True, False, False, True, 1) == "k_walk<3, false, false>"
     assert bench.walk_kernel_name(True, True, False, True, 1) == "k_walk<3, true, false>"
     hdr = (ROOT / "paper_2412_12487_amd" / "csrc" / "echo_internal.h").read_text()
