@@ -1004,8 +1004,13 @@ __device__ uint32_t forest_factor_compact(const OverlapArgs &a, uint32_t m, cons
 // of kFxWaves wavefronts, one (rank, tile) each, shares one copy of the nodes).
 // NC: room for this many comm streams per rank (the cursor and merge state scale with it).
 constexpr int kFxWaves = 4;
+// The fixed-point prorating variant with four comm streams is held to four waves per SIMD
+// (at most 128 registers; left free it took 142, three waves per SIMD, and its 4,096
+// wavefronts on the 1024-rank workload ran in two rounds): a few spilled registers cost far
+// less than the second round.
 template <bool PRORATE, bool DETECT, int FOREST, int NC>
-__global__ __launch_bounds__(64 * (FOREST == 2 ? kFxWaves : 1)) void k_overlap(OverlapArgs a) {
+__global__ __launch_bounds__(64 * (FOREST == 2 ? kFxWaves : 1))
+__attribute__((amdgpu_waves_per_eu(PRORATE && DETECT && FOREST == 0 && NC == 4 ? 4 : 1))) void k_overlap(OverlapArgs a) {
     constexpr bool EXT = PRORATE || FOREST != 0;  // output: extra time per op instead of a mask
     constexpr int W = FOREST == 2 ? kFxWaves : 1;      // wavefronts per workgroup
     constexpr int STAGE = FOREST == 2 ? kIdStage / 4 : kIdStage;
