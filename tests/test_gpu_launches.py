@@ -110,6 +110,28 @@ def test_pass_split_by_tile_cap(E, max_tiles, R):
         G.close()
 
 
+@pytest.mark.parametrize("max_tiles", [3, 5])
+def test_final_mask_variants_across_split_launches(E, max_tiles):
+    """Config 1 with 520 scenarios (nine tiles, the last ragged), one refinement.  The final
+    pass fetches only flagged mask rows when its launches average four tiles or more: at
+    most five tiles per launch (5 + 4) it does, at most three (3 + 3 + 3) it fetches whole
+    rows.  Both give every start, finish, step and digest of the oracle."""
+    import torch
+    g = configs.graph(1)
+    sc = scenarios.draw(520, np.random.default_rng(23), bw_inter=(50_000, 400_000), bw_intra=(50_000, 400_000),
+                        alpha=(2_000, 20_000), slowdown=(65536, 91750), jitter=(6554, 9), ar_algo_random=True)
+    G = E.Graph(g, 0)
+    try:
+        G.set_launch_tiles(max_tiles)
+        G.set_timing(True)
+        gpu = gpu_run(E, g, sc, 1, graph=G)
+        torch.cuda.synchronize()
+        assert _walk_launches_per_pass(G) == [-(-9 // max_tiles)] * 2
+        assert_same(gpu, oracle.run(g, sc, 1, threads=THREADS))
+    finally:
+        G.close()
+
+
 def test_launch_tile_cap_rejects_negative(E):
     G = E.Graph(configs.graph(1), 0)
     try:
