@@ -276,7 +276,7 @@ def cc_variant(sc, args):
 
 # A final mask pass whose launches average at least this many 64-scenario tiles runs the walk
 # variant that fetches only flagged mask rows (the library's kFlagRowTiles).
-FLAG_ROW_TILES = 4
+FLAG_ROW_TILES = 2
 
 
 def walk_kernel_name(refined, final, digest, ext, n_tiles, launches=1):

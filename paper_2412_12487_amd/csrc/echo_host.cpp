@@ -961,11 +961,11 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
         int64_t per_launch = std::max<int64_t>(1, std::min<int64_t>(n_tiles, cap / g->dg.n_blocks));
         if (g->max_launch_tiles > 0) per_launch = std::min<int64_t>(per_launch, g->max_launch_tiles);
         // A final mask pass whose launches average at least kFlagRowTiles tiles writes enough
-        // timelines per unit of its chain of items to be bound by HBM, and fetches only the
-        // flagged mask rows; with fewer tiles per launch it is bound by the chain and fetches
-        // whole rows (measured: the 1024-rank graph's four tiles in one launch gain 1.3 ms;
-        // one-tile 32-scenario graphs lose 0.5-2 ms, the 8192-rank graph's one tile per launch
-        // 1.1 ms per launch).
+        // timelines per unit of its chain of items for the fetched bytes to count, and fetches
+        // only the flagged mask rows; with fewer tiles per launch it is bound by the chain and
+        // fetches whole rows (measured on the 1024-rank graph: three tiles in one launch gain
+        // 1.35 ms, four 1.3 ms, two neither gain nor lose; one-tile 32-scenario graphs lose
+        // 0.5-2 ms, the 8192-rank graph's one tile per launch 1.1 ms per launch).
         const int64_t n_launches = (n_tiles + per_launch - 1) / per_launch;
         const bool flag_rows = fin && n_tiles >= kFlagRowTiles * n_launches;
         if (p > 0) {

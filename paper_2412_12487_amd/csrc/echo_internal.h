@@ -78,7 +78,7 @@ constexpr int kResolve = 3;
 // looked up per cost class -- the (type, S, N, M, K) tuple that fixes T(c, s)
 // for a scenario -- and a block stages its most used classes in LDS.
 constexpr int kBlockWalkers = 8;
-constexpr int kFlagRowTiles = 4;    // final mask passes of this many tiles per launch fetch only flagged rows
+constexpr int kFlagRowTiles = 2;    // final mask passes of this many tiles per launch fetch only flagged rows
 constexpr int kBlock = 32;          // walk items fetched (and overlap masks staged) per round
 constexpr int kChannels = 8;          // LDS barrier channels per block
 constexpr int kClassSlots = 8;        // LDS cost classes per block

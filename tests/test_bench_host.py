@@ -57,7 +57,7 @@ def test_walk_passes_split_launches():
 
 def _timed(pass_ms, launches):
     return {"n_scen": 128, "pass_ms": pass_ms, "pass_launches": launches,
-            "pass_kernels": [bench.walk_kernel_name(k > 0, k == len(pass_ms) - 1, False, False, 2)
+            "pass_kernels": [bench.walk_kernel_name(k > 0, k == len(pass_ms) - 1, False, False, 1)
                              for k in range(len(pass_ms))],
             "pass_index": list(range(len(pass_ms)))}
 

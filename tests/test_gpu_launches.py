@@ -110,12 +110,12 @@ def test_pass_split_by_tile_cap(E, max_tiles, R):
         G.close()
 
 
-@pytest.mark.parametrize("max_tiles", [3, 5])
+@pytest.mark.parametrize("max_tiles", [2, 3])
 def test_final_mask_variants_across_split_launches(E, max_tiles):
     """Config 1 with 520 scenarios (nine tiles, the last ragged), one refinement.  The final
-    pass fetches only flagged mask rows when its launches average four tiles or more: at
-    most five tiles per launch (5 + 4) it does, at most three (3 + 3 + 3) it fetches whole
-    rows.  Both give every start, finish, step and digest of the oracle."""
+    pass fetches only flagged mask rows when its launches average two tiles or more: at
+    most three tiles per launch (3 + 3 + 3) it does, at most two (2 + 2 + 2 + 2 + 1) it
+    fetches whole rows.  Both give every start, finish, step and digest of the oracle."""
     import torch
     g = configs.graph(1)
     sc = scenarios.draw(520, np.random.default_rng(23), bw_inter=(50_000, 400_000), bw_intra=(50_000, 400_000),
