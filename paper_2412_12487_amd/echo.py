@@ -78,6 +78,10 @@ def lib():
         return _lib
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    # torch first: libecho.so then binds to the HIP runtime torch has loaded, so the process
+    # has one.  Loaded the other way round, the library would bring in the system's runtime
+    # first and torch could no longer open the GPU ("No HIP GPUs are available").
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     L.echo_load_graph.argtypes = [ctypes.POINTER(_Desc), ctypes.c_int, ctypes.POINTER(P)]

@@ -209,3 +209,29 @@ def test_every_walk_variant_keeps_two_workgroups_per_cu(E):
             G.close()
     assert chains[2] == 6 and chains[3] == 9
     assert chains[0] == chains[2]
+
+
+def test_library_loaded_before_torch_touches_the_gpu():
+    """A fresh process that loads a graph before any torch call, then hands torch-allocated
+    scenarios to it: the binding loads torch's HIP runtime before libecho.so, so both share
+    one runtime and the compose matches the oracle."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = (
+        "import numpy as np, oracle\n"
+        "import paper_2412_12487_amd as E\n"
+        "from workloads import configs\n"
+        "g = configs.graph(1)\n"
+        "G = E.Graph(g, 0)\n"
+        "sc = configs.scenario_batch(1)\n"
+        "d, n = E.scenarios_to_device(sc)\n"
+        "out = G.compose(d, n, 1, timelines=False, digest=True)\n"
+        "ref = oracle.run(g, sc, 1, timelines=False)\n"
+        "assert np.array_equal(out['step'].cpu().numpy(), ref['step'])\n"
+        "assert np.array_equal(out['digest'].cpu().numpy().view(np.uint64), ref['digest'])\n"
+        "G.close()\n"
+        "print('ok')\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=110)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok"), r.stdout + r.stderr

@@ -151,6 +151,39 @@ def test_walkers_of_several_ranks_tiny(E, rpw):
         G.close()
 
 
+def test_random_graphs_every_final_pass_variant(E):
+    """300 random graphs with 65-256 scenarios (two to four tiles), one or two refinements or
+    the fixed-point and prorated validators, some with one to three tiles per walk launch:
+    the final pass runs with flagged mask rows, whole rows and flagged extra times.  Every
+    start, finish, step and digest against the oracle."""
+    for seed in range(300):
+        rng = np.random.default_rng(90_000 + seed)
+        g = _random_graph(rng, int(rng.integers(2, 40)), int(rng.integers(5, 60)), int(rng.integers(0, 40)))
+        n = int(rng.choice([65, 100, 130, 192, 256]))
+        sc = scenarios.draw(n, rng, bw_inter=(20000, 400000), bw_intra=(50000, 400000), alpha=(0, 20000),
+                            ar_algo_random=True, slowdown=(65536, 150000), jitter=(5000, seed))
+        R = int(rng.integers(1, 3))
+        variant = int(rng.integers(0, 3))
+        kw = [{}, {"until_stable": True}, {"prorate": True}][variant]
+        if variant == 1:
+            R = 6
+        ref = oracle.run(g, sc, R, threads=THREADS, **kw)
+        G = E.Graph(g, 0)
+        try:
+            if rng.integers(0, 2):
+                G.set_launch_tiles(int(rng.integers(1, 4)))
+            d, ns = E.scenarios_to_device(sc)
+            out = G.compose(d, ns, R, timelines=True, digest=True, refinements=variant > 0, **kw)
+            gpu = {"step": out["step"].cpu().numpy(), "digest": out["digest"].cpu().numpy().view(np.uint64),
+                   "start": out["start"].cpu().numpy(), "finish": out["finish"].cpu().numpy()}
+            assert_same(gpu, ref)
+            if variant > 0:
+                np.testing.assert_array_equal(out["refinements"].cpu().numpy(), ref["refinements"],
+                                              err_msg=f"refinements, seed {seed}")
+        finally:
+            G.close()
+
+
 @pytest.mark.parametrize("seed", range(6))
 @pytest.mark.parametrize("rpw", [2, 5, 16])
 def test_walkers_of_several_ranks_random(E, seed, rpw):
