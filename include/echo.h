@@ -245,6 +245,10 @@ int echo_cc_cost(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int6
  * synchronisation), so once an eager call with at least as many scenarios
  * and the same options has sized the workspace, it can be recorded by HIP
  * stream capture and replayed as a graph (kernel timing must be off).
+ * The walk runs as cooperative launches (every wavefront of a launch
+ * resident at once).  Observed on MI355X: once one process has made such
+ * launches on a GPU, another process's are refused and the call returns
+ * ECHO_ERR_HIP, so compose from one process per GPU.
  */
 int echo_compose_batch(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, int32_t n_refine,
                        int64_t *d_start, int64_t *d_finish, int64_t *d_step, uint64_t *d_digest,
