@@ -84,6 +84,10 @@ __device__ __forceinline__ int64_t q16u(int64_t d0, uint32_t f) {
 __device__ __forceinline__ int64_t jittered(int64_t d0, int32_t v, const Jitter &jt) {
     return q16u(d0, jitter_factor(v, jt));
 }
+// the same for a base duration known to be below 2^32 ns
+__device__ __forceinline__ int64_t jittered32(uint32_t d0, int32_t v, const Jitter &jt) {
+    return (int64_t)(((uint64_t)d0 * jitter_factor(v, jt) + 32768ull) >> 16);
+}
 
 __device__ __forceinline__ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -609,6 +613,20 @@ __global__ __launch_bounds__(kBlockWalkers * 64) __attribute__((amdgpu_waves_per
         // fast flags of the round, one bit per item
         const uint64_t fast_bits = __builtin_amdgcn_read_exec() &
                                    __ballot((lane < nb) && (lane < 32) && (cur.y & kFast));
+        // What a fast item needs besides its op and duration, as bits of the round taken
+        // once, so that its loop reads two lanes per item instead of four: the items that
+        // store a start or finish of their own (passes that do not store every one), the
+        // compute items with a staged row, and whether every duration of the round fits
+        // 32 bits (lane 32 + j holds the high word of item j's).
+        const uint32_t need_bits = (uint32_t)(__builtin_amdgcn_read_exec() &
+                                              __ballot(lane < 32 && ((uint32_t)cur.y & (kNeedS | kNeedF))));
+        const uint32_t stg_bits =
+            !REFINED ? 0u
+            : kFlagged ? want
+                       : (uint32_t)(__builtin_amdgcn_read_exec() &
+                                    __ballot(lane < 32 && item_kind((uint32_t)cur.y) == ECHO_COMPUTE));
+        const bool small_round =
+            __builtin_amdgcn_readfirstlane((__builtin_amdgcn_read_exec() & __ballot(lane >= 32 && cur.y != 0)) == 0);
         int j = 0;
         bool second_half = false;     // the round's second half of staged rows settled
         while (j < nb) {
@@ -635,27 +653,43 @@ __global__ __launch_bounds__(kBlockWalkers * 64) __attribute__((amdgpu_waves_per
             if (kFlagged && j < kHalf && run_end > kHalf) run_end = kHalf;
             int64_t s0 = lf0;
 // ALL: the pass stores every start and finish, so the items' own needs are not consulted;
-// JIT: some lane draws jitter (the branch stays out of the loop)
-#define FAST_RUN(ALL, JIT)                                                                       \
+// JIT: some lane draws jitter (the branch stays out of the loop); SMALL: every duration
+// of the round is below 2^32 ns.  The item's metadata word is read only where it is used
+// (a staged row's class, an item's own stores).
+#define FAST_RUN(ALL, JIT, SMALL)                                                                \
             for (; j < run_end; ++j) {                                                           \
                 const int32_t op = __builtin_amdgcn_readlane(cur.x, j);                          \
-                const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);             \
-                const int64_t dur = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) | \
-                                              (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32)); \
-                const bool stg = staged(meta, j);                                                \
-                if (stg) read_staged(j, meta);                                                   \
-                int64_t d = (JIT) ? jittered(dur, op, jt) : dur;                                 \
+                const uint32_t dlo = (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32);         \
+                const int64_t dur = (SMALL) ? (int64_t)dlo                                       \
+                    : (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) | dlo); \
+                const bool stg = REFINED && ((stg_bits >> j) & 1u);                              \
+                uint32_t meta = 0;                                                               \
+                if (stg) {                                                                       \
+                    if (!PRORATE) meta = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);          \
+                    read_staged(j, meta);                                                        \
+                }                                                                                \
+                int64_t d = !(JIT) ? dur : (SMALL) ? jittered32(dlo, op, jt) : jittered(dur, op, jt); \
                 if (stg) d = apply_staged(d, meta, j);                                           \
                 const int64_t f = s0 + d;                                                        \
-                if ((ALL) || (meta & kNeedS)) put(sbase + (int64_t)op * ns + col, s0);           \
-                if ((ALL) || (meta & kNeedF)) put(fbase + (int64_t)op * ns + col, f);            \
+                if (ALL) {                                                                       \
+                    put(sbase + (int64_t)op * ns + col, s0);                                     \
+                    put(fbase + (int64_t)op * ns + col, f);                                      \
+                } else if ((need_bits >> j) & 1u) {                                              \
+                    const uint32_t nm = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);           \
+                    if (nm & kNeedS) put(sbase + (int64_t)op * ns + col, s0);                    \
+                    if (nm & kNeedF) put(fbase + (int64_t)op * ns + col, f);                     \
+                }                                                                                \
                 if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)s0) ^ (uint64_t)f);     \
                 s0 = f;                                                                          \
             }
             if (keep) {
-                if (any_jitter) FAST_RUN(true, true) else FAST_RUN(true, false)
+                if (!any_jitter) FAST_RUN(true, false, false)
+                else if (small_round) FAST_RUN(true, true, true)
+                else FAST_RUN(true, true, false)
             } else {
-                if (any_jitter) FAST_RUN(false, true) else FAST_RUN(false, false)
+                if (!any_jitter) FAST_RUN(false, false, false)
+                else if (small_round) FAST_RUN(false, true, true)
+                else FAST_RUN(false, true, false)
             }
 #undef FAST_RUN
             // durations are never negative: the run's last finish is its latest time
