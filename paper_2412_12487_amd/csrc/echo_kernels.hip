@@ -654,11 +654,11 @@ __global__ __launch_bounds__(kBlockWalkers * 64) __attribute__((amdgpu_waves_per
             int64_t s0 = lf0;
 // ALL: the pass stores every start and finish, so the items' own needs are not consulted;
 // JIT: some lane draws jitter (the branch stays out of the loop); SMALL: every duration
-// of the round is below 2^32 ns.  The item's metadata word is read only where it is used
-// (a staged row's class, an item's own stores).
+// of the round is below 2^32 ns.  The item's metadata word, and without jitter its op, are
+// read only where they are used (a staged row's class, an item's own stores).
 #define FAST_RUN(ALL, JIT, SMALL)                                                                \
             for (; j < run_end; ++j) {                                                           \
-                const int32_t op = __builtin_amdgcn_readlane(cur.x, j);                          \
+                const int32_t op = ((JIT) || (ALL) || DIGEST) ? __builtin_amdgcn_readlane(cur.x, j) : 0; \
                 const uint32_t dlo = (uint32_t)__builtin_amdgcn_readlane(cur.x, j + 32);         \
                 const int64_t dur = (SMALL) ? (int64_t)dlo                                       \
                     : (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane(cur.y, j + 32) << 32) | dlo); \
@@ -675,21 +675,25 @@ __global__ __launch_bounds__(kBlockWalkers * 64) __attribute__((amdgpu_waves_per
                     put(sbase + (int64_t)op * ns + col, s0);                                     \
                     put(fbase + (int64_t)op * ns + col, f);                                      \
                 } else if ((need_bits >> j) & 1u) {                                              \
+                    const int32_t sop = ((JIT) || DIGEST) ? op : __builtin_amdgcn_readlane(cur.x, j); \
                     const uint32_t nm = (uint32_t)__builtin_amdgcn_readlane(cur.y, j);           \
-                    if (nm & kNeedS) put(sbase + (int64_t)op * ns + col, s0);                    \
-                    if (nm & kNeedF) put(fbase + (int64_t)op * ns + col, f);                     \
+                    if (nm & kNeedS) put(sbase + (int64_t)sop * ns + col, s0);                   \
+                    if (nm & kNeedF) put(fbase + (int64_t)sop * ns + col, f);                    \
                 }                                                                                \
                 if (DIGEST) dig += mix64(mix64((uint64_t)op ^ (uint64_t)s0) ^ (uint64_t)f);     \
                 s0 = f;                                                                          \
             }
             if (keep) {
+                // (stores every start and finish: the high word's read is not worth a variant)
                 if (!any_jitter) FAST_RUN(true, false, false)
                 else if (small_round) FAST_RUN(true, true, true)
                 else FAST_RUN(true, true, false)
             } else {
-                if (!any_jitter) FAST_RUN(false, false, false)
-                else if (small_round) FAST_RUN(false, true, true)
-                else FAST_RUN(false, true, false)
+                if (small_round) {
+                    if (any_jitter) FAST_RUN(false, true, true) else FAST_RUN(false, false, true)
+                } else {
+                    if (any_jitter) FAST_RUN(false, true, false) else FAST_RUN(false, false, false)
+                }
             }
 #undef FAST_RUN
             // durations are never negative: the run's last finish is its latest time
