@@ -319,12 +319,18 @@ __device__ __forceinline__ int64_t inflate(int64_t d, uint32_t m, const uint32_t
     return q16(d, F);
 }
 // The same for a mask whose class row (entries t = 0..3 of the op's class) was read
-// ahead: no branch, an empty mask keeps F = 65536.
+// ahead: no branch, an empty mask keeps F = 65536.  Entry t takes part through an AND
+// with bit t of m widened to a whole word (all ones or zero), and the largest is taken
+// three at a time.
 __device__ __forceinline__ int64_t inflate_row(int64_t d, uint32_t m, const uint32_t x[kTypes]) {
-    uint32_t F = 65536u;
+    static_assert(kTypes == 4, "two three-way maxima cover 65536 and four entries");
+    uint32_t a[kTypes];
 #pragma unroll
-    for (int t = 0; t < kTypes; ++t) F = ((m >> t) & 1u) && x[t] > F ? x[t] : F;
-    return q16(d, F);
+    for (int t = 0; t < kTypes; ++t) a[t] = x[t] & (uint32_t)__builtin_amdgcn_sbfe((int)m, t, 1);
+    const uint32_t F0 = a[0] > 65536u ? a[0] : 65536u;
+    const uint32_t F1 = F0 > a[1] ? F0 : a[1];
+    const uint32_t F2 = a[2] > a[3] ? a[2] : a[3];
+    return q16(d, F1 > F2 ? F1 : F2);
 }
 // s_waitcnt immediate for "lgkmcnt(0)" on gfx9-family targets (vmcnt and expcnt left at their maxima)
 constexpr int kWaitLgkm0 = 0xC07F;
@@ -814,10 +820,12 @@ WalkKernel walk_kernel(int in, bool final_pass, bool digest) {
 // One wavefront per (rank, tile).  Compute ops of one stream run back to back,
 // and so do the comm ops of one stream, so for each comm stream a cursor that
 // only moves forward finds every comm op overlapping the current compute op.
-// After compute op v the cursor of each comm stream sits on the first comm op
-// that ends after v started; for the next compute op v', "that comm op starts
-// at or after v' ends" proves both "no overlap" and "cursor stays" -- one
-// compare per comm stream in the common case.  A compute op's interval is
+// After compute op v the cursor of each comm stream sits on a comm op that ends
+// after v started (at or after v finished, once v had to look at that stream:
+// every later compute op of v's stream starts at or after v's finish); for the next
+// compute op v', "that comm op starts at or after v' ends" proves both "no
+// overlap" and "cursor stays" -- one compare per comm stream in the common
+// case.  A compute op's interval is
 // rebuilt rather than read: a chained op starts where the previous compute op
 // of its stream finished, and every finish is start + base duration (the same
 // jitter draw as the composer pass, inflated by the factor that pass used);
@@ -1362,6 +1370,32 @@ __attribute__((amdgpu_waves_per_eu(PRORATE && DETECT && FOREST == 0 && NC == 4 ?
                     for (int k = 0; k < NC; ++k) {
                         if (k >= ncs) break;
                         if (!(cs[k] < fv)) continue;
+                        if (!PRORATE) {
+                            // The cursor walks the intervals that start before v ends; one
+                            // that also ends before then is behind every later op of this
+                            // compute stream (each starts at or after v's finish) and is
+                            // passed for good, so every comm interval is loaded once, when the
+                            // cursor reaches it.
+                            while (cs[k] < fv) {
+                                const int64_t lo = sv > cs[k] ? sv : cs[k], hi = fv < cf[k] ? fv : cf[k];
+                                if (lo < hi) {
+                                    const uint32_t ty = comm_type(kb[k] + p[k]);
+                                    m |= 1u << ty;
+                                    NOTE_FOREST(kb[k] + p[k], ty)
+                                }
+                                if (cf[k] >= fv) break;    // reaches v's end: later ops may overlap it
+                                ++p[k];
+                                if (p[k] < nk[k]) {
+                                    const int64_t c = comm_id(kb[k] + p[k]);
+                                    cs[k] = (sbase + c * ns)[col];
+                                    cf[k] = (fbase + c * ns)[col];
+                                } else {
+                                    cs[k] = kInf;
+                                    cf[k] = kInf;
+                                }
+                            }
+                            continue;
+                        }
                         while (cf[k] <= sv) {              // ends before v starts: never again
                             ++p[k];
                             if (p[k] < nk[k]) {
@@ -1372,22 +1406,6 @@ __attribute__((amdgpu_waves_per_eu(PRORATE && DETECT && FOREST == 0 && NC == 4 ?
                                 cs[k] = kInf;
                                 cf[k] = kInf;
                             }
-                        }
-                        if (PRORATE) continue;
-                        int32_t q = p[k];
-                        int64_t qs = cs[k], qf = cf[k];
-                        while (qs < fv) {
-                            const int64_t lo = sv > qs ? sv : qs, hi = fv < qf ? fv : qf;
-                            if (lo < hi) {
-                                const uint32_t ty = comm_type(kb[k] + q);
-                                m |= 1u << ty;
-                                NOTE_FOREST(kb[k] + q, ty)
-                            }
-                            if (qf >= fv) break;           // the next one starts after v ends
-                            if (++q >= nk[k]) break;
-                            const int64_t c = comm_id(kb[k] + q);
-                            qs = (sbase + c * ns)[col];
-                            qf = (fbase + c * ns)[col];
                         }
                     }
                     if (PRORATE) {
@@ -1567,6 +1585,11 @@ hipError_t launch_walk(const WalkArgs &a, int32_t n_blocks, hipStream_t stream) 
                                       dim3(kBlockWalkers * kLanes), params, 0, stream);
 }
 
+template <bool PRORATE, bool DETECT, int FOREST, int NC>
+void launch_overlap_kernel(const OverlapArgs &a, dim3 grid, dim3 block, size_t lds, hipStream_t stream) {
+    hipLaunchKernelGGL((k_overlap<PRORATE, DETECT, FOREST, NC>), grid, block, lds, stream, a);
+}
+
 template <int NC>
 hipError_t launch_overlap_nc(const OverlapArgs &a, int32_t n_ranks, hipStream_t stream) {
     const int64_t units = (int64_t)n_ranks * a.n_tiles;
@@ -1577,19 +1600,19 @@ hipError_t launch_overlap_nc(const OverlapArgs &a, int32_t n_ranks, hipStream_t 
         // compact ensemble in LDS: kFxWaves (rank, tile) units per workgroup share its nodes
         const dim3 g2((unsigned)((units + kFxWaves - 1) / kFxWaves)), b2(kLanes * kFxWaves);
         const size_t lds = sizeof(uint32_t) * ((size_t)a.fx.n_words + (size_t)a.n_trees);
-        if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, 2, NC>), g2, b2, lds, stream, a);
-        else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, 2, NC>), g2, b2, lds, stream, a);
-        else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, 2, NC>), g2, b2, lds, stream, a);
-        else hipLaunchKernelGGL((k_overlap<false, false, 2, NC>), g2, b2, lds, stream, a);
+        if (prorate && a.chg) launch_overlap_kernel<true, true, 2, NC>(a, g2, b2, lds, stream);
+        else if (prorate) launch_overlap_kernel<true, false, 2, NC>(a, g2, b2, lds, stream);
+        else if (a.chg) launch_overlap_kernel<false, true, 2, NC>(a, g2, b2, lds, stream);
+        else launch_overlap_kernel<false, false, 2, NC>(a, g2, b2, lds, stream);
     } else if (forest) {
-        if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, 1, NC>), grid, block, 0, stream, a);
-        else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, 1, NC>), grid, block, 0, stream, a);
-        else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, 1, NC>), grid, block, 0, stream, a);
-        else hipLaunchKernelGGL((k_overlap<false, false, 1, NC>), grid, block, 0, stream, a);
-    } else if (prorate && a.chg) hipLaunchKernelGGL((k_overlap<true, true, 0, NC>), grid, block, 0, stream, a);
-    else if (prorate) hipLaunchKernelGGL((k_overlap<true, false, 0, NC>), grid, block, 0, stream, a);
-    else if (a.chg) hipLaunchKernelGGL((k_overlap<false, true, 0, NC>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((k_overlap<false, false, 0, NC>), grid, block, 0, stream, a);
+        if (prorate && a.chg) launch_overlap_kernel<true, true, 1, NC>(a, grid, block, 0, stream);
+        else if (prorate) launch_overlap_kernel<true, false, 1, NC>(a, grid, block, 0, stream);
+        else if (a.chg) launch_overlap_kernel<false, true, 1, NC>(a, grid, block, 0, stream);
+        else launch_overlap_kernel<false, false, 1, NC>(a, grid, block, 0, stream);
+    } else if (prorate && a.chg) launch_overlap_kernel<true, true, 0, NC>(a, grid, block, 0, stream);
+    else if (prorate) launch_overlap_kernel<true, false, 0, NC>(a, grid, block, 0, stream);
+    else if (a.chg) launch_overlap_kernel<false, true, 0, NC>(a, grid, block, 0, stream);
+    else launch_overlap_kernel<false, false, 0, NC>(a, grid, block, 0, stream);
     return hipGetLastError();
 }
 
