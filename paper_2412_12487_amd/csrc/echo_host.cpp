@@ -108,6 +108,7 @@ struct echo_graph_s {
     void *scratch = nullptr;           // this GPU's fixed workspace array (echo_compose_batch_static)
     hipError_t scratch_error = hipSuccess;
     DeviceGraph dg;
+    std::vector<int32_t> counted_coll; // collective of each index among those met by counting
     std::vector<void *> owned;         // device allocations of the graph
     // workspace, grown on demand
     int64_t *class_cost = nullptr;
@@ -519,6 +520,16 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
         slot_base[c] = n_slots;
         n_slots += cN[c];
     }
+    // the rest meet by counting arrivals in device memory: they get indices of their own,
+    // so that the arrival maxima and counts a compose clears cover them only
+    std::vector<int32_t> counted(nc, -1), counted_coll, counted_N;
+    for (int64_t c = 0; c < nc; ++c)
+        if (!(coll_aux[c] & (kAuxLocal | kAuxSlots))) {
+            counted[c] = (int32_t)counted_coll.size();
+            counted_coll.push_back((int32_t)c);
+            counted_N.push_back(cN[c]);
+        }
+    auto item_coll = [&](int64_t c) { return counted[c] >= 0 ? counted[c] : (int32_t)c; };
 
     // walk lists: each walker's ops by (key, rank, program order), key = level
     // for compute/memcpy, the launch level for a comm op
@@ -562,7 +573,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
             const int64_t c = d->op_coll[v];
             // the collective's first member slot (slot mode), else unused
             it.far_off = slot_base[c] >= 0 ? (int32_t)slot_base[c] : (int32_t)far.size();
-            it.coll = (int32_t)c;
+            it.coll = item_coll(c);
             it.dur = ccls[c];    // the cost class its finish reads
             it.nfar = 0;
             it.aux = coll_aux[d->op_coll[v]] | ((uint32_t)op_slot[v] << 5);
@@ -650,7 +661,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
                           (sv < 0 ? kNoReg : 0u);
                 it.nfar = (int32_t)((int64_t)far.size() - f0);
                 it.far_off = (int32_t)f0;
-                it.coll = d->op_kind[v] == ECHO_COMM ? (int32_t)d->op_coll[v] : -1;
+                it.coll = d->op_kind[v] == ECHO_COMM ? item_coll(d->op_coll[v]) : -1;
                 it.aux = d->op_kind[v] == ECHO_COMM
                              ? coll_aux[d->op_coll[v]] | ((uint32_t)op_slot[v] << 5)
                              : 0u;
@@ -798,6 +809,8 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
     dg.n_blocks = (int32_t)nblk;
     dg.max_comm_streams = max_comm_streams;
     dg.n_slots = n_slots;
+    dg.n_counted = (int64_t)counted_coll.size();
+    g->counted_coll = std::move(counted_coll);
 #define UP(dst, src)                                                        \
     do {                                                                    \
         e = upload(&dst, src);                                              \
@@ -825,6 +838,7 @@ int load(const echo_graph_desc *d, int device, int32_t min_rpw, echo_graph *out)
         UP(dt.type, h.type);
     }
     UP(dg.members, cN);
+    UP(dg.counted_members, counted_N);
     UP(dg.block_class, block_class);
     UP(dg.cl_off, cl_off);
     UP(dg.cl, cl);
@@ -886,8 +900,8 @@ int ensure_workspace(echo_graph g, const ComposeShape &sh, int32_t n_refine, int
     const int64_t ns = sh.ns;
     int rc;
     if ((rc = ensure(&g->class_cost, &g->class_cost_n, (size_t)(g->dg.classes.n * ns), "class cost"))) return rc;
-    if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->n_colls * ns), "arrivals"))) return rc;
-    if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->n_colls * sh.n_tiles), "arrival counts"))) return rc;
+    if ((rc = ensure(&g->arrive, &g->arrive_n, (size_t)(g->dg.n_counted * ns), "arrivals"))) return rc;
+    if ((rc = ensure(&g->count, &g->count_n, (size_t)(g->dg.n_counted * sh.n_tiles), "arrival counts"))) return rc;
     if ((rc = ensure(&g->slots, &g->slots_n, (size_t)(g->dg.n_slots * ns), "member slots"))) return rc;
     // overlap masks, then one flag byte per (item row, tile): whether the row has a nonzero one
     if (n_refine > 0 && !sh.ext &&
@@ -928,7 +942,8 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
     const bool until_stable = sh.until_stable, prorate = sh.prorate, forest = sh.forest, ext = sh.ext;
     unsigned *stable = until_stable ? ws.chg + ns : nullptr;
     hipError_t e;
-    const int64_t n_arrive = g->n_colls * ns, n_count = g->n_colls * n_tiles, n_slot_values = g->dg.n_slots * ns;
+    const int64_t n_arrive = g->dg.n_counted * ns, n_count = g->dg.n_counted * n_tiles,
+                  n_slot_values = g->dg.n_slots * ns;
     g->timed_kinds.clear();
     const bool timing = timed && g->timing;
     Timed tm{g, stream};
@@ -1015,7 +1030,7 @@ int enqueue_compose(echo_graph g, const echo_scenario *d_scen, int32_t n_scen, c
             a.items = g->dg.items;
             a.walk_off = g->dg.walk_off;
             a.far = g->dg.far;
-            a.c_N = g->dg.members;
+            a.c_N = g->dg.counted_members;
             a.block_class = g->dg.block_class;
             a.scen = d_scen;
             a.class_cost = ws.class_cost;
@@ -1093,8 +1108,13 @@ int walk_chain(echo_graph g, const int64_t w[3], int64_t out[4]) {
         const int32_t x = runnable.back();
         runnable.pop_back();
         for (; pos[x] < off[x + 1]; ++pos[x]) {
-            const WalkItem &it = items[pos[x]];
+            WalkItem it = items[pos[x]];
             const int kind = item_kind(it.meta);
+            if ((kind == ECHO_COMM || kind == kResolve) && !((uint32_t)it.aux & (kAuxLocal | kAuxSlots))) {
+                if (it.coll < 0 || it.coll >= (int32_t)g->counted_coll.size())
+                    return fail(ECHO_ERR_ARG, "internal: walk item of op %d has no counted collective", it.op);
+                it.coll = g->counted_coll[it.coll];
+            }
             Pt p = cur[x];
             if (kind == kResolve) {
                 if (arrived[it.coll] < members[it.coll]) {     // some member has not launched yet
@@ -1223,8 +1243,8 @@ int echo_compose_batch_static(echo_graph g, const echo_scenario *d_scen, int32_t
         constexpr int64_t kCap = ECHO_SCRATCH_BYTES;
         const int64_t parts[5] = {
             g->dg.classes.n * sh.ns * (int64_t)sizeof(int64_t),              // class costs
-            g->n_colls * sh.ns * (int64_t)sizeof(unsigned long long),       // arrival maxima
-            g->n_colls * sh.n_tiles * (int64_t)sizeof(unsigned),             // arrival counts
+            g->dg.n_counted * sh.ns * (int64_t)sizeof(unsigned long long),   // arrival maxima
+            g->dg.n_counted * sh.n_tiles * (int64_t)sizeof(unsigned),         // arrival counts
             n_refine > 0 ? sh.mrows * (sh.mstride + sh.n_tiles) : 0,         // overlap masks and row flags
             g->dg.n_slots * sh.ns * (int64_t)sizeof(int64_t),               // member slots
         };

@@ -45,7 +45,9 @@ struct WalkItem {
     uint32_t meta;      // kind | slot << 2 | class << 5 | regmask << 8 | fast << 16 | noreg << 17
                         // | need start << 18 | need finish << 19 | fold << 20
     int32_t far_off;    // predecessors read back from memory: far[far_off .. +nfar)
-    int32_t coll;       // collective of a comm op, -1 otherwise
+    int32_t coll;       // collective of a comm op, -1 otherwise; of a collective met by counting
+                        // arrivals in device memory (neither in LDS nor through member slots),
+                        // its index among those collectives
     int64_t dur;        // base duration of compute / memcpy ops; resolve item: cost class
     int32_t nfar;
     int32_t aux;
@@ -202,6 +204,8 @@ struct DeviceGraph {
     CompactForest fx;                  // the ensemble in LDS form, when it fits
     int32_t max_comm_streams = 0;    // the most streams with comm ops on one rank
     int64_t n_slots = 0;             // member slots of the collectives met through slots
+    int64_t n_counted = 0;           // collectives met by counting arrivals in device memory
+    int32_t *counted_members = nullptr;   // [n_counted] their member ops present
 };
 
 constexpr int kClassMetrics = 4;
@@ -210,7 +214,7 @@ struct WalkArgs {
     const WalkItem *items;
     const int64_t *walk_off;
     const int32_t *far;
-    const int32_t *c_N;              // [coll] member ops present (arrivals that complete the barrier)
+    const int32_t *c_N;              // [counted coll] member ops present (arrivals that complete the barrier)
     const int32_t *block_class;
     const echo_scenario *scen;
     const int64_t *class_cost;       // [class][scen]
@@ -222,8 +226,8 @@ struct WalkArgs {
     int64_t mstride;
     const unsigned *stable;          // non-null: skip the pass when *stable (every scenario at its fixed point)
     int64_t *start, *finish;         // [op][scen]
-    unsigned long long *arrive;      // [coll][scen] latest member launch
-    unsigned *count;                 // [coll][tile] members arrived
+    unsigned long long *arrive;      // [counted coll][scen] latest member launch
+    unsigned *count;                 // [counted coll][tile] members arrived
     int64_t *slots;                  // [slot][scen] launch time of a slot collective's member, -1 before it
     int64_t *step;                   // [scen]
     uint64_t *digest;                // [scen] or null

@@ -104,15 +104,16 @@ def test_static_compose_allocates_nothing(E):
 
 
 def test_static_compose_refuses_what_does_not_fit(E):
-    """The config-1 graph with 16384 scenarios needs about 70 MB of workspace, more
-    than the fixed 64 MiB array: ECHO_ERR_RANGE before any launch; the graph then
-    composes the whole enumeration batch (4096 scenarios, about 18 MiB); missing
-    outputs are argument errors."""
+    """The config-1 graph with 32768 scenarios needs more workspace than the fixed
+    64 MiB array (its overlap masks alone, one byte per walk item and scenario, take at
+    least 2912 x 32768 bytes, 95 MB): ECHO_ERR_RANGE before any launch; the graph then
+    composes the whole enumeration batch (4096 scenarios); missing outputs are argument
+    errors."""
     import torch
     g = configs.graph(1)
     G = E.Graph(g, 0)
     try:
-        sc = configs.scenario_batch(4, n=16384)
+        sc = configs.scenario_batch(4, n=32768)
         d, n = E.scenarios_to_device(sc)
         with pytest.raises(E.EchoError) as x:
             G.compose_static(d, n, 1, _outputs(G, n, digest=False))
