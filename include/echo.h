@@ -392,10 +392,11 @@ int echo_walk_chain(echo_graph g, const int64_t weight_ps[3], int64_t out[4]);
  * d_start and d_finish ([n_ops][n_scen] int64) and d_step are required (the
  * walk keeps its working times there); d_digest may be NULL.  Kernel timing
  * (echo_set_timing) is not recorded.  The workspace, each part rounded up to
- * 256 bytes, is 8 * n_classes * n_scen (cost classes) + 8 * n_colls * n_scen
- * (arrivals) + 4 * n_colls * ceil(n_scen / 64) (counts) + 8 * n_slots * n_scen
- * (n_slots: the member ops of collectives of at most eight members that are
- * met in device memory, not in one workgroup) + with n_refine > 0
+ * 256 bytes, is 8 * n_classes * n_scen (cost classes) + 8 * n_counted * n_scen
+ * (arrivals) + 4 * n_counted * ceil(n_scen / 64) (counts; n_counted: the
+ * collectives of more than eight members met in device memory, not in one
+ * workgroup) + 8 * n_slots * n_scen (n_slots: the member ops of collectives of
+ * at most eight members met in device memory) + with n_refine > 0
  * (n_items + 32) * 65 * ceil(n_scen / 64) bytes (masks and a flag byte per
  * row and tile; n_items = ops + comm ops); a call needing more returns
  * ECHO_ERR_RANGE before enqueuing anything.
