@@ -110,6 +110,30 @@ def test_walk_chain_hand_cases(E):
     with E.Graph(b.graph()) as G:
         got = _chain(G, (1000, 300, 700))
         assert got == {"ps": 6700, "items": 6, "lds_barriers": 0, "global_barriers": 1}, got
+    # the same all-reduce as collective 1 behind a P2P between ranks 0 and 1 (collective 0,
+    # met in LDS): the all-reduce is the first collective met by counting, index 0 among
+    # those, and the analysis must still see its 16 members.  Every rank: one op (rank 15:
+    # three), the all-reduce, one op; then rank 0 sends and rank 1 receives and runs one
+    # more op.  Rank 1's chain: 3 ops and the launch of rank 15 (4000), all-reduce resolve
+    # (+1000 +700), op (6700), recv launch (7700; rank 0's send launch is also at 7700),
+    # recv resolve (+1000 +300), op: 10000 ps over 9 items.
+    b = Builder(16)
+    p2p = b.collective(P2P, 1000)
+    c = b.collective(AR, 1 << 20)
+    for r in range(16):
+        prev = []
+        for _ in range(3 if r == 15 else 1):
+            prev = [b.compute(r, 5, preds=prev)]
+        x = b.comm(r, c, preds=prev)
+        y = b.compute(r, 5, preds=[x])
+        if r == 0:
+            b.comm(0, p2p, stream=3, preds=[y])
+        elif r == 1:
+            z = b.comm(1, p2p, stream=4, preds=[y])
+            b.compute(1, 5, preds=[z])
+    with E.Graph(b.graph()) as G:
+        got = _chain(G, (1000, 300, 700))
+        assert got == {"ps": 10000, "items": 9, "lds_barriers": 1, "global_barriers": 1}, got
 
 
 def test_walk_chain_covers_the_longest_walk_list(E):
