@@ -1060,10 +1060,10 @@ __attribute__((amdgpu_waves_per_eu(PRORATE && DETECT && FOREST == 0 && NC == 4 ?
     constexpr bool EXT = PRORATE || FOREST != 0;  // output: extra time per op instead of a mask
     constexpr int W = FOREST == 2 ? kFxWaves : 1;      // wavefronts per workgroup
     constexpr int STAGE = FOREST == 2 ? kIdStage / 4 : kIdStage;
-    // unchained starts prefetched per round: all but the ensemble variants prefetch fewer,
-    // for the registers the block checks take (four wavefronts per SIMD for the mask and
-    // prorating variants with four comm streams)
-    constexpr int NPRE = FOREST ? kPre : (DETECT || PRORATE) ? kPre / 4 : kPre / 2;
+    // unchained starts prefetched per round: as many as the registers allow while the
+    // variants with four comm streams keep four wavefronts per SIMD (the prorating and
+    // fixed-point variants hold more state for their block checks and interval merges)
+    constexpr int NPRE = FOREST ? kPre : PRORATE ? kPre / 4 : DETECT ? (NC == 4 ? kPre / 2 : kPre / 4) : NC == 4 ? kPre : kPre / 2;
     __shared__ int64_t feat[FOREST == 1 ? 12 * kLanes : 1];   // the ensemble's feature vectors, one per lane
     __shared__ uint16_t fbin[FOREST == 2 ? W * kFxRows * kLanes : 1];   // compact: bin rows per lane
     extern __shared__ uint32_t fwords[];         // compact: the ensemble's nodes
